@@ -1,0 +1,321 @@
+/*
+ * l1csr oracle — plain CPU definitions of every operation on the hot path of
+ * l1-regularised compressed learning (Lee & Lee, "Compressed Learning of Deep
+ * Neural Networks for OpenCL-Capable Embedded Systems", Appl. Sci. 2019).
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke
+ * check and the CPU-baseline leg of the benchmark may load this library.
+ * It shares no code, header or table with the HIP implementation.
+ *
+ * Conventions (the same ones the library's public header documents):
+ *   - W is an N x K matrix in CSR: row_ptr[N+1], col_idx[nnz] (strictly
+ *     increasing inside a row), vals[nnz]; indices are int32.
+ *   - Dense operands keep the batch index contiguous: X[K][B], Y[N][B],
+ *     dY[N][B], dX[K][B] with leading dimensions ld* >= B; dW, Z are [N][K].
+ *     Y = W.X is the transpose of the paper's X_T = X_B.W' (Section 3.2).
+ *   - Every reduction accumulates in double, in the order stated next to it,
+ *     and rounds once to float at the end.
+ *   - Built with -ffp-contract=off so that no product is fused silently.
+ *
+ * Return value of every int function: 0 on success, negative on bad
+ * arguments (-1) or insufficient output capacity (-2).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+#define ORC_ECAPACITY (-2)
+
+int orc_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* ------------------------------------------------------------------------
+ * Forward product (Section 3.2, "Forward: X_T <- X_B W'", dense x compressed').
+ * In batch-contiguous layout:  Y[i][b] = sum_{p in row i} vals[p] * X[col[p]][b].
+ * Summation order: p ascending.
+ * ---------------------------------------------------------------------- */
+int orc_spmm_fwd(int32_t N, int32_t K, int32_t B,
+                 const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                 const float *X, int64_t ldx, float *Y, int64_t ldy) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    #pragma omp parallel
+    {
+        double *acc = (double *)malloc(sizeof(double) * (size_t)(B > 0 ? B : 1));
+        #pragma omp for schedule(dynamic, 16)
+        for (int32_t i = 0; i < N; ++i) {
+            for (int32_t b = 0; b < B; ++b) acc[b] = 0.0;
+            for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+                const double w = (double)vals[p];
+                const float *xr = X + (int64_t)col_idx[p] * ldx;
+                for (int32_t b = 0; b < B; ++b) acc[b] += w * (double)xr[b];
+            }
+            for (int32_t b = 0; b < B; ++b) Y[(int64_t)i * ldy + b] = (float)acc[b];
+        }
+        free(acc);
+    }
+    (void)K;
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Backward product for the data gradient (Section 3.2, "Backward:
+ * dLoss/dX_B <- dLoss/dX_T W", dense x compressed).  In batch-contiguous layout:
+ *   dX[k][b] = sum_{p : col[p] = k} vals[p] * dY[row(p)][b].
+ * Written as the scatter over W's nonzeros in CSR order (row ascending, then
+ * p ascending), which is the definition read directly off the CSR arrays.
+ * Threads split the batch index only, so every sum keeps that order.
+ * ---------------------------------------------------------------------- */
+int orc_spmm_bwd_t(int32_t N, int32_t K, int32_t B,
+                   const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                   const float *dY, int64_t ldy, float *dX, int64_t ldx) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    const int32_t CH = 32; /* batch columns per task */
+    const int32_t nchunks = (B + CH - 1) / CH;
+    #pragma omp parallel
+    {
+        double *acc = (double *)malloc(sizeof(double) * ((size_t)K * CH + 1));
+        #pragma omp for schedule(dynamic, 1)
+        for (int32_t c = 0; c < nchunks; ++c) {
+            const int32_t b0 = c * CH;
+            const int32_t nb = (B - b0) < CH ? (B - b0) : CH;
+            memset(acc, 0, sizeof(double) * (size_t)K * CH);
+            for (int32_t i = 0; i < N; ++i)
+                for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+                    const double w = (double)vals[p];
+                    const float *dyr = dY + (int64_t)i * ldy + b0;
+                    double *a = acc + (size_t)col_idx[p] * CH;
+                    for (int32_t j = 0; j < nb; ++j) a[j] += w * (double)dyr[j];
+                }
+            for (int32_t k = 0; k < K; ++k)
+                for (int32_t j = 0; j < nb; ++j)
+                    dX[(int64_t)k * ldx + b0 + j] = (float)acc[(size_t)k * CH + j];
+        }
+        free(acc);
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Dense weight gradient of the l1 phase (the gradient that enters the
+ * minibatch proximal step, Eq. (prox); the paper leaves its computation to
+ * the dense framework):  dW[i][k] = sum_b dY[i][b] * X[k][b], b ascending.
+ * No 1/|B| factor: the caller's dY already carries the loss scaling.
+ * ---------------------------------------------------------------------- */
+int orc_dense_wgrad(int32_t N, int32_t K, int32_t B,
+                    const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                    float *dW, int64_t ldw) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B || ldw < K) return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int32_t i = 0; i < N; ++i) {
+        const float *dyr = dY + (int64_t)i * ldy;
+        for (int32_t k = 0; k < K; ++k) {
+            const float *xr = X + (int64_t)k * ldx;
+            double acc = 0.0;
+            for (int32_t b = 0; b < B; ++b) acc += (double)dyr[b] * (double)xr[b];
+            dW[(int64_t)i * ldw + k] = (float)acc;
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Weight gradient of the debiasing phase (Section 2.4: retraining without the
+ * regulariser, zero-valued weights excluded from training).  The gradient is
+ * the dense one sampled on W's pattern:
+ *   gv[p] = sum_b dY[row(p)][b] * X[col[p]][b], b ascending.
+ * ---------------------------------------------------------------------- */
+int orc_sddmm(int32_t N, int32_t K, int32_t B,
+              const int32_t *row_ptr, const int32_t *col_idx,
+              const float *dY, int64_t ldy, const float *X, int64_t ldx, float *gv) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int32_t i = 0; i < N; ++i) {
+        const float *dyr = dY + (int64_t)i * ldy;
+        for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+            const float *xr = X + (int64_t)col_idx[p] * ldx;
+            double acc = 0.0;
+            for (int32_t b = 0; b < B; ++b) acc += (double)dyr[b] * (double)xr[b];
+            gv[p] = (float)acc;
+        }
+    }
+    (void)K;
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Soft-thresholding operator: the closed form of prox of t*||.||_1
+ * (Section 2.2):  [prox(z)]_i = sgn(z_i) * max(|z_i| - t, 0).
+ * Evaluated in double, the precision of the paper's prox kernel (Fig. 4).
+ * The "+ 0.0" turns the -0.0 that sgn(z) * 0 gives for negative z into the
+ * canonical +0.0; it does not change any nonzero result.
+ * ---------------------------------------------------------------------- */
+static double sgn(double z) { return (double)((z > 0.0) - (z < 0.0)); }
+
+double orc_soft_threshold(double z, double t) {
+    return sgn(z) * fmax(fabs(z) - t, 0.0) + 0.0;
+}
+
+/* The prox step's threshold: eta * lambda (Eq. (prox): prox of eta*Psi with
+ * Psi = lambda*||w||_1; Fig. 4 uses lambda*learning_rate).  The product of two
+ * floats is exact in double. */
+double orc_threshold(float eta, float lambda) { return (double)eta * (double)lambda; }
+
+/* The prox step's argument A = w - eta*g (Eq. (prox); Fig. 4's caption says A
+ * holds w^k - eta G(w^k)).  eta*g is exact in double, so this rounds once. */
+double orc_prox_arg(float w, float g, float eta) { return (double)w - (double)eta * (double)g; }
+
+/* ------------------------------------------------------------------------
+ * Minibatch proximal gradient step on the dense A of Fig. 4 (Eq. (prox)):
+ *   Z[i][k] = float( S_t( w_ik - eta * G[i][k] ) ),  t = eta * lambda,
+ * with w_ik = 0 where W has no entry (every one of the N*K weights takes part,
+ * so a zero weight may become nonzero again).  row_counts[i] (optional)
+ * receives the number of nonzero Z[i][k].
+ * ---------------------------------------------------------------------- */
+int orc_prox_dense(int32_t N, int32_t K,
+                   const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                   const float *G, int64_t ldg, float eta, float lambda,
+                   float *Z, int64_t ldz, int32_t *row_counts) {
+    if (N < 0 || K < 0 || ldg < K || ldz < K) return ORC_EINVAL;
+    const double t = orc_threshold(eta, lambda);
+    #pragma omp parallel
+    {
+        float *wrow = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+        #pragma omp for schedule(dynamic, 8)
+        for (int32_t i = 0; i < N; ++i) {
+            for (int32_t k = 0; k < K; ++k) wrow[k] = 0.0f;
+            for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) wrow[col_idx[p]] = vals[p];
+            int32_t cnt = 0;
+            for (int32_t k = 0; k < K; ++k) {
+                const double z = orc_prox_arg(wrow[k], G[(int64_t)i * ldg + k], eta);
+                const float s = (float)orc_soft_threshold(z, t);
+                Z[(int64_t)i * ldz + k] = s;
+                cnt += (s != 0.0f);
+            }
+            if (row_counts) row_counts[i] = cnt;
+        }
+        free(wrow);
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * The same step restricted to W's stored entries (debiasing with lambda = 0
+ * is plain SGD on the fixed pattern, Section 2.4; lambda > 0 gives the
+ * support-restricted prox):  vals_out[p] = float( S_t(vals[p] - eta*gv[p]) ).
+ * vals_out may alias vals.
+ * ---------------------------------------------------------------------- */
+int orc_prox_csr(int32_t nnz, const float *vals, const float *gv,
+                 float eta, float lambda, float *vals_out) {
+    if (nnz < 0) return ORC_EINVAL;
+    const double t = orc_threshold(eta, lambda);
+    for (int32_t p = 0; p < nnz; ++p)
+        vals_out[p] = (float)orc_soft_threshold(orc_prox_arg(vals[p], gv[p], eta), t);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Dense -> CSR (Section 3.1: store only the nonzero values; Fig. 1(iii)).
+ * Keeps the entries with |Z[i][k]| > t (t = 0 after a prox step) in row-major
+ * order.  Writes row_ptr[N+1] and, when nnz <= capacity, col_idx/vals.
+ * *nnz_out always receives the required nnz; returns -2 when it exceeds
+ * capacity (row_ptr is still written).
+ * ---------------------------------------------------------------------- */
+int orc_recompress(int32_t N, int32_t K, const float *Z, int64_t ldz, float t,
+                   int32_t *row_ptr, int32_t *col_idx, float *vals,
+                   int64_t capacity, int64_t *nnz_out) {
+    if (N < 0 || K < 0 || ldz < K || capacity < 0) return ORC_EINVAL;
+    int64_t nnz = 0;
+    row_ptr[0] = 0;
+    for (int32_t i = 0; i < N; ++i) {
+        for (int32_t k = 0; k < K; ++k) {
+            const float z = Z[(int64_t)i * ldz + k];
+            if (fabsf(z) > t) {
+                if (nnz < capacity) { col_idx[nnz] = k; vals[nnz] = z; }
+                ++nnz;
+            }
+        }
+        row_ptr[i + 1] = (int32_t)nnz;
+    }
+    *nnz_out = nnz;
+    return nnz <= capacity ? ORC_OK : ORC_ECAPACITY;
+}
+
+/* ------------------------------------------------------------------------
+ * CSR -> CSR without its explicit zeros (after a support-restricted prox).
+ * Out-of-place: the output arrays must not alias the input ones.
+ * ---------------------------------------------------------------------- */
+int orc_compact(int32_t N, const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out, int64_t *nnz_out) {
+    if (N < 0) return ORC_EINVAL;
+    int64_t nnz = 0;
+    row_ptr_out[0] = 0;
+    for (int32_t i = 0; i < N; ++i) {
+        for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+            if (vals[p] != 0.0f) { col_idx_out[nnz] = col_idx[p]; vals_out[nnz] = vals[p]; ++nnz; }
+        row_ptr_out[i + 1] = (int32_t)nnz;
+    }
+    *nnz_out = nnz;
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Layer glue of the fully connected networks the method trains (the paper
+ * trains ReLU networks with a softmax cross-entropy loss; its He
+ * initialisation targets ReLU units).  These follow the textbook definitions.
+ * ---------------------------------------------------------------------- */
+
+/* ReLU(x) = max(x, 0), with +0.0 for x <= 0. */
+int orc_relu_fwd(int64_t n, const float *x, float *y) {
+    for (int64_t j = 0; j < n; ++j) y[j] = x[j] > 0.0f ? x[j] : 0.0f;
+    return ORC_OK;
+}
+
+/* d/dx ReLU = 1 for x > 0, 0 otherwise (0 at x = 0). */
+int orc_relu_bwd(int64_t n, const float *x, const float *dy, float *dx) {
+    for (int64_t j = 0; j < n; ++j) dx[j] = x[j] > 0.0f ? dy[j] : 0.0f;
+    return ORC_OK;
+}
+
+/* Mean softmax cross-entropy over the batch.  logits[C][B] (class-major,
+ * batch contiguous, leading dimension ld), labels[B] in [0, C).
+ * loss = (1/B) sum_b ( log sum_c exp(z_cb) - z_{label_b, b} ),
+ * dlogits[c][b] = (softmax(z_.b)_c - [c == label_b]) / B.
+ * The column maximum is subtracted before exp (exact in real arithmetic). */
+int orc_softmax_xent(int32_t C, int32_t B, const float *logits, int64_t ld,
+                     const int32_t *labels, float *dlogits, double *loss) {
+    if (C <= 0 || B < 0 || ld < B) return ORC_EINVAL;
+    double total = 0.0;
+    for (int32_t b = 0; b < B; ++b) {
+        if (labels[b] < 0 || labels[b] >= C) return ORC_EINVAL;
+        double m = (double)logits[b];
+        for (int32_t c = 1; c < C; ++c) m = fmax(m, (double)logits[(int64_t)c * ld + b]);
+        double s = 0.0;
+        for (int32_t c = 0; c < C; ++c) s += exp((double)logits[(int64_t)c * ld + b] - m);
+        total += log(s) + m - (double)logits[(int64_t)labels[b] * ld + b];
+        for (int32_t c = 0; c < C; ++c) {
+            const double pc = exp((double)logits[(int64_t)c * ld + b] - m) / s;
+            dlogits[(int64_t)c * ld + b] = (float)((pc - (c == labels[b] ? 1.0 : 0.0)) / (double)B);
+        }
+    }
+    *loss = B > 0 ? total / (double)B : 0.0;
+    return ORC_OK;
+}
