@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Throughput of the l1-phase CSR training step on one MI355X.
+
+A step is one pass of the hot path over one batch of the large fully
+connected layer 9216 -> 4096 (W: 4096 x 9216 CSR, 9% density with Zipf(1.1)
+row lengths, batch 1024, fp32):
+
+    Y  = W.X                      csr_spmm_fwd
+    CSC(W)                        csc_build
+    dX = W^T.dY                   csr_spmm_bwd_t
+    dW = dY.X^T                   dense_wgrad     (fp32 matrix cores)
+    Z  = S_t(W - eta*dW)          prox_l1_step    (in place over dW)
+    W' = CSR(Z)                   csr_recompress
+
+Every step reads the same resident inputs and writes W' to its own buffers,
+so all timed steps do identical work.  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sparse train-step GFLOP/s (nnz-effective) and achieved HBM GB/s vs peak"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_MFMA_F32_TFLOPS = 157.3   # MI355X dense fp32 matrix
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=256,
+                    help="rows of W in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_1905_07931_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel_file, src_hash):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel source (else None)."""
+    path = os.path.join(PROFILES, kernel_file)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic_json:"):
+                d = json.loads(line.split(":", 1)[1])
+                if d.get("source_hash") == src_hash:
+                    return d.get("bytes_per_launch")
+    return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the hot path is "
+              "built and measured on a single MI355X, multi-GPU sharding is not part of it.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L1.lib()  # fail loudly if the HIP library is missing
+
+    t0 = time.time()
+    Lr = synth.fc9216_4096(seed=0)
+    gen_s = time.time() - t0
+    N, K, B, nnz = Lr.N, Lr.K, Lr.B, Lr.nnz
+    eta, lam = Lr.eta, Lr.lam
+
+    W = L1.CSR.from_host(Lr.row_ptr, Lr.col_idx, Lr.vals, K, device=dev)
+    X = torch.from_numpy(Lr.X).to(dev)
+    dY = torch.from_numpy(Lr.dY).to(dev)
+    Y = torch.empty((N, B), dtype=torch.float32, device=dev)
+    dX = torch.empty((K, B), dtype=torch.float32, device=dev)
+    dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+    cnt = torch.empty(N, dtype=torch.int32, device=dev)
+    csc = L1.CSC(torch.empty(K + 1, dtype=torch.int32, device=dev),
+                 torch.empty(nnz, dtype=torch.int32, device=dev),
+                 torch.empty(nnz, dtype=torch.int32, device=dev))
+    Wout = L1.CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(N * K, dtype=torch.int32, device=dev),
+                  torch.empty(N * K, dtype=torch.float32, device=dev), None)
+
+    names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_step",
+             "csr_recompress"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        L1.csr_spmm_fwd(W, X, Y)
+        mark(1)
+        L1.csc_build(W, csc)
+        mark(2)
+        L1.csr_spmm_bwd_t(W, dY, csc, dX)
+        mark(3)
+        L1.dense_wgrad(dY, X, dW)
+        mark(4)
+        L1.prox_l1_step(L1.PROX_DENSE, W, dW, eta, lam, Z=dW, row_counts=cnt)
+        mark(5)
+        L1.csr_recompress(dW, 0.0, row_counts=cnt, out=Wout)
+        mark(6)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # whole-step timing: K back-to-back steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    # per-kernel durations with events between the calls (same stream)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    per = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
+           for i, n in enumerate(names)}
+
+    nnz_out = int(Wout.row_ptr[-1].item())
+    flops_step = 2.0 * nnz * B * 2 + 2.0 * N * K * B          # fwd + bwd + dense dW
+    flops_nnz_only = 6.0 * nnz * B
+    gflops = flops_step / (ms_per_step * 1e-3) / 1e9
+
+    # algorithmic bytes (each operand once)
+    csr_in = 8.0 * nnz + 4.0 * (N + 1)
+    csr_out = 8.0 * nnz_out + 4.0 * (N + 1)
+    bytes_prox = 4.0 * N * K + csr_in + 4.0 * N * K + 4.0 * N         # dW in, W in, Z out, counts
+    bytes_recompress = 4.0 * N * K + 4.0 * N + csr_out                # Z in, counts, CSR out
+    prox_recompress_gbs = (bytes_prox + bytes_recompress) / (
+        (per["prox_l1_step"] + per["csr_recompress"]) * 1e-3) / 1e9
+
+    dom = max(per, key=per.get)
+    wg_flops = 2.0 * N * K * B
+    wg_tflops = wg_flops / (per["dense_wgrad"] * 1e-3) / 1e12
+    if dom == "dense_wgrad":
+        traffic = counter_traffic("dense_wgrad_fc9216x4096_pmc.txt", source_hash("gemm.hip"))
+        roof = {"kernel": "dense_wgrad", "bound": "mfma", "achieved": round(wg_tflops, 2),
+                "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(wg_tflops / PEAK_MFMA_F32_TFLOPS, 4), "traffic": traffic,
+                "algorithmic_flops": wg_flops}
+    else:
+        # fall back to the kernel that took longest, on the HBM roof
+        alg = {"prox_l1_step": bytes_prox, "csr_recompress": bytes_recompress}.get(dom)
+        ach = (alg / (per[dom] * 1e-3) / 1e9) if alg else None
+        roof = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": (ach / PEAK_HBM_GBS) if ach else None, "traffic": None}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(Lr, args.cpu_rows)
+
+    out = {
+        "metric": METRIC, "value": round(gflops, 1), "unit": "GFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "fc9216x4096_b1024_d9_zipf_l1_step", "N": N, "K": K, "B": B,
+                   "nnz": nnz, "density": 0.09, "row_lengths": "zipf s=1.1", "eta": eta,
+                   "lambda": lam, "phase": "l1 (fwd, csc, bwd, dense dW, prox, recompress)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "gflops_nnz_only": round(flops_nnz_only / (ms_per_step * 1e-3) / 1e9, 1),
+        "prox_recompress_hbm_gbs": round(prox_recompress_gbs, 1),
+        "prox_recompress_hbm_frac": round(prox_recompress_gbs / PEAK_HBM_GBS, 4),
+        "nnz_out": nnz_out,
+        "input_gen_s": round(gen_s, 2),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(Lr, rows):
+    """The oracle on a bounded sample of the same step: the first `rows` rows of W
+    (their forward rows, their share of the backward sum, their dense dW rows,
+    prox and recompression), scaled to the full step."""
+    import oracle
+
+    N, K, B = Lr.N, Lr.K, Lr.B
+    rows = min(rows, N)
+    rp = Lr.row_ptr[: rows + 1].copy()
+    nz = int(rp[-1])
+    ci = Lr.col_idx[:nz]
+    v = Lr.vals[:nz]
+    dY = Lr.dY[:rows]
+    t0 = time.perf_counter()
+    oracle.spmm_fwd(rp, ci, v, Lr.X)
+    oracle.spmm_bwd_t(rp, ci, v, dY, K)
+    dW = oracle.dense_wgrad(dY, Lr.X)
+    Z, _ = oracle.prox_dense(rp, ci, v, dW, Lr.eta, Lr.lam, K)
+    oracle.recompress(Z)
+    sec = time.perf_counter() - t0
+    flops = 2.0 * nz * B * 2 + 2.0 * rows * K * B
+    return {"value": round(flops / sec / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {rows} of {N} rows of W ({nz} nnz): fwd, bwd share, dense dW, prox, "
+                      f"recompress; {sec:.2f} s"}
+
+
+if __name__ == "__main__":
+    main()

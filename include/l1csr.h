@@ -1,0 +1,232 @@
+/*
+ * l1csr — the data-parallel hot path of l1-regularised compressed learning
+ * (S. Lee and J. Lee, "Compressed Learning of Deep Neural Networks for
+ * OpenCL-Capable Embedded Systems", Appl. Sci. 9(8), 2019) on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * One training step of a layer whose N x K weight matrix W is kept in CSR:
+ *   forward            Y  = W . X                 csr_spmm_fwd
+ *   backward (data)    dX = W^T . dY              csr_spmm_bwd_t (+ csc_build)
+ *   weight gradient    dW = dY . X^T  (l1 phase)  dense_wgrad
+ *                      gv = (dY . X^T) on W's pattern (debiasing)  sddmm_masked_wgrad
+ *   proximal step      Z  = S_t(W - eta*dW), t = eta*lambda        prox_l1_step
+ *   recompression      Z -> CSR                   csr_recompress
+ *
+ * Conventions shared by every call
+ *   - CSR: row_ptr[n_rows+1] (row_ptr[0] = 0, non-decreasing), col_idx[nnz]
+ *     strictly increasing inside each row, vals[nnz]; int32 indices, float32
+ *     values (Section 3.1 and Fig. 1(iii): ptr / indices / data).
+ *   - Dense activations keep the batch index contiguous: X[K][B], Y[N][B],
+ *     dY[N][B], dX[K][B], each with a leading dimension ld >= B (the paper's
+ *     "internal_cols" of the row-major Dmat / result, Figs. 2-3).  Y = W.X is
+ *     the transpose of the paper's X_T = X_B.W' (Section 3.2), the same numbers.
+ *   - dW, Z are [N][K] row-major with leading dimension >= K.
+ *   - Every pointer argument is DEVICE memory unless its comment says "host".
+ *     All device buffers are owned and allocated by the caller; no call
+ *     allocates or frees memory.  Scratch space is passed in as (ws, ws_bytes),
+ *     sized by l1csr_workspace_bytes().
+ *   - Every call only enqueues work on `stream` and returns without waiting,
+ *     except csr_recompress with capacity < n_rows*n_cols (documented there).
+ *   - Arguments are validated on the host before anything is launched:
+ *     a null pointer, a negative size, ld < row length, a non-finite or
+ *     negative eta/lambda, or a workspace that is too small returns
+ *     L1CSR_EINVAL and launches nothing.  CSR well-formedness is a
+ *     precondition, not checked by the hot calls.  A HIP launch error
+ *     returns L1CSR_EHIP.  Values must be finite (precondition).
+ *   - Calls on the same stream are ordered; calls that share output buffers on
+ *     different streams race.
+ */
+#ifndef L1CSR_H
+#define L1CSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum l1csr_status {
+    L1CSR_OK = 0,
+    L1CSR_EINVAL = -1,       /* bad argument; nothing launched */
+    L1CSR_ECAPACITY = -2,    /* output capacity too small (csr_recompress) */
+    L1CSR_EHIP = -4,         /* a HIP runtime or launch error */
+    L1CSR_EUNSUPPORTED = -5  /* valid but unsupported combination */
+};
+
+/* prox_l1_step modes */
+enum l1csr_prox_mode {
+    L1CSR_PROX_DENSE = 0,    /* every one of the N*K weights, dense gradient */
+    L1CSR_PROX_CSR = 1       /* W's stored entries only, gradient per entry  */
+};
+
+/* workspace queries (l1csr_workspace_bytes) */
+enum l1csr_op {
+    L1CSR_OP_CSC_BUILD = 1,
+    L1CSR_OP_RECOMPRESS = 2,
+    L1CSR_OP_SDDMM = 3,
+    L1CSR_OP_SPMM = 4,
+    L1CSR_OP_COMPACT = 5,
+    L1CSR_OP_SOFTMAX_XENT = 6
+};
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *l1csr_status_str(int status);
+
+/* Bytes of scratch that `op` needs for the given sizes (0 if none).  nnz is an
+ * upper bound on the number of stored entries; B the batch size. */
+size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz, int32_t B);
+
+/*
+ * Forward product, Section 3.2 "Forward: X_T <- X_B W'" (dense x compressed'),
+ * in batch-contiguous layout:
+ *     Y[i][b] = sum_{p = row_ptr[i]}^{row_ptr[i+1]-1} vals[p] * X[col_idx[p]][b]
+ * for 0 <= i < n_rows, 0 <= b < B.  X is [n_cols][ldx], Y is [n_rows][ldy];
+ * every Y[i][0..B) is written (an empty row gives zeros).  nnz is the host-side
+ * number of stored entries (row_ptr[n_rows]); it sizes the launch.
+ * Summation order is unspecified (fp32 accumulation).
+ */
+int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                 const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                 const float *X, int64_t ldx, int32_t B,
+                 float *Y, int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Column-major copy of W's structure (CSC) for the backward product.  Section
+ * 3.2 notes that the dense x compressed product reads W by columns and cannot
+ * be coalesced unless such a column-wise copy is stored; this builds it.
+ *     col_ptr[n_cols+1], row_idx[nnz], perm[nnz]
+ * with row_idx strictly increasing inside each column (the unique canonical
+ * CSC) and perm[q] = the CSR position of CSC entry q, so that the value of CSC
+ * entry q is vals[perm[q]] and a values-only update of W (debiasing) keeps the
+ * copy valid.  Deterministic.  ws must hold
+ * l1csr_workspace_bytes(L1CSR_OP_CSC_BUILD, n_rows, n_cols, nnz, 0) bytes.
+ */
+int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz,
+              const int32_t *row_ptr, const int32_t *col_idx,
+              int32_t *col_ptr, int32_t *row_idx, int32_t *perm,
+              void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward product for the data gradient, Section 3.2 "Backward:
+ * dLoss/dX_B <- dLoss/dX_T W" (dense x compressed), batch-contiguous:
+ *     dX[k][b] = sum_{p : col_idx[p] = k} vals[p] * dY[row(p)][b]
+ * for 0 <= k < n_cols.  With a CSC copy (col_ptr, row_idx, perm from
+ * csc_build, all non-NULL) the sum is a deterministic gather.  With all three
+ * NULL the call scatters with float atomics instead (summation order, and so
+ * the low bits, vary from run to run); dX is zeroed first by the call.
+ * dY is [n_rows][ldy], dX is [n_cols][ldx].
+ */
+int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                   const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                   const int32_t *col_ptr, const int32_t *row_idx, const int32_t *perm,
+                   const float *dY, int64_t ldy, int32_t B,
+                   float *dX, int64_t ldx, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Dense weight gradient of the l1 phase (the minibatch gradient that enters
+ * the proximal step, Eq. (prox)):
+ *     dW[i][k] = sum_{b < B} dY[i][b] * X[k][b]      (dW = dY . X^T)
+ * dY [N][ldy], X [K][ldx], dW [N][ldw], ldw >= K.  No 1/B factor: dY carries
+ * the loss scaling.  fp32 inputs and fp32 matrix-core accumulation.
+ */
+int dense_wgrad(int32_t N, int32_t K, int32_t B,
+                const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                float *dW, int64_t ldw, hipStream_t stream);
+
+/*
+ * Weight gradient of the debiasing phase (Section 2.4: retrain without the
+ * regulariser with the zero weights excluded), i.e. the dense gradient sampled
+ * on W's pattern:
+ *     gv[p] = sum_{b < B} dY[row(p)][b] * X[col_idx[p]][b],  0 <= p < nnz.
+ * gv has nnz entries (host nnz = row_ptr[n_rows]).  ws must hold
+ * l1csr_workspace_bytes(L1CSR_OP_SDDMM, n_rows, n_cols, nnz, B) bytes.
+ */
+int sddmm_masked_wgrad(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                       const int32_t *row_ptr, const int32_t *col_idx,
+                       const float *dY, int64_t ldy, const float *X, int64_t ldx, int32_t B,
+                       float *gv, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Minibatch proximal gradient step, Eq. (prox), with the soft-threshold
+ * closed form of Section 2.2 and the elementwise kernel of Fig. 4:
+ *     S_t(z) = sgn(z) * max(|z| - t, 0),   t = eta * lambda,
+ *     z = w - eta * g.
+ * The arithmetic is done in double (the precision of the paper's kernels):
+ * eta*g and eta*lambda are exact in double, z rounds once, S_t(z) rounds once
+ * more to float.  Zero results are +0.0.
+ *
+ * mode L1CSR_PROX_DENSE: g = G[i][k] ([n_rows][ldg], ldg >= n_cols), w = the
+ *   CSR value at (i, k) or 0 where W has no entry (all N*K weights take part,
+ *   so zero weights can become nonzero).  Writes Z[i][k] ([n_rows][ldz]; Z may
+ *   be the same buffer as G with ldz == ldg) and, if row_counts is not NULL,
+ *   row_counts[i] = number of nonzero Z[i][.].  vals is read only.
+ * mode L1CSR_PROX_CSR: g = G[p] (one gradient per stored entry, as produced by
+ *   sddmm_masked_wgrad), vals[p] <- S_t(vals[p] - eta*G[p]) in place for
+ *   0 <= p < nnz; the pattern is unchanged (entries that become 0 stay stored;
+ *   csr_compact drops them).  lambda = 0 is plain SGD (debiasing).  Z,
+ *   row_counts, ldg, ldz are ignored.
+ */
+int prox_l1_step(int mode, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                 const int32_t *row_ptr, const int32_t *col_idx, float *vals,
+                 const float *G, int64_t ldg, float eta, float lambda,
+                 float *Z, int64_t ldz, int32_t *row_counts, hipStream_t stream);
+
+/*
+ * Dense -> CSR (Section 3.1: store only the nonzero weights).  Keeps the
+ * entries with |Z[i][k]| > t in row-major order (t = 0 after prox_l1_step) and
+ * writes the canonical CSR: row_ptr_out[n_rows+1], col_idx_out[nnz'],
+ * vals_out[nnz'].  row_counts (nullable) are the per-row counts prox_l1_step
+ * produced for the same Z and t = 0; when NULL they are recomputed.
+ * d_nnz_out (nullable, device) receives nnz'.
+ *   capacity >= n_rows*n_cols: never overflows and never waits (hot path).
+ *   capacity <  n_rows*n_cols: the call counts first, waits for the stream,
+ *     and returns L1CSR_ECAPACITY with *h_nnz_required (host, nullable) = nnz'
+ *     if nnz' > capacity (row_ptr_out is then valid, col/vals untouched);
+ *     otherwise it fills and sets *h_nnz_required = nnz'.
+ * ws must hold l1csr_workspace_bytes(L1CSR_OP_RECOMPRESS, n_rows, n_cols, 0, 0).
+ */
+int csr_recompress(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz, float t,
+                   const int32_t *row_counts,
+                   int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                   int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                   void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * CSR -> CSR without its stored zeros (after a support-restricted prox step in
+ * CSR mode).  Out of place: the output arrays must not overlap the input ones
+ * and hold at least nnz entries.  d_nnz_out (nullable, device) receives the new
+ * count.  ws as l1csr_workspace_bytes(L1CSR_OP_COMPACT, n_rows, 0, nnz, 0).
+ */
+int csr_compact(int32_t n_rows, int64_t nnz,
+                const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                int32_t *d_nnz_out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Layer glue of the fully connected ReLU networks the method trains (their
+ * He initialisation, Section 4, targets ReLU units).  n elements, any layout.
+ *   relu_fwd: y = x > 0 ? x : +0
+ *   relu_bwd: dx = x > 0 ? dy : +0      (x is the pre-activation)
+ */
+int l1csr_relu_fwd(int64_t n, const float *x, float *y, hipStream_t stream);
+int l1csr_relu_bwd(int64_t n, const float *x, const float *dy, float *dx, hipStream_t stream);
+
+/*
+ * Mean softmax cross-entropy over the batch for logits[C][ld] (class-major,
+ * batch contiguous) and labels[B] in [0, C) (device int32):
+ *   loss = (1/B) sum_b ( log sum_c exp(z_cb) - z_{label_b, b} )   -> *loss (device)
+ *   dlogits[c][b] = (softmax(z_.b)_c - [c == label_b]) / B        ([C][ld])
+ * A label outside [0, C) is a precondition violation (its column is zeroed).
+ * ws as l1csr_workspace_bytes(L1CSR_OP_SOFTMAX_XENT, C, 0, 0, B).
+ */
+int l1csr_softmax_xent(int32_t C, int32_t B, const float *logits, int64_t ld,
+                       const int32_t *labels, float *dlogits, float *loss,
+                       void *ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* L1CSR_H */

@@ -1,0 +1,413 @@
+"""l1csr: the training hot path of l1-regularised compressed learning on MI355X.
+
+A thin ctypes binding over ``libl1csr.so`` (built by
+``python -m paper_1905_07931_amd.build``).  The functions keep the names of
+the C ABI in ``include/l1csr.h``; they only check and marshal arguments
+(torch tensors on the GPU -> device pointers, torch's current HIP stream) and
+raise :class:`L1CSRError` on a non-zero status.  Every computation runs in the
+library's HIP kernels; there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+__all__ = [
+    "CSR", "CSC", "L1CSRError", "lib", "status_str", "workspace_bytes",
+    "csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
+    "prox_l1_step", "csr_recompress", "csr_compact", "relu_fwd", "relu_bwd", "softmax_xent",
+    "PROX_DENSE", "PROX_CSR",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
+
+OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED = 0, -1, -2, -4, -5
+PROX_DENSE, PROX_CSR = 0, 1
+OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
+
+
+class L1CSRError(RuntimeError):
+    def __init__(self, name, status):
+        self.status = status
+        super().__init__(f"{name} failed: {status_str(status)} ({status})")
+
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_1905_07931_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        i32, i64, f32, vp, sz = C.c_int32, C.c_int64, C.c_float, C.c_void_p, C.c_size_t
+        L.l1csr_status_str.argtypes = [C.c_int]
+        L.l1csr_status_str.restype = C.c_char_p
+        L.l1csr_workspace_bytes.argtypes = [C.c_int, i32, i32, i64, i32]
+        L.l1csr_workspace_bytes.restype = sz
+        L.csr_spmm_fwd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
+        L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
+                                     vp, sz, vp]
+        L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
+        L.sddmm_masked_wgrad.argtypes = [i32, i32, i64, vp, vp, vp, i64, vp, i64, i32, vp, vp, sz, vp]
+        L.prox_l1_step.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, i64,
+                                   vp, vp]
+        L.csr_recompress.argtypes = [i32, i32, vp, i64, f32, vp, vp, vp, vp, i64, vp,
+                                     C.POINTER(C.c_int64), vp, sz, vp]
+        L.csr_compact.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
+        L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
+        L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
+        for name in ("csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad",
+                     "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "csr_compact",
+                     "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
+            getattr(L, name).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return lib().l1csr_status_str(int(status)).decode()
+
+
+def workspace_bytes(op: int, n_rows: int, n_cols: int, nnz: int, B: int) -> int:
+    return int(lib().l1csr_workspace_bytes(op, n_rows, n_cols, nnz, B))
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _check(rc, name):
+    if rc != OK:
+        raise L1CSRError(name, rc)
+
+
+def _p(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dev(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    return t
+
+
+def _vec(t, dtype, name):
+    _dev(t, dtype, name)
+    if t.dim() != 1 or (t.numel() > 1 and t.stride(0) != 1):
+        raise ValueError(f"{name} must be a contiguous 1-D tensor")
+    return t
+
+
+def _mat(t, name):
+    """A [rows][ld] float32 matrix with unit column stride; returns (rows, cols, ld)."""
+    torch = _torch()
+    _dev(t, torch.float32, name)
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    rows, cols = t.shape
+    if cols > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name} must have a contiguous last dimension")
+    ld = t.stride(0) if rows > 1 else max(cols, 1)
+    return rows, cols, ld
+
+
+_ws_cache: dict = {}
+
+
+def _workspace(nbytes, device):
+    if nbytes == 0:
+        return None, 0
+    torch = _torch()
+    key = (device.index, torch.cuda.current_stream(device).cuda_stream)
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    return buf, nbytes
+
+
+@dataclass
+class CSR:
+    """An N x K CSR matrix in device memory (int32 indices, float32 values).
+
+    ``nnz`` is the host-side count when known; after :func:`csr_recompress`
+    without a host wait it is ``None`` and ``row_ptr[-1]`` holds it on device.
+    ``col_idx``/``vals`` may be longer than nnz (capacity).
+    """
+    n_rows: int
+    n_cols: int
+    row_ptr: "object"
+    col_idx: "object"
+    vals: "object"
+    nnz: int | None = None
+
+    def host_nnz(self) -> int:
+        if self.nnz is None:
+            self.nnz = int(self.row_ptr[-1].item())
+        return self.nnz
+
+    def validate_shapes(self):
+        torch = _torch()
+        _vec(self.row_ptr, torch.int32, "row_ptr")
+        _vec(self.col_idx, torch.int32, "col_idx")
+        _vec(self.vals, torch.float32, "vals")
+        if self.row_ptr.numel() != self.n_rows + 1:
+            raise ValueError("row_ptr must have n_rows + 1 entries")
+        nnz = self.nnz if self.nnz is not None else self.col_idx.numel()
+        if self.col_idx.numel() < nnz or self.vals.numel() < nnz:
+            raise ValueError("col_idx/vals shorter than nnz")
+        return nnz
+
+    @staticmethod
+    def from_host(row_ptr, col_idx, vals, n_cols, device="cuda", capacity=None):
+        torch = _torch()
+        import numpy as np
+        rp = torch.as_tensor(np.ascontiguousarray(row_ptr, dtype=np.int32), device=device)
+        nnz = int(rp[-1].item()) if rp.numel() else 0
+        cap = max(nnz if capacity is None else capacity, 1)
+        ci = torch.zeros(cap, dtype=torch.int32, device=device)
+        v = torch.zeros(cap, dtype=torch.float32, device=device)
+        if nnz:
+            ci[:nnz] = torch.as_tensor(np.ascontiguousarray(col_idx[:nnz], dtype=np.int32), device=device)
+            v[:nnz] = torch.as_tensor(np.ascontiguousarray(vals[:nnz], dtype=np.float32), device=device)
+        return CSR(rp.numel() - 1, n_cols, rp, ci, v, nnz)
+
+    def to_host(self):
+        nnz = self.host_nnz()
+        return (self.row_ptr.cpu().numpy(), self.col_idx[:nnz].cpu().numpy(),
+                self.vals[:nnz].cpu().numpy())
+
+
+@dataclass
+class CSC:
+    """Column-major structure of a CSR matrix: col_ptr, row_idx, perm (CSR positions)."""
+    col_ptr: "object"
+    row_idx: "object"
+    perm: "object"
+
+
+# ---------------------------------------------------------------------------
+# the ABI, one function per entry point
+# ---------------------------------------------------------------------------
+
+def csr_spmm_fwd(W: CSR, X, Y=None, stream=None):
+    """Y = W . X  (X [K][B], Y [N][B], batch contiguous)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    K, B, ldx = _mat(X, "X")
+    if K != W.n_cols:
+        raise ValueError(f"X has {K} rows, W has {W.n_cols} columns")
+    if Y is None:
+        Y = torch.empty((W.n_rows, B), dtype=torch.float32, device=X.device)
+    N, By, ldy = _mat(Y, "Y")
+    if N != W.n_rows or By != B:
+        raise ValueError("Y must be [n_rows][B]")
+    _check(lib().csr_spmm_fwd(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
+                              _p(X), ldx, B, _p(Y), ldy, None, 0, _stream(stream)), "csr_spmm_fwd")
+    return Y
+
+
+def csc_build(W: CSR, out: CSC | None = None, stream=None) -> CSC:
+    """Deterministic CSC copy of W's structure (col_ptr, row_idx, perm)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    dev = W.row_ptr.device
+    if out is None:
+        cap = max(W.col_idx.numel(), 1)
+        out = CSC(torch.empty(W.n_cols + 1, dtype=torch.int32, device=dev),
+                  torch.empty(cap, dtype=torch.int32, device=dev),
+                  torch.empty(cap, dtype=torch.int32, device=dev))
+    if nnz is None or W.nnz is None:
+        nnz = W.col_idx.numel()  # capacity bound; the kernels read row_ptr
+    ws, wsb = _workspace(workspace_bytes(OP_CSC_BUILD, W.n_rows, W.n_cols, nnz, 0), dev)
+    _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(out.col_ptr),
+                           _p(out.row_idx), _p(out.perm), _p(ws), wsb, _stream(stream)), "csc_build")
+    return out
+
+
+def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
+    """dX = W^T . dY through the CSC copy (deterministic) or, with csc=None, float atomics."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    N, B, ldy = _mat(dY, "dY")
+    if N != W.n_rows:
+        raise ValueError("dY must be [n_rows][B]")
+    if dX is None:
+        dX = torch.empty((W.n_cols, B), dtype=torch.float32, device=dY.device)
+    K, Bx, ldx = _mat(dX, "dX")
+    if K != W.n_cols or Bx != B:
+        raise ValueError("dX must be [n_cols][B]")
+    cp = ri = pm = None
+    if csc is not None:
+        cp, ri, pm = csc.col_ptr, csc.row_idx, csc.perm
+    _check(lib().csr_spmm_bwd_t(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
+                                _p(cp), _p(ri), _p(pm), _p(dY), ldy, B, _p(dX), ldx, None, 0,
+                                _stream(stream)), "csr_spmm_bwd_t")
+    return dX
+
+
+def dense_wgrad(dY, X, dW=None, stream=None):
+    """dW = dY . X^T on the fp32 matrix cores."""
+    torch = _torch()
+    N, B, ldy = _mat(dY, "dY")
+    K, Bx, ldx = _mat(X, "X")
+    if Bx != B:
+        raise ValueError("dY and X must share the batch dimension")
+    if dW is None:
+        dW = torch.empty((N, K), dtype=torch.float32, device=dY.device)
+    Nw, Kw, ldw = _mat(dW, "dW")
+    if (Nw, Kw) != (N, K):
+        raise ValueError("dW must be [N][K]")
+    _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, _stream(stream)),
+           "dense_wgrad")
+    return dW
+
+
+def sddmm_masked_wgrad(W: CSR, dY, X, gv=None, stream=None):
+    """gv[p] = (dY . X^T)[row(p), col(p)] on W's pattern."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    N, B, ldy = _mat(dY, "dY")
+    K, Bx, ldx = _mat(X, "X")
+    if N != W.n_rows or K != W.n_cols or Bx != B:
+        raise ValueError("shape mismatch")
+    if gv is None:
+        gv = torch.empty(max(nnz, 1), dtype=torch.float32, device=dY.device)
+    ws, wsb = _workspace(workspace_bytes(OP_SDDMM, W.n_rows, W.n_cols, nnz, B), dY.device)
+    _check(lib().sddmm_masked_wgrad(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(dY),
+                                    ldy, _p(X), ldx, B, _p(gv), _p(ws), wsb, _stream(stream)),
+           "sddmm_masked_wgrad")
+    return gv
+
+
+def prox_l1_step(mode, W: CSR, G, eta, lam, Z=None, row_counts=None, stream=None):
+    """Eq. (prox).  Dense mode returns Z (may be G itself); CSR mode updates W.vals in place."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    if mode == PROX_CSR:
+        _vec(G, torch.float32, "G")
+        if G.numel() < nnz:
+            raise ValueError("G must hold one gradient per stored entry")
+        _check(lib().prox_l1_step(PROX_CSR, W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx),
+                                  _p(W.vals), _p(G), 0, float(eta), float(lam), None, 0, None,
+                                  _stream(stream)), "prox_l1_step")
+        return W
+    N, K, ldg = _mat(G, "G")
+    if (N, K) != (W.n_rows, W.n_cols):
+        raise ValueError("G must be [n_rows][n_cols]")
+    if Z is None:
+        Z = torch.empty((N, K), dtype=torch.float32, device=G.device)
+    Nz, Kz, ldz = _mat(Z, "Z")
+    if (Nz, Kz) != (N, K):
+        raise ValueError("Z must be [n_rows][n_cols]")
+    if row_counts is not None:
+        _vec(row_counts, torch.int32, "row_counts")
+    _check(lib().prox_l1_step(PROX_DENSE, W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx),
+                              _p(W.vals), _p(G), ldg, float(eta), float(lam), _p(Z), ldz,
+                              _p(row_counts), _stream(stream)), "prox_l1_step")
+    return Z
+
+
+def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = None, stream=None):
+    """Dense Z -> canonical CSR keeping |Z| > t.
+
+    With the default capacity (N*K) the call never waits and the result's
+    ``nnz`` is None (read ``row_ptr[-1]``).  With a smaller capacity it waits
+    and raises L1CSRError(ECAPACITY) if the result does not fit.
+    """
+    torch = _torch()
+    N, K, ldz = _mat(Z, "Z")
+    dev = Z.device
+    if out is None:
+        cap = N * K if capacity is None else int(capacity)
+        out = CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
+    cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
+    ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev)
+    need = C.c_int64(-1)
+    _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
+                                _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
+                                _stream(stream)), "csr_recompress")
+    out.nnz = need.value if need.value >= 0 else None
+    return out
+
+
+def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:
+    """Copy of W without its stored zeros (out of place)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    dev = W.row_ptr.device
+    if out is None:
+        cap = max(nnz, 1)
+        out = CSR(W.n_rows, W.n_cols, torch.empty(W.n_rows + 1, dtype=torch.int32, device=dev),
+                  torch.empty(cap, dtype=torch.int32, device=dev),
+                  torch.empty(cap, dtype=torch.float32, device=dev), None)
+    ws, wsb = _workspace(workspace_bytes(OP_COMPACT, W.n_rows, 0, nnz, 0), dev)
+    _check(lib().csr_compact(W.n_rows, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(out.row_ptr),
+                             _p(out.col_idx), _p(out.vals), None, _p(ws), wsb, _stream(stream)),
+           "csr_compact")
+    out.nnz = None
+    return out
+
+
+def relu_fwd(x, y=None, stream=None):
+    torch = _torch()
+    _dev(x, torch.float32, "x")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    y = torch.empty_like(x) if y is None else y
+    _check(lib().l1csr_relu_fwd(x.numel(), _p(x), _p(y), _stream(stream)), "l1csr_relu_fwd")
+    return y
+
+
+def relu_bwd(x, dy, dx=None, stream=None):
+    torch = _torch()
+    _dev(x, torch.float32, "x")
+    _dev(dy, torch.float32, "dy")
+    if not (x.is_contiguous() and dy.is_contiguous()) or x.shape != dy.shape:
+        raise ValueError("x and dy must be contiguous and of the same shape")
+    dx = torch.empty_like(x) if dx is None else dx
+    _check(lib().l1csr_relu_bwd(x.numel(), _p(x), _p(dy), _p(dx), _stream(stream)), "l1csr_relu_bwd")
+    return dx
+
+
+def softmax_xent(logits, labels, dlogits=None, loss=None, stream=None):
+    """Mean softmax cross-entropy over batch columns; returns (loss[1], dlogits)."""
+    torch = _torch()
+    Cn, B, ld = _mat(logits, "logits")
+    _vec(labels, torch.int32, "labels")
+    if dlogits is None:
+        dlogits = torch.empty_like(logits)
+    _, _, ldd = _mat(dlogits, "dlogits")
+    if ldd != ld:
+        raise ValueError("dlogits must share the leading dimension of logits")
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=logits.device)
+    ws, wsb = _workspace(workspace_bytes(OP_SOFTMAX_XENT, Cn, 0, 0, B), logits.device)
+    _check(lib().l1csr_softmax_xent(Cn, B, _p(logits), ld, _p(labels), _p(dlogits), _p(loss),
+                                    _p(ws), wsb, _stream(stream)), "l1csr_softmax_xent")
+    return loss, dlogits

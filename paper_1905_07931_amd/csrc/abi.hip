@@ -1,0 +1,248 @@
+// C ABI of the l1csr library: host-side validation, workspace sizing and
+// dispatch to the gfx950 kernels.  Every entry point validates all of its
+// arguments before launching anything and only enqueues work on the caller's
+// stream (csr_recompress with a short capacity is the one documented wait).
+#include <math.h>
+
+#include "../../include/l1csr.h"
+#include "common.hpp"
+#include "launch.hpp"
+
+using namespace l1csr;
+
+namespace {
+
+constexpr int64_t kMaxGridY = 65535;
+
+int hip_status(hipError_t e) { return e == hipSuccess ? L1CSR_OK : L1CSR_EHIP; }
+
+bool finite_f(float x) { return isfinite(x) != 0; }
+
+size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// a [rows][ld] matrix with rows > 0 and cols > 0 needs a pointer and ld >= cols
+bool bad_dense(const void *p, int64_t rows, int64_t cols, int64_t ld) {
+    if (ld < cols || ld < 0) return true;
+    if (rows > 0 && cols > 0 && p == nullptr) return true;
+    return false;
+}
+
+bool bad_csr(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+             const int32_t *col_idx, const void *vals, bool need_vals) {
+    if (n_rows < 0 || n_cols < 0 || nnz < 0) return true;
+    if (nnz > (int64_t)n_rows * (int64_t)n_cols) return true;
+    if (nnz > INT32_MAX) return true;
+    if (n_rows > 0 && row_ptr == nullptr) return true;
+    if (nnz > 0 && (col_idx == nullptr || (need_vals && vals == nullptr))) return true;
+    return false;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *l1csr_status_str(int status) {
+    switch (status) {
+        case L1CSR_OK: return "ok";
+        case L1CSR_EINVAL: return "invalid argument";
+        case L1CSR_ECAPACITY: return "output capacity too small";
+        case L1CSR_EHIP: return "HIP runtime or launch error";
+        case L1CSR_EUNSUPPORTED: return "unsupported size or combination";
+        default: return "unknown status";
+    }
+}
+
+size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz, int32_t B) {
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return 0;
+    switch (op) {
+        case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols));
+        case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
+        case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(nnz, B));
+        case L1CSR_OP_SPMM: return 0;
+        case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
+        case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
+        default: return 0;
+    }
+}
+
+int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                 const int32_t *col_idx, const float *vals, const float *X, int64_t ldx, int32_t B,
+                 float *Y, int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true) || B < 0) return L1CSR_EINVAL;
+    if (bad_dense(X, n_cols, B, ldx) || bad_dense(Y, n_rows, B, ldy)) return L1CSR_EINVAL;
+    if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    return hip_status(launch_spmm_rows(n_rows, nnz, row_ptr, col_idx, vals, nullptr, X, ldx, B, Y,
+                                       ldy, stream));
+}
+
+int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+              const int32_t *col_idx, int32_t *col_ptr, int32_t *row_idx, int32_t *perm, void *ws,
+              size_t ws_bytes, hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, nullptr, false)) return L1CSR_EINVAL;
+    if (col_ptr == nullptr) return L1CSR_EINVAL;
+    if (nnz > 0 && (row_idx == nullptr || perm == nullptr)) return L1CSR_EINVAL;
+    if (n_rows > 0 && n_cols > 0 &&
+        (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols)))
+        return L1CSR_EINVAL;
+    if (ceil_div(n_cols, 16384) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    return hip_status(launch_csc_build(n_rows, n_cols, row_ptr, col_idx, col_ptr, row_idx, perm, ws,
+                                       stream));
+}
+
+int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                   const int32_t *col_idx, const float *vals, const int32_t *col_ptr,
+                   const int32_t *row_idx, const int32_t *perm, const float *dY, int64_t ldy,
+                   int32_t B, float *dX, int64_t ldx, void *ws, size_t ws_bytes,
+                   hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    // CSC path: col_ptr given (row_idx and perm too unless nnz == 0); atomic path: all NULL
+    const bool use_csc = col_ptr != nullptr;
+    if (!use_csc && (row_idx != nullptr || perm != nullptr)) return L1CSR_EINVAL;
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return L1CSR_EINVAL;
+    if (use_csc) {
+        if (nnz > 0 && (row_idx == nullptr || perm == nullptr || vals == nullptr)) return L1CSR_EINVAL;
+    } else if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) {
+        return L1CSR_EINVAL;
+    }
+    if (nnz > (int64_t)n_rows * (int64_t)n_cols) return L1CSR_EINVAL;
+    if (bad_dense(dY, n_rows, B, ldy) || bad_dense(dX, n_cols, B, ldx)) return L1CSR_EINVAL;
+    if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    if (use_csc)
+        return hip_status(launch_spmm_rows(n_cols, nnz, col_ptr, row_idx, vals, perm, dY, ldy, B, dX,
+                                           ldx, stream));
+    return hip_status(launch_spmm_scatter_atomic(n_rows, n_cols, row_ptr, col_idx, vals, dY, ldy, B,
+                                                 dX, ldx, stream));
+}
+
+int dense_wgrad(int32_t N, int32_t K, int32_t B, const float *dY, int64_t ldy, const float *X,
+                int64_t ldx, float *dW, int64_t ldw, hipStream_t stream) {
+    if (N < 0 || K < 0 || B < 0) return L1CSR_EINVAL;
+    if (bad_dense(dY, N, B, ldy) || bad_dense(X, K, B, ldx) || bad_dense(dW, N, K, ldw))
+        return L1CSR_EINVAL;
+    if (ceil_div(N, 128) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    return hip_status(launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
+}
+
+int sddmm_masked_wgrad(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                       const int32_t *col_idx, const float *dY, int64_t ldy, const float *X,
+                       int64_t ldx, int32_t B, float *gv, void *ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, nullptr, false) || B < 0)
+        return L1CSR_EINVAL;
+    if (nnz > 0 && gv == nullptr) return L1CSR_EINVAL;
+    if (bad_dense(dY, n_rows, B, ldy) || bad_dense(X, n_cols, B, ldx)) return L1CSR_EINVAL;
+    const size_t need = sddmm_workspace_bytes(nnz, B);
+    if (need > 0 && (ws == nullptr || ws_bytes < need)) return L1CSR_EINVAL;
+    if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    return hip_status(
+        launch_sddmm(n_rows, nnz, row_ptr, col_idx, dY, ldy, X, ldx, B, gv, ws, stream));
+}
+
+int prox_l1_step(int mode, int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                 const int32_t *col_idx, float *vals, const float *G, int64_t ldg, float eta,
+                 float lambda, float *Z, int64_t ldz, int32_t *row_counts, hipStream_t stream) {
+    if (!finite_f(eta) || !finite_f(lambda) || eta <= 0.f || lambda < 0.f) return L1CSR_EINVAL;
+    const double t = (double)eta * (double)lambda;  // exact in double
+    if (mode == L1CSR_PROX_CSR) {
+        if (nnz < 0 || (nnz > 0 && (vals == nullptr || G == nullptr))) return L1CSR_EINVAL;
+        return hip_status(launch_prox_csr(nnz, vals, G, eta, t, stream));
+    }
+    if (mode != L1CSR_PROX_DENSE) return L1CSR_EINVAL;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(G, n_rows, n_cols, ldg) || bad_dense(Z, n_rows, n_cols, ldz)) return L1CSR_EINVAL;
+    if (n_rows > 0 && n_cols > 0 && Z != G) {
+        // distinct buffers must not overlap; the same buffer needs the same ld
+        const char *g0 = reinterpret_cast<const char *>(G);
+        const char *g1 = g0 + sizeof(float) * ((n_rows - 1) * ldg + n_cols);
+        const char *z0 = reinterpret_cast<const char *>(Z);
+        const char *z1 = z0 + sizeof(float) * ((n_rows - 1) * ldz + n_cols);
+        if (z0 < g1 && g0 < z1) return L1CSR_EINVAL;
+    }
+    if (Z == G && ldz != ldg) return L1CSR_EINVAL;
+    return hip_status(launch_prox_dense(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, Z, ldz,
+                                        row_counts, stream));
+}
+
+int csr_recompress(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz, float t,
+                   const int32_t *row_counts, int32_t *row_ptr_out, int32_t *col_idx_out,
+                   float *vals_out, int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                   void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n_rows < 0 || n_cols < 0 || capacity < 0 || !finite_f(t)) return L1CSR_EINVAL;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
+    if (bad_dense(Z, n_rows, n_cols, ldz) || row_ptr_out == nullptr) return L1CSR_EINVAL;
+    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    int *counts = const_cast<int *>(row_counts);
+    if (counts == nullptr && n_rows > 0) {
+        if (ws == nullptr || ws_bytes < sizeof(int) * (size_t)n_rows) return L1CSR_EINVAL;
+        counts = static_cast<int *>(ws);
+    }
+    hipError_t e = hipSuccess;
+    if (row_counts == nullptr) e = launch_count_rows(n_rows, n_cols, Z, ldz, t, counts, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    e = launch_exclusive_scan(counts, row_ptr_out, n_rows, d_nnz_out, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    if (capacity < total) {
+        int32_t h = 0;
+        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        if (h_nnz_required) *h_nnz_required = h;
+        if (h > capacity) return L1CSR_ECAPACITY;
+    } else if (h_nnz_required) {
+        *h_nnz_required = -1;  // unknown on the host (no wait)
+    }
+    return hip_status(launch_recompress_fill(n_rows, n_cols, Z, ldz, t, row_ptr_out, col_idx_out,
+                                             vals_out, capacity, stream));
+}
+
+int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,
+                const float *vals, int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                int32_t *d_nnz_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n_rows < 0 || nnz < 0 || nnz > INT32_MAX) return L1CSR_EINVAL;
+    if (n_rows > 0 && (row_ptr == nullptr || row_ptr_out == nullptr)) return L1CSR_EINVAL;
+    if (nnz > 0 && (col_idx == nullptr || vals == nullptr || col_idx_out == nullptr ||
+                    vals_out == nullptr))
+        return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < sizeof(int) * (size_t)n_rows)) return L1CSR_EINVAL;
+    if (n_rows == 0) {
+        if (row_ptr_out == nullptr) return L1CSR_EINVAL;
+        hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
+        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
+        return hip_status(e);
+    }
+    int *counts = static_cast<int *>(ws);
+    hipError_t e = launch_compact_count(n_rows, row_ptr, vals, counts, stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(counts, row_ptr_out, n_rows, d_nnz_out, stream);
+    if (e == hipSuccess)
+        e = launch_compact_fill(n_rows, row_ptr, col_idx, vals, row_ptr_out, col_idx_out, vals_out,
+                                stream);
+    return hip_status(e);
+}
+
+int l1csr_relu_fwd(int64_t n, const float *x, float *y, hipStream_t stream) {
+    if (n < 0 || (n > 0 && (x == nullptr || y == nullptr))) return L1CSR_EINVAL;
+    return hip_status(launch_relu_fwd(n, x, y, stream));
+}
+
+int l1csr_relu_bwd(int64_t n, const float *x, const float *dy, float *dx, hipStream_t stream) {
+    if (n < 0 || (n > 0 && (x == nullptr || dy == nullptr || dx == nullptr))) return L1CSR_EINVAL;
+    return hip_status(launch_relu_bwd(n, x, dy, dx, stream));
+}
+
+int l1csr_softmax_xent(int32_t C, int32_t B, const float *logits, int64_t ld,
+                       const int32_t *labels, float *dlogits, float *loss, void *ws,
+                       size_t ws_bytes, hipStream_t stream) {
+    if (C <= 0 || B < 0 || loss == nullptr) return L1CSR_EINVAL;
+    if (bad_dense(logits, C, B, ld) || bad_dense(dlogits, C, B, ld)) return L1CSR_EINVAL;
+    if (B > 0 && labels == nullptr) return L1CSR_EINVAL;
+    if (B > 0 && (ws == nullptr || ws_bytes < sizeof(float) * (size_t)ceil_div(B, 256)))
+        return L1CSR_EINVAL;
+    return hip_status(
+        launch_softmax_xent(C, B, logits, ld, labels, dlogits, loss, static_cast<float *>(ws), stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,159 @@
+// Dense weight gradient dW[N][K] = dY[N][B] . X[K][B]^T on the fp32 matrix
+// cores (v_mfma_f32_32x32x2_f32).
+//
+// Both operands keep the reduction index (the batch) contiguous, the natural
+// layout for the matrix-core operand fragments.  A 256-thread workgroup owns a
+// 128x128 tile of dW as 2x2 waves of 64x64, each wave 2x2 MFMA tiles of 32x32.
+// Reduction chunks of 32 are staged through LDS (double buffered; the next
+// chunk's global loads are in flight during the current chunk's MFMAs).
+//
+// Reduction-index assignment: an MFMA step multiplies the pairs k in {0, 1}
+// held by lane halves 0 and 1.  Any bijection between the chunk's 32 batch
+// indices and (step, half) gives the same sum as long as the A and B fragments
+// use the same one; lane half h takes batch indices [16h, 16h + 16) of the
+// chunk, step s index 16h + s, so each lane reads its fragments as contiguous
+// float4s from LDS.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace l1csr {
+
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int LDS_STRIDE = BK + 4;  // 36 floats: conflict-free 16-byte fragment reads
+constexpr int kThreads = 256;
+constexpr int kLoadsPerThread = (BM * BK / 4) / kThreads;  // float4 loads per operand: 4
+
+template <bool V4>
+__device__ __forceinline__ void load_tile(const float *__restrict__ src, int64_t ld, int rows,
+                                          int kred, int row0, int k0, float4 (&r)[kLoadsPerThread]) {
+#pragma unroll
+    for (int i = 0; i < kLoadsPerThread; ++i) {
+        const int f = threadIdx.x + i * kThreads;  // float4 index inside the tile
+        const int rr = f >> 3;                      // 8 float4 per tile row
+        const int kk = (f & 7) * 4;
+        const int grow = row0 + rr;
+        const int gk = k0 + kk;
+        if (V4 && grow < rows && gk + 3 < kred) {
+            r[i] = *reinterpret_cast<const float4 *>(src + (int64_t)grow * ld + gk);
+        } else {
+            const float *p = src + (int64_t)grow * ld + gk;
+            const bool rv = grow < rows;
+            r[i].x = (rv && gk + 0 < kred) ? p[0] : 0.f;
+            r[i].y = (rv && gk + 1 < kred) ? p[1] : 0.f;
+            r[i].z = (rv && gk + 2 < kred) ? p[2] : 0.f;
+            r[i].w = (rv && gk + 3 < kred) ? p[3] : 0.f;
+        }
+    }
+}
+
+__device__ __forceinline__ void store_tile(float *lds, const float4 (&r)[kLoadsPerThread]) {
+#pragma unroll
+    for (int i = 0; i < kLoadsPerThread; ++i) {
+        const int f = threadIdx.x + i * kThreads;
+        const int rr = f >> 3;
+        const int kk = (f & 7) * 4;
+        *reinterpret_cast<float4 *>(lds + rr * LDS_STRIDE + kk) = r[i];
+    }
+}
+
+template <bool V4>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_f32_mfma_kernel(
+    int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
+    int64_t ldb, float *__restrict__ C, int64_t ldc) {
+    __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
+
+    const int tile_n = blockIdx.x, tile_m = blockIdx.y;
+    const int m0 = tile_m * BM, n0 = tile_n * BN;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+    const int lr = lane & 31;  // row inside a 32x32 tile (A) / column (B)
+    const int lh = lane >> 5;  // lane half: which 16 reduction indices
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    const int nchunks = (Kr + BK - 1) / BK;
+    float4 ra[kLoadsPerThread], rb[kLoadsPerThread];
+    load_tile<V4>(A, lda, M, Kr, m0, 0, ra);
+    load_tile<V4>(Bt, ldb, Nn, Kr, n0, 0, rb);
+    store_tile(As[0], ra);
+    store_tile(Bs[0], rb);
+    __syncthreads();
+
+    for (int c = 0; c < nchunks; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < nchunks) {
+            load_tile<V4>(A, lda, M, Kr, m0, (c + 1) * BK, ra);
+            load_tile<V4>(Bt, ldb, Nn, Kr, n0, (c + 1) * BK, rb);
+        }
+        const float *as0 = As[buf] + (wm + lr) * LDS_STRIDE + lh * 16;
+        const float *as1 = as0 + 32 * LDS_STRIDE;
+        const float *bs0 = Bs[buf] + (wn + lr) * LDS_STRIDE + lh * 16;
+        const float *bs1 = bs0 + 32 * LDS_STRIDE;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 a0 = *reinterpret_cast<const float4 *>(as0 + 4 * q);
+            const float4 a1 = *reinterpret_cast<const float4 *>(as1 + 4 * q);
+            const float4 b0 = *reinterpret_cast<const float4 *>(bs0 + 4 * q);
+            const float4 b1 = *reinterpret_cast<const float4 *>(bs1 + 4 * q);
+            const float av0[4] = {a0.x, a0.y, a0.z, a0.w};
+            const float av1[4] = {a1.x, a1.y, a1.z, a1.w};
+            const float bv0[4] = {b0.x, b0.y, b0.z, b0.w};
+            const float bv1[4] = {b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av0[s], bv0[s], acc[0][0], 0, 0, 0);
+                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av0[s], bv1[s], acc[0][1], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av1[s], bv0[s], acc[1][0], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av1[s], bv1[s], acc[1][1], 0, 0, 0);
+            }
+        }
+        if (c + 1 < nchunks) {
+            store_tile(As[buf ^ 1], ra);
+            store_tile(Bs[buf ^ 1], rb);
+        }
+        __syncthreads();
+    }
+
+    // D layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
+    // row 8*(r/4) + 4*(l/32) + r%4, column l%32 of the 32x32 tile.
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int col = n0 + wn + b * 32 + lr;
+            if (col >= Nn) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                if (row < M) C[(int64_t)row * ldc + col] = acc[a][b][r];
+            }
+        }
+}
+
+}  // namespace
+
+hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                            int64_t ldx, float *dW, int64_t ldw, hipStream_t s) {
+    if (N == 0 || K == 0) return hipSuccess;
+    dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
+    const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
+    if (v4)
+        wgrad_f32_mfma_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
+    else
+        wgrad_f32_mfma_kernel<false><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
+    return hipGetLastError();
+}
+
+}  // namespace l1csr

@@ -1,0 +1,68 @@
+// Internal launchers: one per kernel family, called by the C ABI after the
+// arguments have been validated on the host.  Each returns hipSuccess or the
+// launch error.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace l1csr {
+
+// spmm.hip -----------------------------------------------------------------
+hipError_t launch_spmm_rows(int n_rows, int64_t nnz, const int *ptr, const int *idx,
+                            const float *vals, const int *perm, const float *X, int64_t ldx,
+                            int B, float *Y, int64_t ldy, hipStream_t s);
+hipError_t launch_spmm_scatter_atomic(int n_rows, int n_cols, const int *ptr, const int *idx,
+                                      const float *vals, const float *dY, int64_t ldy, int B,
+                                      float *dX, int64_t ldx, hipStream_t s);
+
+// csc.hip ------------------------------------------------------------------
+size_t csc_workspace_bytes(int n_rows, int n_cols);
+hipError_t launch_csc_build(int n_rows, int n_cols, const int *ptr, const int *idx,
+                            int *col_ptr, int *row_idx, int *perm, void *ws, hipStream_t s);
+
+// scan.hip -----------------------------------------------------------------
+// out[0] = 0, out[j+1] = in[0] + ... + in[j] for j < n (out has n+1 entries);
+// optionally also writes the total to *total_out.
+hipError_t launch_exclusive_scan(const int *in, int *out, int n, int *total_out, hipStream_t s);
+hipError_t launch_fill_i32(int *p, int64_t n, int v, hipStream_t s);
+hipError_t launch_fill_f32(float *p, int64_t n, float v, hipStream_t s);
+hipError_t launch_fill_rows_f32(float *p, int64_t rows, int64_t cols, int64_t ld, float v,
+                                hipStream_t s);
+
+// gemm.hip -----------------------------------------------------------------
+hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                            int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
+
+// sddmm.hip ----------------------------------------------------------------
+size_t sddmm_workspace_bytes(int64_t nnz, int B);
+hipError_t launch_sddmm(int n_rows, int64_t nnz, const int *ptr, const int *idx, const float *dY,
+                        int64_t ldy, const float *X, int64_t ldx, int B, float *gv, void *ws,
+                        hipStream_t s);
+
+// prox.hip -----------------------------------------------------------------
+hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *idx,
+                             const float *vals, const float *G, int64_t ldg, float eta, double t,
+                             float *Z, int64_t ldz, int *row_counts, hipStream_t s);
+hipError_t launch_prox_csr(int64_t nnz, float *vals, const float *g, float eta, double t,
+                           hipStream_t s);
+
+// recompress.hip -----------------------------------------------------------
+hipError_t launch_count_rows(int n_rows, int n_cols, const float *Z, int64_t ldz, float t,
+                             int *counts, hipStream_t s);
+hipError_t launch_recompress_fill(int n_rows, int n_cols, const float *Z, int64_t ldz, float t,
+                                  const int *row_ptr, int *col_idx, float *vals, int64_t capacity,
+                                  hipStream_t s);
+hipError_t launch_compact_count(int n_rows, const int *ptr, const float *vals, int *counts,
+                                hipStream_t s);
+hipError_t launch_compact_fill(int n_rows, const int *ptr, const int *idx, const float *vals,
+                               const int *ptr_out, int *idx_out, float *vals_out, hipStream_t s);
+
+// glue.hip -----------------------------------------------------------------
+hipError_t launch_relu_fwd(int64_t n, const float *x, float *y, hipStream_t s);
+hipError_t launch_relu_bwd(int64_t n, const float *x, const float *dy, float *dx, hipStream_t s);
+hipError_t launch_softmax_xent(int C, int B, const float *z, int64_t ld, const int *labels,
+                               float *dz, float *loss, float *ws, hipStream_t s);
+
+}  // namespace l1csr

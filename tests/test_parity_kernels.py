@@ -1,0 +1,302 @@
+"""Each ABI call on the GPU against the CPU oracle, on the same seeded inputs.
+
+Bar: bit-exact for structure (row pointers, column indices, CSC, masks, prox
+outputs, recompression) and for any sum on the dyadic grid; within 1e-4 of
+the order-independent scale m = sum |a_k b_k| for fp32 sums of real data.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1905_07931_amd as L1
+from paper_1905_07931_amd import synth
+
+from _helpers import TOL, assert_scaled_close, bits_equal, csc_reference, cuda, h, t
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # (N, K, B, nnz, seed)
+    (1, 1, 1, 1, 0), (7, 5, 3, 12, 1), (64, 65, 63, 700, 2), (65, 64, 64, 2000, 3),
+    (33, 90, 17, 0, 4), (300, 784, 64, 23520, 0), (130, 257, 65, 9000, 5), (40, 300, 256, 5000, 6),
+    (16, 20, 1, 120, 7), (3, 4100, 129, 6000, 8),
+]
+
+
+def _ids(s):
+    return "N{}K{}B{}nnz{}".format(*s[:4])
+
+
+def _layer(shape):
+    N, K, B, nnz, seed = shape
+    return synth.fc_layer(N, K, B, nnz, seed=seed)
+
+
+def _W(L):
+    return L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+
+
+def _absL(L):
+    return np.abs(L.vals), np.abs(L.X), np.abs(L.dY)
+
+
+# ----------------------------------------------------------------------------
+# forward product
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+def test_spmm_fwd(shape):
+    L = _layer(shape)
+    Y = h(L1.csr_spmm_fwd(_W(L), t(L.X)))
+    ref = oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)
+    av, ax, _ = _absL(L)
+    m = oracle.spmm_fwd(L.row_ptr, L.col_idx, av, ax)
+    assert_scaled_close(Y, ref, m, what="Y")
+
+
+def test_spmm_fwd_padded_leading_dimension():
+    L = synth.fc_layer(50, 70, 37, 900, seed=11)
+    import torch
+    Xp = torch.zeros((70, 41), dtype=torch.float32, device=cuda())
+    Xp[:, :37] = t(L.X)
+    Yp = torch.full((50, 43), 7.0, dtype=torch.float32, device=cuda())
+    L1.csr_spmm_fwd(_W(L), Xp[:, :37], Yp[:, :37])
+    ref = oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)
+    m = oracle.spmm_fwd(L.row_ptr, L.col_idx, np.abs(L.vals), L.X)
+    assert_scaled_close(h(Yp)[:, :37], ref, m, what="Y")
+    assert np.all(h(Yp)[:, 37:] == 7.0)  # padding untouched
+
+
+def test_spmm_fwd_dyadic_bit_exact():
+    L = synth.dyadic_layer(70, 300, 256, 6000, seed=3, empty_rows=(0, 5, 69), full_rows=(10,))
+    Y = h(L1.csr_spmm_fwd(_W(L), t(L.X)))
+    assert bits_equal(Y, oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X))
+
+
+# ----------------------------------------------------------------------------
+# CSC copy and backward product
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+def test_csc_build_bit_exact(shape):
+    L = _layer(shape)
+    csc = L1.csc_build(_W(L))
+    cp, ri, pm = csc_reference(L.row_ptr, L.col_idx, L.K)
+    assert bits_equal(h(csc.col_ptr), cp)
+    assert bits_equal(h(csc.row_idx)[: L.nnz], ri)
+    assert bits_equal(h(csc.perm)[: L.nnz], pm)
+
+
+def test_csc_build_wide_matrix_column_tiles():
+    # more than one LDS tile of columns and a ragged row chunk
+    L = synth.fc_layer(45, 40000, 1, 30000, seed=12)
+    csc = L1.csc_build(_W(L))
+    cp, ri, pm = csc_reference(L.row_ptr, L.col_idx, L.K)
+    assert bits_equal(h(csc.col_ptr), cp)
+    assert bits_equal(h(csc.row_idx)[: L.nnz], ri)
+    assert bits_equal(h(csc.perm)[: L.nnz], pm)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("path", ["csc", "atomic"])
+def test_spmm_bwd_t(shape, path):
+    L = _layer(shape)
+    W = _W(L)
+    csc = L1.csc_build(W) if path == "csc" else None
+    dX = h(L1.csr_spmm_bwd_t(W, t(L.dY), csc))
+    ref = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, L.vals, L.dY, L.K)
+    av, _, ady = _absL(L)
+    m = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, av, ady, L.K)
+    assert_scaled_close(dX, ref, m, what="dX")
+
+
+def test_spmm_bwd_dyadic_bit_exact_and_deterministic():
+    L = synth.dyadic_layer(90, 200, 128, 5000, seed=4, empty_rows=(1,), full_rows=(3, 4))
+    W = _W(L)
+    csc = L1.csc_build(W)
+    ref = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, L.vals, L.dY, L.K)
+    a = h(L1.csr_spmm_bwd_t(W, t(L.dY), csc))
+    assert bits_equal(a, ref)
+    assert bits_equal(h(L1.csr_spmm_bwd_t(W, t(L.dY), None)), ref)
+
+
+def test_spmm_bwd_csc_stays_valid_after_value_update():
+    # debiasing changes values only: the CSC copy reads them through perm
+    L = synth.fc_layer(60, 80, 32, 1500, seed=13)
+    W = _W(L)
+    csc = L1.csc_build(W)
+    W.vals.mul_(-0.5)
+    dX = h(L1.csr_spmm_bwd_t(W, t(L.dY), csc))
+    v2 = (L.vals * np.float32(-0.5)).astype(np.float32)
+    ref = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, v2, L.dY, L.K)
+    m = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, np.abs(v2), np.abs(L.dY), L.K)
+    assert_scaled_close(dX, ref, m, what="dX")
+
+
+# ----------------------------------------------------------------------------
+# dense weight gradient (fp32 matrix cores)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("NKB", [(1, 1, 1), (7, 5, 3), (129, 130, 33), (300, 784, 64),
+                                 (257, 1000, 100), (128, 128, 32), (64, 300, 256), (5, 9, 0)])
+def test_dense_wgrad(NKB):
+    N, K, B = NKB
+    rng = np.random.default_rng(N * 7 + K)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    X = rng.random((K, B)).astype(np.float32)
+    dW = h(L1.dense_wgrad(t(dY), t(X)))
+    ref = oracle.dense_wgrad(dY, X)
+    m = oracle.dense_wgrad(np.abs(dY), X)
+    assert_scaled_close(dW, ref, m, what="dW")
+
+
+def test_dense_wgrad_batch_one_bit_exact_and_padded():
+    rng = np.random.default_rng(1)
+    dY = rng.standard_normal((70, 1)).astype(np.float32)
+    X = rng.standard_normal((150, 1)).astype(np.float32)
+    assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), oracle.dense_wgrad(dY, X))
+    # leading dimensions not a multiple of 4 (scalar loads)
+    import torch
+    dY2 = rng.standard_normal((33, 45)).astype(np.float32)
+    X2 = rng.random((66, 45)).astype(np.float32)
+    dYp = torch.zeros((33, 47), device=cuda()); dYp[:, :45] = t(dY2)
+    Xp = torch.zeros((66, 51), device=cuda()); Xp[:, :45] = t(X2)
+    dWp = torch.full((33, 70), 3.0, device=cuda())
+    L1.dense_wgrad(dYp[:, :45], Xp[:, :45], dWp[:, :66])
+    assert_scaled_close(h(dWp)[:, :66], oracle.dense_wgrad(dY2, X2),
+                        oracle.dense_wgrad(np.abs(dY2), X2), what="dW")
+    assert np.all(h(dWp)[:, 66:] == 3.0)
+
+
+def test_dense_wgrad_dyadic_bit_exact():
+    L = synth.dyadic_layer(200, 300, 256, 10, seed=5)
+    assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
+
+
+# ----------------------------------------------------------------------------
+# masked weight gradient
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", SHAPES + [(20, 30, 5000, 300, 9), (50, 500, 2048, 2500, 10)],
+                         ids=_ids)
+def test_sddmm(shape):
+    L = _layer(shape)
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    ref = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
+    m = oracle.sddmm(L.row_ptr, L.col_idx, np.abs(L.dY), L.X)
+    assert_scaled_close(gv, ref, m, what="gv")
+
+
+def test_sddmm_dyadic_bit_exact():
+    L = synth.dyadic_layer(40, 60, 1100, 900, seed=6, empty_rows=(2,), full_rows=(7,))
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    assert bits_equal(gv, oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X))
+
+
+# ----------------------------------------------------------------------------
+# prox, recompression, compaction (bit-exact)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("eta,lam", [(0.01, 1e-4), (0.5, 0.3), (2.0 ** -7, 2.0 ** -4)])
+def test_prox_dense_and_recompress_bit_exact(shape, eta, lam):
+    L = _layer(shape)
+    rng = np.random.default_rng(shape[-1])
+    G = (rng.standard_normal((L.N, L.K)) * 0.05).astype(np.float32)
+    W = _W(L)
+    cnt = t(np.zeros(L.N, np.int32))
+    Z = L1.prox_l1_step(L1.PROX_DENSE, W, t(G), eta, lam, row_counts=cnt)
+    Zr, cr = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, G, eta, lam, L.K)
+    assert bits_equal(h(Z), Zr)
+    assert bits_equal(h(cnt), cr)
+    out = L1.csr_recompress(Z, 0.0, row_counts=cnt)
+    rp, ci, v = oracle.recompress(Zr, 0.0)
+    assert bits_equal(h(out.row_ptr), rp)
+    nnz = int(rp[-1])
+    assert bits_equal(h(out.col_idx)[:nnz], ci)
+    assert bits_equal(h(out.vals)[:nnz], v)
+
+
+def test_prox_dense_in_place_and_threshold_ties():
+    L = synth.dyadic_layer(64, 300, 64, 4000, seed=7, empty_rows=(3,), full_rows=(9,))
+    dW = oracle.dense_wgrad(L.dY, L.X)
+    G = t(dW)
+    Z = L1.prox_l1_step(L1.PROX_DENSE, _W(L), G, L.eta, L.lam, Z=G)  # Z aliases G
+    Zr, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, dW, L.eta, L.lam, L.K)
+    assert bits_equal(h(Z), Zr)
+    # the dyadic grid produces exact ties |z| == t, which must give +0
+    t_ = np.float64(np.float32(L.eta)) * np.float64(np.float32(L.lam))
+    D = oracle.densify(L.row_ptr, L.col_idx, L.vals, L.K).astype(np.float64)
+    z = D - np.float64(np.float32(L.eta)) * dW.astype(np.float64)
+    assert np.any(np.abs(z) == t_)
+
+
+def test_recompress_without_counts_threshold_and_capacity():
+    rng = np.random.default_rng(3)
+    Zh = rng.standard_normal((37, 301)).astype(np.float32)
+    Zh[rng.random(Zh.shape) < 0.7] = 0
+    Zh[4] = 0
+    Zh[5] = 1
+    Zh[6, 10] = -0.0
+    for thr in (0.0, 0.5):
+        out = L1.csr_recompress(t(Zh), thr)
+        rp, ci, v = oracle.recompress(Zh, thr)
+        nnz = int(rp[-1])
+        assert bits_equal(h(out.row_ptr), rp)
+        assert bits_equal(h(out.col_idx)[:nnz], ci) and bits_equal(h(out.vals)[:nnz], v)
+    need = int(np.count_nonzero(Zh))
+    with pytest.raises(L1.L1CSRError) as ei:
+        L1.csr_recompress(t(Zh), 0.0, capacity=need - 1)
+    assert ei.value.status == L1.ECAPACITY
+    out = L1.csr_recompress(t(Zh), 0.0, capacity=need)
+    assert out.nnz == need
+    rp, ci, v = oracle.recompress(Zh, 0.0)
+    assert bits_equal(h(out.col_idx)[:need], ci)
+
+
+def test_recompress_fig1_example():
+    A = np.array([[1, 7, 0, 0], [0, 2, 8, 0], [5, 0, 3, 9], [0, 6, 0, 4]], np.float32)
+    out = L1.csr_recompress(t(A), 0.0)
+    assert h(out.row_ptr).tolist() == [0, 2, 4, 7, 9]
+    assert h(out.col_idx)[:9].tolist() == [0, 1, 1, 2, 0, 2, 3, 1, 3]
+    assert h(out.vals)[:9].tolist() == [1, 7, 2, 8, 5, 3, 9, 6, 4]
+
+
+def test_prox_csr_and_compact_bit_exact():
+    L = synth.fc_layer(80, 120, 16, 3000, seed=14)
+    gv = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
+    for lam in (0.0, 0.05):
+        W = _W(L)
+        L1.prox_l1_step(L1.PROX_CSR, W, t(gv), 0.01, lam)
+        ref = oracle.prox_csr(L.vals, gv, 0.01, lam)
+        assert bits_equal(h(W.vals)[: L.nnz], ref)
+        assert bits_equal(h(W.row_ptr), L.row_ptr) and bits_equal(h(W.col_idx)[: L.nnz], L.col_idx)
+        if lam > 0:
+            assert np.count_nonzero(ref == 0) > 0
+            C = L1.csr_compact(W)
+            rp, ci, v = oracle.compact(L.row_ptr, L.col_idx, ref)
+            assert bits_equal(h(C.row_ptr), rp)
+            assert bits_equal(h(C.col_idx)[: rp[-1]], ci) and bits_equal(h(C.vals)[: rp[-1]], v)
+
+
+# ----------------------------------------------------------------------------
+# layer glue
+# ----------------------------------------------------------------------------
+
+def test_relu_bit_exact():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal(10007).astype(np.float32)
+    x[:3] = [0.0, -0.0, 1e-40]
+    dy = rng.standard_normal(10007).astype(np.float32)
+    assert bits_equal(h(L1.relu_fwd(t(x))), oracle.relu_fwd(x))
+    assert bits_equal(h(L1.relu_bwd(t(x), t(dy))), oracle.relu_bwd(x, dy))
+
+
+@pytest.mark.parametrize("C,B", [(10, 256), (10, 1), (3, 1000), (10, 16384)])
+def test_softmax_xent(C, B):
+    rng = np.random.default_rng(C + B)
+    z = (rng.standard_normal((C, B)) * 4).astype(np.float32)
+    lab = rng.integers(0, C, size=B).astype(np.int32)
+    loss, dz = L1.softmax_xent(t(z), t(lab))
+    lr, dzr = oracle.softmax_xent(z, lab)
+    assert abs(float(h(loss)[0]) - lr) <= 1e-5 * max(1.0, abs(lr))
+    assert np.max(np.abs(h(dz) - dzr)) <= 1e-6 / B * 10
