@@ -103,9 +103,7 @@ def main():
     dX = torch.empty((K, B), dtype=torch.float32, device=dev)
     dW = torch.empty((N, K), dtype=torch.float32, device=dev)
     cnt = torch.empty(N, dtype=torch.int32, device=dev)
-    csc = L1.CSC(torch.empty(K + 1, dtype=torch.int32, device=dev),
-                 torch.empty(nnz, dtype=torch.int32, device=dev),
-                 torch.empty(nnz, dtype=torch.int32, device=dev))
+    csc = L1.CSC.empty(K, nnz, dev)
     Wout = L1.CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
                   torch.empty(N * K, dtype=torch.int32, device=dev),
                   torch.empty(N * K, dtype=torch.float32, device=dev), None)

@@ -83,9 +83,12 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
  * in batch-contiguous layout:
  *     Y[i][b] = sum_{p = row_ptr[i]}^{row_ptr[i+1]-1} vals[p] * X[col_idx[p]][b]
  * for 0 <= i < n_rows, 0 <= b < B.  X is [n_cols][ldx], Y is [n_rows][ldy];
- * every Y[i][0..B) is written (an empty row gives zeros).  nnz is the host-side
- * number of stored entries (row_ptr[n_rows]); it sizes the launch.
- * Summation order is unspecified (fp32 accumulation).
+ * every Y[i][0..B) is written (an empty row gives zeros).  nnz is the number
+ * of stored entries (row_ptr[n_rows]) or an upper bound on it (it only picks
+ * the kernel).  ws (nullable) enables the LDS-tiled kernel and must then hold
+ * l1csr_workspace_bytes(L1CSR_OP_SPMM, n_rows, n_cols, nnz, B) bytes; without
+ * it a row-per-wave kernel runs.  Each Y entry is summed by one wave in
+ * ascending p order (fp32 fused multiply-adds), so results are reproducible.
  */
 int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
                  const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
@@ -93,34 +96,44 @@ int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
                  float *Y, int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Column-major copy of W's structure (CSC) for the backward product.  Section
- * 3.2 notes that the dense x compressed product reads W by columns and cannot
- * be coalesced unless such a column-wise copy is stored; this builds it.
- *     col_ptr[n_cols+1], row_idx[nnz], perm[nnz]
+ * Column-major copy of W (CSC) for the backward product.  Section 3.2 notes
+ * that the dense x compressed product reads W by columns and cannot be
+ * coalesced unless such a column-wise copy is stored; this builds it:
+ *     col_ptr[n_cols+1], row_idx[nnz], perm[nnz], vals_t[nnz]
  * with row_idx strictly increasing inside each column (the unique canonical
- * CSC) and perm[q] = the CSR position of CSC entry q, so that the value of CSC
- * entry q is vals[perm[q]] and a values-only update of W (debiasing) keeps the
- * copy valid.  Deterministic.  ws must hold
+ * CSC), perm[q] = the CSR position of CSC entry q and vals_t[q] = vals[perm[q]].
+ * Deterministic.  ws must hold
  * l1csr_workspace_bytes(L1CSR_OP_CSC_BUILD, n_rows, n_cols, nnz, 0) bytes.
  */
 int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz,
-              const int32_t *row_ptr, const int32_t *col_idx,
-              int32_t *col_ptr, int32_t *row_idx, int32_t *perm,
+              const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+              int32_t *col_ptr, int32_t *row_idx, int32_t *perm, float *vals_t,
               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Refresh the CSC values after an update of W's values only (debiasing keeps
+ * the pattern, Section 2.4): vals_t[q] = vals[perm[q]] for 0 <= q < nnz', where
+ * nnz' = col_ptr[n_cols] is read on the device and nnz is an upper bound on it
+ * (it sizes the launch).
+ */
+int csc_update_vals(int32_t n_cols, int64_t nnz, const int32_t *col_ptr, const int32_t *perm,
+                    const float *vals, float *vals_t, hipStream_t stream);
 
 /*
  * Backward product for the data gradient, Section 3.2 "Backward:
  * dLoss/dX_B <- dLoss/dX_T W" (dense x compressed), batch-contiguous:
  *     dX[k][b] = sum_{p : col_idx[p] = k} vals[p] * dY[row(p)][b]
- * for 0 <= k < n_cols.  With a CSC copy (col_ptr, row_idx, perm from
- * csc_build, all non-NULL) the sum is a deterministic gather.  With all three
- * NULL the call scatters with float atomics instead (summation order, and so
- * the low bits, vary from run to run); dX is zeroed first by the call.
- * dY is [n_rows][ldy], dX is [n_cols][ldx].
+ * for 0 <= k < n_cols.  With a CSC copy (col_ptr, row_idx, vals_t from
+ * csc_build, all non-NULL) this is the forward product of W^T: a gather in
+ * ascending row order, reproducible; ws (nullable) as for csr_spmm_fwd with
+ * the dimensions swapped, l1csr_workspace_bytes(L1CSR_OP_SPMM, n_cols, n_rows,
+ * nnz, B).  With all three NULL the call scatters W's CSR with float atomics
+ * instead (the summation order, and so the low bits, vary from run to run);
+ * dX is zeroed first by the call.  dY is [n_rows][ldy], dX is [n_cols][ldx].
  */
 int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz,
                    const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
-                   const int32_t *col_ptr, const int32_t *row_idx, const int32_t *perm,
+                   const int32_t *col_ptr, const int32_t *row_idx, const float *vals_t,
                    const float *dY, int64_t ldy, int32_t B,
                    float *dX, int64_t ldx, void *ws, size_t ws_bytes, hipStream_t stream);
 

@@ -15,7 +15,7 @@ from dataclasses import dataclass
 
 __all__ = [
     "CSR", "CSC", "L1CSRError", "lib", "status_str", "workspace_bytes",
-    "csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
+    "csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
     "prox_l1_step", "csr_recompress", "csr_compact", "relu_fwd", "relu_bwd", "softmax_xent",
     "PROX_DENSE", "PROX_CSR",
 ]
@@ -50,7 +50,8 @@ def lib():
         L.l1csr_workspace_bytes.argtypes = [C.c_int, i32, i32, i64, i32]
         L.l1csr_workspace_bytes.restype = sz
         L.csr_spmm_fwd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
-        L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csc_update_vals.argtypes = [i32, i64, vp, vp, vp, vp, vp]
         L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
                                      vp, sz, vp]
         L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
@@ -63,7 +64,7 @@ def lib():
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
         L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
-        for name in ("csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad",
+        for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "csr_compact",
                      "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
             getattr(L, name).restype = C.c_int
@@ -203,10 +204,21 @@ class CSR:
 
 @dataclass
 class CSC:
-    """Column-major structure of a CSR matrix: col_ptr, row_idx, perm (CSR positions)."""
+    """Column-major copy of a CSR matrix: col_ptr, row_idx, perm (CSR position of
+    each entry) and vals_t (its value)."""
     col_ptr: "object"
     row_idx: "object"
     perm: "object"
+    vals_t: "object"
+
+    @staticmethod
+    def empty(n_cols, capacity, device):
+        torch = _torch()
+        cap = max(int(capacity), 1)
+        return CSC(torch.empty(n_cols + 1, dtype=torch.int32, device=device),
+                   torch.empty(cap, dtype=torch.int32, device=device),
+                   torch.empty(cap, dtype=torch.int32, device=device),
+                   torch.empty(cap, dtype=torch.float32, device=device))
 
 
 # ---------------------------------------------------------------------------
@@ -225,27 +237,32 @@ def csr_spmm_fwd(W: CSR, X, Y=None, stream=None):
     N, By, ldy = _mat(Y, "Y")
     if N != W.n_rows or By != B:
         raise ValueError("Y must be [n_rows][B]")
+    ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_rows, W.n_cols, nnz, B), X.device)
     _check(lib().csr_spmm_fwd(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
-                              _p(X), ldx, B, _p(Y), ldy, None, 0, _stream(stream)), "csr_spmm_fwd")
+                              _p(X), ldx, B, _p(Y), ldy, _p(ws), wsb, _stream(stream)),
+           "csr_spmm_fwd")
     return Y
 
 
 def csc_build(W: CSR, out: CSC | None = None, stream=None) -> CSC:
-    """Deterministic CSC copy of W's structure (col_ptr, row_idx, perm)."""
-    torch = _torch()
+    """Deterministic CSC copy of W (col_ptr, row_idx, perm, vals_t)."""
     nnz = W.validate_shapes()
     dev = W.row_ptr.device
     if out is None:
-        cap = max(W.col_idx.numel(), 1)
-        out = CSC(torch.empty(W.n_cols + 1, dtype=torch.int32, device=dev),
-                  torch.empty(cap, dtype=torch.int32, device=dev),
-                  torch.empty(cap, dtype=torch.int32, device=dev))
-    if nnz is None or W.nnz is None:
-        nnz = W.col_idx.numel()  # capacity bound; the kernels read row_ptr
+        out = CSC.empty(W.n_cols, W.col_idx.numel(), dev)
     ws, wsb = _workspace(workspace_bytes(OP_CSC_BUILD, W.n_rows, W.n_cols, nnz, 0), dev)
-    _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(out.col_ptr),
-                           _p(out.row_idx), _p(out.perm), _p(ws), wsb, _stream(stream)), "csc_build")
+    _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
+                           _p(out.col_ptr), _p(out.row_idx), _p(out.perm), _p(out.vals_t), _p(ws),
+                           wsb, _stream(stream)), "csc_build")
     return out
+
+
+def csc_update_vals(W: CSR, csc: CSC, stream=None) -> CSC:
+    """vals_t <- vals[perm] after a values-only update of W."""
+    nnz = W.validate_shapes()
+    _check(lib().csc_update_vals(W.n_cols, nnz, _p(csc.col_ptr), _p(csc.perm), _p(W.vals),
+                                 _p(csc.vals_t), _stream(stream)), "csc_update_vals")
+    return csc
 
 
 def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
@@ -260,11 +277,13 @@ def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
     K, Bx, ldx = _mat(dX, "dX")
     if K != W.n_cols or Bx != B:
         raise ValueError("dX must be [n_cols][B]")
-    cp = ri = pm = None
+    cp = ri = vt = ws = None
+    wsb = 0
     if csc is not None:
-        cp, ri, pm = csc.col_ptr, csc.row_idx, csc.perm
+        cp, ri, vt = csc.col_ptr, csc.row_idx, csc.vals_t
+        ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_cols, W.n_rows, nnz, B), dY.device)
     _check(lib().csr_spmm_bwd_t(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
-                                _p(cp), _p(ri), _p(pm), _p(dY), ldy, B, _p(dX), ldx, None, 0,
+                                _p(cp), _p(ri), _p(vt), _p(dY), ldy, B, _p(dX), ldx, _p(ws), wsb,
                                 _stream(stream)), "csr_spmm_bwd_t")
     return dX
 

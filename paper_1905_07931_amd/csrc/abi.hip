@@ -58,7 +58,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
         case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols));
         case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(nnz, B));
-        case L1CSR_OP_SPMM: return 0;
+        case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
         default: return 0;
@@ -68,51 +68,57 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
 int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
                  const int32_t *col_idx, const float *vals, const float *X, int64_t ldx, int32_t B,
                  float *Y, int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
     if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true) || B < 0) return L1CSR_EINVAL;
     if (bad_dense(X, n_cols, B, ldx) || bad_dense(Y, n_rows, B, ldy)) return L1CSR_EINVAL;
+    if (ws != nullptr && ws_bytes < spmm_workspace_bytes(n_rows, n_cols, nnz, B)) return L1CSR_EINVAL;
     if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
-    return hip_status(launch_spmm_rows(n_rows, nnz, row_ptr, col_idx, vals, nullptr, X, ldx, B, Y,
-                                       ldy, stream));
+    return hip_status(launch_spmm(n_rows, n_cols, nnz, row_ptr, col_idx, vals, X, ldx, B, Y, ldy, ws,
+                                  stream));
 }
 
 int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
-              const int32_t *col_idx, int32_t *col_ptr, int32_t *row_idx, int32_t *perm, void *ws,
-              size_t ws_bytes, hipStream_t stream) {
-    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, nullptr, false)) return L1CSR_EINVAL;
+              const int32_t *col_idx, const float *vals, int32_t *col_ptr, int32_t *row_idx,
+              int32_t *perm, float *vals_t, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
     if (col_ptr == nullptr) return L1CSR_EINVAL;
-    if (nnz > 0 && (row_idx == nullptr || perm == nullptr)) return L1CSR_EINVAL;
+    if (nnz > 0 && (row_idx == nullptr || perm == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
     if (n_rows > 0 && n_cols > 0 &&
         (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols)))
         return L1CSR_EINVAL;
-    if (ceil_div(n_cols, 16384) > kMaxGridY) return L1CSR_EUNSUPPORTED;
-    return hip_status(launch_csc_build(n_rows, n_cols, row_ptr, col_idx, col_ptr, row_idx, perm, ws,
-                                       stream));
+    if (ceil_div(n_rows, 32) > INT32_MAX || ceil_div(n_cols, 4096) > kMaxGridY)
+        return L1CSR_EUNSUPPORTED;
+    return hip_status(launch_csc_build(n_rows, n_cols, nnz, row_ptr, col_idx, vals, col_ptr, row_idx, perm,
+                                       vals_t, ws, stream));
+}
+
+int csc_update_vals(int32_t n_cols, int64_t nnz, const int32_t *col_ptr, const int32_t *perm,
+                    const float *vals, float *vals_t, hipStream_t stream) {
+    if (n_cols < 0 || nnz < 0 || nnz > INT32_MAX || col_ptr == nullptr) return L1CSR_EINVAL;
+    if (nnz > 0 && (perm == nullptr || vals == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
+    return hip_status(launch_csc_gather_vals(n_cols, nnz, col_ptr, perm, vals, vals_t, stream));
 }
 
 int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
                    const int32_t *col_idx, const float *vals, const int32_t *col_ptr,
-                   const int32_t *row_idx, const int32_t *perm, const float *dY, int64_t ldy,
+                   const int32_t *row_idx, const float *vals_t, const float *dY, int64_t ldy,
                    int32_t B, float *dX, int64_t ldx, void *ws, size_t ws_bytes,
                    hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
-    // CSC path: col_ptr given (row_idx and perm too unless nnz == 0); atomic path: all NULL
+    // CSC path: col_ptr given (row_idx and vals_t too unless nnz == 0); atomic path: all NULL
     const bool use_csc = col_ptr != nullptr;
-    if (!use_csc && (row_idx != nullptr || perm != nullptr)) return L1CSR_EINVAL;
+    if (!use_csc && (row_idx != nullptr || vals_t != nullptr)) return L1CSR_EINVAL;
     if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return L1CSR_EINVAL;
+    if (nnz > (int64_t)n_rows * (int64_t)n_cols || nnz > INT32_MAX) return L1CSR_EINVAL;
     if (use_csc) {
-        if (nnz > 0 && (row_idx == nullptr || perm == nullptr || vals == nullptr)) return L1CSR_EINVAL;
+        if (nnz > 0 && (row_idx == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
+        if (ws != nullptr && ws_bytes < spmm_workspace_bytes(n_cols, n_rows, nnz, B)) return L1CSR_EINVAL;
     } else if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) {
         return L1CSR_EINVAL;
     }
-    if (nnz > (int64_t)n_rows * (int64_t)n_cols) return L1CSR_EINVAL;
     if (bad_dense(dY, n_rows, B, ldy) || bad_dense(dX, n_cols, B, ldx)) return L1CSR_EINVAL;
     if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
-    if (use_csc)
-        return hip_status(launch_spmm_rows(n_cols, nnz, col_ptr, row_idx, vals, perm, dY, ldy, B, dX,
-                                           ldx, stream));
+    if (use_csc)  // the forward product of the transposed matrix
+        return hip_status(launch_spmm(n_cols, n_rows, nnz, col_ptr, row_idx, vals_t, dY, ldy, B, dX,
+                                      ldx, ws, stream));
     return hip_status(launch_spmm_scatter_atomic(n_rows, n_cols, row_ptr, col_idx, vals, dY, ldy, B,
                                                  dX, ldx, stream));
 }

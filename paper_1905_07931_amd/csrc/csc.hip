@@ -1,16 +1,19 @@
-// Deterministic CSR -> CSC (structure only, plus the CSR position of every
-// entry) for the backward product.
+// Deterministic CSR -> CSC for the backward product: column pointers, the row
+// of every entry, its CSR position (perm) and its value in CSC order.
 //
-// Rows are taken in chunks of 32.  For one chunk and one tile of columns a
-// workgroup builds, in LDS, a 32-bit mask per column whose bit r says "row r
-// of the chunk has an entry in this column" (atomicOr: order independent).
-// Then for an entry (row r of chunk c, column k):
-//     position = col_ptr[k]                         (entries of earlier columns)
-//              + sum_{c' < c} popcount(mask_{c'}[k]) (earlier chunks, same column)
-//              + popcount(mask_c[k] & ((1<<r)-1))    (earlier rows of this chunk)
-// which orders each column by row without sorting and without any
-// order-dependent atomics.  Passes: count -> per-column chunk scan ->
-// column-pointer scan -> scatter (the scatter rebuilds the masks).
+// Rows are taken in chunks of 32 and columns in tiles of up to 4096 (segment
+// pointers per (row, tile) come from the same planning pass as the products).
+// For one (chunk, tile) a workgroup builds in LDS a 32-bit mask per column
+// whose bit r says "row r of the chunk has an entry in this column"
+// (atomicOr, so the result does not depend on order).  An entry (row r of
+// chunk c, column k) then goes to
+//     col_ptr[k]                              entries of earlier columns
+//   + sum_{c' < c} popcount(mask_{c'}[k])     same column, earlier chunks
+//   + popcount(mask_c[k] & ((1 << r) - 1))    same column, earlier rows of c
+// which orders every column by row (the canonical CSC) without sorting and
+// without order-dependent atomics.
+// Passes: segment pointers -> counts -> per-column chunk scan -> column
+// pointer scan -> scatter (rebuilds the masks, bases staged in LDS).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -19,114 +22,187 @@ namespace l1csr {
 namespace {
 
 constexpr int kChunkRows = 32;
-constexpr int kMaxTileCols = 16384;  // 64 KB of masks
+constexpr int kTileShift = 12;
+constexpr int kTileCols = 1 << kTileShift;
 constexpr int kCscThreads = 512;
 
-__device__ __forceinline__ void build_masks(int n_rows, const int *__restrict__ ptr,
-                                            const int *__restrict__ idx, int chunk, int k0,
-                                            int k1, uint32_t *M) {
+__device__ __forceinline__ void build_masks(int n_rows, const int *__restrict__ seg, int ntc,
+                                            const int *__restrict__ idx, int chunk, int t, int k0,
+                                            int ncols_tile, uint32_t *M) {
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     const int nwaves = blockDim.x >> 6;
-    for (int k = threadIdx.x; k < k1 - k0; k += blockDim.x) M[k] = 0u;
+    for (int k = threadIdx.x; k < ncols_tile; k += blockDim.x) M[k] = 0u;
     __syncthreads();
     for (int r = wave; r < kChunkRows; r += nwaves) {
         const int row = chunk * kChunkRows + r;
         if (row >= n_rows) break;
-        const int s = ptr[row], e = ptr[row + 1];
+        const int *sr = seg + (int64_t)row * (ntc + 1) + t;
+        const int s = sr[0], e = sr[1];
         for (int p = s + lane; p < e; p += kWave) {
-            const int k = idx[p];
-            if (k >= k0 && k < k1) atomicOr(&M[k - k0], 1u << r);
+            const int k = idx[p] - k0;
+            if (k >= 0 && k < ncols_tile) atomicOr(&M[k], 1u << r);
         }
     }
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kCscThreads) void csc_count_kernel(int n_rows, int n_cols,
-                                                                const int *__restrict__ ptr,
+__global__ __launch_bounds__(kCscThreads) void csc_count_kernel(int n_rows, int n_cols, int ntc,
+                                                                const int *__restrict__ seg,
                                                                 const int *__restrict__ idx,
                                                                 int *__restrict__ cnt) {
-    extern __shared__ uint32_t M[];
-    const int chunk = blockIdx.x;
-    const int k0 = blockIdx.y * kMaxTileCols;
-    const int k1 = min(n_cols, k0 + kMaxTileCols);
-    build_masks(n_rows, ptr, idx, chunk, k0, k1, M);
-    for (int k = threadIdx.x; k < k1 - k0; k += blockDim.x)
-        cnt[(int64_t)chunk * n_cols + k0 + k] = __popc(M[k]);
+    __shared__ uint32_t M[kTileCols];
+    const int chunk = blockIdx.x, t = blockIdx.y;
+    const int k0 = t * kTileCols;
+    const int nct = min(kTileCols, n_cols - k0);
+    build_masks(n_rows, seg, ntc, idx, chunk, t, k0, nct, M);
+    int *c = cnt + (int64_t)chunk * n_cols + k0;
+    for (int k = threadIdx.x; k < nct; k += blockDim.x) c[k] = __popc(M[k]);
 }
 
-// cnt[c][k] <- sum_{c' < c} cnt[c'][k]; tot[k] <- sum_c cnt[c][k]
-__global__ void csc_colscan_kernel(int n_chunks, int n_cols, int *__restrict__ cnt,
-                                   int *__restrict__ tot) {
+// cnt[c][k] <- sum_{c' < c} cnt[c'][k];  tot[k] <- sum_c cnt[c][k]
+__global__ __launch_bounds__(256) void csc_colscan_kernel(int n_chunks, int n_cols,
+                                                          int *__restrict__ cnt,
+                                                          int *__restrict__ tot) {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= n_cols) return;
     int run = 0;
-    for (int c = 0; c < n_chunks; ++c) {
+    int c = 0;
+    for (; c + 8 <= n_chunks; c += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = cnt[(int64_t)(c + u) * n_cols + k];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            cnt[(int64_t)(c + u) * n_cols + k] = run;
+            run += v[u];
+        }
+    }
+    for (; c < n_chunks; ++c) {
         const int64_t o = (int64_t)c * n_cols + k;
-        const int t = cnt[o];
+        const int v = cnt[o];
         cnt[o] = run;
-        run += t;
+        run += v;
     }
     tot[k] = run;
 }
 
+// writes perm only: the row and the value of each CSC entry follow from it in
+// a coalesced pass (csc_finish_kernel), so this pass does one scattered store
+// per entry instead of three
 __global__ __launch_bounds__(kCscThreads) void csc_scatter_kernel(
-    int n_rows, int n_cols, const int *__restrict__ ptr, const int *__restrict__ idx,
-    const int *__restrict__ cnt, const int *__restrict__ col_ptr, int *__restrict__ row_idx,
-    int *__restrict__ perm) {
-    extern __shared__ uint32_t M[];
-    const int chunk = blockIdx.x;
-    const int k0 = blockIdx.y * kMaxTileCols;
-    const int k1 = min(n_cols, k0 + kMaxTileCols);
-    build_masks(n_rows, ptr, idx, chunk, k0, k1, M);
+    int n_rows, int n_cols, int ntc, const int *__restrict__ seg, const int *__restrict__ idx,
+    const int *__restrict__ cnt, const int *__restrict__ col_ptr, int *__restrict__ perm) {
+    __shared__ uint32_t M[kTileCols];
+    __shared__ int base[kTileCols];
+    const int chunk = blockIdx.x, t = blockIdx.y;
+    const int k0 = t * kTileCols;
+    const int nct = min(kTileCols, n_cols - k0);
+    const int *c = cnt + (int64_t)chunk * n_cols + k0;
+    for (int k = threadIdx.x; k < nct; k += blockDim.x) base[k] = col_ptr[k0 + k] + c[k];
+    build_masks(n_rows, seg, ntc, idx, chunk, t, k0, nct, M);  // ends with a barrier
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     const int nwaves = blockDim.x >> 6;
     for (int r = wave; r < kChunkRows; r += nwaves) {
         const int row = chunk * kChunkRows + r;
         if (row >= n_rows) break;
-        const int s = ptr[row], e = ptr[row + 1];
+        const int *sr = seg + (int64_t)row * (ntc + 1) + t;
+        const int s = sr[0], e = sr[1];
         const uint32_t below = (1u << r) - 1u;
         for (int p = s + lane; p < e; p += kWave) {
-            const int k = idx[p];
-            if (k >= k0 && k < k1) {
-                const int pos = col_ptr[k] + cnt[(int64_t)chunk * n_cols + k] +
-                                __popc(M[k - k0] & below);
-                row_idx[pos] = row;
-                perm[pos] = p;
+            const int k = idx[p] - k0;
+            if (k >= 0 && k < nct) {
+                perm[base[k] + __popc(M[k] & below)] = p;
             }
         }
     }
 }
 
+// row_idx[q] = the row holding CSR position perm[q] (binary search of the
+// row pointers), vals_t[q] = vals[perm[q]]
+__global__ __launch_bounds__(256) void csc_finish_kernel(int n_rows, int64_t nnz,
+                                                         const int *__restrict__ ptr,
+                                                         const int *__restrict__ perm,
+                                                         const float *__restrict__ vals,
+                                                         int *__restrict__ row_idx,
+                                                         float *__restrict__ vals_t) {
+    const int64_t n = min(nnz, (int64_t)ptr[n_rows]);  // nnz may be a capacity bound
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int p = perm[q];
+        int lo = 0, hi = n_rows - 1;  // last row with ptr[row] <= p
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (ptr[mid] <= p) lo = mid; else hi = mid - 1;
+        }
+        row_idx[q] = lo;
+        vals_t[q] = vals[p];
+    }
+}
+
+__global__ void gather_vals_kernel(int n_cols, const int *__restrict__ col_ptr,
+                                   const int *__restrict__ perm, const float *__restrict__ vals,
+                                   float *__restrict__ vals_t) {
+    const int64_t nnz = col_ptr[n_cols];
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * blockDim.x)
+        vals_t[q] = vals[perm[q]];
+}
+
+struct csc_layout {
+    int n_chunks, ntc;
+    int64_t seg_ints, cnt_ints;
+};
+
+csc_layout layout(int n_rows, int n_cols) {
+    csc_layout l;
+    l.n_chunks = (int)ceil_div(n_rows, kChunkRows);
+    l.ntc = (int)ceil_div(n_cols, kTileCols);
+    l.seg_ints = (int64_t)n_rows * (l.ntc + 1);
+    l.cnt_ints = (int64_t)l.n_chunks * n_cols;
+    return l;
+}
+
 }  // namespace
 
 size_t csc_workspace_bytes(int n_rows, int n_cols) {
-    const int64_t n_chunks = ceil_div(n_rows, kChunkRows);
-    return sizeof(int) * (size_t)(n_chunks * (int64_t)n_cols + n_cols + 1);
+    const csc_layout l = layout(n_rows, n_cols);
+    return sizeof(int) * (size_t)(l.seg_ints + l.cnt_ints + n_cols + 1);
 }
 
-hipError_t launch_csc_build(int n_rows, int n_cols, const int *ptr, const int *idx, int *col_ptr,
-                            int *row_idx, int *perm, void *ws, hipStream_t s) {
+hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                            const float *vals, int *col_ptr, int *row_idx, int *perm,
+                            float *vals_t, void *ws, hipStream_t s) {
     if (n_cols == 0) return launch_fill_i32(col_ptr, 1, 0, s);
-    const int n_chunks = (int)ceil_div(n_rows, kChunkRows);
-    int *cnt = static_cast<int *>(ws);
-    int *tot = cnt + (int64_t)n_chunks * n_cols;
     if (n_rows == 0) return launch_fill_i32(col_ptr, (int64_t)n_cols + 1, 0, s);
-    const int tiles = (int)ceil_div(n_cols, kMaxTileCols);
-    const int tile_cols = n_cols < kMaxTileCols ? n_cols : kMaxTileCols;
-    const size_t lds = sizeof(uint32_t) * (size_t)tile_cols;
-    dim3 grid(n_chunks, tiles);
-    csc_count_kernel<<<grid, kCscThreads, lds, s>>>(n_rows, n_cols, ptr, idx, cnt);
-    hipError_t e = hipGetLastError();
+    const csc_layout l = layout(n_rows, n_cols);
+    int *seg = static_cast<int *>(ws);
+    int *cnt = seg + l.seg_ints;
+    int *tot = cnt + l.cnt_ints;
+    hipError_t e = launch_seg(n_rows, l.ntc, kTileShift, ptr, idx, seg, s);
     if (e != hipSuccess) return e;
-    csc_colscan_kernel<<<(unsigned)ceil_div(n_cols, 256), 256, 0, s>>>(n_chunks, n_cols, cnt, tot);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    e = launch_exclusive_scan(tot, col_ptr, n_cols, nullptr, s);
-    if (e != hipSuccess) return e;
-    csc_scatter_kernel<<<grid, kCscThreads, lds, s>>>(n_rows, n_cols, ptr, idx, cnt, col_ptr, row_idx,
-                                                      perm);
+    dim3 grid(l.n_chunks, l.ntc);
+    csc_count_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    csc_colscan_kernel<<<(unsigned)ceil_div(n_cols, 256), 256, 0, s>>>(l.n_chunks, n_cols, cnt, tot);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_exclusive_scan(tot, col_ptr, n_cols, nullptr, s)) != hipSuccess) return e;
+    csc_scatter_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt, col_ptr, perm);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (nnz == 0) return hipSuccess;
+    int64_t g = ceil_div(nnz, 256);
+    if (g > 65536) g = 65536;
+    csc_finish_kernel<<<(unsigned)g, 256, 0, s>>>(n_rows, nnz, ptr, perm, vals, row_idx, vals_t);
+    return hipGetLastError();
+}
+
+hipError_t launch_csc_gather_vals(int n_cols, int64_t nnz_bound, const int *col_ptr, const int *perm,
+                                  const float *vals, float *vals_t, hipStream_t s) {
+    if (nnz_bound == 0) return hipSuccess;
+    int64_t g = ceil_div(nnz_bound, 256);
+    if (g > 65536) g = 65536;
+    gather_vals_kernel<<<(unsigned)g, 256, 0, s>>>(n_cols, col_ptr, perm, vals, vals_t);
     return hipGetLastError();
 }
 

@@ -10,17 +10,28 @@
 namespace l1csr {
 
 // spmm.hip -----------------------------------------------------------------
-hipError_t launch_spmm_rows(int n_rows, int64_t nnz, const int *ptr, const int *idx,
-                            const float *vals, const int *perm, const float *X, int64_t ldx,
-                            int B, float *Y, int64_t ldy, hipStream_t s);
+// Y = A.X for a CSR operand A (n_rows x n_cols); ws (nullable) holds the plan
+// and partial rows of the tiled kernel, spmm_workspace_bytes(n_rows, n_cols,
+// nnz, B) bytes (0: the tiled kernel is not used for these sizes).
+size_t spmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B);
+hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                       const float *vals, const float *X, int64_t ldx, int B, float *Y,
+                       int64_t ldy, void *ws, hipStream_t s);
 hipError_t launch_spmm_scatter_atomic(int n_rows, int n_cols, const int *ptr, const int *idx,
                                       const float *vals, const float *dY, int64_t ldy, int B,
                                       float *dX, int64_t ldx, hipStream_t s);
+// seg[row][t] = first position of the row with column >= t << shift, t = 0..ntiles
+hipError_t launch_seg(int n_rows, int ntiles, int shift, const int *ptr, const int *idx, int *seg,
+                      hipStream_t s);
 
 // csc.hip ------------------------------------------------------------------
 size_t csc_workspace_bytes(int n_rows, int n_cols);
-hipError_t launch_csc_build(int n_rows, int n_cols, const int *ptr, const int *idx,
-                            int *col_ptr, int *row_idx, int *perm, void *ws, hipStream_t s);
+hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                            const float *vals, int *col_ptr, int *row_idx, int *perm,
+                            float *vals_t, void *ws, hipStream_t s);
+// vals_t[q] = vals[perm[q]] for q < col_ptr[n_cols] (read on the device)
+hipError_t launch_csc_gather_vals(int n_cols, int64_t nnz_bound, const int *col_ptr, const int *perm,
+                                  const float *vals, float *vals_t, hipStream_t s);
 
 // scan.hip -----------------------------------------------------------------
 // out[0] = 0, out[j+1] = in[0] + ... + in[j] for j < n (out has n+1 entries);

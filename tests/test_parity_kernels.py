@@ -53,6 +53,51 @@ def test_spmm_fwd(shape):
     assert_scaled_close(Y, ref, m, what="Y")
 
 
+# Shapes that drive the LDS-tiled kernel through each vector width (the width
+# follows from the batch: 64*VEC columns per workgroup), several 64-row X
+# tiles, a ragged batch tail, ragged row blocks and both rows-per-wave plans.
+TILED = [  # (N, K, B, nnz, seed)
+    (300, 784, 64, 23520, 20),      # VEC 1
+    (2000, 300, 128, 30000, 21),    # VEC 2
+    (4096, 300, 1024, 61440, 22),   # VEC 4, 4 rows per wave
+    (4096, 300, 1020, 61440, 23),   # VEC 4, ragged last batch chunk
+    (9000, 333, 1024, 150000, 24),  # VEC 4, 8 rows per wave, ragged tile and row block
+]
+
+
+@pytest.mark.parametrize("shape", TILED, ids=_ids)
+def test_spmm_fwd_tiled_widths(shape):
+    L = _layer(shape)
+    Y = h(L1.csr_spmm_fwd(_W(L), t(L.X)))
+    ref = oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)
+    m = oracle.spmm_fwd(L.row_ptr, L.col_idx, np.abs(L.vals), L.X)
+    assert_scaled_close(Y, ref, m, what="Y")
+
+
+@pytest.mark.parametrize("shape", [(300, 4096, 1024, 61440, 25), (64, 8192, 1024, 30000, 26)],
+                         ids=_ids)
+def test_spmm_bwd_tiled_widths(shape):
+    L = _layer(shape)
+    W = _W(L)
+    dX = h(L1.csr_spmm_bwd_t(W, t(L.dY), L1.csc_build(W)))
+    ref = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, L.vals, L.dY, L.K)
+    m = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, np.abs(L.vals), np.abs(L.dY), L.K)
+    assert_scaled_close(dX, ref, m, what="dX")
+
+
+def test_spmm_power_law_rows_dyadic_bit_exact():
+    # Zipf row lengths (a few full rows, many short ones) through the tiled
+    # kernel on the dyadic grid: every sum is exact, so the bits must match
+    import numpy as np_
+    rng = np_.random.default_rng(27)
+    N, K, B = 4096, 512, 256
+    rp, ci = synth.zipf_pattern(rng, N, K, 90000, 1.1)
+    vals = (rng.integers(1, 17, ci.shape[0]) * rng.choice([-1.0, 1.0], ci.shape[0]) / 16).astype(np_.float32)
+    X = (rng.integers(0, 17, (K, B)) / 16).astype(np_.float32)
+    W = L1.CSR.from_host(rp, ci, vals, K, device=cuda())
+    assert bits_equal(h(L1.csr_spmm_fwd(W, t(X))), oracle.spmm_fwd(rp, ci, vals, X))
+
+
 def test_spmm_fwd_padded_leading_dimension():
     L = synth.fc_layer(50, 70, 37, 900, seed=11)
     import torch
@@ -84,6 +129,7 @@ def test_csc_build_bit_exact(shape):
     assert bits_equal(h(csc.col_ptr), cp)
     assert bits_equal(h(csc.row_idx)[: L.nnz], ri)
     assert bits_equal(h(csc.perm)[: L.nnz], pm)
+    assert bits_equal(h(csc.vals_t)[: L.nnz], L.vals[pm])
 
 
 def test_csc_build_wide_matrix_column_tiles():
@@ -120,11 +166,12 @@ def test_spmm_bwd_dyadic_bit_exact_and_deterministic():
 
 
 def test_spmm_bwd_csc_stays_valid_after_value_update():
-    # debiasing changes values only: the CSC copy reads them through perm
+    # debiasing changes values only: the CSC structure is kept, values refreshed through perm
     L = synth.fc_layer(60, 80, 32, 1500, seed=13)
     W = _W(L)
     csc = L1.csc_build(W)
     W.vals.mul_(-0.5)
+    L1.csc_update_vals(W, csc)
     dX = h(L1.csr_spmm_bwd_t(W, t(L.dY), csc))
     v2 = (L.vals * np.float32(-0.5)).astype(np.float32)
     ref = oracle.spmm_bwd_t(L.row_ptr, L.col_idx, v2, L.dY, L.K)
