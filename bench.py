@@ -9,8 +9,7 @@ row lengths, batch 1024, fp32):
     CSC(W)                        csc_build
     dX = W^T.dY                   csr_spmm_bwd_t
     dW = dY.X^T                   dense_wgrad     (fp32 matrix cores)
-    Z  = S_t(W - eta*dW)          prox_l1_step    (in place over dW)
-    W' = CSR(Z)                   csr_recompress
+    W' = CSR(S_t(W - eta*dW))     prox_l1_recompress (prox + recompression in one call)
 
 Every step reads the same resident inputs and writes W' to its own buffers,
 so all timed steps do identical work.  Prints ONE JSON line.
@@ -43,8 +42,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=256,
-                    help="rows of W in the oracle's timed sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum host time spent timing the oracle")
     return ap.parse_args()
 
 
@@ -102,14 +101,12 @@ def main():
     Y = torch.empty((N, B), dtype=torch.float32, device=dev)
     dX = torch.empty((K, B), dtype=torch.float32, device=dev)
     dW = torch.empty((N, K), dtype=torch.float32, device=dev)
-    cnt = torch.empty(N, dtype=torch.int32, device=dev)
     csc = L1.CSC.empty(K, nnz, dev)
     Wout = L1.CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
                   torch.empty(N * K, dtype=torch.int32, device=dev),
                   torch.empty(N * K, dtype=torch.float32, device=dev), None)
 
-    names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_step",
-             "csr_recompress"]
+    names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_recompress"]
 
     def step(ev=None):
         def mark(i):
@@ -124,10 +121,8 @@ def main():
         mark(3)
         L1.dense_wgrad(dY, X, dW)
         mark(4)
-        L1.prox_l1_step(L1.PROX_DENSE, W, dW, eta, lam, Z=dW, row_counts=cnt)
+        L1.prox_l1_recompress(W, dW, eta, lam, out=Wout)
         mark(5)
-        L1.csr_recompress(dW, 0.0, row_counts=cnt, out=Wout)
-        mark(6)
 
     for _ in range(args.warmup):
         step()
@@ -144,7 +139,8 @@ def main():
     ms_per_step = start.elapsed_time(end) / args.steps
 
     # per-kernel durations with events between the calls (same stream)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     for s in range(args.steps):
         step(evs[s])
@@ -157,13 +153,12 @@ def main():
     flops_nnz_only = 6.0 * nnz * B
     gflops = flops_step / (ms_per_step * 1e-3) / 1e9
 
-    # algorithmic bytes (each operand once)
+    # algorithmic bytes of the prox + recompression (each operand once): dW in,
+    # W in (CSR), W' out (CSR)
     csr_in = 8.0 * nnz + 4.0 * (N + 1)
     csr_out = 8.0 * nnz_out + 4.0 * (N + 1)
-    bytes_prox = 4.0 * N * K + csr_in + 4.0 * N * K + 4.0 * N         # dW in, W in, Z out, counts
-    bytes_recompress = 4.0 * N * K + 4.0 * N + csr_out                # Z in, counts, CSR out
-    prox_recompress_gbs = (bytes_prox + bytes_recompress) / (
-        (per["prox_l1_step"] + per["csr_recompress"]) * 1e-3) / 1e9
+    bytes_prox = 4.0 * N * K + csr_in + csr_out
+    prox_recompress_gbs = bytes_prox / (per["prox_l1_recompress"] * 1e-3) / 1e9
 
     dom = max(per, key=per.get)
     wg_flops = 2.0 * N * K * B
@@ -176,14 +171,14 @@ def main():
                 "algorithmic_flops": wg_flops}
     else:
         # fall back to the kernel that took longest, on the HBM roof
-        alg = {"prox_l1_step": bytes_prox, "csr_recompress": bytes_recompress}.get(dom)
+        alg = {"prox_l1_recompress": bytes_prox}.get(dom)
         ach = (alg / (per[dom] * 1e-3) / 1e9) if alg else None
         roof = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": (ach / PEAK_HBM_GBS) if ach else None, "traffic": None}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(Lr, args.cpu_rows)
+        cpu = cpu_baseline(Lr, args.cpu_seconds)
 
     out = {
         "metric": METRIC, "value": round(gflops, 1), "unit": "GFLOP/s", "n_gpus": 1,
@@ -205,31 +200,29 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(Lr, rows):
-    """The oracle on a bounded sample of the same step: the first `rows` rows of W
-    (their forward rows, their share of the backward sum, their dense dW rows,
-    prox and recompression), scaled to the full step."""
+def cpu_baseline(Lr, min_seconds):
+    """The oracle timed on the host cores on the same step: the whole layer
+    (fwd, bwd, dense dW, prox, recompression), repeated until at least
+    `min_seconds` have elapsed (at most 5 runs); the median run is reported."""
     import oracle
 
     N, K, B = Lr.N, Lr.K, Lr.B
-    rows = min(rows, N)
-    rp = Lr.row_ptr[: rows + 1].copy()
-    nz = int(rp[-1])
-    ci = Lr.col_idx[:nz]
-    v = Lr.vals[:nz]
-    dY = Lr.dY[:rows]
-    t0 = time.perf_counter()
-    oracle.spmm_fwd(rp, ci, v, Lr.X)
-    oracle.spmm_bwd_t(rp, ci, v, dY, K)
-    dW = oracle.dense_wgrad(dY, Lr.X)
-    Z, _ = oracle.prox_dense(rp, ci, v, dW, Lr.eta, Lr.lam, K)
-    oracle.recompress(Z)
-    sec = time.perf_counter() - t0
-    flops = 2.0 * nz * B * 2 + 2.0 * rows * K * B
+    times = []
+    while len(times) < 5 and (sum(times) < min_seconds or len(times) < 1):
+        t0 = time.perf_counter()
+        oracle.spmm_fwd(Lr.row_ptr, Lr.col_idx, Lr.vals, Lr.X)
+        oracle.spmm_bwd_t(Lr.row_ptr, Lr.col_idx, Lr.vals, Lr.dY, K)
+        dW = oracle.dense_wgrad(Lr.dY, Lr.X)
+        Z, _ = oracle.prox_dense(Lr.row_ptr, Lr.col_idx, Lr.vals, dW, Lr.eta, Lr.lam, K)
+        oracle.recompress(Z)
+        times.append(time.perf_counter() - t0)
+        del dW, Z
+    sec = float(np.median(times))
+    flops = 2.0 * Lr.nnz * B * 2 + 2.0 * N * K * B
     return {"value": round(flops / sec / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"first {rows} of {N} rows of W ({nz} nnz): fwd, bwd share, dense dW, prox, "
-                      f"recompress; {sec:.2f} s"}
+            "sample": f"the full step ({N}x{K} CSR, {Lr.nnz} nnz, B={B}): fwd, bwd, dense dW, prox, "
+                      f"recompress; median of {len(times)} runs, {sec:.2f} s each"}
 
 
 if __name__ == "__main__":

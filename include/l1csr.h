@@ -68,7 +68,8 @@ enum l1csr_op {
     L1CSR_OP_SDDMM = 3,
     L1CSR_OP_SPMM = 4,
     L1CSR_OP_COMPACT = 5,
-    L1CSR_OP_SOFTMAX_XENT = 6
+    L1CSR_OP_SOFTMAX_XENT = 6,
+    L1CSR_OP_PROX_RECOMPRESS = 7
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -205,6 +206,23 @@ int csr_recompress(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz, 
                    int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
                    int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * prox_l1_step (dense mode) followed by csr_recompress (t = 0) in one call,
+ * without materialising Z: the l1-phase weight update of Eq. (prox) from the
+ * CSR weights W and the dense gradient G straight to the new CSR W'.  The
+ * output is bit-identical to the two calls.  G is read twice (a counting pass
+ * and a filling pass); row_ptr_out, col_idx_out, vals_out, capacity,
+ * d_nnz_out and h_nnz_required behave as in csr_recompress.  The output arrays
+ * must not overlap W's.  ws as
+ * l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0).
+ */
+int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                       const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                       const float *G, int64_t ldg, float eta, float lambda,
+                       int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                       int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                       void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * CSR -> CSR without its stored zeros (after a support-restricted prox step in

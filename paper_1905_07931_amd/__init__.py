@@ -16,7 +16,7 @@ from dataclasses import dataclass
 __all__ = [
     "CSR", "CSC", "L1CSRError", "lib", "status_str", "workspace_bytes",
     "csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
-    "prox_l1_step", "csr_recompress", "csr_compact", "relu_fwd", "relu_bwd", "softmax_xent",
+    "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "relu_fwd", "relu_bwd", "softmax_xent",
     "PROX_DENSE", "PROX_CSR",
 ]
 
@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so
 OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED = 0, -1, -2, -4, -5
 PROX_DENSE, PROX_CSR = 0, 1
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
+OP_PROX_RECOMPRESS = 7
 
 
 class L1CSRError(RuntimeError):
@@ -60,13 +61,15 @@ def lib():
                                    vp, vp]
         L.csr_recompress.argtypes = [i32, i32, vp, i64, f32, vp, vp, vp, vp, i64, vp,
                                      C.POINTER(C.c_int64), vp, sz, vp]
+        L.prox_l1_recompress.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp,
+                                         i64, vp, C.POINTER(C.c_int64), vp, sz, vp]
         L.csr_compact.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
         L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
-                     "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "csr_compact",
-                     "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
+                     "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
+                     "csr_compact", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -371,6 +374,30 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
     _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
                                 _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
                                 _stream(stream)), "csr_recompress")
+    out.nnz = need.value if need.value >= 0 else None
+    return out
+
+
+def prox_l1_recompress(W: CSR, G, eta, lam, capacity=None, out: CSR | None = None, stream=None):
+    """W' = CSR(S_{eta*lam}(W - eta*G)) in one call (same bits as prox + recompress)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    N, K, ldg = _mat(G, "G")
+    if (N, K) != (W.n_rows, W.n_cols):
+        raise ValueError("G must be [n_rows][n_cols]")
+    dev = G.device
+    if out is None:
+        cap = N * K if capacity is None else int(capacity)
+        out = CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
+    cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev)
+    need = C.c_int64(-1)
+    _check(lib().prox_l1_recompress(N, K, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(G), ldg,
+                                    float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
+                                    _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
+                                    _stream(stream)), "prox_l1_recompress")
     out.nnz = need.value if need.value >= 0 else None
     return out
 

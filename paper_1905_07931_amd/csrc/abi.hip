@@ -55,11 +55,12 @@ const char *l1csr_status_str(int status) {
 size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz, int32_t B) {
     if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return 0;
     switch (op) {
-        case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols));
+        case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols, nnz));
         case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(nnz, B));
         case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
+        case L1CSR_OP_PROX_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
         default: return 0;
     }
@@ -83,7 +84,7 @@ int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_pt
     if (col_ptr == nullptr) return L1CSR_EINVAL;
     if (nnz > 0 && (row_idx == nullptr || perm == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
     if (n_rows > 0 && n_cols > 0 &&
-        (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols)))
+        (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols, nnz)))
         return L1CSR_EINVAL;
     if (ceil_div(n_rows, 32) > INT32_MAX || ceil_div(n_cols, 4096) > kMaxGridY)
         return L1CSR_EUNSUPPORTED;
@@ -203,6 +204,40 @@ int csr_recompress(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz, 
     }
     return hip_status(launch_recompress_fill(n_rows, n_cols, Z, ldz, t, row_ptr_out, col_idx_out,
                                              vals_out, capacity, stream));
+}
+
+int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                       const int32_t *col_idx, const float *vals, const float *G, int64_t ldg,
+                       float eta, float lambda, int32_t *row_ptr_out, int32_t *col_idx_out,
+                       float *vals_out, int64_t capacity, int32_t *d_nnz_out,
+                       int64_t *h_nnz_required, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (!finite_f(eta) || !finite_f(lambda) || eta <= 0.f || lambda < 0.f) return L1CSR_EINVAL;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(G, n_rows, n_cols, ldg) || row_ptr_out == nullptr || capacity < 0)
+        return L1CSR_EINVAL;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
+    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < sizeof(int) * (size_t)n_rows)) return L1CSR_EINVAL;
+    if (row_ptr_out == row_ptr) return L1CSR_EINVAL;  // out of place
+    const double t = (double)eta * (double)lambda;     // exact in double
+    int *counts = static_cast<int *>(ws);
+    hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, counts,
+                                     stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(counts, row_ptr_out, n_rows, d_nnz_out, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    if (capacity < total) {
+        int32_t h = 0;
+        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        if (h_nnz_required) *h_nnz_required = h;
+        if (h > capacity) return L1CSR_ECAPACITY;
+    } else if (h_nnz_required) {
+        *h_nnz_required = -1;
+    }
+    return hip_status(launch_prox_fill(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t,
+                                       row_ptr_out, col_idx_out, vals_out, capacity, stream));
 }
 
 int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,

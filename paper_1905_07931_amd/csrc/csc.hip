@@ -32,14 +32,28 @@ __device__ __forceinline__ void build_masks(int n_rows, const int *__restrict__ 
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     const int nwaves = blockDim.x >> 6;
+    constexpr int kRowsPerWave = kChunkRows / (kCscThreads / kWave);
+    // bounds of this wave's rows, then their first entries, before any use
+    int sb[kRowsPerWave], eb[kRowsPerWave], k1st[kRowsPerWave];
+#pragma unroll
+    for (int u = 0; u < kRowsPerWave; ++u) {
+        const int row = chunk * kChunkRows + wave + u * nwaves;
+        sb[u] = eb[u] = 0;
+        if (row < n_rows) {
+            const int *sr = seg + (int64_t)row * (ntc + 1) + t;
+            sb[u] = sr[0];
+            eb[u] = sr[1];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsPerWave; ++u) k1st[u] = sb[u] + lane < eb[u] ? idx[sb[u] + lane] - k0 : -1;
     for (int k = threadIdx.x; k < ncols_tile; k += blockDim.x) M[k] = 0u;
     __syncthreads();
-    for (int r = wave; r < kChunkRows; r += nwaves) {
-        const int row = chunk * kChunkRows + r;
-        if (row >= n_rows) break;
-        const int *sr = seg + (int64_t)row * (ntc + 1) + t;
-        const int s = sr[0], e = sr[1];
-        for (int p = s + lane; p < e; p += kWave) {
+#pragma unroll
+    for (int u = 0; u < kRowsPerWave; ++u) {
+        const int r = wave + u * nwaves;
+        if (k1st[u] >= 0 && k1st[u] < ncols_tile) atomicOr(&M[k1st[u]], 1u << r);
+        for (int p = sb[u] + kWave + lane; p < eb[u]; p += kWave) {
             const int k = idx[p] - k0;
             if (k >= 0 && k < ncols_tile) atomicOr(&M[k], 1u << r);
         }
@@ -87,12 +101,11 @@ __global__ __launch_bounds__(256) void csc_colscan_kernel(int n_chunks, int n_co
     tot[k] = run;
 }
 
-// writes perm only: the row and the value of each CSC entry follow from it in
-// a coalesced pass (csc_finish_kernel), so this pass does one scattered store
-// per entry instead of three
+// one scattered 8-byte store per entry, (row, CSR position), into a staging
+// array; csc_finish_kernel then writes row_idx, perm and vals_t coalesced
 __global__ __launch_bounds__(kCscThreads) void csc_scatter_kernel(
     int n_rows, int n_cols, int ntc, const int *__restrict__ seg, const int *__restrict__ idx,
-    const int *__restrict__ cnt, const int *__restrict__ col_ptr, int *__restrict__ perm) {
+    const int *__restrict__ cnt, const int *__restrict__ col_ptr, int2 *__restrict__ pairs) {
     __shared__ uint32_t M[kTileCols];
     __shared__ int base[kTileCols];
     const int chunk = blockIdx.x, t = blockIdx.y;
@@ -113,31 +126,27 @@ __global__ __launch_bounds__(kCscThreads) void csc_scatter_kernel(
         for (int p = s + lane; p < e; p += kWave) {
             const int k = idx[p] - k0;
             if (k >= 0 && k < nct) {
-                perm[base[k] + __popc(M[k] & below)] = p;
+                pairs[base[k] + __popc(M[k] & below)] = make_int2(row, p);
             }
         }
     }
 }
 
-// row_idx[q] = the row holding CSR position perm[q] (binary search of the
-// row pointers), vals_t[q] = vals[perm[q]]
+// row_idx[q], perm[q] from the staged pairs; vals_t[q] = vals[perm[q]]
 __global__ __launch_bounds__(256) void csc_finish_kernel(int n_rows, int64_t nnz,
                                                          const int *__restrict__ ptr,
-                                                         const int *__restrict__ perm,
+                                                         const int2 *__restrict__ pairs,
                                                          const float *__restrict__ vals,
                                                          int *__restrict__ row_idx,
+                                                         int *__restrict__ perm,
                                                          float *__restrict__ vals_t) {
     const int64_t n = min(nnz, (int64_t)ptr[n_rows]);  // nnz may be a capacity bound
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n;
          q += (int64_t)gridDim.x * blockDim.x) {
-        const int p = perm[q];
-        int lo = 0, hi = n_rows - 1;  // last row with ptr[row] <= p
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (ptr[mid] <= p) lo = mid; else hi = mid - 1;
-        }
-        row_idx[q] = lo;
-        vals_t[q] = vals[p];
+        const int2 rp = pairs[q];
+        row_idx[q] = rp.x;
+        perm[q] = rp.y;
+        vals_t[q] = vals[rp.y];
     }
 }
 
@@ -152,23 +161,26 @@ __global__ void gather_vals_kernel(int n_cols, const int *__restrict__ col_ptr,
 
 struct csc_layout {
     int n_chunks, ntc;
-    int64_t seg_ints, cnt_ints;
+    int64_t seg_ints, cnt_ints, tot_ints, pair_ints;  // pairs start 8-byte aligned
 };
 
-csc_layout layout(int n_rows, int n_cols) {
+csc_layout layout(int n_rows, int n_cols, int64_t nnz) {
     csc_layout l;
     l.n_chunks = (int)ceil_div(n_rows, kChunkRows);
     l.ntc = (int)ceil_div(n_cols, kTileCols);
     l.seg_ints = (int64_t)n_rows * (l.ntc + 1);
     l.cnt_ints = (int64_t)l.n_chunks * n_cols;
+    l.tot_ints = ((int64_t)n_cols + 2) & ~(int64_t)1;
+    if ((l.seg_ints + l.cnt_ints) & 1) l.tot_ints += 1;
+    l.pair_ints = 2 * nnz;
     return l;
 }
 
 }  // namespace
 
-size_t csc_workspace_bytes(int n_rows, int n_cols) {
-    const csc_layout l = layout(n_rows, n_cols);
-    return sizeof(int) * (size_t)(l.seg_ints + l.cnt_ints + n_cols + 1);
+size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz) {
+    const csc_layout l = layout(n_rows, n_cols, nnz);
+    return sizeof(int) * (size_t)(l.seg_ints + l.cnt_ints + l.tot_ints + l.pair_ints);
 }
 
 hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
@@ -176,10 +188,11 @@ hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr,
                             float *vals_t, void *ws, hipStream_t s) {
     if (n_cols == 0) return launch_fill_i32(col_ptr, 1, 0, s);
     if (n_rows == 0) return launch_fill_i32(col_ptr, (int64_t)n_cols + 1, 0, s);
-    const csc_layout l = layout(n_rows, n_cols);
+    const csc_layout l = layout(n_rows, n_cols, nnz);
     int *seg = static_cast<int *>(ws);
     int *cnt = seg + l.seg_ints;
     int *tot = cnt + l.cnt_ints;
+    int2 *pairs = reinterpret_cast<int2 *>(tot + l.tot_ints);
     hipError_t e = launch_seg(n_rows, l.ntc, kTileShift, ptr, idx, seg, s);
     if (e != hipSuccess) return e;
     dim3 grid(l.n_chunks, l.ntc);
@@ -188,12 +201,12 @@ hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr,
     csc_colscan_kernel<<<(unsigned)ceil_div(n_cols, 256), 256, 0, s>>>(l.n_chunks, n_cols, cnt, tot);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(tot, col_ptr, n_cols, nullptr, s)) != hipSuccess) return e;
-    csc_scatter_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt, col_ptr, perm);
+    csc_scatter_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt, col_ptr, pairs);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (nnz == 0) return hipSuccess;
     int64_t g = ceil_div(nnz, 256);
     if (g > 65536) g = 65536;
-    csc_finish_kernel<<<(unsigned)g, 256, 0, s>>>(n_rows, nnz, ptr, perm, vals, row_idx, vals_t);
+    csc_finish_kernel<<<(unsigned)g, 256, 0, s>>>(n_rows, nnz, ptr, pairs, vals, row_idx, perm, vals_t);
     return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ hipError_t launch_seg(int n_rows, int ntiles, int shift, const int *ptr, const i
                       hipStream_t s);
 
 // csc.hip ------------------------------------------------------------------
-size_t csc_workspace_bytes(int n_rows, int n_cols);
+size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz);
 hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
                             const float *vals, int *col_ptr, int *row_idx, int *perm,
                             float *vals_t, void *ws, hipStream_t s);
@@ -58,6 +58,14 @@ hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *
                              float *Z, int64_t ldz, int *row_counts, hipStream_t s);
 hipError_t launch_prox_csr(int64_t nnz, float *vals, const float *g, float eta, double t,
                            hipStream_t s);
+// fused prox + recompression: per-row counts, then the compacted output
+hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *idx,
+                             const float *vals, const float *G, int64_t ldg, float eta, double t,
+                             int *counts, hipStream_t s);
+hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *idx,
+                            const float *vals, const float *G, int64_t ldg, float eta, double t,
+                            const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
+                            hipStream_t s);
 
 // recompress.hip -----------------------------------------------------------
 hipError_t launch_count_rows(int n_rows, int n_cols, const float *Z, int64_t ldz, float t,

@@ -93,6 +93,137 @@ __global__ void prox_csr_kernel(int64_t nnz, float *__restrict__ vals, const flo
         vals[p] = soft_threshold(vals[p], g[p], eta, t);
 }
 
+
+// Fused prox + recompression, two passes over G without writing Z:
+//   COUNT: counts[row] = number of nonzero S_t(w - eta*g) in the row
+//   FILL:  recompute the same values and compact them into the output CSR at
+//          row_ptr_out[row] (a block-wide prefix per 1024-column chunk: one
+//          ballot per column slot, wave totals through LDS), in column order.
+// One 256-thread workgroup per row; the LDS copy of W's row covers up to
+// kFusedMaxTile columns at once.  A thread issues all of its G loads for the
+// tile and its first W-row entries before waiting on any of them, so a row
+// costs one memory round trip.
+constexpr int kFusedMaxTile = 16384;
+constexpr int kFusedChunks = kFusedMaxTile / (kProxThreads * 4);
+
+template <bool V4, bool FILL>
+__global__ __launch_bounds__(kProxThreads) void prox_rows_kernel(
+    int n_cols, int tile, const int *__restrict__ ptr, const int *__restrict__ idx,
+    const float *__restrict__ vals, const float *__restrict__ G, int64_t ldg, double eta, double t,
+    int *__restrict__ counts, const int *__restrict__ row_ptr_out, int *__restrict__ col_out,
+    float *__restrict__ val_out, int64_t capacity) {
+    extern __shared__ __attribute__((aligned(16))) float wrow[];  // tile floats
+    __shared__ int wave_tot[kProxThreads / kWave];
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int s = ptr[row], e = ptr[row + 1];
+    const float *g = G + (int64_t)row * ldg;
+    int64_t out = FILL ? row_ptr_out[row] : 0;
+    int cnt = 0;
+    for (int k0 = 0; k0 < n_cols; k0 += tile) {
+        const int k1 = min(n_cols, k0 + tile);
+        float4 gq[kFusedChunks];
+#pragma unroll
+        for (int c = 0; c < kFusedChunks; ++c) {
+            const int k = k0 + c * kProxThreads * 4 + tid * 4;
+            if (V4 && k + 3 < k1) {
+                gq[c] = *reinterpret_cast<const float4 *>(g + k);
+            } else {
+                gq[c].x = k + 0 < k1 ? g[k + 0] : 0.f;
+                gq[c].y = k + 1 < k1 ? g[k + 1] : 0.f;
+                gq[c].z = k + 2 < k1 ? g[k + 2] : 0.f;
+                gq[c].w = k + 3 < k1 ? g[k + 3] : 0.f;
+            }
+        }
+        int wi[4];
+        float wv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int p = s + tid + u * kProxThreads;
+            wi[u] = p < e ? idx[p] : -1;
+            wv[u] = p < e ? vals[p] : 0.f;
+        }
+        for (int k = tid * 4; k < tile; k += kProxThreads * 4)
+            *reinterpret_cast<float4 *>(wrow + k) = make_float4(0.f, 0.f, 0.f, 0.f);
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (wi[u] >= k0 && wi[u] < k1) wrow[wi[u] - k0] = wv[u];
+        for (int p = s + tid + 4 * kProxThreads; p < e; p += kProxThreads) {
+            const int k = idx[p];
+            if (k >= k0 && k < k1) wrow[k - k0] = vals[p];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < kFusedChunks; ++c) {
+            const int kb = k0 + c * kProxThreads * 4;
+            if (kb >= k1) continue;  // uniform; keeps gq[c] statically indexed
+            const int k = kb + tid * 4;
+            const float4 w4 = *reinterpret_cast<const float4 *>(wrow + (k - k0));
+            const float wv4[4] = {w4.x, w4.y, w4.z, w4.w};
+            const float gv[4] = {gq[c].x, gq[c].y, gq[c].z, gq[c].w};
+            float o[4];
+            bool keep[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                o[j] = k + j < k1 ? soft_threshold(wv4[j], gv[j], eta, t) : 0.f;
+                keep[j] = o[j] != 0.f;
+                cnt += keep[j];
+            }
+            if (FILL) {
+                uint64_t m[4];
+                int below = 0, wcnt = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    m[j] = wave_ballot(keep[j]);
+                    below += popc_below(m[j]);
+                    wcnt += __popcll(m[j]);
+                }
+                if (lane == 0) wave_tot[wave] = wcnt;
+                __syncthreads();
+                int woff = 0, tot = 0;
+#pragma unroll
+                for (int w = 0; w < kProxThreads / kWave; ++w) {
+                    const int wc = wave_tot[w];
+                    woff += w < wave ? wc : 0;
+                    tot += wc;
+                }
+                int mine = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (keep[j]) {
+                        const int64_t pos = out + woff + below + mine;
+                        if (pos < capacity) {
+                            col_out[pos] = k + j;
+                            val_out[pos] = o[j];
+                        }
+                        ++mine;
+                    }
+                }
+                out += tot;
+                __syncthreads();  // wave_tot is reused by the next chunk
+            }
+        }
+        __syncthreads();  // wrow is reused by the next tile
+    }
+    if (!FILL) {
+        cnt = wave_sum_int(cnt);
+        if (lane == 0) wave_tot[wave] = cnt;
+        __syncthreads();
+        if (tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < kProxThreads / kWave; ++w) tot += wave_tot[w];
+            counts[row] = tot;
+        }
+    }
+}
+
+// LDS row buffer: the whole row when it fits, in whole 1024-column chunks
+int fused_tile(int n_cols) {
+    int tile = (int)ceil_div(n_cols, kProxThreads * 4) * kProxThreads * 4;
+    return tile < kFusedMaxTile ? tile : kFusedMaxTile;
+}
+
 }  // namespace
 
 hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *idx,
@@ -115,6 +246,45 @@ hipError_t launch_prox_csr(int64_t nnz, float *vals, const float *g, float eta, 
     int64_t grid = ceil_div(nnz, 256);
     if (grid > 65536) grid = 65536;
     prox_csr_kernel<<<(unsigned)grid, 256, 0, s>>>(nnz, vals, g, (double)eta, t);
+    return hipGetLastError();
+}
+
+}  // namespace l1csr
+
+namespace l1csr {
+
+hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *idx,
+                             const float *vals, const float *G, int64_t ldg, float eta, double t,
+                             int *counts, hipStream_t s) {
+    if (n_rows == 0) return hipSuccess;
+    const bool v4 = (ldg % 4 == 0) && aligned16(G);
+    const int tile = fused_tile(n_cols);
+    const size_t lds = sizeof(float) * (size_t)tile;
+    if (v4)
+        prox_rows_kernel<true, false><<<n_rows, kProxThreads, lds, s>>>(
+            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+    else
+        prox_rows_kernel<false, false><<<n_rows, kProxThreads, lds, s>>>(
+            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *idx,
+                            const float *vals, const float *G, int64_t ldg, float eta, double t,
+                            const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
+                            hipStream_t s) {
+    if (n_rows == 0) return hipSuccess;
+    const bool v4 = (ldg % 4 == 0) && aligned16(G);
+    const int tile = fused_tile(n_cols);
+    const size_t lds = sizeof(float) * (size_t)tile;
+    if (v4)
+        prox_rows_kernel<true, true><<<n_rows, kProxThreads, lds, s>>>(
+            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, row_ptr_out, col_out,
+            val_out, capacity);
+    else
+        prox_rows_kernel<false, true><<<n_rows, kProxThreads, lds, s>>>(
+            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, row_ptr_out, col_out,
+            val_out, capacity);
     return hipGetLastError();
 }
 

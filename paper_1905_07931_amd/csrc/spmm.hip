@@ -69,14 +69,23 @@ __global__ __launch_bounds__(256) void seg_kernel(int n_rows, int ntiles, int sh
     const int lane = threadIdx.x & 63;
     const int s = ptr[row], e = ptr[row + 1];
     int *sr = seg + (int64_t)row * (ntiles + 1);
-    for (int p = s + lane; p < e; p += kWave) {
-        const int tp = idx[p] >> shift;
-        const int tprev = p > s ? (idx[p - 1] >> shift) : -1;
-        const int tend = tp < ntiles ? tp : ntiles;  // malformed columns stay in bounds
-        for (int t = tprev + 1; t <= tend; ++t) sr[t] = p;
+    // one binary search per tile boundary (lanes over tiles); the result stays
+    // inside [s, e] even for a malformed row
+    for (int t = lane; t <= ntiles; t += kWave) {
+        int lo = s, hi = e;
+        if (t == 0) {
+            hi = s;
+        } else if (t < ntiles) {
+            const int key = t << shift;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (idx[mid] < key) lo = mid + 1; else hi = mid;
+            }
+        } else {
+            lo = e;
+        }
+        sr[t] = lo;
     }
-    const int tlast = e > s ? (idx[e - 1] >> shift) : -1;
-    for (int t = tlast + 1 + lane; t <= ntiles; t += kWave) sr[t] = e;
 }
 
 // pieces of a row: ceil(len / cap), at least one (an empty row is one empty piece)

@@ -263,6 +263,39 @@ def test_prox_dense_and_recompress_bit_exact(shape, eta, lam):
     assert bits_equal(h(out.vals)[:nnz], v)
 
 
+@pytest.mark.parametrize("NK", [(7, 5), (64, 300), (33, 1031), (40, 9000), (5, 20000)])
+def test_prox_l1_recompress_fused_bit_exact(NK):
+    # one call: W - eta*G -> soft threshold -> CSR, against the oracle's prox + recompress;
+    # covers ragged rows (K % 4 != 0) and rows longer than one LDS pass (K > 8192)
+    N, K = NK
+    L = synth.fc_layer(N, K, 4, int(0.1 * N * K), seed=N + K)
+    rng = np.random.default_rng(N * K)
+    G = (rng.standard_normal((N, K)) * 0.05).astype(np.float32)
+    G[0, : min(K, 7)] = 0.0  # zero gradient on some (maybe stored) weights
+    for eta, lam in [(0.01, 1e-4), (0.5, 0.3)]:
+        out = L1.prox_l1_recompress(_W(L), t(G), eta, lam)
+        Zr, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, G, eta, lam, K)
+        rp, ci, v = oracle.recompress(Zr)
+        n = int(rp[-1])
+        assert bits_equal(h(out.row_ptr), rp)
+        assert bits_equal(h(out.col_idx)[:n], ci) and bits_equal(h(out.vals)[:n], v)
+
+
+def test_prox_l1_recompress_capacity():
+    L = synth.fc_layer(30, 50, 4, 150, seed=3)
+    rng = np.random.default_rng(3)
+    G = (rng.standard_normal((30, 50)) * 0.05).astype(np.float32)
+    Zr, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, G, 0.5, 0.05, 50)
+    need = int(np.count_nonzero(Zr))
+    with pytest.raises(L1.L1CSRError) as ei:
+        L1.prox_l1_recompress(_W(L), t(G), 0.5, 0.05, capacity=need - 1)
+    assert ei.value.status == L1.ECAPACITY
+    out = L1.prox_l1_recompress(_W(L), t(G), 0.5, 0.05, capacity=need)
+    assert out.nnz == need
+    rp, ci, v = oracle.recompress(Zr)
+    assert bits_equal(h(out.col_idx)[:need], ci) and bits_equal(h(out.vals)[:need], v)
+
+
 def test_prox_dense_in_place_and_threshold_ties():
     L = synth.dyadic_layer(64, 300, 64, 4000, seed=7, empty_rows=(3,), full_rows=(9,))
     dW = oracle.dense_wgrad(L.dY, L.X)
