@@ -1,0 +1,155 @@
+"""Host-side checks of the C ABI: the built library exports every function the
+header declares, the status strings and workspace sizes, and argument
+validation (calls that must return L1CSR_EINVAL before launching anything).
+
+No call here launches a kernel.  The validation calls run only on a machine
+without a GPU device node, so that a validation mistake can never reach a
+kernel with the placeholder pointers used here.
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "l1csr.h")
+LIB = os.path.join(ROOT, "paper_1905_07931_amd", "libl1csr.so")
+
+OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED = 0, -1, -2, -4, -5
+NO_GPU = not os.path.exists("/dev/kfd")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?(?:int|size_t|char)\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_1905_07931_amd import build
+        build.build(verbose=False)
+    lib = C.CDLL(LIB)
+    lib.l1csr_status_str.restype = C.c_char_p
+    lib.l1csr_status_str.argtypes = [C.c_int]
+    lib.l1csr_workspace_bytes.restype = C.c_size_t
+    lib.l1csr_workspace_bytes.argtypes = [C.c_int, C.c_int32, C.c_int32, C.c_int64, C.c_int32]
+    return lib
+
+
+def test_header_declares_the_hot_path_calls():
+    names = declared_functions()
+    for n in ["csr_spmm_fwd", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad", "prox_l1_step",
+              "csr_recompress", "prox_l1_recompress", "csc_build", "csc_update_vals", "csr_compact",
+              "l1csr_workspace_bytes", "l1csr_status_str"]:
+        assert n in names, n
+
+
+def test_library_exports_every_declared_function(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(lib):
+    seen = set()
+    for code in (OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED):
+        s = lib.l1csr_status_str(code).decode()
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 5
+    assert lib.l1csr_status_str(12345).decode() == "unknown status"
+
+
+def test_workspace_sizes(lib):
+    ws = lib.l1csr_workspace_bytes
+    assert ws(99, 10, 10, 10, 10) == 0                 # unknown op
+    assert ws(1, -1, 10, 10, 10) == 0                  # negative size
+    for op in range(1, 8):
+        for dims in [(1, 1, 1, 1), (300, 784, 23520, 64), (4096, 9216, 3397386, 1024)]:
+            b = ws(op, *dims)
+            assert b % 256 == 0, (op, dims, b)
+    # the sizes grow with the problem
+    assert ws(1, 4096, 9216, 3397386, 0) >= ws(1, 300, 784, 23520, 0) > 0
+    assert ws(4, 4096, 9216, 3397386, 1024) > ws(4, 4096, 300, 61440, 1024) > 0
+    assert ws(3, 4096, 9216, 3397386, 1024) > 0
+    assert ws(2, 4096, 9216, 0, 0) >= 4 * 4097
+    assert ws(7, 4096, 9216, 0, 0) >= 4 * 4097
+
+
+P = C.c_void_p(4096)  # placeholder non-null pointer; never dereferenced by a rejected call
+NUL = None
+S = None              # default stream
+
+
+def _f(x):
+    return C.c_float(x)
+
+
+def _setup(lib):
+    lib.csr_spmm_fwd.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
+                                 C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
+                                 C.c_size_t, C.c_void_p]
+    lib.dense_wgrad.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
+                                C.c_int64, C.c_void_p, C.c_int64, C.c_void_p]
+    lib.prox_l1_step.argtypes = [C.c_int, C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
+                                 C.c_void_p, C.c_void_p, C.c_int64, C.c_float, C.c_float, C.c_void_p,
+                                 C.c_int64, C.c_void_p, C.c_void_p]
+    lib.csr_recompress.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_float, C.c_void_p,
+                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p,
+                                   C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.prox_l1_recompress.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
+                                       C.c_void_p, C.c_void_p, C.c_int64, C.c_float, C.c_float,
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p,
+                                       C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.sddmm_masked_wgrad.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
+                                       C.c_void_p, C.c_int64, C.c_void_p, C.c_int64, C.c_int32,
+                                       C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.csc_build.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
+                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                              C.c_void_p]
+    lib.csr_spmm_bwd_t.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
+                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                   C.c_int64, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
+                                   C.c_size_t, C.c_void_p]
+
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_invalid_arguments_are_rejected_before_launch(lib):
+    _setup(lib)
+    # SpMM: negative size, missing pointer, short leading dimension, nnz > N*K, short workspace
+    assert lib.csr_spmm_fwd(-1, 4, 0, P, P, P, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
+    assert lib.csr_spmm_fwd(4, 4, 3, NUL, P, P, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
+    assert lib.csr_spmm_fwd(4, 4, 3, P, P, P, P, 7, 8, P, 8, NUL, 0, S) == EINVAL
+    assert lib.csr_spmm_fwd(4, 4, 3, P, P, P, P, 8, 8, P, 7, NUL, 0, S) == EINVAL
+    assert lib.csr_spmm_fwd(4, 4, 17, P, P, P, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
+    assert lib.l1csr_workspace_bytes(4, 4096, 300, 61440, 1024) > 1
+    assert lib.csr_spmm_fwd(4096, 300, 61440, P, P, P, P, 1024, 1024, P, 1024, P, 1, S) == EINVAL
+    # dense dW: short ld, missing output
+    assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, S) == EINVAL
+    # prox: non-finite or negative eta / lambda, bad mode
+    nan, inf = float("nan"), float("inf")
+    for eta, lam in [(nan, 0.1), (0.1, nan), (inf, 0.1), (0.1, -1.0), (-0.1, 0.1)]:
+        assert lib.prox_l1_step(0, 4, 4, 3, P, P, P, P, 4, eta, lam, P, 4, NUL, S) == EINVAL
+    assert lib.prox_l1_step(7, 4, 4, 3, P, P, P, P, 4, 0.1, 0.1, P, 4, NUL, S) == EINVAL
+    assert lib.prox_l1_step(0, 4, 4, 3, P, P, P, P, 3, 0.1, 0.1, P, 4, NUL, S) == EINVAL
+    # recompress: non-finite threshold, missing outputs, short workspace
+    assert lib.csr_recompress(4, 4, P, 4, nan, NUL, P, P, P, 16, NUL, NUL, P, 4096, S) == EINVAL
+    assert lib.csr_recompress(4, 4, P, 4, 0.0, NUL, NUL, P, P, 16, NUL, NUL, P, 4096, S) == EINVAL
+    assert lib.csr_recompress(4, 4, P, 4, 0.0, NUL, P, P, P, 16, NUL, NUL, P, 1, S) == EINVAL
+    # fused prox + recompress: output aliasing the input CSR, short workspace
+    assert lib.prox_l1_recompress(4, 4, 3, P, P, P, P, 4, 0.1, 0.1, P, P, P, 16, NUL, NUL, P, 4096,
+                                  S) == EINVAL
+    Q = C.c_void_p(8192)
+    assert lib.prox_l1_recompress(4, 4, 3, P, P, P, P, 4, 0.1, 0.1, Q, Q, Q, 16, NUL, NUL, P, 1,
+                                  S) == EINVAL
+    # SDDMM: missing output
+    assert lib.sddmm_masked_wgrad(4, 4, 3, P, P, P, 8, P, 8, 8, NUL, P, 1 << 20, S) == EINVAL
+    # CSC build: missing workspace
+    assert lib.csc_build(4, 4, 3, P, P, P, P, P, P, P, NUL, 0, S) == EINVAL
+    # backward: half a CSC (row_idx without col_ptr)
+    assert lib.csr_spmm_bwd_t(4, 4, 3, P, P, P, NUL, P, NUL, P, 8, 8, P, 8, NUL, 0, S) == EINVAL

@@ -1,0 +1,369 @@
+"""Whole training steps of the paper's layer shapes on the GPU, against the oracle.
+
+Each step chains the ABI calls the way a training loop does (forward, CSC,
+backward, weight gradient, proximal step, recompression, and the debiasing
+step on a fixed pattern, Sections 2.3-2.4 and 3.1-3.3).  Every stage is
+compared with the oracle applied to that stage's GPU inputs:
+  - sums (products, gradients): |gpu - oracle| <= 1e-4 * m, m = sum |a_k b_k|;
+  - prox / recompression / compaction / ReLU: bit-exact (fed the GPU's own
+    gradient, so the comparison is well posed);
+  - structure (row pointers, column indices, CSC): bit-exact.
+For the single-layer l1 steps the fully independent oracle step (its own
+gradient) is also run: every entry where its new pattern differs from the
+GPU's must lie in the rounding band of the threshold, | |z| - eta*lambda | <=
+eta * 1e-4 * m_ik, with z = w - eta*g and m_ik = sum_b |dY[i,b] X[k,b]|.
+
+At the full sizes (4096 x 9216, batch 1024; 4096 x 4096, batch 512) products
+are checked on a seeded sample of output rows / columns that the oracle
+computes one by one; the prox and recompression are checked in full.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1905_07931_amd as L1
+from paper_1905_07931_amd import synth
+
+from _helpers import TOL, assert_scaled_close, bits_equal, csc_reference, cuda, h, t
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ----------------------------------------------------------------------------
+# oracle-side checks of one stage
+# ----------------------------------------------------------------------------
+
+def rows_of(rp, ci, v, rows):
+    """The CSR of a subset of rows (in the given order)."""
+    rp = np.asarray(rp, np.int64)
+    lens = np.array([rp[r + 1] - rp[r] for r in rows], np.int64)
+    sub_rp = np.zeros(len(rows) + 1, np.int32)
+    sub_rp[1:] = np.cumsum(lens)
+    if lens.sum() == 0:
+        return sub_rp, np.zeros(0, np.int32), np.zeros(0, np.float32)
+    sub_ci = np.concatenate([ci[rp[r]:rp[r + 1]] for r in rows]).astype(np.int32)
+    sub_v = np.concatenate([v[rp[r]:rp[r + 1]] for r in rows]).astype(np.float32)
+    return sub_rp, sub_ci, sub_v
+
+
+def check_fwd(W, X, Y, rows=None, what="Y"):
+    rp, ci, v = W
+    if rows is not None:
+        rp, ci, v = rows_of(rp, ci, v, rows)
+        Y = Y[rows]
+    ref = oracle.spmm_fwd(rp, ci, v, X)
+    m = oracle.spmm_fwd(rp, ci, np.abs(v), np.abs(X))
+    assert_scaled_close(Y, ref, m, what=what)
+
+
+def transposed_rows(rp, ci, v, cols):
+    """Rows `cols` of W^T as a CSR (each in ascending row order of W)."""
+    ci = np.asarray(ci)
+    flag = np.zeros(int(ci.max()) + 1 if len(ci) else 1, bool)
+    flag[[c for c in cols if c < len(flag)]] = True
+    sel = np.nonzero(flag[ci])[0] if len(ci) else np.zeros(0, np.int64)
+    r = np.searchsorted(np.asarray(rp, np.int64), sel, side="right") - 1
+    c = ci[sel]
+    sub_rp = np.zeros(len(cols) + 1, np.int32)
+    parts_r, parts_v = [], []
+    for j, k in enumerate(cols):
+        m = c == k
+        parts_r.append(r[m])
+        parts_v.append(np.asarray(v)[sel[m]])
+        sub_rp[j + 1] = sub_rp[j] + int(m.sum())
+    return (sub_rp, np.concatenate(parts_r).astype(np.int32) if parts_r else np.zeros(0, np.int32),
+            np.concatenate(parts_v).astype(np.float32) if parts_v else np.zeros(0, np.float32))
+
+
+def check_bwd(W, K, dY, dX, cols=None, what="dX"):
+    rp, ci, v = W
+    if cols is None:
+        ref = oracle.spmm_bwd_t(rp, ci, v, dY, K)
+        m = oracle.spmm_bwd_t(rp, ci, np.abs(v), np.abs(dY), K)
+        assert_scaled_close(dX, ref, m, what=what)
+        return
+    WT = transposed_rows(rp, ci, v, cols)
+    ref = oracle.spmm_fwd(*WT, dY)
+    m = oracle.spmm_fwd(WT[0], WT[1], np.abs(WT[2]), np.abs(dY))
+    assert_scaled_close(dX[cols], ref, m, what=what)
+
+
+def check_dw(dY, X, dW, rows=None, what="dW"):
+    if rows is not None:
+        dY, dW = dY[rows], dW[rows]
+    ref = oracle.dense_wgrad(dY, X)
+    m = oracle.dense_wgrad(np.abs(dY), np.abs(X))
+    assert_scaled_close(dW, ref, m, what=what)
+
+
+def check_sddmm(W, dY, X, gv, rows=None, what="gv"):
+    rp, ci, _ = W
+    if rows is not None:
+        rp64 = np.asarray(rp, np.int64)
+        gv = np.concatenate([gv[rp64[r]:rp64[r + 1]] for r in rows]) if len(rows) else gv[:0]
+        rp, ci, _ = rows_of(rp, ci, np.zeros(len(ci), np.float32), rows)
+        dY = dY[rows]
+    ref = oracle.sddmm(rp, ci, dY, X)
+    m = oracle.sddmm(rp, ci, np.abs(dY), np.abs(X))
+    assert_scaled_close(gv, ref, m, what=what)
+
+
+def check_prox_recompress(W, dW, eta, lam, K, out):
+    """The GPU's new CSR equals the oracle's prox + recompression of the GPU's dW, bit for bit."""
+    rp, ci, v = W
+    Z, _ = oracle.prox_dense(rp, ci, v, dW, eta, lam, K)
+    rpn, cin, vn = oracle.recompress(Z)
+    n = int(rpn[-1])
+    assert out.host_nnz() == n
+    assert bits_equal(h(out.row_ptr), rpn), "row_ptr"
+    assert bits_equal(h(out.col_idx)[:n], cin), "col_idx"
+    assert bits_equal(h(out.vals)[:n], vn), "vals"
+    return rpn, cin, vn
+
+
+def independent_band_check(W, dY, X, eta, lam, K, new_W):
+    """Pattern of the fully independent oracle step vs the GPU's: every
+    difference lies in the rounding band of the threshold.  Returns the count."""
+    rp, ci, v = W
+    dWr = oracle.dense_wgrad(dY, X)
+    Zi, _ = oracle.prox_dense(rp, ci, v, dWr, eta, lam, K)
+    mask_i = Zi != 0
+    N = len(rp) - 1
+    mask_g = np.zeros((N, K), bool)
+    rows_g = np.repeat(np.arange(N), np.diff(np.asarray(new_W[0], np.int64)))
+    mask_g[rows_g, new_W[1]] = True
+    diff = np.argwhere(mask_i != mask_g)
+    if len(diff):
+        Wd = oracle.densify(rp, ci, v, K)
+        thr = np.float64(eta) * np.float64(lam)
+        for i, k in diff:
+            z = np.float64(Wd[i, k]) - np.float64(eta) * np.float64(dWr[i, k])
+            m = np.sum(np.abs(dY[i].astype(np.float64)) * np.abs(X[k].astype(np.float64)))
+            assert abs(abs(z) - thr) <= eta * TOL * m, (int(i), int(k), z, thr, m)
+    return len(diff)
+
+
+# ----------------------------------------------------------------------------
+# single-layer l1 steps
+# ----------------------------------------------------------------------------
+
+def l1_step(L, W, host, rows=None, cols=None, band=True):
+    """fwd, CSC, bwd, dense dW, prox + recompress; every stage checked."""
+    X, dY = L.X, L.dY
+    Xg, dYg = t(X), t(dY)
+    Y = L1.csr_spmm_fwd(W, Xg)
+    csc = L1.csc_build(W)
+    dX = L1.csr_spmm_bwd_t(W, dYg, csc)
+    dW = L1.dense_wgrad(dYg, Xg)
+    out = L1.prox_l1_recompress(W, dW, L.eta, L.lam)
+    dWh = h(dW)
+    check_fwd(host, X, h(Y), rows)
+    col_ptr, row_idx, perm = csc_reference(host[0], host[1], L.K)
+    n = int(host[0][-1])
+    assert bits_equal(h(csc.col_ptr), col_ptr)
+    assert bits_equal(h(csc.row_idx)[:n], row_idx) and bits_equal(h(csc.perm)[:n], perm)
+    check_bwd(host, L.K, dY, h(dX), cols)
+    check_dw(dY, X, dWh, rows)
+    new = check_prox_recompress(host, dWh, L.eta, L.lam, L.K, out)
+    n_band = independent_band_check(host, dY, X, L.eta, L.lam, L.K, new) if band else None
+    return out, new, n_band
+
+
+def test_fc784x300_l1_step():
+    L = synth.fc784_300(seed=0)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+    out, new, n_band = l1_step(L, W, (L.row_ptr, L.col_idx, L.vals))
+    # almost every zero weight has |dW| > lambda here, so the layer regrows nearly dense
+    assert int(new[0][-1]) > 0.99 * L.N * L.K
+    assert n_band <= 10
+
+
+def test_fc9216x4096_zipf_l1_step_full_size():
+    L = synth.fc9216_4096(seed=0)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+    rng = np.random.default_rng(90)
+    # sampled rows include the longest (dense) rows and some of the shortest
+    lens = np.diff(L.row_ptr)
+    order = np.argsort(lens)
+    rows = np.unique(np.concatenate([order[-8:], order[:8], rng.choice(L.N, 48, replace=False)]))
+    cols = rng.choice(L.K, 64, replace=False)
+    out, new, n_band = l1_step(L, W, (L.row_ptr, L.col_idx, L.vals), rows=rows, cols=cols)
+    assert n_band <= 1e-5 * L.N * L.K
+
+
+def test_empty_layer_regrows_then_empties():
+    """nnz = 0: the products are zero; the prox grows entries with |eta*g| > eta*lambda.
+    A lambda above every |g| then deletes the whole layer (an empty CSR)."""
+    L = synth.fc_layer(70, 90, 33, 0, seed=31)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+    out, new, _ = l1_step(L, W, (L.row_ptr, L.col_idx, L.vals))
+    assert 0 < int(new[0][-1]) <= L.N * L.K
+    big = synth.fc_layer(70, 90, 33, 0, seed=31)
+    big.lam = 1e6
+    out2, new2, _ = l1_step(big, out, new)
+    assert int(new2[0][-1]) == 0 and not np.any(new2[0])
+    # and a step on the empty result works again
+    out3, new3, _ = l1_step(L, out2, new2)
+    assert int(new3[0][-1]) == int(new[0][-1])
+
+
+# ----------------------------------------------------------------------------
+# MLP 784-300-100-10: l1-phase step, then a debiasing step
+# ----------------------------------------------------------------------------
+
+def test_mlp_784_300_100_10_l1_then_debias_step():
+    layers, X, labels = synth.mlp_784_300_100_10(seed=0)
+    B = X.shape[1]
+    eta, lam = 0.01, 1e-4
+    dev = cuda()
+    Ws = [L1.CSR.from_host(Lj.row_ptr, Lj.col_idx, Lj.vals, Lj.K, device=dev) for Lj in layers]
+    host = [(Lj.row_ptr, Lj.col_idx, Lj.vals) for Lj in layers]
+    Xg, lab = t(X), t(labels)
+
+    def forward():
+        inputs, pre = [Xg], []
+        for j, W in enumerate(Ws):
+            A = L1.csr_spmm_fwd(W, inputs[-1])
+            check_fwd(host[j], h(inputs[-1]), h(A), what=f"A{j + 1}")
+            pre.append(A)
+            if j < 2:
+                H = L1.relu_fwd(A)
+                assert bits_equal(h(H), oracle.relu_fwd(h(A)))
+                inputs.append(H)
+        return inputs, pre
+
+    def backward(inputs, pre):
+        loss, dZ = L1.softmax_xent(pre[2], lab)
+        lr, dzr = oracle.softmax_xent(h(pre[2]), labels)
+        assert abs(float(h(loss)[0]) - lr) <= 1e-5 * max(1.0, abs(lr))
+        assert np.max(np.abs(h(dZ) - dzr)) <= 1e-5 / B
+        deltas = [None, None, dZ]
+        for j in (2, 1):
+            csc = L1.csc_build(Ws[j])
+            dH = L1.csr_spmm_bwd_t(Ws[j], deltas[j], csc)
+            check_bwd(host[j], Ws[j].n_cols, h(deltas[j]), h(dH), what=f"dH{j}")
+            dA = L1.relu_bwd(pre[j - 1], dH)
+            assert bits_equal(h(dA), oracle.relu_bwd(h(pre[j - 1]), h(dH)))
+            deltas[j - 1] = dA
+        return lr, deltas
+
+    # l1 phase
+    inputs, pre = forward()
+    loss0, deltas = backward(inputs, pre)
+    assert np.isfinite(loss0)
+    for j in range(3):
+        dW = L1.dense_wgrad(deltas[j], inputs[j])
+        dWh = h(dW)
+        check_dw(h(deltas[j]), h(inputs[j]), dWh, what=f"dW{j + 1}")
+        out = L1.prox_l1_recompress(Ws[j], dW, eta, lam)
+        host[j] = check_prox_recompress(host[j], dWh, eta, lam, Ws[j].n_cols, out)
+        Ws[j] = out
+    # debiasing: gradient on the pattern, SGD, pattern unchanged
+    inputs, pre = forward()
+    loss1, deltas = backward(inputs, pre)
+    assert np.isfinite(loss1)
+    for j in range(3):
+        W = Ws[j]
+        nnz = W.host_nnz()
+        gv = L1.sddmm_masked_wgrad(W, deltas[j], inputs[j])
+        gvh = h(gv)[:nnz]
+        check_sddmm(host[j], h(deltas[j]), h(inputs[j]), gvh, what=f"gv{j + 1}")
+        L1.prox_l1_step(L1.PROX_CSR, W, gv, eta, 0.0)
+        ref = oracle.prox_csr(host[j][2], gvh, eta, 0.0)
+        assert bits_equal(h(W.vals)[:nnz], ref)
+        assert bits_equal(h(W.row_ptr), host[j][0]) and bits_equal(h(W.col_idx)[:nnz], host[j][1])
+        host[j] = (host[j][0], host[j][1], ref)
+
+
+# ----------------------------------------------------------------------------
+# LeNet-5 conv2 lowered by im2col: masked gradient over 16384 columns, CSR prox
+# ----------------------------------------------------------------------------
+
+def test_conv2_im2col_step():
+    L = synth.conv2_im2col(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    host = (L.row_ptr, L.col_idx, L.vals)
+    Xg, dYg = t(L.X), t(L.dY)
+    Y = L1.csr_spmm_fwd(W, Xg)
+    check_fwd(host, L.X, h(Y))
+    csc = L1.csc_build(W)
+    dX = L1.csr_spmm_bwd_t(W, dYg, csc)
+    check_bwd(host, L.K, L.dY, h(dX))
+    gv = L1.sddmm_masked_wgrad(W, dYg, Xg)
+    gvh = h(gv)[: L.nnz]
+    check_sddmm(host, L.dY, L.X, gvh)
+    L1.prox_l1_step(L1.PROX_CSR, W, gv, L.eta, L.lam)
+    ref = oracle.prox_csr(L.vals, gvh, L.eta, L.lam)
+    assert bits_equal(h(W.vals)[: L.nnz], ref)
+    C = L1.csr_compact(W)
+    rp, ci, v = oracle.compact(L.row_ptr, L.col_idx, ref)
+    assert bits_equal(h(C.row_ptr), rp)
+    assert bits_equal(h(C.col_idx)[: rp[-1]], ci) and bits_equal(h(C.vals)[: rp[-1]], v)
+
+
+# ----------------------------------------------------------------------------
+# FC 4096 x 4096, batch 512: 20 alternating l1 / debiasing iterations
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("pct", [1, 5, 20, 50])
+def test_fc4096_density_sweep_alternating_steps(pct):
+    cal = json.load(open(os.path.join(GOLDEN, "fc4096_lambda.json")))
+    lam = cal["lambda"][str(pct)]
+    L = synth.fc4096_sweep(pct / 100)
+    eta, N, K = L.eta, L.N, L.K
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=cuda())
+    host = (L.row_ptr, L.col_idx, L.vals)
+    rng = np.random.default_rng(4096 + pct)
+    csc = None
+    history = []
+    for it in range(20):
+        X, dY = synth.fc4096_batch(it)
+        Xg, dYg = t(X), t(dY)
+        rows = rng.choice(N, 32, replace=False)
+        cols = rng.choice(K, 32, replace=False)
+        if it % 2 == 0:
+            # l1 step; the CSC of this pattern was built at the previous (debiasing) step
+            csc = L1.csc_build(W) if csc is None else L1.csc_update_vals(W, csc)
+            Y = L1.csr_spmm_fwd(W, Xg)
+            dX = L1.csr_spmm_bwd_t(W, dYg, csc)
+            dW = L1.dense_wgrad(dYg, Xg)
+            out = L1.prox_l1_recompress(W, dW, eta, lam)
+            dWh = h(dW)
+            check_fwd(host, X, h(Y), rows, what=f"Y it{it}")
+            check_bwd(host, K, dY, h(dX), cols, what=f"dX it{it}")
+            check_dw(dY, X, dWh, rows, what=f"dW it{it}")
+            new = check_prox_recompress(host, dWh, eta, lam, K, out)
+            if it == 0:
+                old = oracle.densify(*host, K) != 0
+                flips = np.count_nonzero((oracle.densify(*new, K) != 0) != old)
+                assert abs(flips / L.nnz - 0.02) < 0.002, flips / L.nnz
+            W, host = out, new
+        else:
+            # debiasing step on the new pattern: CSC rebuilt, masked gradient, SGD
+            csc = L1.csc_build(W)
+            nnz = W.host_nnz()
+            if it == 1:
+                col_ptr, row_idx, perm = csc_reference(host[0], host[1], K)
+                assert bits_equal(h(csc.col_ptr), col_ptr) and bits_equal(h(csc.perm)[:nnz], perm)
+            Y = L1.csr_spmm_fwd(W, Xg)
+            dX = L1.csr_spmm_bwd_t(W, dYg, csc)
+            gv = L1.sddmm_masked_wgrad(W, dYg, Xg)
+            gvh = h(gv)[:nnz]
+            check_fwd(host, X, h(Y), rows, what=f"Y it{it}")
+            check_bwd(host, K, dY, h(dX), cols, what=f"dX it{it}")
+            check_sddmm(host, dY, X, gvh, rows, what=f"gv it{it}")
+            L1.prox_l1_step(L1.PROX_CSR, W, gv, eta, 0.0)
+            ref = oracle.prox_csr(host[2], gvh, eta, 0.0)
+            assert bits_equal(h(W.vals)[:nnz], ref)
+            assert bits_equal(h(W.col_idx)[:nnz], host[1])
+            host = (host[0], host[1], ref)
+        history.append(int(host[0][-1]))
+    # the pattern changes by a few percent per l1 step, not wholesale
+    for a, b in zip(history[::2], history[2::2]):
+        assert abs(b - a) <= 0.25 * max(a, 1)
