@@ -1,28 +1,35 @@
 // CSR x dense products with the batch index contiguous (forward Y = W.X and,
 // over the CSC copy, backward dX = W^T.dY).
 //
-// Tiled kernel (the hot path).  A 1024-thread workgroup owns a chunk of
-// 64*VEC batch columns and a set of rows; each wave keeps up to MAXRW rows x
-// VEC accumulators per lane in registers.  The dense operand is staged
-// through LDS in 64 KB tiles (KT rows x 64*VEC columns); for each tile every
-// wave walks the tile's segment of each of its rows: the (column, value)
-// pairs of a segment are loaded by the lanes (coalesced, the next row's pairs
-// in flight while the current row computes), written to a per-wave LDS slot
-// and read back as broadcasts, and each nonzero costs one LDS read of the X
-// row (lanes over the batch, conflict-free) and VEC fused multiply-adds.
+// Streamed tiled kernel (the hot path).  One 1024-thread workgroup per CU owns
+// a chunk of BB = 64*VEC batch columns and a set of rows; every lane keeps VEC
+// accumulators for each of the wave's row pieces.  The dense operand passes
+// through LDS in 64 KB tiles of KT rows, double buffered: while the waves work
+// on tile t, the direct global->LDS loads of tile t+1 are in flight.
 //
-// Load balance (power-law row lengths): a row longer than the average wave
-// load is cut into "pieces" of at most that length; pieces are sorted by
-// length (bucketed) and dealt to the waves in snake order, so every wave gets
-// about the same number of nonzeros.  A row's pieces are summed by a fix-up
-// pass in piece order, and every piece is summed by one wave in CSR order,
-// so the result does not depend on the schedule.  The grid is exactly two
-// workgroups per CU, mapped so that the workgroups resident on one XCD share
-// a batch chunk (the same slice of X in that XCD's L2).
+// The nonzeros are not read from the CSR arrays inside the kernel.  A
+// planning pass writes, for every wave and tile, a chunk of a "pair stream":
+// a header with the pair count of each of the wave's pieces in the tile, then
+// the pairs (byte offset of the X row inside the tile, value), each piece's
+// run padded to an even count with a zero pair.  The wave's chunk of tile t+1
+// is loaded into LDS together with X, so the inner loop reads two pairs with
+// one broadcast LDS read and then two X rows, with no global latency and no
+// per-segment bookkeeping.  A chunk longer than its LDS slot is finished from
+// global memory.
 //
-// Rows kernel (small or very sparse operands, where a workgroup would use few
-// of a staged tile's X rows): one wave per (row, batch chunk) reading X
-// directly from the cache hierarchy.
+// Load balance (power-law row lengths): a row longer than half the mean wave
+// load is cut into k pieces, piece j taking every k-th nonzero of the row, so
+// a piece of a dense row spreads evenly over the tiles (contiguous pieces
+// would pile one wave's work into a few tiles and stall the workgroup at
+// every tile barrier).  Pieces are sorted by length (bucketed) and dealt to
+// the waves in snake order.  A split row's pieces write partial rows that a
+// fix-up pass sums in piece order; every piece is summed by one wave in a
+// fixed order, so the result does not depend on the schedule.  The grid maps
+// blocks to XCDs so that the workgroups of one XCD share a batch chunk (the
+// same slice of X in that XCD's L2).
+//
+// Rows kernel (small, narrow or very sparse operands): one wave per (row,
+// batch chunk) reading X directly from the cache hierarchy.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -55,7 +62,7 @@ __device__ __forceinline__ void store_vec(float *p, const float (&x)[VEC]) {
 }
 
 // ---------------------------------------------------------------------------
-// planning: segment pointers, pieces, length order
+// planning: segment pointers, pieces, length order, pair stream
 // ---------------------------------------------------------------------------
 
 // seg[row][t] = first position p of the row with idx[p] >= t << shift
@@ -97,16 +104,19 @@ __global__ void piece_count_kernel(int n_rows, const int *__restrict__ ptr, int 
     }
 }
 
-// piece descriptors (row, first position, end position, row is split)
+// piece v = (row, first position of the row, j, k): every k-th entry of the
+// row starting at its j-th
 __global__ void piece_fill_kernel(int n_rows, const int *__restrict__ ptr,
                                   const int *__restrict__ pbeg, int4 *__restrict__ piece) {
     for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < n_rows; r += gridDim.x * blockDim.x) {
-        const int s = ptr[r], len = ptr[r + 1] - s;
         const int v0 = pbeg[r], k = pbeg[r + 1] - v0;
-        for (int j = 0; j < k; ++j)
-            piece[v0 + j] = make_int4(r, s + (int)((int64_t)len * j / k),
-                                      s + (int)((int64_t)len * (j + 1) / k), k > 1);
+        for (int j = 0; j < k; ++j) piece[v0 + j] = make_int4(r, ptr[r], j, k);
     }
+}
+
+// entries of a piece (row length len): positions j, j + k, ... < len
+__device__ __forceinline__ int piece_len(int len, int j, int k) {
+    return len > j ? (len - j + k - 1) / k : 0;
 }
 
 constexpr int kBuckets = 129;  // 4 buckets per octave of the piece length, plus empty
@@ -121,6 +131,7 @@ __device__ __forceinline__ int length_key(int len) {
 // order[] = pieces by decreasing length bucket (order inside a bucket is
 // arbitrary: it only decides which wave computes a piece)
 __global__ __launch_bounds__(1024) void order_kernel(const int *__restrict__ n_pieces_ptr,
+                                                     const int *__restrict__ ptr,
                                                      const int4 *__restrict__ piece,
                                                      int *__restrict__ order) {
     __shared__ int hist[kBuckets];
@@ -129,7 +140,10 @@ __global__ __launch_bounds__(1024) void order_kernel(const int *__restrict__ n_p
     const int tid = threadIdx.x;
     for (int k = tid; k < kBuckets; k += blockDim.x) hist[k] = 0;
     __syncthreads();
-    for (int v = tid; v < n; v += blockDim.x) atomicAdd(&hist[length_key(piece[v].z - piece[v].y)], 1);
+    for (int v = tid; v < n; v += blockDim.x) {
+        const int4 pc = piece[v];
+        atomicAdd(&hist[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1);
+    }
     __syncthreads();
     if (tid == 0) {
         int run = 0;
@@ -139,25 +153,191 @@ __global__ __launch_bounds__(1024) void order_kernel(const int *__restrict__ n_p
         }
     }
     __syncthreads();
-    for (int v = tid; v < n; v += blockDim.x)
-        order[atomicAdd(&start[length_key(piece[v].z - piece[v].y)], 1)] = v;
+    for (int v = tid; v < n; v += blockDim.x) {
+        const int4 pc = piece[v];
+        order[atomicAdd(&start[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1)] = v;
+    }
 }
 
-// ---------------------------------------------------------------------------
-// tiled kernel
-// ---------------------------------------------------------------------------
-
 constexpr int kNW = 16;             // waves per workgroup (1024 threads)
-constexpr int kTileFloats = 16384;  // 64 KB of X per tile: two workgroups per CU
+constexpr int kTileFloats = 16384;  // 64 KB of X per tile buffer
+constexpr int kChunk = 1024;        // bytes of a wave's pair stream staged per tile
 
 template <int VEC>
 struct tiled_cfg {
     static constexpr int BB = kWave * VEC;       // batch columns per workgroup
     static constexpr int KT = kTileFloats / BB;  // X rows per tile
-    static constexpr int SHIFT = VEC == 1 ? 8 : (VEC == 2 ? 7 : 6);
-    static constexpr int MAXRW = VEC == 1 ? 16 : (VEC == 2 ? 12 : 8);  // pieces per wave in registers
+    static constexpr int SHIFT = VEC == 2 ? 7 : 6;
+    static constexpr int MAXRW = VEC == 2 ? 24 : 12;          // pieces per wave in registers
+    static constexpr int HDR = ((2 * MAXRW + 15) / 16) * 16;  // chunk header: uint16 count per piece
     static_assert((1 << SHIFT) == KT, "tile height must be a power of two");
 };
+
+// the piece in slot i of wave g: sorted position i*nw + g, snake order over rounds
+__device__ __forceinline__ int slot_piece(int i, int g, int nw, int rw, int n_pieces,
+                                          const int *__restrict__ order) {
+    const int64_t j = (int64_t)i * nw + ((i & 1) ? (nw - 1 - g) : g);
+    return (i < rw && j < n_pieces) ? order[j] : -1;
+}
+
+// strided position bound of a piece in a tile: the number of its entries
+// (positions first + j + m*k, m = 0, 1, ...) that lie before position p
+__device__ __forceinline__ int piece_before(int p, int first, int j, int k, int plen) {
+    const int d = p - first - j;
+    if (d <= 0) return 0;
+    const int m = k == 1 ? d : (d + k - 1) / k;
+    return m < plen ? m : plen;
+}
+
+// per (wave, tile): bytes of the stream chunk (header + padded pair runs);
+// one thread per (wave, tile)
+template <int VEC>
+__global__ __launch_bounds__(256) void stream_size_kernel(
+    int nw, int rw, int ntiles, const int *__restrict__ n_pieces_ptr, const int *__restrict__ ptr,
+    const int4 *__restrict__ piece, const int *__restrict__ order, const int *__restrict__ seg,
+    int *__restrict__ csize) {
+    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (id >= (int64_t)nw * ntiles) return;
+    const int g = (int)(id / ntiles), t = (int)(id - (int64_t)g * ntiles);
+    const int n_pieces = *n_pieces_ptr;
+    int bytes = HDR;
+    for (int i = 0; i < rw && i < MAXRW; ++i) {
+        const int pv = slot_piece(i, g, nw, rw, n_pieces, order);
+        if (pv < 0) continue;
+        const int4 pc = piece[pv];
+        const int plen = piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w);
+        const int *sr = seg + (int64_t)pc.x * (ntiles + 1);
+        const int n = piece_before(sr[t + 1], pc.y, pc.z, pc.w, plen) -
+                      piece_before(sr[t], pc.y, pc.z, pc.w, plen);
+        bytes += 8 * (n + (n & 1));
+    }
+    csize[id] = bytes;
+}
+
+// chunk offsets inside each wave's stream (exclusive scan over tiles) and the
+// wave's total; one wave per stream
+__global__ __launch_bounds__(256) void stream_scan_kernel(int nw, int ntiles, int *__restrict__ csize,
+                                                          int *__restrict__ wsize) {
+    const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (g >= nw) return;
+    const int lane = threadIdx.x & 63;
+    int *c = csize + (int64_t)g * ntiles;
+    int carry = 0;
+    for (int t0 = 0; t0 < ntiles; t0 += kWave) {
+        const int t = t0 + lane;
+        const int v = t < ntiles ? c[t] : 0;
+        const int inc = wave_incl_scan(v);
+        if (t < ntiles) c[t] = carry + inc - v;
+        carry += __shfl(inc, kWave - 1, kWave);
+    }
+    if (lane == 0) wsize[g] = carry;
+}
+
+// slot table of every wave: (row, first strided position, stride k, entries)
+// of the piece in slot i, or row = -1
+__global__ __launch_bounds__(256) void slot_table_kernel(int nw, int rw, const int *__restrict__ n_pieces_ptr,
+                                                         const int *__restrict__ ptr,
+                                                         const int4 *__restrict__ piece,
+                                                         const int *__restrict__ order,
+                                                         int4 *__restrict__ table) {
+    const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (id >= (int64_t)nw * rw) return;
+    const int g = (int)(id / rw), i = (int)(id - (int64_t)g * rw);
+    const int pv = slot_piece(i, g, nw, rw, *n_pieces_ptr, order);
+    int4 e = make_int4(-1, 0, 1, 0);
+    if (pv >= 0) {
+        const int4 pc = piece[pv];
+        e = make_int4(pc.x, pc.y + pc.z, pc.w, piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w));
+    }
+    table[id] = e;
+}
+
+// writes the chunks of (wave g, tiles t0 .. t0 + 64/G - 1): lane group tau of
+// G lanes handles tile t0 + tau, lane i of the group the piece in slot i
+template <int VEC>
+__global__ __launch_bounds__(256) void stream_fill_kernel(
+    int nw, int rw, int ntiles, const int *__restrict__ idx, const float *__restrict__ vals,
+    const int4 *__restrict__ table, const int *__restrict__ seg, const int *__restrict__ coff,
+    const int *__restrict__ woff, char *__restrict__ stream) {
+    constexpr int BB = tiled_cfg<VEC>::BB, KT = tiled_cfg<VEC>::KT;
+    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    constexpr int G = MAXRW <= 16 ? 16 : 32;  // lanes per tile (>= MAXRW and >= HDR / 2)
+    constexpr int TPW = kWave / G;            // tiles per wave
+    static_assert(G >= MAXRW && G >= HDR / 2, "a lane per slot and per header word");
+    const int tiles_per_g = (ntiles + TPW - 1) / TPW;
+    const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (id >= (int64_t)nw * tiles_per_g) return;
+    const int lane = threadIdx.x & 63;
+    const int g = (int)(id / tiles_per_g);
+    const int t0 = (int)(id - (int64_t)g * tiles_per_g) * TPW;
+    const int tau = lane / G, i = lane - tau * G;
+    const int t = t0 + tau;
+    const bool tile_ok = t < ntiles;
+    // this lane's slot in its tile: strided entries [m0, m0 + n) of the piece
+    int n = 0, pbase = 0, k = 1;
+    if (tile_ok && i < rw) {
+        const int4 e = table[(int64_t)g * rw + i];
+        if (e.x >= 0) {
+            const int *sr = seg + (int64_t)e.x * (ntiles + 1);
+            const int m0 = piece_before(sr[t], e.y, 0, e.z, e.w);
+            n = piece_before(sr[t + 1], e.y, 0, e.z, e.w) - m0;
+            k = e.z;
+            pbase = e.y + m0 * k;
+        }
+    }
+    const int np = n + (n & 1);  // padded to whole units
+    // prefix over the slots of the group: first pair of this slot inside the chunk
+    int incl = np;
+#pragma unroll
+    for (int d = 1; d < G; d <<= 1) {
+        const int u = __shfl_up(incl, d, G);
+        if (i >= d) incl += u;
+    }
+    const int start = incl - np;
+    char *chunk = stream + (tile_ok ? woff[g] + coff[(int64_t)g * ntiles + t] : 0);
+    // header: uint16 padded count per slot (zero past rw)
+    if (tile_ok && i < HDR / 2) reinterpret_cast<unsigned short *>(chunk)[i] = (unsigned short)(i < MAXRW ? np : 0);
+    // copy, tile by tile: lane q of the wave takes the q-th pair of the chunk
+    // (slot data is broadcast with readlane, which reads a lane whether or not
+    // it is still active in the loop)
+    for (int tt = 0; tt < TPW; ++tt) {
+        const int tg = t0 + tt;
+        if (tg >= ntiles) break;
+        const int total = lane_bcast(incl, tt * G + G - 1);  // pairs of tile tg (padded)
+        int2 *pp = reinterpret_cast<int2 *>(stream + woff[g] + coff[(int64_t)g * ntiles + tg] + HDR);
+        const int k0 = tg * KT;
+        for (int q = lane; q < total; q += kWave) {
+            // slot of pair q: the last slot whose start is <= q
+            int s_start = 0, s_n = 0, s_base = 0, s_k = 1;
+            for (int j = 0; j < rw && j < MAXRW; ++j) {
+                const int st = lane_bcast(start, tt * G + j);
+                const int nj = lane_bcast(n, tt * G + j);
+                const int bj = lane_bcast(pbase, tt * G + j);
+                const int kj = lane_bcast(k, tt * G + j);
+                if (st <= q) {
+                    s_start = st;
+                    s_n = nj;
+                    s_base = bj;
+                    s_k = kj;
+                }
+            }
+            const int u = q - s_start;
+            int2 v = make_int2(0, 0);  // the padding pair of an odd run
+            if (u < s_n) {
+                const int p = s_base + u * s_k;
+                v = make_int2((idx[p] - k0) * (BB * 4), __float_as_int(vals[p]));
+            }
+            pp[q] = v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// streamed tiled kernel
+// ---------------------------------------------------------------------------
+
+typedef __attribute__((address_space(3))) void lds_void;
 
 // Blocks are handed to the 8 XCDs round-robin; give XCD x a contiguous range
 // of the (chunk-major) work list so its resident workgroups share a chunk.
@@ -168,23 +348,35 @@ __device__ __forceinline__ void map_block(int bid, int nblocks, int nrb, int &rb
     rb = w - ch * nrb;
 }
 
-template <int VEC, bool XV4>
-__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) void
-spmm_tiled_kernel(int rw, int n_cols, const int *__restrict__ idx, const float *__restrict__ vals,
-                  const int *__restrict__ seg, const int4 *__restrict__ piece,
-                  const int *__restrict__ order, const int *__restrict__ n_pieces_ptr,
-                  const float *__restrict__ X, int64_t ldx, int B, float *__restrict__ Y,
-                  int64_t ldy, float *__restrict__ part, int nrb) {
-    constexpr int BB = tiled_cfg<VEC>::BB;
-    constexpr int KT = tiled_cfg<VEC>::KT;
-    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW;
-    constexpr int Q = BB / 4;                       // float4 per tile row
-    constexpr int PER = (KT * Q) / (kNW * kWave);   // float4 per thread per tile
-    __shared__ __attribute__((aligned(16))) float Xs[KT * BB];
-    __shared__ int2 slot[kNW][kWave];  // per-wave broadcast slot: (X row offset, value bits)
+// acc += v0 * X[o0] + v1 * X[o1] for the two (byte offset, value) pairs of a unit
+template <int VEC>
+__device__ __forceinline__ void fma_unit(const char *xb, int4 pr, float (&acc)[VEC]) {
+    float x0[VEC], x1[VEC];
+    load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
+    load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.z), x1);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+        acc[e] = fmaf(__int_as_float(pr.y), x0[e], acc[e]);
+        acc[e] = fmaf(__int_as_float(pr.w), x1[e], acc[e]);
+    }
+}
 
-    const int n_pieces = uniform(*n_pieces_ptr);
-    const int ntiles = (n_cols + KT - 1) / KT;
+template <int VEC>
+__global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
+    int rw, int n_cols, int ntiles, const int *__restrict__ n_pieces_ptr,
+    const int4 *__restrict__ piece, const int *__restrict__ order, const char *__restrict__ stream,
+    const int *__restrict__ woff, const float *__restrict__ X, int64_t ldx, int B,
+    float *__restrict__ Y, int64_t ldy, float *__restrict__ part, int nrb) {
+    constexpr int BB = tiled_cfg<VEC>::BB, KT = tiled_cfg<VEC>::KT;
+    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    constexpr int Q = BB / 4;  // 16-byte pieces of a tile row
+    // two tile buffers and two stream buffers as separate arrays: the compiler
+    // can then see that reads of one never alias the loads into the other
+    __shared__ __attribute__((aligned(16))) float Xs0[kTileFloats];
+    __shared__ __attribute__((aligned(16))) float Xs1[kTileFloats];
+    __shared__ __attribute__((aligned(16))) char St0[kNW * kChunk];
+    __shared__ __attribute__((aligned(16))) char St1[kNW * kChunk];
+
     int rb, ch;
     map_block(blockIdx.x, gridDim.x, nrb, rb, ch);
     const int wave = threadIdx.x >> 6;
@@ -192,20 +384,29 @@ spmm_tiled_kernel(int rw, int n_cols, const int *__restrict__ idx, const float *
     const int nw = nrb * kNW;
     const int g = rb * kNW + wave;
     const int b0 = ch * BB;
+    const int n_pieces = uniform(*n_pieces_ptr);
+    int64_t off = woff[g];
 
-    // pieces of this wave: sorted position i*nw + g, snake order over rounds;
-    // lane i holds the descriptor of piece i
-    int pc[MAXRW];
-    int4 my = make_int4(0, 0, 0, 0);
-    int my_piece = -1;
+    // async loads of tile t: X rows [t*KT, t*KT + KT) x columns [b0, b0 + BB)
+    // (clamped into the matrix: rows or columns outside it are never read
+    // back) and this wave's stream chunk
+    auto issue = [&](int t, float *xd, char *sd, int64_t soff) {
+        const int k0 = t * KT;
 #pragma unroll
-    for (int i = 0; i < MAXRW; ++i) {
-        const int j = i * nw + ((i & 1) ? (nw - 1 - g) : g);
-        pc[i] = uniform((i < rw && j < n_pieces) ? order[j] : -1);
-        if (lane == i) my_piece = pc[i];
-    }
-    if (my_piece >= 0) my = piece[my_piece];
-    const int *my_seg = seg + (int64_t)my.x * (ntiles + 1);
+        for (int u = 0; u < kTileFloats / (4 * kNW * kWave); ++u) {
+            const int q = u * (kNW * kWave) + threadIdx.x;
+            const int r = q / Q, c4 = q - r * Q;
+            int k = k0 + r;
+            k = k < n_cols ? k : n_cols - 1;
+            int b = b0 + c4 * 4;
+            b = b + 3 < B ? b : B - 4;
+            __builtin_amdgcn_global_load_lds((const void *)(X + (int64_t)k * ldx + b),
+                                             (lds_void *)(xd + (u * (kNW * kWave) + wave * kWave) * 4),
+                                             16, 0, 0);
+        }
+        __builtin_amdgcn_global_load_lds((const void *)(stream + soff + lane * 16),
+                                         (lds_void *)(sd + wave * kChunk), 16, 0, 0);
+    };
 
     float acc[MAXRW][VEC];
 #pragma unroll
@@ -213,108 +414,63 @@ spmm_tiled_kernel(int rw, int n_cols, const int *__restrict__ idx, const float *
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[i][e] = 0.f;
 
-    const float *xl = Xs + lane * VEC;
-    int2 *ms = slot[wave];
-    for (int t = 0; t < ntiles; ++t) {
-        const int k0 = t * KT;
-        // X tile and this tile's segment of every piece (lane i: piece i)
-        float4 xr[PER];
+    const int lb = lane * VEC * 4;  // byte offset of this lane's columns in a tile row
+    auto tile = [&](int t, const float *xc, const char *scur, float *xn, char *snext) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's loads of tile t landed
+        __syncthreads();                     // ... and every wave's; tile t-1 fully consumed
+        const char *sc = scur + wave * kChunk;
+        int nlen[MAXRW];
+        int tot = 0;
 #pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const int f = threadIdx.x + u * (kNW * kWave);
-            const int rr = f / Q, q = f - rr * Q;
-            const int k = k0 + rr, b = b0 + q * 4;
-            const float *src = X + (int64_t)k * ldx + b;
-            if (XV4 && k < n_cols && b + 3 < B) {
-                xr[u] = *reinterpret_cast<const float4 *>(src);
-            } else {
-                const bool kv = k < n_cols;
-                xr[u].x = (kv && b + 0 < B) ? src[0] : 0.f;
-                xr[u].y = (kv && b + 1 < B) ? src[1] : 0.f;
-                xr[u].z = (kv && b + 2 < B) ? src[2] : 0.f;
-                xr[u].w = (kv && b + 3 < B) ? src[3] : 0.f;
-            }
+        for (int i = 0; i < MAXRW; ++i) {
+            nlen[i] = uniform((int)reinterpret_cast<const unsigned short *>(sc)[i]);
+            tot += nlen[i];
         }
-        int sl = 0, nl = 0;
-        if (my_piece >= 0) {
-            sl = max(my_seg[t], my.y);
-            nl = max(min(my_seg[t + 1], my.z) - sl, 0);
-        }
-        __syncthreads();  // every wave is done with the previous tile
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const int f = threadIdx.x + u * (kNW * kWave);
-            *reinterpret_cast<float4 *>(Xs + f * 4) = xr[u];
-        }
-        __syncthreads();
-
-        // pairs of piece i+1 are loaded while piece i computes
-        int sN = lane_bcast(sl, 0), nN = lane_bcast(nl, 0);
-        int cN = 0;
-        float vN = 0.f;
-        if (lane < nN) {
-            cN = (idx[sN + lane] - k0) * BB;
-            vN = vals[sN + lane];
-        }
+        const int64_t next = off + HDR + 8 * (int64_t)tot;
+        if (t + 1 < ntiles) issue(t + 1, xn, snext, next);
+        const char *xb = reinterpret_cast<const char *>(xc) + lb;
+        int p = HDR;  // byte position of the next unit (two pairs) in the chunk
 #pragma unroll
         for (int i = 0; i < MAXRW; ++i) {
             if (i < rw) {  // (a guard, not a break: keeps every acc[i] statically indexed)
-            const int s = sN, n_total = nN;
-            int c = cN;
-            float v = vN;
-            if (i + 1 < MAXRW) {
-                sN = lane_bcast(sl, i + 1);
-                nN = lane_bcast(nl, i + 1);
-                if (lane < nN) {
-                    cN = (idx[sN + lane] - k0) * BB;
-                    vN = vals[sN + lane];
+                const int pe = p + 8 * nlen[i];
+                const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
+                for (; p + 32 <= pl; p += 32) {
+                    const int4 q0 = *reinterpret_cast<const int4 *>(sc + p);
+                    const int4 q1 = *reinterpret_cast<const int4 *>(sc + p + 16);
+                    fma_unit<VEC>(xb, q0, acc[i]);
+                    fma_unit<VEC>(xb, q1, acc[i]);
                 }
-            }
-            for (int base = 0; base < n_total; base += kWave) {
-                const int n = min(kWave, n_total - base);
-                if (base > 0 && lane < n) {  // segments longer than one wave
-                    c = (idx[s + base + lane] - k0) * BB;
-                    v = vals[s + base + lane];
+                if (p < pl) {
+                    fma_unit<VEC>(xb, *reinterpret_cast<const int4 *>(sc + p), acc[i]);
+                    p += 16;
                 }
-                // one wave writes and reads its own slot: LDS keeps the order
-                if (lane < n) ms[lane] = make_int2(c, __float_as_int(v));
-                int j = 0;
-                for (; j + 4 <= n; j += 4) {
-                    const int2 p0 = ms[j], p1 = ms[j + 1], p2 = ms[j + 2], p3 = ms[j + 3];
-                    float x0[VEC], x1[VEC], x2[VEC], x3[VEC];
-                    load_vec<VEC>(xl + p0.x, x0);
-                    load_vec<VEC>(xl + p1.x, x1);
-                    load_vec<VEC>(xl + p2.x, x2);
-                    load_vec<VEC>(xl + p3.x, x3);
-#pragma unroll
-                    for (int q = 0; q < VEC; ++q) {
-                        acc[i][q] = fmaf(__int_as_float(p0.y), x0[q], acc[i][q]);
-                        acc[i][q] = fmaf(__int_as_float(p1.y), x1[q], acc[i][q]);
-                        acc[i][q] = fmaf(__int_as_float(p2.y), x2[q], acc[i][q]);
-                        acc[i][q] = fmaf(__int_as_float(p3.y), x3[q], acc[i][q]);
-                    }
+                if (p < pe) {  // beyond the staged chunk: the stream in global memory
+                    const char *gs = stream + off;
+                    for (; p < pe; p += 16) fma_unit<VEC>(xb, *reinterpret_cast<const int4 *>(gs + p), acc[i]);
                 }
-                for (; j < n; ++j) {
-                    const int2 p0 = ms[j];
-                    float x0[VEC];
-                    load_vec<VEC>(xl + p0.x, x0);
-#pragma unroll
-                    for (int q = 0; q < VEC; ++q)
-                        acc[i][q] = fmaf(__int_as_float(p0.y), x0[q], acc[i][q]);
-                }
-            }
             }
         }
+        off = next;
+    };
+
+    issue(0, Xs0, St0, off);
+    for (int t = 0; t < ntiles; t += 2) {
+        tile(t, Xs0, St0, Xs1, St1);
+        if (t + 1 < ntiles) tile(t + 1, Xs1, St1, Xs0, St0);
     }
 
     // a whole row goes to Y; a piece of a split row to its partial row
     const int b = b0 + lane * VEC;
 #pragma unroll
     for (int i = 0; i < MAXRW; ++i) {
-        if (pc[i] < 0) continue;
-        const int row = lane_bcast(my.x, i);
-        const int split = lane_bcast(my.w, i);
-        float *dst = split ? part + (int64_t)pc[i] * B + b : Y + (int64_t)row * ldy + b;
+        if (i >= rw) continue;
+        const int pv = uniform(slot_piece(i, g, nw, rw, n_pieces, order));
+        if (pv < 0) continue;
+        const int4 pc = piece[pv];
+        const int row = uniform(pc.x);
+        const bool split = uniform(pc.w) > 1;
+        float *dst = split ? part + (int64_t)pv * B + b : Y + (int64_t)row * ldy + b;
         if (b + VEC - 1 < B) {
             store_vec<VEC>(dst, acc[i]);
         } else {
@@ -453,37 +609,50 @@ struct spmm_plan {
     int rw;      // pieces per wave
     int cap;     // longest piece
     int64_t max_pieces;
+    int64_t stream_bytes;  // bound on the pair stream
 };
 
 spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
     spmm_plan p{};
-    if (!x4 || B < 32 || n_rows < 16 || n_cols <= 0) return p;
-    p.vec = B >= 128 ? 2 : 1;
+    if (!x4 || B < 128 || n_rows < kNW || n_cols <= 0) return p;
+    p.vec = B >= 256 ? 4 : 2;
     const int BB = kWave * p.vec;
+    const int KT = kTileFloats / BB;
+    const int maxrw = p.vec == 2 ? tiled_cfg<2>::MAXRW : tiled_cfg<4>::MAXRW;
+    const int hdr = p.vec == 2 ? tiled_cfg<2>::HDR : tiled_cfg<4>::HDR;
     p.nch = (int)ceil_div(B, BB);
-    // two workgroups per CU over the whole grid, each with at least one row per wave
-    int64_t nrb = 512 / p.nch;
+    // one workgroup per CU over the whole grid, each with at least one row per wave
+    int64_t nrb = 256 / p.nch;
     if (nrb < 1) nrb = 1;
     const int64_t nrb_max = ceil_div(n_rows, kNW);
     if (nrb > nrb_max) nrb = nrb_max;
     // staging an X tile pays off when a workgroup's rows use each X element ~2x
     const double density = (double)nnz / ((double)n_rows * n_cols);
     if (density * (double)n_rows / (double)nrb < 2.0) return p;
-    p.tiled = true;
-    const int64_t nw = nrb * kNW;
-    int64_t cap = ceil_div(nnz, nw);
+    int64_t nw = nrb * kNW;
+    // pieces of at most half the mean load per wave: with the snake deal the
+    // heaviest and lightest waves then differ by a few percent even for
+    // power-law row lengths (a cap of the full mean leaves ~30%)
+    int64_t cap = ceil_div(nnz, 2 * nw);
     if (cap < 64) cap = 64;
     p.cap = (int)(cap > INT32_MAX ? INT32_MAX : cap);
     p.max_pieces = n_rows + ceil_div(nnz, p.cap);
-    const int maxrw = p.vec == 1 ? 16 : (p.vec == 2 ? 12 : 8);
     int64_t rw = ceil_div(p.max_pieces, nw);
     if (rw > maxrw) {
         rw = maxrw;
         nrb = ceil_div(p.max_pieces, (int64_t)kNW * maxrw);
+        nw = nrb * kNW;
     }
     p.rw = (int)rw;
     p.nrb = (int)nrb;
-    p.ntiles = (int)ceil_div(n_cols, kTileFloats / BB);
+    p.ntiles = (int)ceil_div(n_cols, KT);
+    // stream: every pair, one padding pair per (piece, tile) and a header per
+    // (wave, tile); too much padding means the operand is too sparse per tile
+    const int64_t slot_tiles = nw * rw * (int64_t)p.ntiles;
+    if (slot_tiles > 2 * nnz + 4096) return p;
+    p.stream_bytes = 8 * (nnz + slot_tiles) + (int64_t)hdr * nw * p.ntiles + kChunk + 256;
+    if (p.stream_bytes > INT32_MAX / 2 || (int64_t)nrb * p.nch > INT32_MAX) return p;
+    p.tiled = true;
     return p;
 }
 
@@ -492,6 +661,11 @@ struct spmm_ws {
     int4 *piece;  // [max_pieces]
     int *order;   // [max_pieces]
     int *seg;     // [n_rows][ntiles + 1]
+    int4 *table;  // [nw][rw]: slot table
+    int *coff;    // [nw][ntiles]: chunk sizes, then offsets inside the wave's stream
+    int *wsize;   // [nw]
+    int *woff;    // [nw + 1]
+    char *stream; // [stream_bytes]
     float *part;  // [max_pieces][B]
     size_t bytes;
 };
@@ -499,6 +673,7 @@ struct spmm_ws {
 // workspace layout (256-byte aligned parts); base may be 0 to size it
 spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t nw = (size_t)pl.nrb * kNW;
     spmm_ws w{};
     size_t off = 0;
     w.pbeg = reinterpret_cast<int *>(base + off);
@@ -509,6 +684,16 @@ spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     off = al(off + sizeof(int) * (size_t)pl.max_pieces);
     w.seg = reinterpret_cast<int *>(base + off);
     off = al(off + sizeof(int) * (size_t)n_rows * (pl.ntiles + 1));
+    w.table = reinterpret_cast<int4 *>(base + off);
+    off = al(off + sizeof(int4) * nw * (size_t)pl.rw);
+    w.coff = reinterpret_cast<int *>(base + off);
+    off = al(off + sizeof(int) * nw * pl.ntiles);
+    w.wsize = reinterpret_cast<int *>(base + off);
+    off = al(off + sizeof(int) * nw);
+    w.woff = reinterpret_cast<int *>(base + off);
+    off = al(off + sizeof(int) * (nw + 1));
+    w.stream = reinterpret_cast<char *>(base + off);
+    off = al(off + (size_t)pl.stream_bytes);
     w.part = reinterpret_cast<float *>(base + off);
     off = al(off + sizeof(float) * (size_t)pl.max_pieces * B);
     w.bytes = off;
@@ -520,25 +705,35 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
                      const float *vals, const float *X, int64_t ldx, int B, float *Y, int64_t ldy,
                      void *ws, hipStream_t s) {
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
+    const int nw = pl.nrb * kNW;
+    const int64_t chunks = (int64_t)nw * pl.ntiles;
     const unsigned g = (unsigned)ceil_div(n_rows, 256) < 4096 ? (unsigned)ceil_div(n_rows, 256) : 4096;
     piece_count_kernel<<<g, 256, 0, s>>>(n_rows, ptr, pl.cap, w.order);  // counts in order[] scratch
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = launch_exclusive_scan(w.order, w.pbeg, n_rows, nullptr, s)) != hipSuccess) return e;
+    const int *n_pieces = w.pbeg + n_rows;
     piece_fill_kernel<<<g, 256, 0, s>>>(n_rows, ptr, w.pbeg, w.piece);
-    order_kernel<<<1, 1024, 0, s>>>(w.pbeg + n_rows, w.piece, w.order);
-    seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles,
-                                                             tiled_cfg<VEC>::SHIFT, ptr, idx, w.seg);
+    order_kernel<<<1, 1024, 0, s>>>(n_pieces, ptr, w.piece, w.order);
+    seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC>::SHIFT,
+                                                             ptr, idx, w.seg);
+    stream_size_kernel<VEC><<<(unsigned)ceil_div(chunks, 256), 256, 0, s>>>(
+        nw, pl.rw, pl.ntiles, n_pieces, ptr, w.piece, w.order, w.seg, w.coff);
+    stream_scan_kernel<<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.ntiles, w.coff, w.wsize);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
+    slot_table_kernel<<<(unsigned)ceil_div((int64_t)nw * pl.rw, 256), 256, 0, s>>>(
+        nw, pl.rw, n_pieces, ptr, w.piece, w.order, w.table);
+    {
+        constexpr int TPW = kWave / (tiled_cfg<VEC>::MAXRW <= 16 ? 16 : 32);
+        const int64_t fill_waves = (int64_t)nw * ceil_div(pl.ntiles, TPW);
+        stream_fill_kernel<VEC><<<(unsigned)ceil_div(fill_waves, 4), 256, 0, s>>>(
+            nw, pl.rw, pl.ntiles, idx, vals, w.table, w.seg, w.coff, w.woff, w.stream);
+    }
     const unsigned nblocks = (unsigned)((int64_t)pl.nrb * pl.nch);
-    const bool xv4 = (ldx % 4 == 0) && aligned16(X);
-    if (xv4)
-        spmm_tiled_kernel<VEC, true><<<nblocks, kNW * kWave, 0, s>>>(
-            pl.rw, n_cols, idx, vals, w.seg, w.piece, w.order, w.pbeg + n_rows, X, ldx, B, Y, ldy,
-            w.part, pl.nrb);
-    else
-        spmm_tiled_kernel<VEC, false><<<nblocks, kNW * kWave, 0, s>>>(
-            pl.rw, n_cols, idx, vals, w.seg, w.piece, w.order, w.pbeg + n_rows, X, ldx, B, Y, ldy,
-            w.part, pl.nrb);
+    spmm_stream_kernel<VEC><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, n_pieces, w.piece,
+                                                            w.order, w.stream, w.woff, X, ldx, B, Y,
+                                                            ldy, w.part, pl.nrb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     fixup_kernel<<<(unsigned)n_rows, 256, 0, s>>>(n_rows, w.pbeg, w.part, B, Y, ldy);
     return hipGetLastError();
@@ -568,8 +763,8 @@ hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, cons
                     ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 7u) == 0;
     const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, ws != nullptr && v4);
     if (pl.tiled) {
-        if (pl.vec == 2) return run_tiled<2>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
-        return run_tiled<1>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        if (pl.vec == 4) return run_tiled<4>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        return run_tiled<2>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
     }
     const int vec = v4 ? 4 : (v2 ? 2 : 1);
     dim3 grid((unsigned)ceil_div(n_rows, kRowsPerBlock), (unsigned)ceil_div(B, kWave * vec));
