@@ -60,7 +60,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
         case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(nnz, B));
         case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
-        case L1CSR_OP_PROX_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
+        case L1CSR_OP_PROX_RECOMPRESS: return round_up(prox_recompress_workspace_bytes(n_rows, n_cols));
         case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
         default: return 0;
     }
@@ -218,13 +218,25 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
     if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
     if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
-    if (n_rows > 0 && (ws == nullptr || ws_bytes < sizeof(int) * (size_t)n_rows)) return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
+        return L1CSR_EINVAL;
     if (row_ptr_out == row_ptr) return L1CSR_EINVAL;  // out of place
+    if (n_rows == 0) {
+        hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
+        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
+        if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
+        return hip_status(e);
+    }
     const double t = (double)eta * (double)lambda;     // exact in double
+    // scratch: per-slab counts, then their exclusive scan (the output layout)
+    const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
     int *counts = static_cast<int *>(ws);
+    int *off = counts + (((sizeof(int) * (size_t)n_slabs + 255) & ~(size_t)255) / sizeof(int));
+    if (n_slabs > INT32_MAX) return L1CSR_EUNSUPPORTED;
     hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, counts,
                                      stream);
-    if (e == hipSuccess) e = launch_exclusive_scan(counts, row_ptr_out, n_rows, d_nnz_out, stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(counts, off, (int)n_slabs, nullptr, stream);
+    if (e == hipSuccess) e = launch_prox_row_ptr(n_rows, n_cols, off, row_ptr_out, d_nnz_out, stream);
     if (e != hipSuccess) return L1CSR_EHIP;
     if (capacity < total) {
         int32_t h = 0;
@@ -236,8 +248,8 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     } else if (h_nnz_required) {
         *h_nnz_required = -1;
     }
-    return hip_status(launch_prox_fill(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t,
-                                       row_ptr_out, col_idx_out, vals_out, capacity, stream));
+    return hip_status(launch_prox_fill(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, off,
+                                       col_idx_out, vals_out, capacity, stream));
 }
 
 int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,

@@ -94,117 +94,119 @@ __global__ void prox_csr_kernel(int64_t nnz, float *__restrict__ vals, const flo
 }
 
 
-// Fused prox + recompression, two passes over G without writing Z:
-//   COUNT: counts[row] = number of nonzero S_t(w - eta*g) in the row
-//   FILL:  recompute the same values and compact them into the output CSR at
-//          row_ptr_out[row] (a block-wide prefix per 1024-column chunk: one
-//          ballot per column slot, wave totals through LDS), in column order.
-// One 256-thread workgroup per row; the LDS copy of W's row covers up to
-// kFusedMaxTile columns at once.  A thread issues all of its G loads for the
-// tile and its first W-row entries before waiting on any of them, so a row
-// costs one memory round trip.
-constexpr int kFusedMaxTile = 16384;
-constexpr int kFusedChunks = kFusedMaxTile / (kProxThreads * 4);
+// Fused prox + recompression, two passes over G without writing Z.  The work
+// unit is a slab: kSlab consecutive columns of one row, one 256-thread
+// workgroup each, so that many rows are in flight on a CU at once (a slab
+// keeps an 8 KB LDS copy of its part of W's row and two 16-byte G loads per
+// thread in registers).
+//   COUNT: counts[slab] = number of nonzero S_t(w - eta*g) in the slab
+//   FILL:  recompute the same values and compact them to off[slab] in the
+//          output, in column order (a block-wide prefix per 1024-column
+//          chunk: one ballot per column slot, wave totals through LDS).
+// Slabs are numbered row-major, so the exclusive scan of the counts is
+// exactly the CSR layout of the result, and row_ptr[row] = off[row * S].
+constexpr int kSlab = 2048;
+constexpr int kSlabChunks = kSlab / (kProxThreads * 4);
 
 template <bool V4, bool FILL>
-__global__ __launch_bounds__(kProxThreads) void prox_rows_kernel(
-    int n_cols, int tile, const int *__restrict__ ptr, const int *__restrict__ idx,
+__global__ __launch_bounds__(kProxThreads) void prox_slab_kernel(
+    int n_cols, int slabs, const int *__restrict__ ptr, const int *__restrict__ idx,
     const float *__restrict__ vals, const float *__restrict__ G, int64_t ldg, double eta, double t,
-    int *__restrict__ counts, const int *__restrict__ row_ptr_out, int *__restrict__ col_out,
+    int *__restrict__ counts, const int *__restrict__ off, int *__restrict__ col_out,
     float *__restrict__ val_out, int64_t capacity) {
-    extern __shared__ __attribute__((aligned(16))) float wrow[];  // tile floats
+    __shared__ __attribute__((aligned(16))) float wrow[kSlab];
     __shared__ int wave_tot[kProxThreads / kWave];
-    const int row = blockIdx.x;
+    const int64_t blk = blockIdx.x;
+    const int row = (int)(blk / slabs);
+    const int k0 = (int)(blk - (int64_t)row * slabs) * kSlab;
+    const int k1 = min(n_cols, k0 + kSlab);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int s = ptr[row], e = ptr[row + 1];
     const float *g = G + (int64_t)row * ldg;
-    int64_t out = FILL ? row_ptr_out[row] : 0;
+    // every G load of the slab and the first W entries of the row in flight at once
+    float4 gq[kSlabChunks];
+#pragma unroll
+    for (int c = 0; c < kSlabChunks; ++c) {
+        const int k = k0 + c * kProxThreads * 4 + tid * 4;
+        if (V4 && k + 3 < k1) {
+            gq[c] = *reinterpret_cast<const float4 *>(g + k);
+        } else {
+            gq[c].x = k + 0 < k1 ? g[k + 0] : 0.f;
+            gq[c].y = k + 1 < k1 ? g[k + 1] : 0.f;
+            gq[c].z = k + 2 < k1 ? g[k + 2] : 0.f;
+            gq[c].w = k + 3 < k1 ? g[k + 3] : 0.f;
+        }
+    }
+    int wi[4];
+    float wv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int p = s + tid + u * kProxThreads;
+        wi[u] = p < e ? idx[p] : -1;
+        wv[u] = p < e ? vals[p] : 0.f;
+    }
+    for (int k = tid * 4; k < kSlab; k += kProxThreads * 4)
+        *reinterpret_cast<float4 *>(wrow + k) = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        if (wi[u] >= k0 && wi[u] < k1) wrow[wi[u] - k0] = wv[u];
+    for (int p = s + tid + 4 * kProxThreads; p < e; p += kProxThreads) {
+        const int k = idx[p];
+        if (k >= k0 && k < k1) wrow[k - k0] = vals[p];
+    }
+    __syncthreads();
+    int64_t out = FILL ? off[blk] : 0;
     int cnt = 0;
-    for (int k0 = 0; k0 < n_cols; k0 += tile) {
-        const int k1 = min(n_cols, k0 + tile);
-        float4 gq[kFusedChunks];
 #pragma unroll
-        for (int c = 0; c < kFusedChunks; ++c) {
-            const int k = k0 + c * kProxThreads * 4 + tid * 4;
-            if (V4 && k + 3 < k1) {
-                gq[c] = *reinterpret_cast<const float4 *>(g + k);
-            } else {
-                gq[c].x = k + 0 < k1 ? g[k + 0] : 0.f;
-                gq[c].y = k + 1 < k1 ? g[k + 1] : 0.f;
-                gq[c].z = k + 2 < k1 ? g[k + 2] : 0.f;
-                gq[c].w = k + 3 < k1 ? g[k + 3] : 0.f;
-            }
+    for (int c = 0; c < kSlabChunks; ++c) {
+        const int kb = k0 + c * kProxThreads * 4;
+        if (kb >= k1) continue;  // uniform
+        const int k = kb + tid * 4;
+        const float4 w4 = *reinterpret_cast<const float4 *>(wrow + (k - k0));
+        const float wv4[4] = {w4.x, w4.y, w4.z, w4.w};
+        const float gv[4] = {gq[c].x, gq[c].y, gq[c].z, gq[c].w};
+        float o[4];
+        bool keep[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            o[j] = k + j < k1 ? soft_threshold(wv4[j], gv[j], eta, t) : 0.f;
+            keep[j] = o[j] != 0.f;
+            cnt += keep[j];
         }
-        int wi[4];
-        float wv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int p = s + tid + u * kProxThreads;
-            wi[u] = p < e ? idx[p] : -1;
-            wv[u] = p < e ? vals[p] : 0.f;
-        }
-        for (int k = tid * 4; k < tile; k += kProxThreads * 4)
-            *reinterpret_cast<float4 *>(wrow + k) = make_float4(0.f, 0.f, 0.f, 0.f);
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (wi[u] >= k0 && wi[u] < k1) wrow[wi[u] - k0] = wv[u];
-        for (int p = s + tid + 4 * kProxThreads; p < e; p += kProxThreads) {
-            const int k = idx[p];
-            if (k >= k0 && k < k1) wrow[k - k0] = vals[p];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int c = 0; c < kFusedChunks; ++c) {
-            const int kb = k0 + c * kProxThreads * 4;
-            if (kb >= k1) continue;  // uniform; keeps gq[c] statically indexed
-            const int k = kb + tid * 4;
-            const float4 w4 = *reinterpret_cast<const float4 *>(wrow + (k - k0));
-            const float wv4[4] = {w4.x, w4.y, w4.z, w4.w};
-            const float gv[4] = {gq[c].x, gq[c].y, gq[c].z, gq[c].w};
-            float o[4];
-            bool keep[4];
+        if (FILL) {
+            uint64_t m[4];
+            int below = 0, wcnt = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                o[j] = k + j < k1 ? soft_threshold(wv4[j], gv[j], eta, t) : 0.f;
-                keep[j] = o[j] != 0.f;
-                cnt += keep[j];
+                m[j] = wave_ballot(keep[j]);
+                below += popc_below(m[j]);
+                wcnt += __popcll(m[j]);
             }
-            if (FILL) {
-                uint64_t m[4];
-                int below = 0, wcnt = 0;
+            if (lane == 0) wave_tot[wave] = wcnt;
+            __syncthreads();
+            int woff = 0, tot = 0;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    m[j] = wave_ballot(keep[j]);
-                    below += popc_below(m[j]);
-                    wcnt += __popcll(m[j]);
-                }
-                if (lane == 0) wave_tot[wave] = wcnt;
-                __syncthreads();
-                int woff = 0, tot = 0;
+            for (int w = 0; w < kProxThreads / kWave; ++w) {
+                const int wc = wave_tot[w];
+                woff += w < wave ? wc : 0;
+                tot += wc;
+            }
+            int mine = 0;
 #pragma unroll
-                for (int w = 0; w < kProxThreads / kWave; ++w) {
-                    const int wc = wave_tot[w];
-                    woff += w < wave ? wc : 0;
-                    tot += wc;
-                }
-                int mine = 0;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (keep[j]) {
-                        const int64_t pos = out + woff + below + mine;
-                        if (pos < capacity) {
-                            col_out[pos] = k + j;
-                            val_out[pos] = o[j];
-                        }
-                        ++mine;
+            for (int j = 0; j < 4; ++j) {
+                if (keep[j]) {
+                    const int64_t pos = out + woff + below + mine;
+                    if (pos < capacity) {
+                        col_out[pos] = k + j;
+                        val_out[pos] = o[j];
                     }
+                    ++mine;
                 }
-                out += tot;
-                __syncthreads();  // wave_tot is reused by the next chunk
             }
+            out += tot;
+            __syncthreads();  // wave_tot is reused by the next chunk
         }
-        __syncthreads();  // wrow is reused by the next tile
     }
     if (!FILL) {
         cnt = wave_sum_int(cnt);
@@ -213,15 +215,19 @@ __global__ __launch_bounds__(kProxThreads) void prox_rows_kernel(
         if (tid == 0) {
             int tot = 0;
             for (int w = 0; w < kProxThreads / kWave; ++w) tot += wave_tot[w];
-            counts[row] = tot;
+            counts[blk] = tot;
         }
     }
 }
 
-// LDS row buffer: the whole row when it fits, in whole 1024-column chunks
-int fused_tile(int n_cols) {
-    int tile = (int)ceil_div(n_cols, kProxThreads * 4) * kProxThreads * 4;
-    return tile < kFusedMaxTile ? tile : kFusedMaxTile;
+// row_ptr[r] = off[r * slabs] for r <= n_rows (off has n_rows * slabs + 1 entries)
+__global__ void slab_row_ptr_kernel(int n_rows, int slabs, const int *__restrict__ off,
+                                    int *__restrict__ row_ptr, int *__restrict__ nnz_out) {
+    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r <= n_rows; r += gridDim.x * blockDim.x) {
+        const int v = off[(int64_t)r * slabs];
+        row_ptr[r] = v;
+        if (r == n_rows && nnz_out) *nnz_out = v;
+    }
 }
 
 }  // namespace
@@ -253,38 +259,53 @@ hipError_t launch_prox_csr(int64_t nnz, float *vals, const float *g, float eta, 
 
 namespace l1csr {
 
+int prox_slabs(int n_cols) { return n_cols > 0 ? (int)ceil_div(n_cols, kSlab) : 1; }
+
+size_t prox_recompress_workspace_bytes(int n_rows, int n_cols) {
+    const size_t n = (size_t)n_rows * prox_slabs(n_cols);
+    return ((sizeof(int) * n + 255) & ~(size_t)255) + sizeof(int) * (n + 1);
+}
+
 hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *idx,
                              const float *vals, const float *G, int64_t ldg, float eta, double t,
                              int *counts, hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     const bool v4 = (ldg % 4 == 0) && aligned16(G);
-    const int tile = fused_tile(n_cols);
-    const size_t lds = sizeof(float) * (size_t)tile;
+    const int slabs = prox_slabs(n_cols);
+    const unsigned grid = (unsigned)((int64_t)n_rows * slabs);
     if (v4)
-        prox_rows_kernel<true, false><<<n_rows, kProxThreads, lds, s>>>(
-            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+        prox_slab_kernel<true, false><<<grid, kProxThreads, 0, s>>>(
+            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
     else
-        prox_rows_kernel<false, false><<<n_rows, kProxThreads, lds, s>>>(
-            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+        prox_slab_kernel<false, false><<<grid, kProxThreads, 0, s>>>(
+            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_prox_row_ptr(int n_rows, int n_cols, const int *off, int *row_ptr, int *nnz_out,
+                               hipStream_t s) {
+    const int slabs = prox_slabs(n_cols);
+    const unsigned grid = (unsigned)(ceil_div((int64_t)n_rows + 1, 256) < 4096 ? ceil_div((int64_t)n_rows + 1, 256) : 4096);
+    slab_row_ptr_kernel<<<grid, 256, 0, s>>>(n_rows, slabs, off, row_ptr, nnz_out);
     return hipGetLastError();
 }
 
 hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *idx,
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
-                            const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
+                            const int *off, int *col_out, float *val_out, int64_t capacity,
                             hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     const bool v4 = (ldg % 4 == 0) && aligned16(G);
-    const int tile = fused_tile(n_cols);
-    const size_t lds = sizeof(float) * (size_t)tile;
+    const int slabs = prox_slabs(n_cols);
+    const unsigned grid = (unsigned)((int64_t)n_rows * slabs);
     if (v4)
-        prox_rows_kernel<true, true><<<n_rows, kProxThreads, lds, s>>>(
-            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, row_ptr_out, col_out,
-            val_out, capacity);
+        prox_slab_kernel<true, true><<<grid, kProxThreads, 0, s>>>(
+            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
+            capacity);
     else
-        prox_rows_kernel<false, true><<<n_rows, kProxThreads, lds, s>>>(
-            n_cols, tile, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, row_ptr_out, col_out,
-            val_out, capacity);
+        prox_slab_kernel<false, true><<<grid, kProxThreads, 0, s>>>(
+            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
+            capacity);
     return hipGetLastError();
 }
 
