@@ -95,25 +95,6 @@ __global__ __launch_bounds__(256) void seg_kernel(int n_rows, int ntiles, int sh
     }
 }
 
-// pieces of a row: ceil(len / cap), at least one (an empty row is one empty piece)
-__global__ void piece_count_kernel(int n_rows, const int *__restrict__ ptr, int cap,
-                                   int *__restrict__ cnt) {
-    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < n_rows; r += gridDim.x * blockDim.x) {
-        const int len = ptr[r + 1] - ptr[r];
-        cnt[r] = len > cap ? (len + cap - 1) / cap : 1;
-    }
-}
-
-// piece v = (row, first position of the row, j, k): every k-th entry of the
-// row starting at its j-th
-__global__ void piece_fill_kernel(int n_rows, const int *__restrict__ ptr,
-                                  const int *__restrict__ pbeg, int4 *__restrict__ piece) {
-    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < n_rows; r += gridDim.x * blockDim.x) {
-        const int v0 = pbeg[r], k = pbeg[r + 1] - v0;
-        for (int j = 0; j < k; ++j) piece[v0 + j] = make_int4(r, ptr[r], j, k);
-    }
-}
-
 // entries of a piece (row length len): positions j, j + k, ... < len
 __device__ __forceinline__ int piece_len(int len, int j, int k) {
     return len > j ? (len - j + k - 1) / k : 0;
@@ -128,34 +109,97 @@ __device__ __forceinline__ int length_key(int len) {
     return 1 + b * 4 + sub;
 }
 
-// order[] = pieces by decreasing length bucket (order inside a bucket is
-// arbitrary: it only decides which wave computes a piece)
-__global__ __launch_bounds__(1024) void order_kernel(const int *__restrict__ n_pieces_ptr,
-                                                     const int *__restrict__ ptr,
-                                                     const int4 *__restrict__ piece,
-                                                     int *__restrict__ order) {
+constexpr int kPlanThreads = 1024;
+
+// block-wide inclusive scan of one value per thread (all threads must call it)
+__device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kPlanThreads / kWave; ++w) {
+        const int t = wave_tot[w];
+        before += w < wave ? t : 0;
+        total += t;
+    }
+    __syncthreads();  // wave_tot is reused by the next call
+    return before + incl;
+}
+
+// One workgroup plans the pieces and the deal:
+//   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces,
+//           piece j taking every k-th entry from the j-th; pbeg[row] = first
+//           piece of the row, piece[v] = (row, first position, j, k);
+//   order:  pieces by decreasing length bucket (the order inside a bucket only
+//           decides which wave computes a piece, never how it is summed);
+//   table:  slot i of wave g holds the piece at sorted position i*nw + g
+//           (snake order over rounds): (row, first strided position, k,
+//           entries), row = -1 for an empty slot.
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const int *__restrict__ ptr,
+                                                            int cap, int nw, int rw,
+                                                            int *__restrict__ pbeg,
+                                                            int4 *__restrict__ piece,
+                                                            int *__restrict__ order,
+                                                            int4 *__restrict__ table) {
+    __shared__ int wave_tot[kPlanThreads / kWave];
     __shared__ int hist[kBuckets];
     __shared__ int start[kBuckets];
-    const int n = *n_pieces_ptr;
     const int tid = threadIdx.x;
-    for (int k = tid; k < kBuckets; k += blockDim.x) hist[k] = 0;
-    __syncthreads();
-    for (int v = tid; v < n; v += blockDim.x) {
+    // pieces
+    int carry = 0;
+    for (int base = 0; base < n_rows; base += kPlanThreads) {
+        const int r = base + tid;
+        int first = 0, len = 0, k = 0;
+        if (r < n_rows) {
+            first = ptr[r];
+            len = ptr[r + 1] - first;
+            k = len > cap ? (len + cap - 1) / cap : 1;
+        }
+        int total;
+        const int incl = block_incl_scan(k, wave_tot, total);
+        const int v0 = carry + incl - k;
+        if (r < n_rows) {
+            pbeg[r] = v0;
+            for (int j = 0; j < k; ++j) piece[v0 + j] = make_int4(r, first, j, k);
+        }
+        carry += total;
+    }
+    const int n_pieces = carry;
+    if (tid == 0) pbeg[n_rows] = n_pieces;
+    for (int b = tid; b < kBuckets; b += kPlanThreads) hist[b] = 0;
+    __syncthreads();  // also makes piece[] visible to the whole workgroup
+    // order
+    for (int v = tid; v < n_pieces; v += kPlanThreads) {
         const int4 pc = piece[v];
         atomicAdd(&hist[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1);
     }
     __syncthreads();
     if (tid == 0) {
         int run = 0;
-        for (int k = kBuckets - 1; k >= 0; --k) {
-            start[k] = run;
-            run += hist[k];
+        for (int b = kBuckets - 1; b >= 0; --b) {
+            start[b] = run;
+            run += hist[b];
         }
     }
     __syncthreads();
-    for (int v = tid; v < n; v += blockDim.x) {
+    for (int v = tid; v < n_pieces; v += kPlanThreads) {
         const int4 pc = piece[v];
         order[atomicAdd(&start[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1)] = v;
+    }
+    __syncthreads();
+    // slot table
+    for (int64_t id = tid; id < (int64_t)nw * rw; id += kPlanThreads) {
+        const int g = (int)(id / rw), i = (int)(id - (int64_t)g * rw);
+        const int64_t j = (int64_t)i * nw + ((i & 1) ? (nw - 1 - g) : g);
+        int4 e = make_int4(-1, 0, 1, 0);
+        if (j < n_pieces) {
+            const int4 pc = piece[order[j]];
+            e = make_int4(pc.x, pc.y + pc.z, pc.w, piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w));
+        }
+        table[id] = e;
     }
 }
 
@@ -181,76 +225,50 @@ __device__ __forceinline__ int slot_piece(int i, int g, int nw, int rw, int n_pi
 }
 
 // strided position bound of a piece in a tile: the number of its entries
-// (positions first + j + m*k, m = 0, 1, ...) that lie before position p
-__device__ __forceinline__ int piece_before(int p, int first, int j, int k, int plen) {
-    const int d = p - first - j;
+// (positions first + m*k, m = 0, 1, ...) that lie before position p
+__device__ __forceinline__ int piece_before(int p, int first, int k, int plen) {
+    const int d = p - first;
     if (d <= 0) return 0;
     const int m = k == 1 ? d : (d + k - 1) / k;
     return m < plen ? m : plen;
 }
 
-// per (wave, tile): bytes of the stream chunk (header + padded pair runs);
-// one thread per (wave, tile)
+// per wave stream g (one wave each, lanes over tiles): the byte offset of every
+// chunk inside the stream (header + padded pair runs, exclusive scan over the
+// tiles) and the stream's total size
 template <int VEC>
-__global__ __launch_bounds__(256) void stream_size_kernel(
-    int nw, int rw, int ntiles, const int *__restrict__ n_pieces_ptr, const int *__restrict__ ptr,
-    const int4 *__restrict__ piece, const int *__restrict__ order, const int *__restrict__ seg,
-    int *__restrict__ csize) {
-    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
-    const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (id >= (int64_t)nw * ntiles) return;
-    const int g = (int)(id / ntiles), t = (int)(id - (int64_t)g * ntiles);
-    const int n_pieces = *n_pieces_ptr;
-    int bytes = HDR;
-    for (int i = 0; i < rw && i < MAXRW; ++i) {
-        const int pv = slot_piece(i, g, nw, rw, n_pieces, order);
-        if (pv < 0) continue;
-        const int4 pc = piece[pv];
-        const int plen = piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w);
-        const int *sr = seg + (int64_t)pc.x * (ntiles + 1);
-        const int n = piece_before(sr[t + 1], pc.y, pc.z, pc.w, plen) -
-                      piece_before(sr[t], pc.y, pc.z, pc.w, plen);
-        bytes += 8 * (n + (n & 1));
-    }
-    csize[id] = bytes;
-}
-
-// chunk offsets inside each wave's stream (exclusive scan over tiles) and the
-// wave's total; one wave per stream
-__global__ __launch_bounds__(256) void stream_scan_kernel(int nw, int ntiles, int *__restrict__ csize,
+__global__ __launch_bounds__(256) void stream_size_kernel(int nw, int rw, int ntiles,
+                                                          const int4 *__restrict__ table,
+                                                          const int *__restrict__ seg,
+                                                          int *__restrict__ coff,
                                                           int *__restrict__ wsize) {
+    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
     const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (g >= nw) return;
     const int lane = threadIdx.x & 63;
-    int *c = csize + (int64_t)g * ntiles;
+    // lane i holds slot i's piece
+    int4 e = make_int4(-1, 0, 1, 0);
+    if (lane < rw && lane < MAXRW) e = table[(int64_t)g * rw + lane];
     int carry = 0;
     for (int t0 = 0; t0 < ntiles; t0 += kWave) {
         const int t = t0 + lane;
-        const int v = t < ntiles ? c[t] : 0;
-        const int inc = wave_incl_scan(v);
-        if (t < ntiles) c[t] = carry + inc - v;
-        carry += __shfl(inc, kWave - 1, kWave);
+        int bytes = 0;
+        if (t < ntiles) {
+            bytes = HDR;
+            for (int i = 0; i < rw && i < MAXRW; ++i) {
+                const int row = lane_bcast(e.x, i);
+                if (row < 0) continue;
+                const int first = lane_bcast(e.y, i), k = lane_bcast(e.z, i), plen = lane_bcast(e.w, i);
+                const int *sr = seg + (int64_t)row * (ntiles + 1);
+                const int n = piece_before(sr[t + 1], first, k, plen) - piece_before(sr[t], first, k, plen);
+                bytes += 8 * (n + (n & 1));
+            }
+        }
+        const int incl = wave_incl_scan(bytes);
+        if (t < ntiles) coff[(int64_t)g * ntiles + t] = carry + incl - bytes;
+        carry += lane_bcast(incl, kWave - 1);
     }
     if (lane == 0) wsize[g] = carry;
-}
-
-// slot table of every wave: (row, first strided position, stride k, entries)
-// of the piece in slot i, or row = -1
-__global__ __launch_bounds__(256) void slot_table_kernel(int nw, int rw, const int *__restrict__ n_pieces_ptr,
-                                                         const int *__restrict__ ptr,
-                                                         const int4 *__restrict__ piece,
-                                                         const int *__restrict__ order,
-                                                         int4 *__restrict__ table) {
-    const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (id >= (int64_t)nw * rw) return;
-    const int g = (int)(id / rw), i = (int)(id - (int64_t)g * rw);
-    const int pv = slot_piece(i, g, nw, rw, *n_pieces_ptr, order);
-    int4 e = make_int4(-1, 0, 1, 0);
-    if (pv >= 0) {
-        const int4 pc = piece[pv];
-        e = make_int4(pc.x, pc.y + pc.z, pc.w, piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w));
-    }
-    table[id] = e;
 }
 
 // writes the chunks of (wave g, tiles t0 .. t0 + 64/G - 1): lane group tau of
@@ -280,8 +298,8 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
         const int4 e = table[(int64_t)g * rw + i];
         if (e.x >= 0) {
             const int *sr = seg + (int64_t)e.x * (ntiles + 1);
-            const int m0 = piece_before(sr[t], e.y, 0, e.z, e.w);
-            n = piece_before(sr[t + 1], e.y, 0, e.z, e.w) - m0;
+            const int m0 = piece_before(sr[t], e.y, e.z, e.w);
+            n = piece_before(sr[t + 1], e.y, e.z, e.w) - m0;
             k = e.z;
             pbase = e.y + m0 * k;
         }
@@ -298,16 +316,26 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
     char *chunk = stream + (tile_ok ? woff[g] + coff[(int64_t)g * ntiles + t] : 0);
     // header: uint16 padded count per slot (zero past rw)
     if (tile_ok && i < HDR / 2) reinterpret_cast<unsigned short *>(chunk)[i] = (unsigned short)(i < MAXRW ? np : 0);
-    // copy, tile by tile: lane q of the wave takes the q-th pair of the chunk
+    // copy: lane q of the wave takes the q-th pair of the chunk of every tile
+    // of the wave at once, so the loads of all tiles are in flight together
     // (slot data is broadcast with readlane, which reads a lane whether or not
     // it is still active in the loop)
+    int total[TPW];
+    int2 *pp[TPW];
+    int maxtot = 0;
+#pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
         const int tg = t0 + tt;
-        if (tg >= ntiles) break;
-        const int total = lane_bcast(incl, tt * G + G - 1);  // pairs of tile tg (padded)
-        int2 *pp = reinterpret_cast<int2 *>(stream + woff[g] + coff[(int64_t)g * ntiles + tg] + HDR);
-        const int k0 = tg * KT;
-        for (int q = lane; q < total; q += kWave) {
+        total[tt] = tg < ntiles ? lane_bcast(incl, tt * G + G - 1) : 0;  // pairs of tile tg (padded)
+        pp[tt] = reinterpret_cast<int2 *>(stream + (tg < ntiles ? woff[g] + coff[(int64_t)g * ntiles + tg] : 0) + HDR);
+        maxtot = max(maxtot, total[tt]);
+    }
+    for (int q0 = 0; q0 < maxtot; q0 += kWave) {
+        const int q = q0 + lane;
+        int2 v[TPW];
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) {
+            v[tt] = make_int2(0, 0);  // the padding pair of an odd run
             // slot of pair q: the last slot whose start is <= q
             int s_start = 0, s_n = 0, s_base = 0, s_k = 1;
             for (int j = 0; j < rw && j < MAXRW; ++j) {
@@ -323,13 +351,14 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
                 }
             }
             const int u = q - s_start;
-            int2 v = make_int2(0, 0);  // the padding pair of an odd run
-            if (u < s_n) {
+            if (q < total[tt] && u < s_n) {
                 const int p = s_base + u * s_k;
-                v = make_int2((idx[p] - k0) * (BB * 4), __float_as_int(vals[p]));
+                v[tt] = make_int2((idx[p] - (t0 + tt) * KT) * (BB * 4), __float_as_int(vals[p]));
             }
-            pp[q] = v;
         }
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt)
+            if (q < total[tt]) pp[tt][q] = v[tt];
     }
 }
 
@@ -706,24 +735,15 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
                      void *ws, hipStream_t s) {
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
     const int nw = pl.nrb * kNW;
-    const int64_t chunks = (int64_t)nw * pl.ntiles;
-    const unsigned g = (unsigned)ceil_div(n_rows, 256) < 4096 ? (unsigned)ceil_div(n_rows, 256) : 4096;
-    piece_count_kernel<<<g, 256, 0, s>>>(n_rows, ptr, pl.cap, w.order);  // counts in order[] scratch
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if ((e = launch_exclusive_scan(w.order, w.pbeg, n_rows, nullptr, s)) != hipSuccess) return e;
+    hipError_t e;
+    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, pl.cap, nw, pl.rw, w.pbeg, w.piece, w.order, w.table);
     const int *n_pieces = w.pbeg + n_rows;
-    piece_fill_kernel<<<g, 256, 0, s>>>(n_rows, ptr, w.pbeg, w.piece);
-    order_kernel<<<1, 1024, 0, s>>>(n_pieces, ptr, w.piece, w.order);
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC>::SHIFT,
                                                              ptr, idx, w.seg);
-    stream_size_kernel<VEC><<<(unsigned)ceil_div(chunks, 256), 256, 0, s>>>(
-        nw, pl.rw, pl.ntiles, n_pieces, ptr, w.piece, w.order, w.seg, w.coff);
-    stream_scan_kernel<<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.ntiles, w.coff, w.wsize);
+    stream_size_kernel<VEC><<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.rw, pl.ntiles, w.table, w.seg,
+                                                                       w.coff, w.wsize);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
-    slot_table_kernel<<<(unsigned)ceil_div((int64_t)nw * pl.rw, 256), 256, 0, s>>>(
-        nw, pl.rw, n_pieces, ptr, w.piece, w.order, w.table);
     {
         constexpr int TPW = kWave / (tiled_cfg<VEC>::MAXRW <= 16 ? 16 : 32);
         const int64_t fill_waves = (int64_t)nw * ceil_div(pl.ntiles, TPW);
