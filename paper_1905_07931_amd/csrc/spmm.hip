@@ -207,11 +207,15 @@ constexpr int kNW = 16;             // waves per workgroup (1024 threads)
 constexpr int kTileFloats = 16384;  // 64 KB of X per tile buffer
 constexpr int kChunk = 1024;        // bytes of a wave's pair stream staged per tile
 
-template <int VEC>
+// VEC batch columns per lane; HALF: the two half-waves take the two pairs of a
+// unit, each over the same 32*VEC columns (twice the tile height of a
+// full-wave workgroup for the same 64 KB of LDS)
+template <int VEC, bool HALF>
 struct tiled_cfg {
-    static constexpr int BB = kWave * VEC;       // batch columns per workgroup
-    static constexpr int KT = kTileFloats / BB;  // X rows per tile
-    static constexpr int SHIFT = VEC == 2 ? 7 : 6;
+    static constexpr int LANES = HALF ? kWave / 2 : kWave;  // lanes across the batch
+    static constexpr int BB = LANES * VEC;                  // batch columns per workgroup
+    static constexpr int KT = kTileFloats / BB;             // X rows per tile
+    static constexpr int SHIFT = KT == 256 ? 8 : (KT == 128 ? 7 : 6);
     static constexpr int MAXRW = VEC == 2 ? 24 : 12;          // pieces per wave in registers
     static constexpr int HDR = ((2 * MAXRW + 15) / 16) * 16;  // chunk header: uint16 count per piece
     static_assert((1 << SHIFT) == KT, "tile height must be a power of two");
@@ -236,13 +240,13 @@ __device__ __forceinline__ int piece_before(int p, int first, int k, int plen) {
 // per wave stream g (one wave each, lanes over tiles): the byte offset of every
 // chunk inside the stream (header + padded pair runs, exclusive scan over the
 // tiles) and the stream's total size
-template <int VEC>
+template <int VEC, bool HALF>
 __global__ __launch_bounds__(256) void stream_size_kernel(int nw, int rw, int ntiles,
                                                           const int4 *__restrict__ table,
                                                           const int *__restrict__ seg,
                                                           int *__restrict__ coff,
                                                           int *__restrict__ wsize) {
-    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    constexpr int MAXRW = tiled_cfg<VEC, HALF>::MAXRW, HDR = tiled_cfg<VEC, HALF>::HDR;
     const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (g >= nw) return;
     const int lane = threadIdx.x & 63;
@@ -273,13 +277,13 @@ __global__ __launch_bounds__(256) void stream_size_kernel(int nw, int rw, int nt
 
 // writes the chunks of (wave g, tiles t0 .. t0 + 64/G - 1): lane group tau of
 // G lanes handles tile t0 + tau, lane i of the group the piece in slot i
-template <int VEC>
+template <int VEC, bool HALF>
 __global__ __launch_bounds__(256) void stream_fill_kernel(
     int nw, int rw, int ntiles, const int *__restrict__ idx, const float *__restrict__ vals,
     const int4 *__restrict__ table, const int *__restrict__ seg, const int *__restrict__ coff,
     const int *__restrict__ woff, char *__restrict__ stream) {
-    constexpr int BB = tiled_cfg<VEC>::BB, KT = tiled_cfg<VEC>::KT;
-    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    constexpr int BB = tiled_cfg<VEC, HALF>::BB, KT = tiled_cfg<VEC, HALF>::KT;
+    constexpr int MAXRW = tiled_cfg<VEC, HALF>::MAXRW, HDR = tiled_cfg<VEC, HALF>::HDR;
     constexpr int G = MAXRW <= 16 ? 16 : 32;  // lanes per tile (>= MAXRW and >= HDR / 2)
     constexpr int TPW = kWave / G;            // tiles per wave
     static_assert(G >= MAXRW && G >= HDR / 2, "a lane per slot and per header word");
@@ -377,27 +381,39 @@ __device__ __forceinline__ void map_block(int bid, int nblocks, int nrb, int &rb
     rb = w - ch * nrb;
 }
 
-// acc += v0 * X[o0] + v1 * X[o1] for the two (byte offset, value) pairs of a unit
-template <int VEC>
-__device__ __forceinline__ void fma_unit(const char *xb, int4 pr, float (&acc)[VEC]) {
-    float x0[VEC], x1[VEC];
-    load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
-    load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.z), x1);
+// one unit (two (byte offset, value) pairs) at byte position p of the chunk:
+// full wave: acc += v0 * X[o0] + v1 * X[o1]; half waves: the lower half-wave
+// takes pair 0, the upper pair 1 (one 8-byte read each)
+template <int VEC, bool HALF>
+__device__ __forceinline__ void fma_unit_at(const char *base, int p, const char *xb, int half,
+                                            float (&acc)[VEC]) {
+    if constexpr (HALF) {
+        const int2 pr = *reinterpret_cast<const int2 *>(base + p + 8 * half);
+        float x0[VEC];
+        load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-        acc[e] = fmaf(__int_as_float(pr.y), x0[e], acc[e]);
-        acc[e] = fmaf(__int_as_float(pr.w), x1[e], acc[e]);
+        for (int e = 0; e < VEC; ++e) acc[e] = fmaf(__int_as_float(pr.y), x0[e], acc[e]);
+    } else {
+        const int4 pr = *reinterpret_cast<const int4 *>(base + p);
+        float x0[VEC], x1[VEC];
+        load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
+        load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.z), x1);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            acc[e] = fmaf(__int_as_float(pr.y), x0[e], acc[e]);
+            acc[e] = fmaf(__int_as_float(pr.w), x1[e], acc[e]);
+        }
     }
 }
 
-template <int VEC>
+template <int VEC, bool HALF>
 __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
     int rw, int n_cols, int ntiles, const int *__restrict__ n_pieces_ptr,
     const int4 *__restrict__ piece, const int *__restrict__ order, const char *__restrict__ stream,
     const int *__restrict__ woff, const float *__restrict__ X, int64_t ldx, int B,
     float *__restrict__ Y, int64_t ldy, float *__restrict__ part, int nrb) {
-    constexpr int BB = tiled_cfg<VEC>::BB, KT = tiled_cfg<VEC>::KT;
-    constexpr int MAXRW = tiled_cfg<VEC>::MAXRW, HDR = tiled_cfg<VEC>::HDR;
+    constexpr int BB = tiled_cfg<VEC, HALF>::BB, KT = tiled_cfg<VEC, HALF>::KT;
+    constexpr int MAXRW = tiled_cfg<VEC, HALF>::MAXRW, HDR = tiled_cfg<VEC, HALF>::HDR;
     constexpr int Q = BB / 4;  // 16-byte pieces of a tile row
     // two tile buffers and two stream buffers as separate arrays: the compiler
     // can then see that reads of one never alias the loads into the other
@@ -418,20 +434,38 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
 
     // async loads of tile t: X rows [t*KT, t*KT + KT) x columns [b0, b0 + BB)
     // (clamped into the matrix: rows or columns outside it are never read
-    // back) and this wave's stream chunk
-    auto issue = [&](int t, float *xd, char *sd, int64_t soff) {
-        const int k0 = t * KT;
+    // back) and this wave's stream chunk.  Each thread's four source
+    // addresses move by KT rows per tile; rows are clamped on the last tile only.
+    constexpr int NU = kTileFloats / (4 * kNW * kWave);  // 16-byte loads per thread per tile
+    const float *xsrc[NU];
+    int xrow[NU];
 #pragma unroll
-        for (int u = 0; u < kTileFloats / (4 * kNW * kWave); ++u) {
-            const int q = u * (kNW * kWave) + threadIdx.x;
-            const int r = q / Q, c4 = q - r * Q;
-            int k = k0 + r;
-            k = k < n_cols ? k : n_cols - 1;
-            int b = b0 + c4 * 4;
-            b = b + 3 < B ? b : B - 4;
-            __builtin_amdgcn_global_load_lds((const void *)(X + (int64_t)k * ldx + b),
-                                             (lds_void *)(xd + (u * (kNW * kWave) + wave * kWave) * 4),
-                                             16, 0, 0);
+    for (int u = 0; u < NU; ++u) {
+        const int q = u * (kNW * kWave) + threadIdx.x;
+        const int r = q / Q, c4 = q - r * Q;
+        int b = b0 + c4 * 4;
+        b = b + 3 < B ? b : B - 4;
+        xrow[u] = r;
+        xsrc[u] = X + (int64_t)r * ldx + b;
+    }
+    const int64_t tile_stride = (int64_t)KT * ldx;
+    auto issue = [&](int t, float *xd, char *sd, int64_t soff) {
+        const int64_t step = (int64_t)t * tile_stride;
+        if ((t + 1) * KT <= n_cols) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                __builtin_amdgcn_global_load_lds((const void *)(xsrc[u] + step),
+                                                 (lds_void *)(xd + (u * (kNW * kWave) + wave * kWave) * 4),
+                                                 16, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int k = t * KT + xrow[u];
+                const int64_t back = k < n_cols ? 0 : (int64_t)(k - (n_cols - 1)) * ldx;
+                __builtin_amdgcn_global_load_lds((const void *)(xsrc[u] + step - back),
+                                                 (lds_void *)(xd + (u * (kNW * kWave) + wave * kWave) * 4),
+                                                 16, 0, 0);
+            }
         }
         __builtin_amdgcn_global_load_lds((const void *)(stream + soff + lane * 16),
                                          (lds_void *)(sd + wave * kChunk), 16, 0, 0);
@@ -443,7 +477,9 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[i][e] = 0.f;
 
-    const int lb = lane * VEC * 4;  // byte offset of this lane's columns in a tile row
+    constexpr int LANES = tiled_cfg<VEC, HALF>::LANES;
+    const int half = HALF ? lane >> 5 : 0;
+    const int lb = (lane & (LANES - 1)) * VEC * 4;  // byte offset of this lane's columns in a tile row
     auto tile = [&](int t, const float *xc, const char *scur, float *xn, char *snext) {
         __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's loads of tile t landed
         __syncthreads();                     // ... and every wave's; tile t-1 fully consumed
@@ -451,9 +487,11 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
         int nlen[MAXRW];
         int tot = 0;
 #pragma unroll
-        for (int i = 0; i < MAXRW; ++i) {
-            nlen[i] = uniform((int)reinterpret_cast<const unsigned short *>(sc)[i]);
-            tot += nlen[i];
+        for (int w = 0; w < MAXRW / 2; ++w) {
+            const unsigned hw = (unsigned)uniform((int)reinterpret_cast<const unsigned *>(sc)[w]);
+            nlen[2 * w] = (int)(hw & 0xffffu);
+            nlen[2 * w + 1] = (int)(hw >> 16);
+            tot += nlen[2 * w] + nlen[2 * w + 1];
         }
         const int64_t next = off + HDR + 8 * (int64_t)tot;
         if (t + 1 < ntiles) issue(t + 1, xn, snext, next);
@@ -465,18 +503,16 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
                 const int pe = p + 8 * nlen[i];
                 const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
                 for (; p + 32 <= pl; p += 32) {
-                    const int4 q0 = *reinterpret_cast<const int4 *>(sc + p);
-                    const int4 q1 = *reinterpret_cast<const int4 *>(sc + p + 16);
-                    fma_unit<VEC>(xb, q0, acc[i]);
-                    fma_unit<VEC>(xb, q1, acc[i]);
+                    fma_unit_at<VEC, HALF>(sc, p, xb, half, acc[i]);
+                    fma_unit_at<VEC, HALF>(sc, p + 16, xb, half, acc[i]);
                 }
                 if (p < pl) {
-                    fma_unit<VEC>(xb, *reinterpret_cast<const int4 *>(sc + p), acc[i]);
+                    fma_unit_at<VEC, HALF>(sc, p, xb, half, acc[i]);
                     p += 16;
                 }
                 if (p < pe) {  // beyond the staged chunk: the stream in global memory
                     const char *gs = stream + off;
-                    for (; p < pe; p += 16) fma_unit<VEC>(xb, *reinterpret_cast<const int4 *>(gs + p), acc[i]);
+                    for (; p < pe; p += 16) fma_unit_at<VEC, HALF>(gs, p, xb, half, acc[i]);
                 }
             }
         }
@@ -489,11 +525,18 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
         if (t + 1 < ntiles) tile(t + 1, Xs1, St1, Xs0, St0);
     }
 
+    // half waves: the two halves hold partial sums of the same columns
+    if constexpr (HALF) {
+#pragma unroll
+        for (int i = 0; i < MAXRW; ++i)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[i][e] += __shfl_xor(acc[i][e], kWave / 2, kWave);
+    }
     // a whole row goes to Y; a piece of a split row to its partial row
-    const int b = b0 + lane * VEC;
+    const int b = b0 + (lane & (LANES - 1)) * VEC;
 #pragma unroll
     for (int i = 0; i < MAXRW; ++i) {
-        if (i >= rw) continue;
+        if (i >= rw || half) continue;
         const int pv = uniform(slot_piece(i, g, nw, rw, n_pieces, order));
         if (pv < 0) continue;
         const int4 pc = piece[pv];
@@ -631,6 +674,7 @@ __global__ __launch_bounds__(256) void spmm_scatter_atomic_kernel(
 // which path a product takes, and the shape of the tiled launch
 struct spmm_plan {
     bool tiled;
+    bool half;   // half-wave units (twice the tile height)
     int vec;     // batch columns per lane
     int ntiles;  // X tiles
     int nch;     // batch chunks of 64 x vec columns
@@ -641,15 +685,13 @@ struct spmm_plan {
     int64_t stream_bytes;  // bound on the pair stream
 };
 
-spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
-    spmm_plan p{};
-    if (!x4 || B < 128 || n_rows < kNW || n_cols <= 0) return p;
-    p.vec = B >= 256 ? 4 : 2;
-    const int BB = kWave * p.vec;
-    const int KT = kTileFloats / BB;
-    const int maxrw = p.vec == 2 ? tiled_cfg<2>::MAXRW : tiled_cfg<4>::MAXRW;
-    const int hdr = p.vec == 2 ? tiled_cfg<2>::HDR : tiled_cfg<4>::HDR;
-    p.nch = (int)ceil_div(B, BB);
+// the launch shape for (vec, half): returns false if the tiled kernel does not suit
+template <int VEC, bool HALF>
+bool shape_plan(spmm_plan &p, int n_rows, int n_cols, int64_t nnz, int B) {
+    using cfg = tiled_cfg<VEC, HALF>;
+    p.vec = VEC;
+    p.half = HALF;
+    p.nch = (int)ceil_div(B, cfg::BB);
     // one workgroup per CU over the whole grid, each with at least one row per wave
     int64_t nrb = 256 / p.nch;
     if (nrb < 1) nrb = 1;
@@ -657,7 +699,7 @@ spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
     if (nrb > nrb_max) nrb = nrb_max;
     // staging an X tile pays off when a workgroup's rows use each X element ~2x
     const double density = (double)nnz / ((double)n_rows * n_cols);
-    if (density * (double)n_rows / (double)nrb < 2.0) return p;
+    if (density * (double)n_rows / (double)nrb < 2.0) return false;
     int64_t nw = nrb * kNW;
     // pieces of at most half the mean load per wave: with the snake deal the
     // heaviest and lightest waves then differ by a few percent even for
@@ -667,21 +709,42 @@ spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
     p.cap = (int)(cap > INT32_MAX ? INT32_MAX : cap);
     p.max_pieces = n_rows + ceil_div(nnz, p.cap);
     int64_t rw = ceil_div(p.max_pieces, nw);
-    if (rw > maxrw) {
-        rw = maxrw;
-        nrb = ceil_div(p.max_pieces, (int64_t)kNW * maxrw);
+    if (rw > cfg::MAXRW) {
+        rw = cfg::MAXRW;
+        nrb = ceil_div(p.max_pieces, (int64_t)kNW * cfg::MAXRW);
         nw = nrb * kNW;
     }
     p.rw = (int)rw;
     p.nrb = (int)nrb;
-    p.ntiles = (int)ceil_div(n_cols, KT);
+    p.ntiles = (int)ceil_div(n_cols, cfg::KT);
     // stream: every pair, one padding pair per (piece, tile) and a header per
     // (wave, tile); too much padding means the operand is too sparse per tile
     const int64_t slot_tiles = nw * rw * (int64_t)p.ntiles;
-    if (slot_tiles > 2 * nnz + 4096) return p;
-    p.stream_bytes = 8 * (nnz + slot_tiles) + (int64_t)hdr * nw * p.ntiles + kChunk + 256;
-    if (p.stream_bytes > INT32_MAX / 2 || (int64_t)nrb * p.nch > INT32_MAX) return p;
-    p.tiled = true;
+    if (slot_tiles > 2 * nnz + 4096) return false;
+    p.stream_bytes = 8 * (nnz + slot_tiles) + (int64_t)cfg::HDR * nw * p.ntiles + kChunk + 256;
+    if (p.stream_bytes > INT32_MAX / 2 || (int64_t)nrb * p.nch > INT32_MAX) return false;
+    return true;
+}
+
+spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
+    spmm_plan p{};
+    if (!x4 || B < 128 || n_rows < kNW || n_cols <= 0) return p;
+    if (B >= 256) {
+        // half-wave units halve the number of tiles; they pay off while a
+        // wave's chunk of a tile (about nnz / (waves * tiles) pairs) still
+        // fits its 1 KB LDS slot
+        spmm_plan h{};
+        if (shape_plan<4, true>(h, n_rows, n_cols, nnz, B)) {
+            const double per_chunk = (double)nnz / ((double)h.nrb * kNW * h.ntiles);
+            if (per_chunk <= 0.75 * (kChunk - tiled_cfg<4, true>::HDR) / 8.0) {
+                h.tiled = true;
+                return h;
+            }
+        }
+        p.tiled = shape_plan<4, false>(p, n_rows, n_cols, nnz, B);
+    } else {
+        p.tiled = shape_plan<2, false>(p, n_rows, n_cols, nnz, B);
+    }
     return p;
 }
 
@@ -729,7 +792,7 @@ spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     return w;
 }
 
-template <int VEC>
+template <int VEC, bool HALF>
 hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr, const int *idx,
                      const float *vals, const float *X, int64_t ldx, int B, float *Y, int64_t ldy,
                      void *ws, hipStream_t s) {
@@ -738,20 +801,20 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
     hipError_t e;
     plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, pl.cap, nw, pl.rw, w.pbeg, w.piece, w.order, w.table);
     const int *n_pieces = w.pbeg + n_rows;
-    seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC>::SHIFT,
+    seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,
                                                              ptr, idx, w.seg);
-    stream_size_kernel<VEC><<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.rw, pl.ntiles, w.table, w.seg,
+    stream_size_kernel<VEC, HALF><<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.rw, pl.ntiles, w.table, w.seg,
                                                                        w.coff, w.wsize);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
     {
-        constexpr int TPW = kWave / (tiled_cfg<VEC>::MAXRW <= 16 ? 16 : 32);
+        constexpr int TPW = kWave / (tiled_cfg<VEC, HALF>::MAXRW <= 16 ? 16 : 32);
         const int64_t fill_waves = (int64_t)nw * ceil_div(pl.ntiles, TPW);
-        stream_fill_kernel<VEC><<<(unsigned)ceil_div(fill_waves, 4), 256, 0, s>>>(
+        stream_fill_kernel<VEC, HALF><<<(unsigned)ceil_div(fill_waves, 4), 256, 0, s>>>(
             nw, pl.rw, pl.ntiles, idx, vals, w.table, w.seg, w.coff, w.woff, w.stream);
     }
     const unsigned nblocks = (unsigned)((int64_t)pl.nrb * pl.nch);
-    spmm_stream_kernel<VEC><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, n_pieces, w.piece,
+    spmm_stream_kernel<VEC, HALF><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, n_pieces, w.piece,
                                                             w.order, w.stream, w.woff, X, ldx, B, Y,
                                                             ldy, w.part, pl.nrb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -783,8 +846,10 @@ hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, cons
                     ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 7u) == 0;
     const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, ws != nullptr && v4);
     if (pl.tiled) {
-        if (pl.vec == 4) return run_tiled<4>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
-        return run_tiled<2>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        if (pl.vec == 4 && pl.half)
+            return run_tiled<4, true>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        if (pl.vec == 4) return run_tiled<4, false>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        return run_tiled<2, false>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
     }
     const int vec = v4 ? 4 : (v2 ? 2 : 1);
     dim3 grid((unsigned)ceil_div(n_rows, kRowsPerBlock), (unsigned)ceil_div(B, kWave * vec));
