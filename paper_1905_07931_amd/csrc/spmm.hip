@@ -381,20 +381,33 @@ __device__ __forceinline__ void map_block(int bid, int nblocks, int nrb, int &rb
     rb = w - ch * nrb;
 }
 
-// one unit (two (byte offset, value) pairs) at byte position p of the chunk:
-// full wave: acc += v0 * X[o0] + v1 * X[o1]; half waves: the lower half-wave
-// takes pair 0, the upper pair 1 (one 8-byte read each)
+// A unit is two (byte offset, value) pairs.  Full wave: every lane takes both
+// pairs; half waves: the lower half-wave takes pair 0, the upper pair 1.
+template <bool HALF>
+struct unit_t {
+    using type = int4;
+};
+template <>
+struct unit_t<true> {
+    using type = int2;
+};
+
+template <bool HALF>
+__device__ __forceinline__ typename unit_t<HALF>::type load_unit(const char *base, int p, int half) {
+    using U = typename unit_t<HALF>::type;
+    return *reinterpret_cast<const U *>(base + p + (HALF ? 8 * half : 0));
+}
+
+// acc += v * X[o] for the pair(s) of a unit this lane takes
 template <int VEC, bool HALF>
-__device__ __forceinline__ void fma_unit_at(const char *base, int p, const char *xb, int half,
-                                            float (&acc)[VEC]) {
+__device__ __forceinline__ void fma_unit(const char *xb, typename unit_t<HALF>::type pr,
+                                         float (&acc)[VEC]) {
     if constexpr (HALF) {
-        const int2 pr = *reinterpret_cast<const int2 *>(base + p + 8 * half);
         float x0[VEC];
         load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] = fmaf(__int_as_float(pr.y), x0[e], acc[e]);
     } else {
-        const int4 pr = *reinterpret_cast<const int4 *>(base + p);
         float x0[VEC], x1[VEC];
         load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.x), x0);
         load_vec<VEC>(reinterpret_cast<const float *>(xb + pr.z), x1);
@@ -496,23 +509,58 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
         const int64_t next = off + HDR + 8 * (int64_t)tot;
         if (t + 1 < ntiles) issue(t + 1, xn, snext, next);
         const char *xb = reinterpret_cast<const char *>(xc) + lb;
-        int p = HDR;  // byte position of the next unit (two pairs) in the chunk
+        int p = HDR;  // byte position of the next unit in the chunk
+        if constexpr (HALF) {
+            // half waves read the units one step ahead: qa, qb hold the units at
+            // p and p + 16 (each read clamped inside the chunk; a clamped read is
+            // never used, because a unit past the chunk is read from global
+            // memory instead)
+            using U = typename unit_t<HALF>::type;
+            auto ahead = [&](int pos) { return load_unit<HALF>(sc, pos < kChunk - 16 ? pos : kChunk - 16, half); };
+            U qa = ahead(p), qb = ahead(p + 16);
 #pragma unroll
-        for (int i = 0; i < MAXRW; ++i) {
-            if (i < rw) {  // (a guard, not a break: keeps every acc[i] statically indexed)
-                const int pe = p + 8 * nlen[i];
-                const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
-                for (; p + 32 <= pl; p += 32) {
-                    fma_unit_at<VEC, HALF>(sc, p, xb, half, acc[i]);
-                    fma_unit_at<VEC, HALF>(sc, p + 16, xb, half, acc[i]);
+            for (int i = 0; i < MAXRW; ++i) {
+                if (i < rw) {  // (a guard, not a break: keeps every acc[i] statically indexed)
+                    const int pe = p + 8 * nlen[i];
+                    const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
+                    for (; p + 32 <= pl; p += 32) {
+                        const U c0 = qa, c1 = qb;
+                        qa = ahead(p + 32);
+                        qb = ahead(p + 48);
+                        fma_unit<VEC, HALF>(xb, c0, acc[i]);
+                        fma_unit<VEC, HALF>(xb, c1, acc[i]);
+                    }
+                    if (p < pl) {
+                        const U c0 = qa;
+                        qa = qb;
+                        qb = ahead(p + 32);
+                        fma_unit<VEC, HALF>(xb, c0, acc[i]);
+                        p += 16;
+                    }
+                    if (p < pe) {  // beyond the staged chunk: the stream in global memory
+                        const char *gs = stream + off;
+                        for (; p < pe; p += 16) fma_unit<VEC, HALF>(xb, load_unit<HALF>(gs, p, half), acc[i]);
+                    }
                 }
-                if (p < pl) {
-                    fma_unit_at<VEC, HALF>(sc, p, xb, half, acc[i]);
-                    p += 16;
-                }
-                if (p < pe) {  // beyond the staged chunk: the stream in global memory
-                    const char *gs = stream + off;
-                    for (; p < pe; p += 16) fma_unit_at<VEC, HALF>(gs, p, xb, half, acc[i]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < MAXRW; ++i) {
+                if (i < rw) {  // (a guard, not a break: keeps every acc[i] statically indexed)
+                    const int pe = p + 8 * nlen[i];
+                    const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
+                    for (; p + 32 <= pl; p += 32) {
+                        fma_unit<VEC, HALF>(xb, load_unit<HALF>(sc, p, half), acc[i]);
+                        fma_unit<VEC, HALF>(xb, load_unit<HALF>(sc, p + 16, half), acc[i]);
+                    }
+                    if (p < pl) {
+                        fma_unit<VEC, HALF>(xb, load_unit<HALF>(sc, p, half), acc[i]);
+                        p += 16;
+                    }
+                    if (p < pe) {  // beyond the staged chunk: the stream in global memory
+                        const char *gs = stream + off;
+                        for (; p < pe; p += 16) fma_unit<VEC, HALF>(xb, load_unit<HALF>(gs, p, half), acc[i]);
+                    }
                 }
             }
         }
