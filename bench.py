@@ -44,6 +44,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host time spent timing the oracle")
+    ap.add_argument("--workload", default="fc9216x4096",
+                    choices=["fc9216x4096", "fc784x300", "mlp784", "conv2", "fc4096_sweep", "all"],
+                    help="fc9216x4096 (default): the metric's workload, one JSON line; the others "
+                         "print one informational JSON line each (no CPU baseline)")
     return ap.parse_args()
 
 
@@ -88,6 +92,15 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     L1.lib()  # fail loudly if the HIP library is missing
+
+    if args.workload != "fc9216x4096":
+        import bench_workloads
+        names = (["fc784x300", "mlp784", "conv2", "fc4096_sweep"] if args.workload == "all"
+                 else [args.workload])
+        for n in names:
+            for line in bench_workloads.run(n, args, dev):
+                print(json.dumps(line), flush=True)
+        return
 
     t0 = time.time()
     Lr = synth.fc9216_4096(seed=0)

@@ -1,0 +1,269 @@
+"""The other layer shapes of the method, timed the way bench.py times the
+9216 -> 4096 step (inputs resident in HBM, warm-up, back-to-back steps between
+two events, per-call events in a second pass).  Each workload yields one
+informational JSON line; bench.py's default line is the metric.
+
+    fc784x300     l1 step of the 784 -> 300 layer, batch 64, 10% density
+    mlp784        MLP 784-300-100-10, batch 256: l1 step then a debiasing step
+    conv2         LeNet-5 conv2 as im2col, 50 x 500 CSR, batch 16384:
+                  fwd, CSC, bwd, masked dW (SDDMM), support-restricted prox, compaction
+    fc4096_sweep  4096 x 4096, batch 512, densities 1/5/20/50%: 20 alternating
+                  l1 / debiasing iterations with the CSR rebuilt after every l1 step
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "sparse train-step GFLOP/s (nnz-effective) and achieved HBM GB/s vs peak"
+
+
+def _timed(torch, step, steps, warmup, names):
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    per = None
+    if names:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
+        for s in range(steps):
+            step(evs[s])
+        torch.cuda.synchronize()
+        per = {n: round(float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)])), 4)
+               for i, n in enumerate(names)}
+    return ms, per
+
+
+def _line(workload, flops, ms, cfg, per=None, **extra):
+    out = {"metric": METRIC, "value": round(flops / (ms * 1e-3) / 1e9, 1), "unit": "GFLOP/s",
+           "n_gpus": 1, "ms_per_step": round(ms, 4), "higher_is_better": True, "dtype": "f32",
+           "data": "synthetic", "config": dict(workload=workload, **cfg), "informational": True}
+    if per:
+        out["kernels_ms"] = per
+    out.update(extra)
+    return out
+
+
+def _csr_out(L1, torch, N, K, dev):
+    return L1.CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(N * K, dtype=torch.int32, device=dev),
+                  torch.empty(N * K, dtype=torch.float32, device=dev), None)
+
+
+def fc784x300(args, dev):
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    L = synth.fc784_300(seed=0)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = torch.from_numpy(L.X).to(dev), torch.from_numpy(L.dY).to(dev)
+    Y = torch.empty((L.N, L.B), dtype=torch.float32, device=dev)
+    dX = torch.empty((L.K, L.B), dtype=torch.float32, device=dev)
+    dW = torch.empty((L.N, L.K), dtype=torch.float32, device=dev)
+    csc = L1.CSC.empty(L.K, L.nnz, dev)
+    Wout = _csr_out(L1, torch, L.N, L.K, dev)
+    names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_recompress"]
+
+    def step(ev=None):
+        mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+        mark(0); L1.csr_spmm_fwd(W, X, Y)
+        mark(1); L1.csc_build(W, csc)
+        mark(2); L1.csr_spmm_bwd_t(W, dY, csc, dX)
+        mark(3); L1.dense_wgrad(dY, X, dW)
+        mark(4); L1.prox_l1_recompress(W, dW, L.eta, L.lam, out=Wout)
+        mark(5)
+    ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+    flops = 4.0 * L.nnz * L.B + 2.0 * L.N * L.K * L.B
+    yield _line("fc784x300_b64_d10_l1_step", flops, ms,
+                dict(N=L.N, K=L.K, B=L.B, nnz=L.nnz, density=0.10), per,
+                nnz_out=int(Wout.row_ptr[-1].item()))
+
+
+def mlp784(args, dev):
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    layers, Xh, labels = synth.mlp_784_300_100_10(seed=0)
+    B = Xh.shape[1]
+    eta, lam = 0.01, 1e-4
+    W0 = [L1.CSR.from_host(l.row_ptr, l.col_idx, l.vals, l.K, device=dev) for l in layers]
+    W1 = [_csr_out(L1, torch, l.N, l.K, dev) for l in layers]
+    X, lab = torch.from_numpy(Xh).to(dev), torch.from_numpy(labels).to(dev)
+    shapes = [(l.N, l.K) for l in layers]
+    A = [torch.empty((n, B), dtype=torch.float32, device=dev) for n, _ in shapes]
+    H = [torch.empty((n, B), dtype=torch.float32, device=dev) for n, _ in shapes[:2]]
+    D = [torch.empty((n, B), dtype=torch.float32, device=dev) for n, _ in shapes]
+    dH = [torch.empty((k, B), dtype=torch.float32, device=dev) for _, k in shapes]
+    dW = [torch.empty((n, k), dtype=torch.float32, device=dev) for n, k in shapes]
+    cscs = [L1.CSC.empty(k, n * k, dev) for n, k in shapes]
+    gvs = [torch.empty(n * k, dtype=torch.float32, device=dev) for n, k in shapes]
+
+    def fwd_bwd(Ws):
+        inp = [X, None, None]
+        for j in range(3):
+            L1.csr_spmm_fwd(Ws[j], inp[j], A[j])
+            if j < 2:
+                L1.relu_fwd(A[j], H[j])
+                inp[j + 1] = H[j]
+        L1.softmax_xent(A[2], lab, dlogits=D[2])
+        for j in (2, 1):
+            csc = L1.csc_build(Ws[j], cscs[j])
+            L1.csr_spmm_bwd_t(Ws[j], D[j], csc, dH[j])
+            L1.relu_bwd(A[j - 1], dH[j], D[j - 1])
+        return inp
+
+    known = [None, None, None]  # nnz of the l1 step's output, learned once
+
+    def step(ev=None):
+        mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+        mark(0)
+        inp = fwd_bwd(W0)
+        for j in range(3):
+            L1.dense_wgrad(D[j], inp[j], dW[j])
+            L1.prox_l1_recompress(W0[j], dW[j], eta, lam, out=W1[j])
+            W1[j].nnz = known[j]
+        mark(1)
+        inp = fwd_bwd(W1)
+        for j in range(3):
+            L1.sddmm_masked_wgrad(W1[j], D[j], inp[j], gvs[j])
+            L1.prox_l1_step(L1.PROX_CSR, W1[j], gvs[j], eta, 0.0)
+        mark(2)
+    # the debiasing step runs on the l1 step's output structure: learn its size once
+    step()
+    torch.cuda.synchronize()
+    for j, w in enumerate(W1):
+        w.nnz = None
+        known[j] = w.host_nnz()
+    ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), ["l1_step", "debias_step"])
+    nnz0 = [l.nnz for l in layers]
+    nnz1 = [w.nnz for w in W1]
+    flops = sum(4.0 * a * B + 2.0 * n * k * B for a, (n, k) in zip(nnz0, shapes)) + \
+        sum(6.0 * a * B for a in nnz1)
+    yield _line("mlp784_300_100_10_b256_l1_then_debias", flops, ms,
+                dict(B=B, nnz=nnz0, nnz_after_l1=nnz1), per)
+
+
+def conv2(args, dev):
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    L = synth.conv2_im2col(seed=0)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    vals0 = W.vals.clone()
+    X, dY = torch.from_numpy(L.X).to(dev), torch.from_numpy(L.dY).to(dev)
+    Y = torch.empty((L.N, L.B), dtype=torch.float32, device=dev)
+    dX = torch.empty((L.K, L.B), dtype=torch.float32, device=dev)
+    gv = torch.empty(L.nnz, dtype=torch.float32, device=dev)
+    csc = L1.CSC.empty(L.K, L.nnz, dev)
+    Wc = L1.CSR(L.N, L.K, torch.empty(L.N + 1, dtype=torch.int32, device=dev),
+                torch.empty(L.nnz, dtype=torch.int32, device=dev),
+                torch.empty(L.nnz, dtype=torch.float32, device=dev), None)
+    names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "sddmm_masked_wgrad", "prox_l1_step_csr",
+             "csr_compact"]
+
+    def step(ev=None):
+        mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+        W.vals.copy_(vals0)  # every step starts from the same weights
+        mark(0); L1.csr_spmm_fwd(W, X, Y)
+        mark(1); L1.csc_build(W, csc)
+        mark(2); L1.csr_spmm_bwd_t(W, dY, csc, dX)
+        mark(3); L1.sddmm_masked_wgrad(W, dY, X, gv)
+        mark(4); L1.prox_l1_step(L1.PROX_CSR, W, gv, L.eta, L.lam)
+        mark(5); L1.csr_compact(W, Wc)
+        mark(6)
+    ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+    flops = 6.0 * L.nnz * L.B
+    # SDDMM reads X and dY once at least: the HBM roof of this shape
+    sddmm_bytes = 4.0 * (L.K + L.N) * L.B + 12.0 * L.nnz
+    yield _line("conv2_im2col_50x500_b16384_d10", flops, ms, dict(N=L.N, K=L.K, B=L.B, nnz=L.nnz), per,
+                sddmm_hbm_gbs=round(sddmm_bytes / (per["sddmm_masked_wgrad"] * 1e-3) / 1e9, 1),
+                spmm_fwd_hbm_gbs=round((4.0 * (L.K + L.N) * L.B + 8.0 * L.nnz) /
+                                       (per["csr_spmm_fwd"] * 1e-3) / 1e9, 1))
+
+
+def fc4096_sweep(args, dev):
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    cal = json.load(open(os.path.join(ROOT, "tests", "golden", "fc4096_lambda.json")))
+    iters = 20
+    batches = [synth.fc4096_batch(t) for t in range(iters)]
+    Xs = [torch.from_numpy(x).to(dev) for x, _ in batches]
+    dYs = [torch.from_numpy(d).to(dev) for _, d in batches]
+    del batches
+    for pct in (1, 5, 20, 50):
+        L = synth.fc4096_sweep(pct / 100)
+        lam = cal["lambda"][str(pct)]
+        N, K, B = L.N, L.K, L.B
+        W0 = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=dev)
+        bufs = [_csr_out(L1, torch, N, K, dev) for _ in range(2)]
+        Y = torch.empty((N, B), dtype=torch.float32, device=dev)
+        dX = torch.empty((K, B), dtype=torch.float32, device=dev)
+        dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+        gv = torch.empty(N * K, dtype=torch.float32, device=dev)
+        csc = L1.CSC.empty(K, N * K, dev)
+        # one untimed pass learns the nnz of every iteration (the host passes it
+        # to the calls, as a training loop that sizes its buffers would)
+        nnz_seq = []
+
+        def run(timed_nnz=None):
+            W = W0
+            k = 0
+            for t in range(iters):
+                if t % 2 == 0:
+                    if W is not W0:
+                        L1.csc_update_vals(W, csc)
+                    else:
+                        L1.csc_build(W, csc)
+                    L1.csr_spmm_fwd(W, Xs[t], Y)
+                    L1.csr_spmm_bwd_t(W, dYs[t], csc, dX)
+                    L1.dense_wgrad(dYs[t], Xs[t], dW)
+                    out = bufs[k % 2]
+                    k += 1
+                    L1.prox_l1_recompress(W, dW, L.eta, lam, out=out)
+                    W = out
+                    if timed_nnz is None:
+                        nnz_seq.append(W.host_nnz())
+                    else:
+                        W.nnz = timed_nnz[t // 2]
+                else:
+                    L1.csc_build(W, csc)
+                    L1.csr_spmm_fwd(W, Xs[t], Y)
+                    L1.csr_spmm_bwd_t(W, dYs[t], csc, dX)
+                    L1.sddmm_masked_wgrad(W, dYs[t], Xs[t], gv)
+                    L1.prox_l1_step(L1.PROX_CSR, W, gv, L.eta, 0.0)
+        run()
+        torch.cuda.synchronize()
+        reps = 3
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            run(nnz_seq)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / (reps * iters)
+        flops = 0.0
+        prev = L.nnz
+        for t in range(iters):
+            if t % 2 == 0:
+                flops += 4.0 * prev * B + 2.0 * N * K * B
+                prev = nnz_seq[t // 2]
+            else:
+                flops += 6.0 * prev * B
+        flops /= iters
+        yield _line(f"fc4096_b512_d{pct}_alternating_l1_debias", flops, ms,
+                    dict(N=N, K=K, B=B, nnz=L.nnz, density=pct / 100, lam=lam, iterations=iters),
+                    None, nnz_after_l1_steps=nnz_seq)
+
+
+def run(name, args, dev):
+    return {"fc784x300": fc784x300, "mlp784": mlp784, "conv2": conv2, "fc4096_sweep": fc4096_sweep}[name](args, dev)

@@ -130,7 +130,9 @@ __device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total)
 }
 
 // One workgroup plans the pieces and the deal:
-//   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces,
+//   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces
+//           (cap = max(64, ceil(nnz / (2 nw))), so there are at most
+//           n_rows + 2 nw pieces),
 //           piece j taking every k-th entry from the j-th; pbeg[row] = first
 //           piece of the row, piece[v] = (row, first position, j, k);
 //   order:  pieces by decreasing length bucket (the order inside a bucket only
@@ -139,7 +141,7 @@ __device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total)
 //           (snake order over rounds): (row, first strided position, k,
 //           entries), row = -1 for an empty slot.
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const int *__restrict__ ptr,
-                                                            int cap, int nw, int rw,
+                                                            int nw, int rw,
                                                             int *__restrict__ pbeg,
                                                             int4 *__restrict__ piece,
                                                             int *__restrict__ order,
@@ -148,6 +150,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const in
     __shared__ int hist[kBuckets];
     __shared__ int start[kBuckets];
     const int tid = threadIdx.x;
+    // pieces of at most half the mean load per wave (from the actual number of
+    // entries, read on the device): with the snake deal the heaviest and
+    // lightest waves then differ by a few percent even for power-law row
+    // lengths (a cap of the full mean leaves ~30%)
+    const int64_t nnz = ptr[n_rows] - ptr[0];
+    int64_t cap64 = (nnz + 2 * (int64_t)nw - 1) / (2 * (int64_t)nw);
+    const int cap = (int)(cap64 < 64 ? 64 : (cap64 > INT32_MAX ? INT32_MAX : cap64));
     // pieces
     int carry = 0;
     for (int base = 0; base < n_rows; base += kPlanThreads) {
@@ -728,7 +737,6 @@ struct spmm_plan {
     int nch;     // batch chunks of 64 x vec columns
     int nrb;     // row groups (workgroups per chunk)
     int rw;      // pieces per wave
-    int cap;     // longest piece
     int64_t max_pieces;
     int64_t stream_bytes;  // bound on the pair stream
 };
@@ -749,19 +757,16 @@ bool shape_plan(spmm_plan &p, int n_rows, int n_cols, int64_t nnz, int B) {
     const double density = (double)nnz / ((double)n_rows * n_cols);
     if (density * (double)n_rows / (double)nrb < 2.0) return false;
     int64_t nw = nrb * kNW;
-    // pieces of at most half the mean load per wave: with the snake deal the
-    // heaviest and lightest waves then differ by a few percent even for
-    // power-law row lengths (a cap of the full mean leaves ~30%)
-    int64_t cap = ceil_div(nnz, 2 * nw);
-    if (cap < 64) cap = 64;
-    p.cap = (int)(cap > INT32_MAX ? INT32_MAX : cap);
-    p.max_pieces = n_rows + ceil_div(nnz, p.cap);
-    int64_t rw = ceil_div(p.max_pieces, nw);
+    // the planner cuts rows into pieces of at most max(64, nnz / (2 nw))
+    // entries (nnz counted on the device), so there are at most n_rows + 2 nw
+    // pieces; more waves if a wave would get more pieces than it has slots
+    int64_t rw = ceil_div(n_rows + 2 * nw, nw);
     if (rw > cfg::MAXRW) {
         rw = cfg::MAXRW;
-        nrb = ceil_div(p.max_pieces, (int64_t)kNW * cfg::MAXRW);
+        nrb = ceil_div(n_rows, (int64_t)kNW * (cfg::MAXRW - 2));
         nw = nrb * kNW;
     }
+    p.max_pieces = n_rows + 2 * nw;
     p.rw = (int)rw;
     p.nrb = (int)nrb;
     p.ntiles = (int)ceil_div(n_cols, cfg::KT);
@@ -847,7 +852,7 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
     const int nw = pl.nrb * kNW;
     hipError_t e;
-    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, pl.cap, nw, pl.rw, w.pbeg, w.piece, w.order, w.table);
+    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, w.pbeg, w.piece, w.order, w.table);
     const int *n_pieces = w.pbeg + n_rows;
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,
                                                              ptr, idx, w.seg);
