@@ -57,7 +57,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
     switch (op) {
         case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols, nnz));
         case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
-        case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(nnz, B));
+        case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_PROX_RECOMPRESS: return round_up(prox_recompress_workspace_bytes(n_rows, n_cols));
@@ -141,11 +141,11 @@ int sddmm_masked_wgrad(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
         return L1CSR_EINVAL;
     if (nnz > 0 && gv == nullptr) return L1CSR_EINVAL;
     if (bad_dense(dY, n_rows, B, ldy) || bad_dense(X, n_cols, B, ldx)) return L1CSR_EINVAL;
-    const size_t need = sddmm_workspace_bytes(nnz, B);
+    const size_t need = sddmm_workspace_bytes(n_rows, n_cols, nnz, B);
     if (need > 0 && (ws == nullptr || ws_bytes < need)) return L1CSR_EINVAL;
     if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
     return hip_status(
-        launch_sddmm(n_rows, nnz, row_ptr, col_idx, dY, ldy, X, ldx, B, gv, ws, stream));
+        launch_sddmm(n_rows, n_cols, nnz, row_ptr, col_idx, dY, ldy, X, ldx, B, gv, ws, stream));
 }
 
 int prox_l1_step(int mode, int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,

@@ -45,12 +45,18 @@ hipError_t launch_fill_rows_f32(float *p, int64_t rows, int64_t cols, int64_t ld
 // gemm.hip -----------------------------------------------------------------
 hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                             int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
+// gv[p] = (dY . X^T)[row(p)][col(p)] through 128x128 matrix-core tiles of the
+// dense product; seg[row][t] = first entry of the row with column >= 128 t,
+// t = 0 .. ceil(K / 128) (launch_seg with shift 7)
+hipError_t launch_sddmm_mfma(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                             int64_t ldx, const int *seg, const int *idx, float *gv, hipStream_t s);
 
 // sddmm.hip ----------------------------------------------------------------
-size_t sddmm_workspace_bytes(int64_t nnz, int B);
-hipError_t launch_sddmm(int n_rows, int64_t nnz, const int *ptr, const int *idx, const float *dY,
-                        int64_t ldy, const float *X, int64_t ldx, int B, float *gv, void *ws,
-                        hipStream_t s);
+// gv[p] = sum_b dY[row(p)][b] X[col(p)][b]; ws holds sddmm_workspace_bytes()
+size_t sddmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B);
+hipError_t launch_sddmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                        const float *dY, int64_t ldy, const float *X, int64_t ldx, int B, float *gv,
+                        void *ws, hipStream_t s);
 
 // prox.hip -----------------------------------------------------------------
 hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *idx,

@@ -1,11 +1,23 @@
 // Masked weight gradient of the debiasing phase:
 //     gv[p] = sum_b dY[row(p)][b] * X[col(p)][b]
-// One wave per (row, batch segment).  The wave keeps its segment of the dY row
-// in registers, and for every nonzero of the row reads the matching segment of
-// the X row (coalesced, lanes over the batch), multiplies and reduces across
-// the wave.  With several batch segments the per-segment partial sums go to
-// scratch and a second pass adds them in segment order, so the result does not
-// depend on scheduling.
+//
+// Work items.  The batch is cut into ranges of NCH chunks (a chunk is 64 lanes
+// x VEC floats) and the columns into ranges of 2^shift, sized so that one
+// (batch range, column range) "unit" of X is about 1 MB.  Every row gets
+// k = ceil(len / lsplit) pieces; piece j of a row takes the row's entries
+// j, j + k, j + 2k, ... that fall inside the unit's column range.  An item is
+// (unit, piece), and one wave handles one item: it keeps its batch range of
+// the dY row in registers, reads the X rows of the piece's entries (coalesced,
+// lanes over the batch), and multiplies.  Items are numbered unit-major and
+// the grid walks them in order, so at any time the chip works on about one
+// unit and every XCD's L2 holds the same 1 MB of X.
+//
+// Reduction over the lanes.  Four entries are reduced together: two
+// permlane32 swaps and one permlane16 swap turn four 64-lane partial vectors
+// into one vector whose 16-lane row r holds 4 lanes' worth of entry r, and
+// four DPP steps finish inside the rows.  The order of the additions is fixed,
+// so the result does not depend on scheduling.  With several batch ranges the
+// per-range sums go to scratch and a second pass adds them in range order.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -13,139 +25,389 @@ namespace l1csr {
 
 namespace {
 
-constexpr int kRowsPerBlock = 4;
+constexpr int kGatherThreads = 256;                 // 4 waves
+constexpr int kGatherBlocks = 256 * 8;              // persistent grid: 8 blocks per CU
+constexpr int64_t kUnitBytes = 1 << 20;             // X bytes per (batch range, column range)
+constexpr int kTargetItems = 8192;                  // enough waves to fill the chip
 
-// R float4 per lane: a segment covers 256*R batch entries (vector path) or
-// 64*R entries (scalar path, VEC4 = false).
-template <int R, bool VEC4>
-__global__ __launch_bounds__(256) void sddmm_rows_kernel(
-    int n_rows, const int *__restrict__ ptr, const int *__restrict__ idx,
-    const float *__restrict__ dY, int64_t ldy, const float *__restrict__ X, int64_t ldx, int B,
-    float *__restrict__ out, int64_t out_stride) {
-    constexpr int W = VEC4 ? 4 : 1;
-    constexpr int SEG = kWave * W * R;
-    const int row = uniform(blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6));
-    if (row >= n_rows) return;
-    const int lane = threadIdx.x & 63;
-    const int seg = blockIdx.y;
-    const int start = uniform(ptr[row]);
-    const int end = uniform(ptr[row + 1]);
-    if (start == end) return;
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
 
-    // batch index of (lane, r, w): seg*SEG + r*64*W + lane*W + w
-    float y[R][W];
-    const float *dyr = dY + (int64_t)row * ldy;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int b = seg * SEG + r * kWave * W + lane * W;
-        if constexpr (VEC4) {
-            if (b < B) {
-                const float4 t = *reinterpret_cast<const float4 *>(dyr + b);
-                y[r][0] = t.x; y[r][1] = t.y; y[r][2] = t.z; y[r][3] = t.w;
-            } else {
-#pragma unroll
-                for (int w = 0; w < W; ++w) y[r][w] = 0.f;
-            }
-        } else {
-            y[r][0] = b < B ? dyr[b] : 0.f;
-        }
+// v_r = per-lane partials of entry r (r < 4).  Returns, in every lane of the
+// 16-lane row r, the sum of v_r over all 64 lanes.
+__device__ __forceinline__ float reduce4(float v0, float v1, float v2, float v3) {
+    // permlane32_swap(a, b): a keeps lanes 0-31 and takes b's lanes 0-31 in its
+    // lanes 32-63; b takes a's lanes 32-63 in its lanes 0-31.
+    const auto s02 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0), __float_as_uint(v2), false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v1), __float_as_uint(v3), false, false);
+    const float w0 = __uint_as_float(s02[0]) + __uint_as_float(s02[1]);  // lanes < 32: entry 0, else 2
+    const float w1 = __uint_as_float(s13[0]) + __uint_as_float(s13[1]);  // lanes < 32: entry 1, else 3
+    // permlane16_swap(a, b): odd 16-lane rows of a trade places with even rows of b
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(w0), __float_as_uint(w1), false, false);
+    float x = __uint_as_float(s[0]) + __uint_as_float(s[1]);             // row r: entry r
+    x += dpp<0x128>(x);  // row_ror:8
+    x += dpp<0x124>(x);  // row_ror:4
+    x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+    x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+    return x;
+}
+
+template <int VEC>
+__device__ __forceinline__ void load_vec(const float *p, float (&v)[VEC]) {
+    if constexpr (VEC == 4) {
+        const float4 t = *reinterpret_cast<const float4 *>(p);
+        v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    } else {
+        v[0] = *p;
     }
+}
 
-    float *o = out + (int64_t)seg * out_stride;
-    for (int base = start; base < end; base += kWave) {
-        const int n = min(kWave, end - base);
-        const int c = lane < n ? idx[base + lane] : 0;
-        float mine = 0.f;
-        for (int j = 0; j < n; ++j) {
-            const int cj = lane_bcast(c, j);
-            const float *xr = X + (int64_t)cj * ldx;
-            float part = 0.f;
+// Extra pieces (row, j), j = 1 .. k_row - 1 with k_row = ceil(len / lsplit),
+// listed in row order; their number goes to *ext_n.  One workgroup walks the
+// rows in tiles with a carried offset.
+__global__ __launch_bounds__(1024) void sddmm_extra_kernel(int n_rows, const int *__restrict__ ptr,
+                                                           int lsplit, int2 *__restrict__ ext,
+                                                           int *__restrict__ ext_n) {
+    __shared__ int wave_tot[16];
+    __shared__ int carry_s;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) carry_s = 0;
+    __syncthreads();
+    for (int base = 0; base < n_rows; base += 1024) {
+        const int i = base + tid;
+        int e = 0;
+        if (i < n_rows) {
+            const int len = ptr[i + 1] - ptr[i];
+            e = len > lsplit ? (len + lsplit - 1) / lsplit - 1 : 0;
+        }
+        const int incl = wave_incl_scan(e);
+        if (lane == 63) wave_tot[wave] = incl;
+        __syncthreads();
+        if (wave == 0) {
+            const int t = lane < 16 ? wave_tot[lane] : 0;
+            const int ti = wave_incl_scan(t);
+            if (lane < 16) wave_tot[lane] = ti - t;
+        }
+        __syncthreads();
+        const int carry = carry_s;
+        const int off = carry + wave_tot[wave] + incl - e;
+        for (int j = 0; j < e; ++j) ext[off + j] = make_int2(i, j + 1);
+        __syncthreads();
+        if (tid == 1023) carry_s = off + e;
+        __syncthreads();
+    }
+    if (tid == 0) *ext_n = carry_s;
+}
+
+// The entries of one item in steps of G: loads of all G entries issued
+// together, reduced four at a time; entry e's sum is collected in lane e of
+// the returned vector (up to 64 entries per call).  FULL: the whole batch
+// range lies inside B (no per-lane guard on the loads).
+template <int VEC, int NCH, int G, bool FULL>
+__device__ __forceinline__ float item_block(const float *__restrict__ X, int64_t ldx, int b_lane, int B,
+                                            const float (&dy)[NCH][VEC], int colv, int m) {
+    constexpr int CH = kWave * VEC;
+    const int lane = threadIdx.x & 63;
+    float res = 0.f;
+    for (int g = 0; g < m; g += G) {
+        float xv[G][NCH][VEC];
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int b = seg * SEG + r * kWave * W + lane * W;
-                if constexpr (VEC4) {
-                    if (b < B) {
-                        const float4 t = *reinterpret_cast<const float4 *>(xr + b);
-                        part = fmaf(y[r][0], t.x, part);
-                        part = fmaf(y[r][1], t.y, part);
-                        part = fmaf(y[r][2], t.z, part);
-                        part = fmaf(y[r][3], t.w, part);
-                    }
+        for (int i = 0; i < G; ++i) {
+            // past the end: repeat the last entry (its sum is not stored)
+            const int ci = lane_bcast(colv, min(g + i, m - 1));
+            const float *xr = X + (int64_t)ci * ldx + b_lane;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULL || b_lane + c * CH < B) {
+                    load_vec<VEC>(xr + c * CH, xv[i][c]);
                 } else {
-                    if (b < B) part = fmaf(y[r][0], xr[b], part);
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) xv[i][c][v] = 0.f;
                 }
             }
-            const float tot = wave_sum(part);
-            if (lane == j) mine = tot;
         }
-        if (lane < n) o[base + lane] = mine;
+        float part[G];
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            float a = 0.f;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) a = fmaf(dy[c][v], xv[i][c][v], a);
+            part[i] = a;
+        }
+#pragma unroll
+        for (int s4 = 0; s4 < G; s4 += 4) {
+            const float tot = reduce4(part[s4], part[s4 + 1], part[s4 + 2], part[s4 + 3]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float v = lane_bcast(tot, 16 * r);
+                if (lane == g + s4 + r) res = v;
+            }
+        }
+    }
+    return res;
+}
+
+// One wave per item, persistent grid.  seg (R > 1) holds the column-range
+// bounds of every row: seg[row][cr] = first entry with column >= cr << shift.
+template <int VEC, int NCH, int G>
+__global__ __launch_bounds__(kGatherThreads) void sddmm_gather_kernel(
+    int n_rows, const int *__restrict__ ptr, const int *__restrict__ idx,
+    const float *__restrict__ dY, int64_t ldy, const float *__restrict__ X, int64_t ldx, int B,
+    int R, int nbr, int lsplit, const int *__restrict__ seg, const int2 *__restrict__ ext,
+    const int *__restrict__ ext_n, float *__restrict__ out, int64_t nnz) {
+    constexpr int CH = kWave * VEC;   // batch entries per chunk
+    constexpr int BRW = NCH * CH;     // batch entries per range
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int P = n_rows + (ext_n ? uniform(*ext_n) : 0);
+    const int64_t total = (int64_t)P * R * nbr;
+    const int64_t stride = (int64_t)gridDim.x * (kGatherThreads / kWave);
+    const int64_t t0 = (int64_t)blockIdx.x * (kGatherThreads / kWave) + wave;
+    // item t = u * P + q, stepped incrementally
+    const int64_t du = stride / P;
+    const int dq = (int)(stride - du * P);
+    int64_t u = t0 / P;
+    int q = (int)(t0 - u * P);
+
+    for (int64_t t = t0; t < total; t += stride) {
+        const int br = (int)(u / R);
+        const int cr = (int)(u - (int64_t)br * R);
+        int row, j;
+        if (q < n_rows) {
+            row = q;
+            j = 0;
+        } else {
+            const int2 e = ext[q - n_rows];
+            row = uniform(e.x);
+            j = uniform(e.y);
+        }
+        u += du;
+        q += dq;
+        if (q >= P) {
+            q -= P;
+            ++u;
+        }
+        const int rs = ptr[row], re = ptr[row + 1];
+        const int len = re - rs;
+        const int k = len > lsplit ? (len + lsplit - 1) / lsplit : 1;
+        int lo = rs, hi = re;
+        if (R > 1) {
+            const int *sr = seg + (int64_t)row * (R + 1) + cr;
+            lo = sr[0];
+            hi = sr[1];
+        }
+        const int first = lo + j;
+        if (first >= hi) continue;
+        const int n = (hi - first + k - 1) / k;
+
+        const int b_lane = br * BRW + lane * VEC;
+        const bool full = (int64_t)(br + 1) * BRW <= B;
+        float dy[NCH][VEC];
+        const float *dyr = dY + (int64_t)row * ldy + b_lane;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (b_lane + c * CH < B) {
+                load_vec<VEC>(dyr + c * CH, dy[c]);
+            } else {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) dy[c][v] = 0.f;
+            }
+        }
+        float *o = out + (int64_t)br * nnz + first;
+        for (int base = 0; base < n; base += kWave) {
+            const int m = min(kWave, n - base);
+            const int colv = lane < m ? idx[first + (int64_t)(base + lane) * k] : 0;
+            const float res = full ? item_block<VEC, NCH, G, true>(X, ldx, b_lane, B, dy, colv, m)
+                                   : item_block<VEC, NCH, G, false>(X, ldx, b_lane, B, dy, colv, m);
+            if (lane < m) o[(int64_t)(base + lane) * k] = res;
+        }
     }
 }
 
-// gv[p] = sum_{s < nseg} part[s][p], s ascending
-__global__ void sddmm_reduce_kernel(int64_t nnz, int nseg, const float *__restrict__ part,
-                                    float *__restrict__ gv) {
-    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < nnz;
-         p += (int64_t)gridDim.x * blockDim.x) {
-        float acc = 0.f;
-        for (int s = 0; s < nseg; ++s) acc += part[(int64_t)s * nnz + p];
-        gv[p] = acc;
+// gv[p] = sum of part[s][p] over the nseg batch ranges.  A workgroup owns 64
+// entries; its four waves add contiguous quarters of the ranges in ascending
+// order and the quarters are added in order, so the result is deterministic.
+__global__ __launch_bounds__(256) void sddmm_reduce_kernel(int64_t nnz, int nseg,
+                                                           const float *__restrict__ part,
+                                                           float *__restrict__ gv) {
+    __shared__ float red[3][kWave];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t p = (int64_t)blockIdx.x * kWave + lane;
+    const int per = (nseg + 3) / 4;
+    const int s0 = min(nseg, wave * per), s1 = min(nseg, s0 + per);
+    float acc = 0.f;
+    if (p < nnz) {
+        int s = s0;
+        for (; s + 8 <= s1; s += 8) {
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = part[(int64_t)(s + i) * nnz + p];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc += v[i];
+        }
+        for (; s < s1; ++s) acc += part[(int64_t)s * nnz + p];
     }
+    if (wave > 0) red[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && p < nnz) gv[p] = ((acc + red[0][lane]) + red[1][lane]) + red[2][lane];
 }
 
-struct plan {
-    int R;
-    bool v4;
-    int seg;
-    int nseg;
+// Matrix-core path: the dense product in 128x128 tiles with a masked
+// epilogue.  It does N*K*B multiply-adds instead of nnz*B, but at the matrix
+// cores' rate and without streaming an X row per entry through L2; it pays off
+// at high density.  Estimated times (us): the gather path moves about 24 TB/s
+// of X rows out of L2; a 128x128 tile takes about 0.15 us per batch entry with
+// two tiles per CU.
+constexpr int kDenseShift = 7;
+
+bool use_dense(int n_rows, int n_cols, int64_t nnz, int B) {
+    const double gather_us = (double)nnz * B * 4.0 / 24e6 + 5.0;
+    const double tiles = (double)ceil_div(n_rows, 128) * (double)ceil_div(n_cols, 128);
+    const double rounds = (double)ceil_div((int64_t)tiles, 512);
+    const double dense_us = rounds * 0.152 * B + 8.0;
+    return dense_us < gather_us;
+}
+
+size_t dense_ws_bytes(int n_rows, int n_cols) {
+    return sizeof(int) * (size_t)n_rows * (size_t)(ceil_div(n_cols, (int64_t)1 << kDenseShift) + 1);
+}
+
+struct gplan {
+    int vec, nch, nbr;
+    int shift, R;
+    int lsplit;
+    bool extras;        // some row can be longer than lsplit
+    int64_t ext_max;    // bound on the number of extra pieces
 };
 
-plan make_plan(int n_rows, int B, bool v4) {
-    plan pl;
-    pl.v4 = v4;
-    const int W = v4 ? 4 : 1;
-    // longest segments that still give enough waves to fill the chip
-    pl.R = 4;
-    if ((int64_t)n_rows * ceil_div(B, kWave * W * 4) < 4096) pl.R = 1;
-    pl.seg = kWave * W * pl.R;
-    pl.nseg = (int)ceil_div(B, pl.seg);
-    if (pl.nseg < 1) pl.nseg = 1;
+int64_t plan_items(int n_rows, int64_t nnz, int R, int nbr, int lsplit) {
+    return (int64_t)nbr * R * (n_rows + nnz / lsplit);
+}
+
+gplan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool v4) {
+    gplan pl;
+    pl.vec = v4 ? 4 : 1;
+    const int ch = kWave * pl.vec;
+    const int64_t nchunks = ceil_div(B, ch);
+    auto shape = [&](int nch) {
+        pl.nch = nch;
+        pl.nbr = (int)ceil_div(nchunks, nch);
+        const int64_t col_bytes = 4 * (int64_t)(B < nch * ch ? B : nch * ch);
+        int shift = 6;
+        while (shift < 30 && ((int64_t)2 << shift) * col_bytes <= kUnitBytes) ++shift;
+        pl.shift = shift;
+        pl.R = (int)ceil_div(n_cols, (int64_t)1 << shift);
+        if (pl.R < 1) pl.R = 1;
+    };
+    // longest batch range (fewest reductions) that still yields enough items,
+    // then shorter pieces if needed
+    const int nchs[3] = {4, 2, 1};
+    int c0 = 0;
+    while (c0 < 2 && nchs[c0] > nchunks) ++c0;
+    bool done = false;
+    for (int c = c0; c < 3 && !done; ++c) {
+        shape(nchs[c]);
+        pl.lsplit = 64 * pl.R;
+        if (plan_items(n_rows, nnz, pl.R, pl.nbr, pl.lsplit) >= kTargetItems) done = true;
+    }
+    if (!done) {
+        while (pl.lsplit > 8 * pl.R && plan_items(n_rows, nnz, pl.R, pl.nbr, pl.lsplit) < kTargetItems)
+            pl.lsplit /= 2;
+    }
+    pl.extras = pl.lsplit < n_cols;
+    pl.ext_max = pl.extras ? nnz / pl.lsplit + 1 : 0;
     return pl;
+}
+
+struct gwork {
+    int *seg;
+    int2 *ext;
+    int *ext_n;
+    float *part;
+    size_t bytes;
+};
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+gwork carve(const gplan &pl, int n_rows, int64_t nnz, void *ws) {
+    gwork w{};
+    char *p = static_cast<char *>(ws);
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char * {
+        char *r = p ? p + off : nullptr;
+        off += align256(bytes);
+        return r;
+    };
+    if (pl.R > 1) w.seg = reinterpret_cast<int *>(take(sizeof(int) * (size_t)n_rows * (pl.R + 1)));
+    if (pl.extras) {
+        w.ext_n = reinterpret_cast<int *>(take(sizeof(int)));
+        w.ext = reinterpret_cast<int2 *>(take(sizeof(int2) * (size_t)pl.ext_max));
+    }
+    if (pl.nbr > 1) w.part = reinterpret_cast<float *>(take(sizeof(float) * (size_t)pl.nbr * nnz));
+    w.bytes = off;
+    return w;
+}
+
+template <int VEC, int NCH>
+void launch_gather(const gplan &pl, const gwork &w, int n_rows, int64_t nnz, const int *ptr,
+                   const int *idx, const float *dY, int64_t ldy, const float *X, int64_t ldx, int B,
+                   float *out, hipStream_t s) {
+    constexpr int G = NCH == 1 ? 8 : 4;
+    const int64_t items = plan_items(n_rows, nnz, pl.R, pl.nbr, pl.lsplit);
+    int64_t blocks = ceil_div(items, kGatherThreads / kWave);
+    if (blocks > kGatherBlocks) blocks = kGatherBlocks;
+    if (blocks < 1) blocks = 1;
+    sddmm_gather_kernel<VEC, NCH, G><<<(unsigned)blocks, kGatherThreads, 0, s>>>(
+        n_rows, ptr, idx, dY, ldy, X, ldx, B, pl.R, pl.nbr, pl.lsplit, w.seg, w.ext, w.ext_n, out, nnz);
 }
 
 }  // namespace
 
-size_t sddmm_workspace_bytes(int64_t nnz, int B) {
-    // worst case over the plans: scalar path with R = 1 (64 entries per segment)
-    const int64_t nseg = ceil_div(B, kWave);
-    return nseg > 1 ? sizeof(float) * (size_t)(nseg * nnz) : 0;
+size_t sddmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B) {
+    if (nnz == 0 || B == 0) return 0;
+    if (use_dense(n_rows, n_cols, nnz, B)) return dense_ws_bytes(n_rows, n_cols);
+    // the larger of the vector and scalar plans
+    const size_t a = carve(make_plan(n_rows, n_cols, nnz, B, true), n_rows, nnz, nullptr).bytes;
+    const size_t b = carve(make_plan(n_rows, n_cols, nnz, B, false), n_rows, nnz, nullptr).bytes;
+    return a > b ? a : b;
 }
 
-hipError_t launch_sddmm(int n_rows, int64_t nnz, const int *ptr, const int *idx, const float *dY,
-                        int64_t ldy, const float *X, int64_t ldx, int B, float *gv, void *ws,
-                        hipStream_t s) {
+hipError_t launch_sddmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                        const float *dY, int64_t ldy, const float *X, int64_t ldx, int B, float *gv,
+                        void *ws, hipStream_t s) {
     if (nnz == 0) return hipSuccess;
     if (B == 0) return launch_fill_f32(gv, nnz, 0.f, s);
-    const bool v4 = (B % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) && aligned16(dY);
-    const plan pl = make_plan(n_rows, B, v4);
-    float *out = pl.nseg > 1 ? static_cast<float *>(ws) : gv;
-    dim3 grid((unsigned)ceil_div(n_rows, kRowsPerBlock), (unsigned)pl.nseg);
-    if (pl.v4) {
-        if (pl.R == 4)
-            sddmm_rows_kernel<4, true><<<grid, 256, 0, s>>>(n_rows, ptr, idx, dY, ldy, X, ldx, B, out, nnz);
-        else
-            sddmm_rows_kernel<1, true><<<grid, 256, 0, s>>>(n_rows, ptr, idx, dY, ldy, X, ldx, B, out, nnz);
-    } else {
-        if (pl.R == 4)
-            sddmm_rows_kernel<4, false><<<grid, 256, 0, s>>>(n_rows, ptr, idx, dY, ldy, X, ldx, B, out, nnz);
-        else
-            sddmm_rows_kernel<1, false><<<grid, 256, 0, s>>>(n_rows, ptr, idx, dY, ldy, X, ldx, B, out, nnz);
+    hipError_t e;
+    if (use_dense(n_rows, n_cols, nnz, B)) {
+        int *seg = static_cast<int *>(ws);
+        const int ntiles = (int)ceil_div(n_cols, (int64_t)1 << kDenseShift);
+        if ((e = launch_seg(n_rows, ntiles, kDenseShift, ptr, idx, seg, s)) != hipSuccess) return e;
+        return launch_sddmm_mfma(n_rows, n_cols, B, dY, ldy, X, ldx, seg, idx, gv, s);
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || pl.nseg == 1) return e;
-    int64_t g = ceil_div(nnz, 256);
-    if (g > 65536) g = 65536;
-    sddmm_reduce_kernel<<<(unsigned)g, 256, 0, s>>>(nnz, pl.nseg, out, gv);
+    const bool v4 = (B % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) && aligned16(dY);
+    const gplan pl = make_plan(n_rows, n_cols, nnz, B, v4);
+    const gwork w = carve(pl, n_rows, nnz, ws);
+    if (pl.R > 1 && (e = launch_seg(n_rows, pl.R, pl.shift, ptr, idx, w.seg, s)) != hipSuccess) return e;
+    if (pl.extras) {
+        sddmm_extra_kernel<<<1, 1024, 0, s>>>(n_rows, ptr, pl.lsplit, w.ext, w.ext_n);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    float *out = pl.nbr > 1 ? w.part : gv;
+    if (pl.vec == 4) {
+        if (pl.nch == 4) launch_gather<4, 4>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+        else if (pl.nch == 2) launch_gather<4, 2>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+        else launch_gather<4, 1>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+    } else {
+        if (pl.nch == 4) launch_gather<1, 4>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+        else if (pl.nch == 2) launch_gather<1, 2>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+        else launch_gather<1, 1>(pl, w, n_rows, nnz, ptr, idx, dY, ldy, X, ldx, B, out, s);
+    }
+    if ((e = hipGetLastError()) != hipSuccess || pl.nbr == 1) return e;
+    sddmm_reduce_kernel<<<(unsigned)ceil_div(nnz, kWave), 256, 0, s>>>(nnz, pl.nbr, w.part, gv);
     return hipGetLastError();
 }
 

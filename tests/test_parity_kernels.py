@@ -233,6 +233,18 @@ def test_sddmm(shape):
     assert_scaled_close(gv, ref, m, what="gv")
 
 
+# large and dense enough that the matrix-core tile path is taken (vector and
+# scalar operand loads; ragged 128-tiles in both dimensions)
+@pytest.mark.parametrize("shape", [(2048, 2048, 256, 2097152, 11), (1100, 1030, 333, 1050000, 12)],
+                         ids=_ids)
+def test_sddmm_dense_tiles(shape):
+    L = _layer(shape)
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    ref = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
+    m = oracle.sddmm(L.row_ptr, L.col_idx, np.abs(L.dY), L.X)
+    assert_scaled_close(gv, ref, m, what="gv")
+
+
 def test_sddmm_dyadic_bit_exact():
     L = synth.dyadic_layer(40, 60, 1100, 900, seed=6, empty_rows=(2,), full_rows=(7,))
     gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
