@@ -228,15 +228,15 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
         return hip_status(e);
     }
     const double t = (double)eta * (double)lambda;     // exact in double
-    // scratch: per-slab counts, then their exclusive scan (the output layout)
+    // scratch: per-slab entry bounds and counts, then the counts' exclusive
+    // scan (the output layout)
     const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
-    int *counts = static_cast<int *>(ws);
-    int *off = counts + (((sizeof(int) * (size_t)n_slabs + 255) & ~(size_t)255) / sizeof(int));
     if (n_slabs > INT32_MAX) return L1CSR_EUNSUPPORTED;
-    hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, counts,
-                                     stream);
-    if (e == hipSuccess) e = launch_exclusive_scan(counts, off, (int)n_slabs, nullptr, stream);
-    if (e == hipSuccess) e = launch_prox_row_ptr(n_rows, n_cols, off, row_ptr_out, d_nnz_out, stream);
+    const prox_ws pw = prox_carve(n_rows, n_cols, ws);
+    hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, pw.seg,
+                                     pw.counts, stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(pw.counts, pw.off, (int)n_slabs, nullptr, stream);
+    if (e == hipSuccess) e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
     if (e != hipSuccess) return L1CSR_EHIP;
     if (capacity < total) {
         int32_t h = 0;
@@ -248,7 +248,7 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     } else if (h_nnz_required) {
         *h_nnz_required = -1;
     }
-    return hip_status(launch_prox_fill(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, off,
+    return hip_status(launch_prox_fill(n_rows, n_cols, pw.seg, col_idx, vals, G, ldg, eta, t, pw.off,
                                        col_idx_out, vals_out, capacity, stream));
 }
 

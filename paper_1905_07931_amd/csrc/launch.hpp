@@ -65,18 +65,24 @@ hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *
 hipError_t launch_prox_csr(int64_t nnz, float *vals, const float *g, float eta, double t,
                            hipStream_t s);
 // fused prox + recompression over row slabs (prox_slabs(n_cols) per row,
-// numbered row-major): counts per slab; their exclusive scan off[] (n_rows *
-// slabs + 1 entries) is the output layout; row_ptr[r] = off[r * slabs]; then
-// the compacted output.  Scratch: prox_recompress_workspace_bytes() holds the
-// counts and then off[] (256-byte aligned).
+// numbered row-major): per-(row, slab) entry bounds of W, counts per slab;
+// their exclusive scan off[] (n_rows * slabs + 1 entries) is the output
+// layout; row_ptr[r] = off[r * slabs]; then the compacted output.  Scratch:
+// prox_carve() splits prox_recompress_workspace_bytes() into counts, off and
+// the bounds (256-byte aligned parts).
 int prox_slabs(int n_cols);
+struct prox_ws {
+    int *counts, *off, *seg;
+    size_t bytes;
+};
+prox_ws prox_carve(int n_rows, int n_cols, void *ws);
 size_t prox_recompress_workspace_bytes(int n_rows, int n_cols);
 hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *idx,
                              const float *vals, const float *G, int64_t ldg, float eta, double t,
-                             int *counts, hipStream_t s);
+                             int *seg, int *counts, hipStream_t s);
 hipError_t launch_prox_row_ptr(int n_rows, int n_cols, const int *off, int *row_ptr, int *nnz_out,
                                hipStream_t s);
-hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *idx,
+hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *idx,
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
                             const int *off, int *col_out, float *val_out, int64_t capacity,
                             hipStream_t s);

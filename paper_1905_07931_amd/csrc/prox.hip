@@ -105,12 +105,15 @@ __global__ void prox_csr_kernel(int64_t nnz, float *__restrict__ vals, const flo
 //          chunk: one ballot per column slot, wave totals through LDS).
 // Slabs are numbered row-major, so the exclusive scan of the counts is
 // exactly the CSR layout of the result, and row_ptr[row] = off[row * S].
-constexpr int kSlab = 2048;
+// seg[row][j] (j = 0 .. S) = first entry of the row with column >= j * kSlab,
+// so a slab reads only its own entries of W.
+constexpr int kSlabShift = 11;
+constexpr int kSlab = 1 << kSlabShift;
 constexpr int kSlabChunks = kSlab / (kProxThreads * 4);
 
 template <bool V4, bool FILL>
 __global__ __launch_bounds__(kProxThreads) void prox_slab_kernel(
-    int n_cols, int slabs, const int *__restrict__ ptr, const int *__restrict__ idx,
+    int n_cols, int slabs, const int *__restrict__ seg, const int *__restrict__ idx,
     const float *__restrict__ vals, const float *__restrict__ G, int64_t ldg, double eta, double t,
     int *__restrict__ counts, const int *__restrict__ off, int *__restrict__ col_out,
     float *__restrict__ val_out, int64_t capacity) {
@@ -118,10 +121,12 @@ __global__ __launch_bounds__(kProxThreads) void prox_slab_kernel(
     __shared__ int wave_tot[kProxThreads / kWave];
     const int64_t blk = blockIdx.x;
     const int row = (int)(blk / slabs);
-    const int k0 = (int)(blk - (int64_t)row * slabs) * kSlab;
+    const int sl = (int)(blk - (int64_t)row * slabs);
+    const int k0 = sl * kSlab;
     const int k1 = min(n_cols, k0 + kSlab);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int s = ptr[row], e = ptr[row + 1];
+    const int *sr = seg + (int64_t)row * (slabs + 1) + sl;
+    const int s = sr[0], e = sr[1];
     const float *g = G + (int64_t)row * ldg;
     // every G load of the slab and the first W entries of the row in flight at once
     float4 gq[kSlabChunks];
@@ -261,24 +266,41 @@ namespace l1csr {
 
 int prox_slabs(int n_cols) { return n_cols > 0 ? (int)ceil_div(n_cols, kSlab) : 1; }
 
-size_t prox_recompress_workspace_bytes(int n_rows, int n_cols) {
+prox_ws prox_carve(int n_rows, int n_cols, void *ws) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t n = (size_t)n_rows * prox_slabs(n_cols);
-    return ((sizeof(int) * n + 255) & ~(size_t)255) + sizeof(int) * (n + 1);
+    prox_ws w{};
+    char *b = static_cast<char *>(ws);
+    size_t o = 0;
+    w.counts = reinterpret_cast<int *>(b + o);
+    o = al(o + sizeof(int) * n);
+    w.off = reinterpret_cast<int *>(b + o);
+    o = al(o + sizeof(int) * (n + 1));
+    w.seg = reinterpret_cast<int *>(b + o);
+    o += sizeof(int) * (size_t)n_rows * (prox_slabs(n_cols) + 1);
+    w.bytes = o;
+    return w;
+}
+
+size_t prox_recompress_workspace_bytes(int n_rows, int n_cols) {
+    return prox_carve(n_rows, n_cols, nullptr).bytes;
 }
 
 hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *idx,
                              const float *vals, const float *G, int64_t ldg, float eta, double t,
-                             int *counts, hipStream_t s) {
+                             int *seg, int *counts, hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     const bool v4 = (ldg % 4 == 0) && aligned16(G);
     const int slabs = prox_slabs(n_cols);
+    hipError_t e = launch_seg(n_rows, slabs, kSlabShift, ptr, idx, seg, s);
+    if (e != hipSuccess) return e;
     const unsigned grid = (unsigned)((int64_t)n_rows * slabs);
     if (v4)
         prox_slab_kernel<true, false><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
     else
         prox_slab_kernel<false, false><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
     return hipGetLastError();
 }
 
@@ -290,7 +312,7 @@ hipError_t launch_prox_row_ptr(int n_rows, int n_cols, const int *off, int *row_
     return hipGetLastError();
 }
 
-hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *idx,
+hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *idx,
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
                             const int *off, int *col_out, float *val_out, int64_t capacity,
                             hipStream_t s) {
@@ -300,11 +322,11 @@ hipError_t launch_prox_fill(int n_rows, int n_cols, const int *ptr, const int *i
     const unsigned grid = (unsigned)((int64_t)n_rows * slabs);
     if (v4)
         prox_slab_kernel<true, true><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
             capacity);
     else
         prox_slab_kernel<false, true><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, ptr, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
             capacity);
     return hipGetLastError();
 }
