@@ -132,24 +132,28 @@ __device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total)
 // One workgroup plans the pieces and the deal:
 //   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces
 //           (cap = max(64, ceil(nnz / (2 nw))), so there are at most
-//           n_rows + 2 nw pieces),
-//           piece j taking every k-th entry from the j-th; pbeg[row] = first
-//           piece of the row, piece[v] = (row, first position, j, k);
-//   order:  pieces by decreasing length bucket (the order inside a bucket only
-//           decides which wave computes a piece, never how it is summed);
-//   table:  slot i of wave g holds the piece at sorted position i*nw + g
-//           (snake order over rounds): (row, first strided position, k,
-//           entries), row = -1 for an empty slot.
+//           n_rows + 2 nw pieces), piece j taking every k-th entry from the
+//           j-th; pbeg[row] = index of the row's first piece (pieces are
+//           numbered row by row, which is the order the fix-up sums them in);
+//   deal:   pieces by decreasing length bucket, the piece at sorted position
+//           p going to slot i = p / nw of wave g = p mod nw, snake order over
+//           rounds (odd rounds reversed).  The order inside a bucket only
+//           decides which wave computes a piece, never how it is summed.
+//   table:  slot i of wave g = (row, first strided position, k, entries), row
+//           = -1 for an empty slot.
+// Rows are taken kPlanRows at a time (kPlanPer per thread, all loads issued
+// together) and kept in registers between the histogram and the deal.
+constexpr int kPlanPer = 8;
+constexpr int kPlanRows = kPlanThreads * kPlanPer;
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const int *__restrict__ ptr,
                                                             int nw, int rw,
                                                             int *__restrict__ pbeg,
-                                                            int4 *__restrict__ piece,
-                                                            int *__restrict__ order,
                                                             int4 *__restrict__ table) {
     __shared__ int wave_tot[kPlanThreads / kWave];
     __shared__ int hist[kBuckets];
     __shared__ int start[kBuckets];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // pieces of at most half the mean load per wave (from the actual number of
     // entries, read on the device): with the snake deal the heaviest and
     // lightest waves then differ by a few percent even for power-law row
@@ -157,58 +161,85 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const in
     const int64_t nnz = ptr[n_rows] - ptr[0];
     int64_t cap64 = (nnz + 2 * (int64_t)nw - 1) / (2 * (int64_t)nw);
     const int cap = (int)(cap64 < 64 ? 64 : (cap64 > INT32_MAX ? INT32_MAX : cap64));
-    // pieces
+    for (int b = tid; b < kBuckets; b += kPlanThreads) hist[b] = 0;
+    __syncthreads();
+    // pass 1: pieces per row, pbeg, bucket histogram
     int carry = 0;
-    for (int base = 0; base < n_rows; base += kPlanThreads) {
-        const int r = base + tid;
-        int first = 0, len = 0, k = 0;
-        if (r < n_rows) {
-            first = ptr[r];
-            len = ptr[r + 1] - first;
-            k = len > cap ? (len + cap - 1) / cap : 1;
+    for (int base = 0; base < n_rows; base += kPlanRows) {
+        int first[kPlanPer + 1];
+#pragma unroll
+        for (int u = 0; u <= kPlanPer; ++u) {
+            const int r = min(base + tid * kPlanPer + u, n_rows);
+            first[u] = ptr[r];
+        }
+        int kk[kPlanPer], mine = 0;
+#pragma unroll
+        for (int u = 0; u < kPlanPer; ++u) {
+            const int len = first[u + 1] - first[u];
+            kk[u] = base + tid * kPlanPer + u < n_rows ? (len > cap ? (len + cap - 1) / cap : 1) : 0;
+            mine += kk[u];
         }
         int total;
-        const int incl = block_incl_scan(k, wave_tot, total);
-        const int v0 = carry + incl - k;
-        if (r < n_rows) {
-            pbeg[r] = v0;
-            for (int j = 0; j < k; ++j) piece[v0 + j] = make_int4(r, first, j, k);
+        int v = carry + block_incl_scan(mine, wave_tot, total) - mine;
+#pragma unroll
+        for (int u = 0; u < kPlanPer; ++u) {
+            const int r = base + tid * kPlanPer + u;
+            if (r < n_rows) pbeg[r] = v;
+            const int len = first[u + 1] - first[u];
+            for (int j = 0; j < kk[u]; ++j) atomicAdd(&hist[length_key(piece_len(len, j, kk[u]))], 1);
+            v += kk[u];
         }
         carry += total;
     }
     const int n_pieces = carry;
     if (tid == 0) pbeg[n_rows] = n_pieces;
-    for (int b = tid; b < kBuckets; b += kPlanThreads) hist[b] = 0;
-    __syncthreads();  // also makes piece[] visible to the whole workgroup
-    // order
-    for (int v = tid; v < n_pieces; v += kPlanThreads) {
-        const int4 pc = piece[v];
-        atomicAdd(&hist[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1);
-    }
     __syncthreads();
-    if (tid == 0) {
-        int run = 0;
-        for (int b = kBuckets - 1; b >= 0; --b) {
-            start[b] = run;
-            run += hist[b];
+    // bucket starts, largest bucket first (one wave, three buckets per lane)
+    if (wave == 0) {
+        int h[3], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const int b = kBuckets - 1 - (lane * 3 + q);
+            h[q] = b >= 0 ? hist[b] : 0;
+            sum += h[q];
+        }
+        int run = wave_incl_scan(sum) - sum;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const int b = kBuckets - 1 - (lane * 3 + q);
+            if (b >= 0) start[b] = run;
+            run += h[q];
         }
     }
     __syncthreads();
-    for (int v = tid; v < n_pieces; v += kPlanThreads) {
-        const int4 pc = piece[v];
-        order[atomicAdd(&start[length_key(piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w))], 1)] = v;
-    }
-    __syncthreads();
-    // slot table
-    for (int64_t id = tid; id < (int64_t)nw * rw; id += kPlanThreads) {
-        const int g = (int)(id / rw), i = (int)(id - (int64_t)g * rw);
-        const int64_t j = (int64_t)i * nw + ((i & 1) ? (nw - 1 - g) : g);
-        int4 e = make_int4(-1, 0, 1, 0);
-        if (j < n_pieces) {
-            const int4 pc = piece[order[j]];
-            e = make_int4(pc.x, pc.y + pc.z, pc.w, piece_len(ptr[pc.x + 1] - pc.y, pc.z, pc.w));
+    // pass 2: deal every piece straight into its slot
+    for (int base = 0; base < n_rows; base += kPlanRows) {
+        int first[kPlanPer + 1];
+#pragma unroll
+        for (int u = 0; u <= kPlanPer; ++u) {
+            const int r = min(base + tid * kPlanPer + u, n_rows);
+            first[u] = ptr[r];
         }
-        table[id] = e;
+#pragma unroll
+        for (int u = 0; u < kPlanPer; ++u) {
+            const int r = base + tid * kPlanPer + u;
+            if (r >= n_rows) continue;
+            const int len = first[u + 1] - first[u];
+            const int k = len > cap ? (len + cap - 1) / cap : 1;
+            for (int j = 0; j < k; ++j) {
+                const int plen = piece_len(len, j, k);
+                const int pos = atomicAdd(&start[length_key(plen)], 1);
+                const int i = pos / nw, gq = pos - i * nw;
+                const int g = (i & 1) ? nw - 1 - gq : gq;
+                if (i < rw) table[(int64_t)g * rw + i] = make_int4(r, first[u] + j, k, plen);
+            }
+        }
+    }
+    // empty slots
+    for (int64_t pos = n_pieces + tid; pos < (int64_t)nw * rw; pos += kPlanThreads) {
+        const int i = (int)(pos / nw), gq = (int)(pos - (int64_t)i * nw);
+        const int g = (i & 1) ? nw - 1 - gq : gq;
+        table[(int64_t)g * rw + i] = make_int4(-1, 0, 1, 0);
     }
 }
 
@@ -229,13 +260,6 @@ struct tiled_cfg {
     static constexpr int HDR = ((2 * MAXRW + 15) / 16) * 16;  // chunk header: uint16 count per piece
     static_assert((1 << SHIFT) == KT, "tile height must be a power of two");
 };
-
-// the piece in slot i of wave g: sorted position i*nw + g, snake order over rounds
-__device__ __forceinline__ int slot_piece(int i, int g, int nw, int rw, int n_pieces,
-                                          const int *__restrict__ order) {
-    const int64_t j = (int64_t)i * nw + ((i & 1) ? (nw - 1 - g) : g);
-    return (i < rw && j < n_pieces) ? order[j] : -1;
-}
 
 // strided position bound of a piece in a tile: the number of its entries
 // (positions first + m*k, m = 0, 1, ...) that lie before position p
@@ -430,8 +454,8 @@ __device__ __forceinline__ void fma_unit(const char *xb, typename unit_t<HALF>::
 
 template <int VEC, bool HALF>
 __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
-    int rw, int n_cols, int ntiles, const int *__restrict__ n_pieces_ptr,
-    const int4 *__restrict__ piece, const int *__restrict__ order, const char *__restrict__ stream,
+    int rw, int n_cols, int ntiles, const int4 *__restrict__ table, const int *__restrict__ pbeg,
+    const int *__restrict__ ptr, const char *__restrict__ stream,
     const int *__restrict__ woff, const float *__restrict__ X, int64_t ldx, int B,
     float *__restrict__ Y, int64_t ldy, float *__restrict__ part, int nrb) {
     constexpr int BB = tiled_cfg<VEC, HALF>::BB, KT = tiled_cfg<VEC, HALF>::KT;
@@ -451,7 +475,6 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
     const int nw = nrb * kNW;
     const int g = rb * kNW + wave;
     const int b0 = ch * BB;
-    const int n_pieces = uniform(*n_pieces_ptr);
     int64_t off = woff[g];
 
     // async loads of tile t: X rows [t*KT, t*KT + KT) x columns [b0, b0 + BB)
@@ -594,11 +617,12 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
 #pragma unroll
     for (int i = 0; i < MAXRW; ++i) {
         if (i >= rw || half) continue;
-        const int pv = uniform(slot_piece(i, g, nw, rw, n_pieces, order));
-        if (pv < 0) continue;
-        const int4 pc = piece[pv];
-        const int row = uniform(pc.x);
-        const bool split = uniform(pc.w) > 1;
+        const int4 e = table[(int64_t)g * rw + i];
+        const int row = uniform(e.x);
+        if (row < 0) continue;
+        const bool split = uniform(e.z) > 1;
+        // pieces of a row are numbered from pbeg[row]; this one is j = first - ptr[row]
+        const int pv = split ? uniform(pbeg[row] + e.y - ptr[row]) : 0;
         float *dst = split ? part + (int64_t)pv * B + b : Y + (int64_t)row * ldy + b;
         if (b + VEC - 1 < B) {
             store_vec<VEC>(dst, acc[i]);
@@ -803,8 +827,6 @@ spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
 
 struct spmm_ws {
     int *pbeg;    // [n_rows + 1]
-    int4 *piece;  // [max_pieces]
-    int *order;   // [max_pieces]
     int *seg;     // [n_rows][ntiles + 1]
     int4 *table;  // [nw][rw]: slot table
     int *coff;    // [nw][ntiles]: chunk sizes, then offsets inside the wave's stream
@@ -823,10 +845,6 @@ spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     size_t off = 0;
     w.pbeg = reinterpret_cast<int *>(base + off);
     off = al(off + sizeof(int) * ((size_t)n_rows + 1));
-    w.piece = reinterpret_cast<int4 *>(base + off);
-    off = al(off + sizeof(int4) * (size_t)pl.max_pieces);
-    w.order = reinterpret_cast<int *>(base + off);
-    off = al(off + sizeof(int) * (size_t)pl.max_pieces);
     w.seg = reinterpret_cast<int *>(base + off);
     off = al(off + sizeof(int) * (size_t)n_rows * (pl.ntiles + 1));
     w.table = reinterpret_cast<int4 *>(base + off);
@@ -852,8 +870,7 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
     const int nw = pl.nrb * kNW;
     hipError_t e;
-    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, w.pbeg, w.piece, w.order, w.table);
-    const int *n_pieces = w.pbeg + n_rows;
+    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, w.pbeg, w.table);
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,
                                                              ptr, idx, w.seg);
     stream_size_kernel<VEC, HALF><<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.rw, pl.ntiles, w.table, w.seg,
@@ -867,8 +884,8 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
             nw, pl.rw, pl.ntiles, idx, vals, w.table, w.seg, w.coff, w.woff, w.stream);
     }
     const unsigned nblocks = (unsigned)((int64_t)pl.nrb * pl.nch);
-    spmm_stream_kernel<VEC, HALF><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, n_pieces, w.piece,
-                                                            w.order, w.stream, w.woff, X, ldx, B, Y,
+    spmm_stream_kernel<VEC, HALF><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, w.table, w.pbeg,
+                                                            ptr, w.stream, w.woff, X, ldx, B, Y,
                                                             ldy, w.part, pl.nrb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     fixup_kernel<<<(unsigned)n_rows, 256, 0, s>>>(n_rows, w.pbeg, w.part, B, Y, ldy);
