@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 METRIC = "sparse train-step GFLOP/s (nnz-effective) and achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_MFMA_F32_TFLOPS = 157.3   # MI355X dense fp32 matrix
+PEAK_MFMA_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -161,6 +162,19 @@ def main():
     per = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
            for i, n in enumerate(names)}
 
+    # dense dW with bf16 operands: reported beside the step, not part of it
+    dWb = torch.empty_like(dW)
+    L1.dense_wgrad(dY, X, dWb, precision=L1.BF16)
+    evb = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    evb[0].record()
+    for s in range(args.steps):
+        L1.dense_wgrad(dY, X, dWb, precision=L1.BF16)
+        evb[s + 1].record()
+    torch.cuda.synchronize()
+    bf16_ms = float(np.mean([evb[s].elapsed_time(evb[s + 1]) for s in range(args.steps)]))
+    del dWb
+
     nnz_out = int(Wout.row_ptr[-1].item())
     flops_step = 2.0 * nnz * B * 2 + 2.0 * N * K * B          # fwd + bwd + dense dW
     flops_nnz_only = 6.0 * nnz * B
@@ -208,6 +222,12 @@ def main():
         "prox_recompress_hbm_gbs": round(prox_recompress_gbs, 1),
         "prox_recompress_hbm_frac": round(prox_recompress_gbs / PEAK_HBM_GBS, 4),
         "nnz_out": nnz_out,
+        "dense_wgrad_bf16": {"ms": round(bf16_ms, 4),
+                             "tflops": round(wg_flops / (bf16_ms * 1e-3) / 1e12, 1),
+                             "peak": PEAK_MFMA_BF16_TFLOPS,
+                             "frac": round(wg_flops / (bf16_ms * 1e-3) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 4),
+                             "note": "operands rounded to bf16, exact products, fp32 sums; outside the "
+                                     "1e-4 fp32 contract and not part of the step"},
         "input_gen_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)

@@ -51,8 +51,15 @@ enum l1csr_status {
     L1CSR_OK = 0,
     L1CSR_EINVAL = -1,       /* bad argument; nothing launched */
     L1CSR_ECAPACITY = -2,    /* output capacity too small (csr_recompress) */
+    L1CSR_EBADCSR = -3,      /* malformed CSR (csr_validate, via its device status) */
     L1CSR_EHIP = -4,         /* a HIP runtime or launch error */
     L1CSR_EUNSUPPORTED = -5  /* valid but unsupported combination */
+};
+
+/* dense_wgrad operand precision */
+enum l1csr_precision {
+    L1CSR_F32 = 0,           /* fp32 operands, fp32 matrix cores: the 1e-4 contract */
+    L1CSR_BF16 = 1           /* operands rounded to bf16 (nearest even), exact products, fp32 sums */
 };
 
 /* prox_l1_step modes */
@@ -143,11 +150,18 @@ int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz,
  * the proximal step, Eq. (prox)):
  *     dW[i][k] = sum_{b < B} dY[i][b] * X[k][b]      (dW = dY . X^T)
  * dY [N][ldy], X [K][ldx], dW [N][ldw], ldw >= K.  No 1/B factor: dY carries
- * the loss scaling.  fp32 inputs and fp32 matrix-core accumulation.
+ * the loss scaling.  Inputs are fp32 in memory either way.
+ * precision L1CSR_F32: fp32 matrix-core products and sums.
+ * precision L1CSR_BF16: every dY and X element is rounded to bf16 (round to
+ *   nearest even) before it is multiplied; products are exact and summed in
+ *   fp32: each operand rounds by at most 2^-8 relative, so |dW - exact| <=
+ *   (2^-7 + 2^-16) sum_b |dY X| plus the fp32 summation error:
+ *   outside the fp32 accuracy contract, reported separately.
+ * Any other precision value returns L1CSR_EINVAL.
  */
 int dense_wgrad(int32_t N, int32_t K, int32_t B,
                 const float *dY, int64_t ldy, const float *X, int64_t ldx,
-                float *dW, int64_t ldw, hipStream_t stream);
+                float *dW, int64_t ldw, int precision, hipStream_t stream);
 
 /*
  * Weight gradient of the debiasing phase (Section 2.4: retrain without the
@@ -234,6 +248,18 @@ int csr_compact(int32_t n_rows, int64_t nnz,
                 const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
                 int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
                 int32_t *d_nnz_out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * CSR well-formedness check (the canonical form of Section 3.1 / Fig. 1 that
+ * every other call assumes): row_ptr[0] = 0, row_ptr non-decreasing,
+ * row_ptr[n_rows] = nnz, 0 <= col_idx < n_cols and strictly increasing inside
+ * each row.  Writes L1CSR_OK or L1CSR_EBADCSR to *d_status (one device int32)
+ * in stream order; the host return value only reports argument or launch
+ * errors.  Reads only row_ptr[0 .. n_rows] and col_idx[0 .. nnz), whatever
+ * they hold.  Not used by the hot calls.
+ */
+int csr_validate(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                 const int32_t *col_idx, int32_t *d_status, hipStream_t stream);
 
 /*
  * Layer glue of the fully connected ReLU networks the method trains (their

@@ -49,6 +49,9 @@ def lib():
         L.orc_spmm_fwd.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
         L.orc_spmm_bwd_t.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
         L.orc_dense_wgrad.argtypes = [i32, i32, i32, _f32p, i64, _f32p, i64, _f32p, i64]
+        L.orc_dense_wgrad_bf16.argtypes = [i32, i32, i32, _f32p, i64, _f32p, i64, _f32p, i64]
+        L.orc_bf16_round.argtypes = [f32]
+        L.orc_bf16_round.restype = f32
         L.orc_sddmm.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, i64, _f32p, i64, _f32p]
         L.orc_soft_threshold.argtypes = [C.c_double, C.c_double]
         L.orc_soft_threshold.restype = C.c_double
@@ -125,6 +128,24 @@ def dense_wgrad(dY, X):
     K = X.shape[0]
     dW = np.empty((N, K), np.float32)
     _check(lib().orc_dense_wgrad(N, K, B, dY, B, X, B, dW, K), "dense_wgrad")
+    return dW
+
+
+def bf16_round(x):
+    """Each element rounded to bf16 (8 significant bits, nearest even), as float32."""
+    x = _c(np.asarray(x, np.float32).reshape(-1), np.float32)
+    f = lib().orc_bf16_round
+    return np.array([f(float(v)) for v in x], np.float32)
+
+
+def dense_wgrad_bf16(dY, X):
+    """dW = bf16(dY).bf16(X)^T with exact products summed in double."""
+    dY = _c(dY, np.float32)
+    X = _c(X, np.float32)
+    N, B = dY.shape
+    K = X.shape[0]
+    dW = np.empty((N, K), np.float32)
+    _check(lib().orc_dense_wgrad_bf16(N, K, B, dY, B, X, B, dW, K), "dense_wgrad_bf16")
     return dW
 
 

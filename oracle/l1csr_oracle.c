@@ -138,6 +138,44 @@ int orc_dense_wgrad(int32_t N, int32_t K, int32_t B,
 }
 
 /* ------------------------------------------------------------------------
+ * bf16 rounding, written from its definition: keep 8 significant bits
+ * (1 implicit + 7 stored), round to nearest, ties to even.  frexp gives
+ * x = m 2^e with 0.5 <= |m| < 1, so m 2^8 holds the 8 kept bits in its integer
+ * part; nearbyint rounds it in the default (nearest-even) mode.  Finite inputs
+ * whose exponent is in the normal range of float (every input here).
+ * ---------------------------------------------------------------------- */
+float orc_bf16_round(float x) {
+    if (x == 0.0f) return x;
+    int e;
+    const double m = frexp((double)x, &e);
+    return (float)ldexp(nearbyint(ldexp(m, 8)), e - 8);
+}
+
+/* Dense weight gradient with bf16 operands (the reduced-precision variant of
+ * the l1-phase gradient): every element of dY and X is rounded to bf16 first,
+ * then dW[i][k] = sum_b bf16(dY[i][b]) * bf16(X[k][b]) in double, b ascending. */
+int orc_dense_wgrad_bf16(int32_t N, int32_t K, int32_t B,
+                         const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                         float *dW, int64_t ldw) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B || ldw < K) return ORC_EINVAL;
+    float *ry = (float *)malloc(sizeof(float) * ((size_t)N * B + 1));
+    float *rx = (float *)malloc(sizeof(float) * ((size_t)K * B + 1));
+    if (!ry || !rx) {
+        free(ry);
+        free(rx);
+        return ORC_EINVAL;
+    }
+    for (int32_t i = 0; i < N; ++i)
+        for (int32_t b = 0; b < B; ++b) ry[(int64_t)i * B + b] = orc_bf16_round(dY[(int64_t)i * ldy + b]);
+    for (int32_t k = 0; k < K; ++k)
+        for (int32_t b = 0; b < B; ++b) rx[(int64_t)k * B + b] = orc_bf16_round(X[(int64_t)k * ldx + b]);
+    const int rc = orc_dense_wgrad(N, K, B, ry, B, rx, B, dW, ldw);
+    free(ry);
+    free(rx);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------
  * Weight gradient of the debiasing phase (Section 2.4: retraining without the
  * regulariser, zero-valued weights excluded from training).  The gradient is
  * the dense one sampled on W's pattern:

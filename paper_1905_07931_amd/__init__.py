@@ -16,14 +16,15 @@ from dataclasses import dataclass
 __all__ = [
     "CSR", "CSC", "L1CSRError", "lib", "status_str", "workspace_bytes",
     "csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
-    "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "relu_fwd", "relu_bwd", "softmax_xent",
-    "PROX_DENSE", "PROX_CSR",
+    "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "csr_validate", "relu_fwd", "relu_bwd",
+    "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
 
-OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED = 0, -1, -2, -4, -5
+OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PROX_DENSE, PROX_CSR = 0, 1
+F32, BF16 = 0, 1
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
 OP_PROX_RECOMPRESS = 7
 
@@ -55,7 +56,7 @@ def lib():
         L.csc_update_vals.argtypes = [i32, i64, vp, vp, vp, vp, vp]
         L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
                                      vp, sz, vp]
-        L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
+        L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, C.c_int, vp]
         L.sddmm_masked_wgrad.argtypes = [i32, i32, i64, vp, vp, vp, i64, vp, i64, i32, vp, vp, sz, vp]
         L.prox_l1_step.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, i64,
                                    vp, vp]
@@ -64,12 +65,13 @@ def lib():
         L.prox_l1_recompress.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp,
                                          i64, vp, C.POINTER(C.c_int64), vp, sz, vp]
         L.csr_compact.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csr_validate.argtypes = [i32, i32, i64, vp, vp, vp, vp]
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
         L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
-                     "csr_compact", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
+                     "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -291,8 +293,9 @@ def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
     return dX
 
 
-def dense_wgrad(dY, X, dW=None, stream=None):
-    """dW = dY . X^T on the fp32 matrix cores."""
+def dense_wgrad(dY, X, dW=None, precision=F32, stream=None):
+    """dW = dY . X^T on the matrix cores: fp32 operands (F32), or operands
+    rounded to bf16 with exact products and fp32 sums (BF16)."""
     torch = _torch()
     N, B, ldy = _mat(dY, "dY")
     K, Bx, ldx = _mat(X, "X")
@@ -303,8 +306,8 @@ def dense_wgrad(dY, X, dW=None, stream=None):
     Nw, Kw, ldw = _mat(dW, "dW")
     if (Nw, Kw) != (N, K):
         raise ValueError("dW must be [N][K]")
-    _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, _stream(stream)),
-           "dense_wgrad")
+    _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, int(precision),
+                             _stream(stream)), "dense_wgrad")
     return dW
 
 
@@ -418,6 +421,26 @@ def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:
            "csr_compact")
     out.nnz = None
     return out
+
+
+def csr_validate(W: CSR, nnz: int | None = None, stream=None) -> bool:
+    """Check on the device that W is a canonical CSR (row_ptr[0] = 0,
+    non-decreasing, row_ptr[N] = nnz, columns in range and strictly increasing
+    in each row).  Waits for the device status and returns True if well formed."""
+    torch = _torch()
+    _vec(W.row_ptr, torch.int32, "row_ptr")
+    _vec(W.col_idx, torch.int32, "col_idx")
+    if W.row_ptr.numel() != W.n_rows + 1:
+        raise ValueError("row_ptr must hold n_rows + 1 entries")
+    n = W.nnz if nnz is None else int(nnz)
+    if n is None:
+        n = W.host_nnz()
+    if n < 0 or n > W.col_idx.numel():
+        raise ValueError("nnz must lie within col_idx")
+    status = torch.empty(1, dtype=torch.int32, device=W.row_ptr.device)
+    _check(lib().csr_validate(W.n_rows, W.n_cols, n, _p(W.row_ptr), _p(W.col_idx), _p(status),
+                              _stream(stream)), "csr_validate")
+    return int(status.item()) == OK
 
 
 def relu_fwd(x, y=None, stream=None):

@@ -46,6 +46,7 @@ const char *l1csr_status_str(int status) {
         case L1CSR_OK: return "ok";
         case L1CSR_EINVAL: return "invalid argument";
         case L1CSR_ECAPACITY: return "output capacity too small";
+        case L1CSR_EBADCSR: return "malformed CSR";
         case L1CSR_EHIP: return "HIP runtime or launch error";
         case L1CSR_EUNSUPPORTED: return "unsupported size or combination";
         default: return "unknown status";
@@ -125,11 +126,14 @@ int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *r
 }
 
 int dense_wgrad(int32_t N, int32_t K, int32_t B, const float *dY, int64_t ldy, const float *X,
-                int64_t ldx, float *dW, int64_t ldw, hipStream_t stream) {
+                int64_t ldx, float *dW, int64_t ldw, int precision, hipStream_t stream) {
     if (N < 0 || K < 0 || B < 0) return L1CSR_EINVAL;
+    if (precision != L1CSR_F32 && precision != L1CSR_BF16) return L1CSR_EINVAL;
     if (bad_dense(dY, N, B, ldy) || bad_dense(X, K, B, ldx) || bad_dense(dW, N, K, ldw))
         return L1CSR_EINVAL;
     if (ceil_div(N, 128) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    if (precision == L1CSR_BF16)
+        return hip_status(launch_wgrad_bf16(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
     return hip_status(launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
 }
 
@@ -274,6 +278,14 @@ int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32
         e = launch_compact_fill(n_rows, row_ptr, col_idx, vals, row_ptr_out, col_idx_out, vals_out,
                                 stream);
     return hip_status(e);
+}
+
+int csr_validate(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                 const int32_t *col_idx, int32_t *d_status, hipStream_t stream) {
+    if (n_rows < 0 || n_cols < 0 || nnz < 0 || nnz > INT32_MAX) return L1CSR_EINVAL;
+    if (row_ptr == nullptr || d_status == nullptr || (nnz > 0 && col_idx == nullptr))
+        return L1CSR_EINVAL;
+    return hip_status(launch_csr_validate(n_rows, n_cols, nnz, row_ptr, col_idx, d_status, stream));
 }
 
 int l1csr_relu_fwd(int64_t n, const float *x, float *y, hipStream_t stream) {

@@ -45,6 +45,9 @@ hipError_t launch_fill_rows_f32(float *p, int64_t rows, int64_t cols, int64_t ld
 // gemm.hip -----------------------------------------------------------------
 hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                             int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
+// the same with operands rounded to bf16 (wgrad_bf16.hip)
+hipError_t launch_wgrad_bf16(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                             int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
 // gv[p] = (dY . X^T)[row(p)][col(p)] through 128x128 matrix-core tiles of the
 // dense product; seg[row][t] = first entry of the row with column >= 128 t,
 // t = 0 .. ceil(K / 128) (launch_seg with shift 7)
@@ -95,6 +98,9 @@ hipError_t launch_recompress_fill(int n_rows, int n_cols, const float *Z, int64_
                                   hipStream_t s);
 hipError_t launch_compact_count(int n_rows, const int *ptr, const float *vals, int *counts,
                                 hipStream_t s);
+// *status = L1CSR_OK or L1CSR_EBADCSR (canonical CSR check)
+hipError_t launch_csr_validate(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                               int *status, hipStream_t s);
 hipError_t launch_compact_fill(int n_rows, const int *ptr, const int *idx, const float *vals,
                                const int *ptr_out, int *idx_out, float *vals_out, hipStream_t s);
 

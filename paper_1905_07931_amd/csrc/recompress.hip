@@ -8,6 +8,7 @@
 //                  + (entries kept by this lane's lower slots)
 // which is column order, so the output is the canonical CSR.  Row pointers
 // come from an exclusive scan of per-row counts.
+#include "../../include/l1csr.h"
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -174,6 +175,48 @@ hipError_t launch_compact_count(int n_rows, const int *ptr, const float *vals, i
     if (n_rows == 0) return hipSuccess;
     compact_count_kernel<<<(unsigned)ceil_div(n_rows, kRowsPerBlock), 256, 0, s>>>(n_rows, ptr, vals,
                                                                                   counts);
+    return hipGetLastError();
+}
+
+namespace {
+
+// One wave per row: pointer checks, then the row's columns in chunks of 64
+// (range and strict increase against the previous entry).  Reads are kept
+// inside row_ptr[0 .. n_rows] and col_idx[0 .. nnz) whatever they hold; a
+// violating wave stores L1CSR_EBADCSR (all writers store the same value).
+__global__ __launch_bounds__(256) void csr_validate_kernel(int n_rows, int n_cols, int64_t nnz,
+                                                           const int *__restrict__ ptr,
+                                                           const int *__restrict__ idx,
+                                                           int *__restrict__ status) {
+    const int lane = threadIdx.x & 63;
+    if (n_rows == 0) {
+        if (blockIdx.x == 0 && threadIdx.x == 0 && (ptr[0] != 0 || nnz != 0)) *status = L1CSR_EBADCSR;
+        return;
+    }
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= n_rows) return;
+    const int s = ptr[row], e = ptr[row + 1];
+    bool bad = (row == 0 && s != 0) || (row == n_rows - 1 && (int64_t)e != nnz) || s < 0 || e < s ||
+               (int64_t)e > nnz;
+    if (!bad) {
+        for (int p = s + lane; p < e; p += kWave) {
+            const int c = idx[p];
+            bool b = c < 0 || c >= n_cols;
+            if (p > s) b = b || idx[p - 1] >= c;
+            bad = bad || b;
+        }
+    }
+    if (wave_ballot(bad) != 0 && lane == 0) *status = L1CSR_EBADCSR;
+}
+
+}  // namespace
+
+hipError_t launch_csr_validate(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                               int *status, hipStream_t s) {
+    hipError_t e = launch_fill_i32(status, 1, L1CSR_OK, s);
+    if (e != hipSuccess) return e;
+    const unsigned grid = n_rows == 0 ? 1u : (unsigned)ceil_div(n_rows, 4);
+    csr_validate_kernel<<<grid, 256, 0, s>>>(n_rows, n_cols, nnz, ptr, idx, status);
     return hipGetLastError();
 }
 

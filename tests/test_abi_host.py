@@ -16,7 +16,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "l1csr.h")
 LIB = os.path.join(ROOT, "paper_1905_07931_amd", "libl1csr.so")
 
-OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED = 0, -1, -2, -4, -5
+OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 NO_GPU = not os.path.exists("/dev/kfd")
 
 
@@ -44,7 +44,7 @@ def test_header_declares_the_hot_path_calls():
     names = declared_functions()
     for n in ["csr_spmm_fwd", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad", "prox_l1_step",
               "csr_recompress", "prox_l1_recompress", "csc_build", "csc_update_vals", "csr_compact",
-              "l1csr_workspace_bytes", "l1csr_status_str"]:
+              "csr_validate", "l1csr_workspace_bytes", "l1csr_status_str"]:
         assert n in names, n
 
 
@@ -55,11 +55,11 @@ def test_library_exports_every_declared_function(lib):
 
 def test_status_strings(lib):
     seen = set()
-    for code in (OK, EINVAL, ECAPACITY, EHIP, EUNSUPPORTED):
+    for code in (OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED):
         s = lib.l1csr_status_str(code).decode()
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == 5
+    assert len(seen) == 6
     assert lib.l1csr_status_str(12345).decode() == "unknown status"
 
 
@@ -93,7 +93,9 @@ def _setup(lib):
                                  C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
                                  C.c_size_t, C.c_void_p]
     lib.dense_wgrad.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
-                                C.c_int64, C.c_void_p, C.c_int64, C.c_void_p]
+                                C.c_int64, C.c_void_p, C.c_int64, C.c_int, C.c_void_p]
+    lib.csr_validate.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
+                                 C.c_void_p]
     lib.prox_l1_step.argtypes = [C.c_int, C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_int64, C.c_float, C.c_float, C.c_void_p,
                                  C.c_int64, C.c_void_p, C.c_void_p]
@@ -127,10 +129,17 @@ def test_invalid_arguments_are_rejected_before_launch(lib):
     assert lib.csr_spmm_fwd(4, 4, 17, P, P, P, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
     assert lib.l1csr_workspace_bytes(4, 4096, 300, 61440, 1024) > 1
     assert lib.csr_spmm_fwd(4096, 300, 61440, P, P, P, P, 1024, 1024, P, 1024, P, 1, S) == EINVAL
-    # dense dW: short ld, missing output
-    assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, S) == EINVAL
+    # dense dW: short ld, missing output, unknown precision
+    assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, 1, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, 2, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, -1, S) == EINVAL
+    # CSR check: negative sizes, missing status or columns
+    assert lib.csr_validate(-1, 4, 0, P, P, P, S) == EINVAL
+    assert lib.csr_validate(4, 4, 3, P, P, NUL, S) == EINVAL
+    assert lib.csr_validate(4, 4, 3, P, NUL, P, S) == EINVAL
+    assert lib.csr_validate(4, 4, -2, P, P, P, S) == EINVAL
     # prox: non-finite or negative eta / lambda, bad mode
     nan, inf = float("nan"), float("inf")
     for eta, lam in [(nan, 0.1), (0.1, nan), (inf, 0.1), (0.1, -1.0), (-0.1, 0.1)]:

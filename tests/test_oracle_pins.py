@@ -207,6 +207,52 @@ def test_dense_wgrad_batch_one_is_exact_outer_product():
     assert np.array_equal(dW, dy * x.T)  # float32 products are correctly rounded
 
 
+def test_bf16_rounding_closed_forms():
+    # bf16 keeps 8 significant bits; the IEEE rule is round to nearest, ties to
+    # the even kept last bit.  Each case is fixed by that definition alone.
+    cases = [
+        (1 + 2 ** -8, 1.0),                  # halfway, kept last bit 0 -> down
+        (1 + 2 ** -7 + 2 ** -8, 1 + 2 ** -6),  # halfway, kept last bit 1 -> up to even
+        (1 + 2 ** -8 + 2 ** -20, 1 + 2 ** -7),  # just above halfway -> up
+        (1 + 2 ** -8 - 2 ** -20, 1.0),        # just below halfway -> down
+        (-(1 + 2 ** -8), -1.0),               # symmetric in the sign
+        (2 - 2 ** -9, 2.0),                   # carries into the next binade
+        (3.0, 3.0), (0.0, 0.0), (-0.5, -0.5),
+        (0.1, 205 * 2.0 ** -11),              # 0x3DCCCCCD -> 0x3DCD = (1 + 77/128) 2^-4
+    ]
+    got = oracle.bf16_round(np.array([c[0] for c in cases], np.float32))
+    for (x, want), g in zip(cases, got):
+        assert float(g) == want, (x, float(g), want)
+    # every output has at most 8 significant bits and lies within half a bf16
+    # ulp (2^-8 relative) of its input
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(20000) * np.exp(rng.uniform(-20, 20, 20000))).astype(np.float32)
+    r = oracle.bf16_round(x)
+    assert np.all((r.view(np.uint32) & 0xFFFF) == 0)
+    assert np.all(np.abs(r.astype(np.float64) - x) <= 2.0 ** -8 * np.abs(x.astype(np.float64)))
+
+
+def test_dense_wgrad_bf16_pins():
+    rng = np.random.default_rng(11)
+    # operands already on the bf16 grid: the same numbers as the fp32 definition
+    dY = oracle.bf16_round(rng.standard_normal(37 * 19)).reshape(37, 19)
+    X = oracle.bf16_round(rng.random(23 * 19)).reshape(23, 19)
+    assert np.array_equal(oracle.dense_wgrad_bf16(dY, X), oracle.dense_wgrad(dY, X))
+    # B = 1: one product of the rounded operands, exact in float32
+    dy = rng.standard_normal((29, 1)).astype(np.float32)
+    x = rng.standard_normal((31, 1)).astype(np.float32)
+    want = oracle.bf16_round(dy).reshape(29, 1) * oracle.bf16_round(x).reshape(1, 31)
+    assert np.array_equal(oracle.dense_wgrad_bf16(dy, x), want)
+    # within the rounding bound of the fp32 result: each operand moves by at most
+    # 2^-8 relative, so |d(ab)| <= (2^-7 + 2^-16)|ab|
+    dY = rng.standard_normal((40, 300)).astype(np.float32)
+    X = rng.random((50, 300)).astype(np.float32)
+    m = np.abs(dY.astype(np.float64)) @ np.abs(X.T.astype(np.float64))
+    d = np.abs(oracle.dense_wgrad_bf16(dY, X).astype(np.float64) - oracle.dense_wgrad(dY, X))
+    assert np.all(d <= (2.0 ** -7 + 2.0 ** -16) * m + 2.0 ** -23 * m)
+    assert np.max(d / m) > 2.0 ** -14  # and the rounding does show
+
+
 def test_dyadic_exact_integer_brute_force():
     L = synth.dyadic_layer(23, 41, 19, 300, seed=9, empty_rows=(2,), full_rows=(5,))
     Wi = np.rint(_dense(L) * 16).astype(np.int64)

@@ -219,6 +219,83 @@ def test_dense_wgrad_dyadic_bit_exact():
     assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
 
 
+# bf16 operands: against the oracle that rounds the operands to bf16 first
+# (products exact, so only fp32 summation separates the two: the 1e-4 bar),
+# and within the bf16 rounding bound of the fp32 result
+@pytest.mark.parametrize("NKB", [(1, 1, 1), (7, 5, 3), (129, 130, 33), (300, 784, 64),
+                                 (257, 1000, 100), (64, 300, 256), (256, 384, 1024), (5, 9, 0)])
+def test_dense_wgrad_bf16(NKB):
+    N, K, B = NKB
+    rng = np.random.default_rng(N * 11 + K)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    X = rng.random((K, B)).astype(np.float32)
+    dW = h(L1.dense_wgrad(t(dY), t(X), precision=L1.BF16))
+    ref = oracle.dense_wgrad_bf16(dY, X)
+    m = oracle.dense_wgrad_bf16(np.abs(dY), X)
+    assert_scaled_close(dW, ref, m, what="dW bf16")
+    m32 = oracle.dense_wgrad(np.abs(dY), X).astype(np.float64)
+    d32 = np.abs(dW.astype(np.float64) - oracle.dense_wgrad(dY, X))
+    assert np.all(d32 <= (2.0 ** -7 + 2.0 ** -16 + 1e-4) * m32 + 1e-30)
+
+
+def test_dense_wgrad_bf16_batch_one_bit_exact_and_padded():
+    # B = 1: each entry is one exact product of the rounded operands, so the
+    # rounding of every operand is checked bit for bit
+    rng = np.random.default_rng(2)
+    dY = rng.standard_normal((70, 1)).astype(np.float32)
+    X = rng.standard_normal((150, 1)).astype(np.float32)
+    assert bits_equal(h(L1.dense_wgrad(t(dY), t(X), precision=L1.BF16)), oracle.dense_wgrad_bf16(dY, X))
+    import torch
+    dY2 = rng.standard_normal((33, 45)).astype(np.float32)
+    X2 = rng.random((66, 45)).astype(np.float32)
+    dYp = torch.zeros((33, 47), device=cuda()); dYp[:, :45] = t(dY2)
+    Xp = torch.zeros((66, 51), device=cuda()); Xp[:, :45] = t(X2)
+    dWp = torch.full((33, 70), 3.0, device=cuda())
+    L1.dense_wgrad(dYp[:, :45], Xp[:, :45], dWp[:, :66], precision=L1.BF16)
+    assert_scaled_close(h(dWp)[:, :66], oracle.dense_wgrad_bf16(dY2, X2),
+                        oracle.dense_wgrad_bf16(np.abs(dY2), X2), what="dW bf16")
+    assert np.all(h(dWp)[:, 66:] == 3.0)
+
+
+# ----------------------------------------------------------------------------
+# CSR well-formedness check
+# ----------------------------------------------------------------------------
+
+def test_csr_validate():
+    import torch
+    L = synth.fc_layer(300, 784, 1, 23520, seed=0)
+    good = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+    assert L1.csr_validate(good)
+    empty = L1.CSR.from_host(np.zeros(6, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), 9,
+                             device=cuda())
+    assert L1.csr_validate(empty)
+    none = L1.CSR(0, 5, torch.zeros(1, dtype=torch.int32, device=cuda()),
+                  torch.zeros(1, dtype=torch.int32, device=cuda()),
+                  torch.zeros(1, dtype=torch.float32, device=cuda()), 0)
+    assert L1.csr_validate(none)
+
+    def broken(edit):
+        rp, ci = L.row_ptr.copy(), L.col_idx.copy()
+        edit(rp, ci)
+        W = L1.CSR(L.N, L.K, t(rp), t(ci), t(L.vals), L.nnz)
+        return L1.csr_validate(W, nnz=L.nnz)
+
+    r5 = int(L.row_ptr[5])
+    assert not broken(lambda rp, ci: rp.__setitem__(0, 1))                        # row_ptr[0] != 0
+    assert not broken(lambda rp, ci: rp.__setitem__(7, rp[6] - 1))                # decreasing
+    assert not broken(lambda rp, ci: rp.__setitem__(L.N, L.nnz - 1))              # last != nnz
+    assert not broken(lambda rp, ci: ci.__setitem__(r5, L.K))                      # column out of range
+    assert not broken(lambda rp, ci: ci.__setitem__(r5, -1))                       # negative column
+    assert not broken(lambda rp, ci: ci.__setitem__(r5 + 1, ci[r5]))               # duplicate
+    assert not broken(lambda rp, ci: ci.__setitem__(slice(r5, r5 + 2), ci[r5:r5 + 2][::-1].copy()))  # unsorted
+    # a column order that only breaks across a row boundary is fine
+    assert broken(lambda rp, ci: None)
+    bad0 = L1.CSR(0, 5, torch.full((1,), 2, dtype=torch.int32, device=cuda()),
+                  torch.zeros(1, dtype=torch.int32, device=cuda()),
+                  torch.zeros(1, dtype=torch.float32, device=cuda()), 0)
+    assert not L1.csr_validate(bad0)
+
+
 # ----------------------------------------------------------------------------
 # masked weight gradient
 # ----------------------------------------------------------------------------
