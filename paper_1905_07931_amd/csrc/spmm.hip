@@ -634,16 +634,30 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
     }
 }
 
-// Y[row] = sum of the partial rows of its pieces, in piece order (split rows only)
+// Y[row] = sum of the partial rows of its pieces, in piece order (split rows
+// only).  Block (row, batch chunk of kFixupCols); the loads of all pieces are
+// issued before the sum.
+constexpr int kFixupCols = 1024;
+
 __global__ __launch_bounds__(256) void fixup_kernel(int n_rows, const int *__restrict__ pbeg,
                                                     const float *__restrict__ part, int B,
                                                     float *__restrict__ Y, int64_t ldy) {
     const int row = blockIdx.x;
     const int v0 = pbeg[row], v1 = pbeg[row + 1];
     if (v1 - v0 < 2) return;
-    for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    const int b1 = min(B, (int)(blockIdx.y + 1) * kFixupCols);
+    for (int b = blockIdx.y * kFixupCols + threadIdx.x; b < b1; b += blockDim.x) {
+        constexpr int U = 8;
         float a = 0.f;
-        for (int v = v0; v < v1; ++v) a += part[(int64_t)v * B + b];
+        int v = v0;
+        for (; v + U <= v1; v += U) {
+            float t[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) t[u] = part[(int64_t)(v + u) * B + b];
+#pragma unroll
+            for (int u = 0; u < U; ++u) a += t[u];
+        }
+        for (; v < v1; ++v) a += part[(int64_t)v * B + b];
         Y[(int64_t)row * ldy + b] = a;
     }
 }
@@ -659,14 +673,20 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(int n_rows, const int *_
                                                         const int *__restrict__ idx,
                                                         const float *__restrict__ vals,
                                                         const float *__restrict__ X, int64_t ldx,
-                                                        int B, float *__restrict__ Y, int64_t ldy) {
-    const int row = uniform(blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6));
+                                                        int B, float *__restrict__ Y, int64_t ldy,
+                                                        int nrb) {
+    // blocks of one XCD take a contiguous run of batch chunks, so the rows that
+    // share an X row segment read it through the same L2
+    int rb, ch;
+    map_block(blockIdx.x, gridDim.x, nrb, rb, ch);
+    const int row = uniform(rb * kRowsPerBlock + (threadIdx.x >> 6));
     if (row >= n_rows) return;
     const int lane = threadIdx.x & 63;
-    const int b = (blockIdx.y * kWave + lane) * VEC;
+    const int b = (ch * kWave + lane) * VEC;
     const bool active = b < B;
     const int start = uniform(ptr[row]);
     const int end = uniform(ptr[row + 1]);
+    constexpr int U = 8;  // X row segments in flight per wave
 
     float acc[VEC];
 #pragma unroll
@@ -681,23 +701,16 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(int n_rows, const int *_
             v = vals[base + lane];
         }
         int j = 0;
-        for (; j + 4 <= n; j += 4) {
-            const int c0 = lane_bcast(c, j), c1 = lane_bcast(c, j + 1);
-            const int c2 = lane_bcast(c, j + 2), c3 = lane_bcast(c, j + 3);
-            const float v0 = lane_bcast(v, j), v1 = lane_bcast(v, j + 1);
-            const float v2 = lane_bcast(v, j + 2), v3 = lane_bcast(v, j + 3);
+        for (; j + U <= n; j += U) {
+            float x[U][VEC];
             if (active) {
-                float x0[VEC], x1[VEC], x2[VEC], x3[VEC];
-                load_vec<VEC>(X + (int64_t)c0 * ldx + b, x0);
-                load_vec<VEC>(X + (int64_t)c1 * ldx + b, x1);
-                load_vec<VEC>(X + (int64_t)c2 * ldx + b, x2);
-                load_vec<VEC>(X + (int64_t)c3 * ldx + b, x3);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    acc[e] = fmaf(v0, x0[e], acc[e]);
-                    acc[e] = fmaf(v1, x1[e], acc[e]);
-                    acc[e] = fmaf(v2, x2[e], acc[e]);
-                    acc[e] = fmaf(v3, x3[e], acc[e]);
+                for (int u = 0; u < U; ++u) load_vec<VEC>(X + (int64_t)lane_bcast(c, j + u) * ldx + b, x[u]);
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const float vu = lane_bcast(v, j + u);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[e] = fmaf(vu, x[u][e], acc[e]);
                 }
             }
         }
@@ -888,7 +901,8 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
                                                             ptr, w.stream, w.woff, X, ldx, B, Y,
                                                             ldy, w.part, pl.nrb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    fixup_kernel<<<(unsigned)n_rows, 256, 0, s>>>(n_rows, w.pbeg, w.part, B, Y, ldy);
+    fixup_kernel<<<dim3((unsigned)n_rows, (unsigned)ceil_div(B, kFixupCols)), 256, 0, s>>>(
+        n_rows, w.pbeg, w.part, B, Y, ldy);
     return hipGetLastError();
 }
 
@@ -922,13 +936,15 @@ hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, cons
         return run_tiled<2, false>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
     }
     const int vec = v4 ? 4 : (v2 ? 2 : 1);
-    dim3 grid((unsigned)ceil_div(n_rows, kRowsPerBlock), (unsigned)ceil_div(B, kWave * vec));
+    const int64_t nrb = ceil_div(n_rows, kRowsPerBlock), nch = ceil_div(B, kWave * vec);
+    if (nrb * nch > INT32_MAX) return hipErrorInvalidConfiguration;
+    const unsigned grid = (unsigned)(nrb * nch);
     if (vec == 4)
-        spmm_rows_kernel<4><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy);
+        spmm_rows_kernel<4><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
     else if (vec == 2)
-        spmm_rows_kernel<2><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy);
+        spmm_rows_kernel<2><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
     else
-        spmm_rows_kernel<1><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy);
+        spmm_rows_kernel<1><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
     return hipGetLastError();
 }
 
