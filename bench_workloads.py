@@ -43,6 +43,30 @@ def _timed(torch, step, steps, warmup, names):
     return ms, per
 
 
+def _graph_timed(torch, step, steps):
+    """The same step captured once into a HIP graph (torch.cuda.CUDAGraph) and
+    replayed back to back: the GPU time without the host's per-launch cost."""
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # workspaces for the capture stream are allocated here
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
 def _line(workload, flops, ms, cfg, per=None, **extra):
     out = {"metric": METRIC, "value": round(flops / (ms * 1e-3) / 1e9, 1), "unit": "GFLOP/s",
            "n_gpus": 1, "ms_per_step": round(ms, 4), "higher_is_better": True, "dtype": "f32",
@@ -82,10 +106,14 @@ def fc784x300(args, dev):
         mark(4); L1.prox_l1_recompress(W, dW, L.eta, L.lam, out=Wout)
         mark(5)
     ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+    nnz_out = int(Wout.row_ptr[-1].item())
+    Wout.nnz = nnz_out
+    ms_graph = _graph_timed(torch, step, max(args.steps, 20))
     flops = 4.0 * L.nnz * L.B + 2.0 * L.N * L.K * L.B
     yield _line("fc784x300_b64_d10_l1_step", flops, ms,
                 dict(N=L.N, K=L.K, B=L.B, nnz=L.nnz, density=0.10), per,
-                nnz_out=int(Wout.row_ptr[-1].item()))
+                nnz_out=nnz_out, ms_per_step_graph=round(ms_graph, 4),
+                value_graph=round(flops / (ms_graph * 1e-3) / 1e9, 1))
 
 
 def mlp784(args, dev):
@@ -144,12 +172,14 @@ def mlp784(args, dev):
         w.nnz = None
         known[j] = w.host_nnz()
     ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), ["l1_step", "debias_step"])
+    ms_graph = _graph_timed(torch, step, max(args.steps, 20))
     nnz0 = [l.nnz for l in layers]
     nnz1 = [w.nnz for w in W1]
     flops = sum(4.0 * a * B + 2.0 * n * k * B for a, (n, k) in zip(nnz0, shapes)) + \
         sum(6.0 * a * B for a in nnz1)
     yield _line("mlp784_300_100_10_b256_l1_then_debias", flops, ms,
-                dict(B=B, nnz=nnz0, nnz_after_l1=nnz1), per)
+                dict(B=B, nnz=nnz0, nnz_after_l1=nnz1), per, ms_per_step_graph=round(ms_graph, 4),
+                value_graph=round(flops / (ms_graph * 1e-3) / 1e9, 1))
 
 
 def conv2(args, dev):
@@ -181,10 +211,12 @@ def conv2(args, dev):
         mark(5); L1.csr_compact(W, Wc)
         mark(6)
     ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+    ms_graph = _graph_timed(torch, step, max(args.steps, 20))
     flops = 6.0 * L.nnz * L.B
     # SDDMM reads X and dY once at least: the HBM roof of this shape
     sddmm_bytes = 4.0 * (L.K + L.N) * L.B + 12.0 * L.nnz
     yield _line("conv2_im2col_50x500_b16384_d10", flops, ms, dict(N=L.N, K=L.K, B=L.B, nnz=L.nnz), per,
+                ms_per_step_graph=round(ms_graph, 4), value_graph=round(flops / (ms_graph * 1e-3) / 1e9, 1),
                 sddmm_hbm_gbs=round(sddmm_bytes / (per["sddmm_masked_wgrad"] * 1e-3) / 1e9, 1),
                 spmm_fwd_hbm_gbs=round((4.0 * (L.K + L.N) * L.B + 8.0 * L.nnz) /
                                        (per["csr_spmm_fwd"] * 1e-3) / 1e9, 1))

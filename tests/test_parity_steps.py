@@ -367,3 +367,61 @@ def test_fc4096_density_sweep_alternating_steps(pct):
     # the pattern changes by a few percent per l1 step, not wholesale
     for a, b in zip(history[::2], history[2::2]):
         assert abs(b - a) <= 0.25 * max(a, 1)
+
+
+def test_graph_replays_match_eager():
+    """The l1 step of the 784 -> 300 layer followed by a debiasing step on its
+    output, captured once into a HIP graph (torch.cuda.CUDAGraph) and replayed
+    three times with eager work and host waits in between: every replay gives
+    the eager result bit for bit (all the kernels are deterministic), after
+    the outputs were overwritten with garbage."""
+    import torch
+    L = synth.fc784_300(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = t(L.X), t(L.dY)
+    X2 = t(np.flip(L.X, 1).copy())
+    Y = torch.empty((L.N, L.B), device=dev)
+    dX = torch.empty((L.K, L.B), device=dev)
+    dW = torch.empty((L.N, L.K), device=dev)
+    gv = torch.empty(L.N * L.K, device=dev)
+    csc = L1.CSC.empty(L.K, L.nnz, dev)
+    W1 = L1.CSR(L.N, L.K, torch.empty(L.N + 1, dtype=torch.int32, device=dev),
+                torch.empty(L.N * L.K, dtype=torch.int32, device=dev),
+                torch.empty(L.N * L.K, dtype=torch.float32, device=dev), None)
+    def step(x, nnz1=None):
+        L1.csr_spmm_fwd(W, x, Y)
+        L1.csc_build(W, csc)
+        L1.csr_spmm_bwd_t(W, dY, csc, dX)
+        L1.dense_wgrad(dY, x, dW)
+        L1.prox_l1_recompress(W, dW, L.eta, L.lam, out=W1)
+        W1.nnz = nnz1  # None: the binding reads it from the device (a host wait)
+        L1.sddmm_masked_wgrad(W1, dY, x, gv)
+        L1.prox_l1_step(L1.PROX_CSR, W1, gv, L.eta, 0.0)
+
+    step(X)
+    torch.cuda.synchronize()
+    n = W1.host_nnz()
+    outs = lambda: [Y, dX, dW, W1.row_ptr, W1.col_idx[:n], W1.vals[:n], gv[:n]]
+    ref = [o.clone() for o in outs()]
+
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(X, n)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step(X, n)  # captured with the structure size known: no host wait inside
+
+    for r in range(3):
+        step(X2)  # eager work on the same buffers between replays
+        torch.cuda.synchronize()
+        for o in outs():
+            o.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs(), ref):
+            assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                               b.view(torch.int32) if b.dtype == torch.float32 else b), r
