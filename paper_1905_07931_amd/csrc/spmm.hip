@@ -322,10 +322,11 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
     static_assert(G >= MAXRW && G >= HDR / 2, "a lane per slot and per header word");
     const int tiles_per_g = (ntiles + TPW - 1) / TPW;
     const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (id >= (int64_t)nw * tiles_per_g) return;
+    // no early exit: the whole workgroup meets at the barrier below
+    const bool wave_ok = id < (int64_t)nw * tiles_per_g;
     const int lane = threadIdx.x & 63;
-    const int g = (int)(id / tiles_per_g);
-    const int t0 = (int)(id - (int64_t)g * tiles_per_g) * TPW;
+    const int g = wave_ok ? (int)(id / tiles_per_g) : 0;
+    const int t0 = wave_ok ? (int)(id - (int64_t)g * tiles_per_g) * TPW : ntiles;
     const int tau = lane / G, i = lane - tau * G;
     const int t = t0 + tau;
     const bool tile_ok = t < ntiles;
@@ -353,17 +354,29 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
     char *chunk = stream + (tile_ok ? woff[g] + coff[(int64_t)g * ntiles + t] : 0);
     // header: uint16 padded count per slot (zero past rw)
     if (tile_ok && i < HDR / 2) reinterpret_cast<unsigned short *>(chunk)[i] = (unsigned short)(i < MAXRW ? np : 0);
+    // slot table of the wave's tiles in LDS: run starts (plus the end), first
+    // position, stride and entries
+    __shared__ int s_start[4][TPW][MAXRW + 1], s_base[4][TPW][MAXRW], s_k[4][TPW][MAXRW],
+        s_n[4][TPW][MAXRW];
+    const int wl = threadIdx.x >> 6;
+    if (i < MAXRW) {
+        s_start[wl][tau][i] = i < rw ? start : incl;  // empty slots start at the end
+        s_base[wl][tau][i] = pbase;
+        s_k[wl][tau][i] = k;
+        s_n[wl][tau][i] = n;
+    }
+    if (i == G - 1) s_start[wl][tau][MAXRW] = incl;
+    __syncthreads();
     // copy: lane q of the wave takes the q-th pair of the chunk of every tile
-    // of the wave at once, so the loads of all tiles are in flight together
-    // (slot data is broadcast with readlane, which reads a lane whether or not
-    // it is still active in the loop)
+    // of the wave at once (coalesced stores, the loads of all tiles in
+    // flight); its slot is found by binary search over the run starts
     int total[TPW];
     int2 *pp[TPW];
     int maxtot = 0;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
         const int tg = t0 + tt;
-        total[tt] = tg < ntiles ? lane_bcast(incl, tt * G + G - 1) : 0;  // pairs of tile tg (padded)
+        total[tt] = tg < ntiles ? s_start[wl][tt][MAXRW] : 0;  // pairs of tile tg (padded)
         pp[tt] = reinterpret_cast<int2 *>(stream + (tg < ntiles ? woff[g] + coff[(int64_t)g * ntiles + tg] : 0) + HDR);
         maxtot = max(maxtot, total[tt]);
     }
@@ -373,24 +386,18 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
 #pragma unroll
         for (int tt = 0; tt < TPW; ++tt) {
             v[tt] = make_int2(0, 0);  // the padding pair of an odd run
-            // slot of pair q: the last slot whose start is <= q
-            int s_start = 0, s_n = 0, s_base = 0, s_k = 1;
-            for (int j = 0; j < rw && j < MAXRW; ++j) {
-                const int st = lane_bcast(start, tt * G + j);
-                const int nj = lane_bcast(n, tt * G + j);
-                const int bj = lane_bcast(pbase, tt * G + j);
-                const int kj = lane_bcast(k, tt * G + j);
-                if (st <= q) {
-                    s_start = st;
-                    s_n = nj;
-                    s_base = bj;
-                    s_k = kj;
+            if (q < total[tt]) {
+                // last slot j with start[j] <= q (starts are non-decreasing)
+                int lo = 0, hi = MAXRW - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_start[wl][tt][mid] <= q) lo = mid; else hi = mid - 1;
                 }
-            }
-            const int u = q - s_start;
-            if (q < total[tt] && u < s_n) {
-                const int p = s_base + u * s_k;
-                v[tt] = make_int2((idx[p] - (t0 + tt) * KT) * (BB * 4), __float_as_int(vals[p]));
+                const int u = q - s_start[wl][tt][lo];
+                if (u < s_n[wl][tt][lo]) {
+                    const int p = s_base[wl][tt][lo] + u * s_k[wl][tt][lo];
+                    v[tt] = make_int2((idx[p] - (t0 + tt) * KT) * (BB * 4), __float_as_int(vals[p]));
+                }
             }
         }
 #pragma unroll
