@@ -555,7 +555,14 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
             // never used, because a unit past the chunk is read from global
             // memory instead)
             using U = typename unit_t<HALF>::type;
-            auto ahead = [&](int pos) { return load_unit<HALF>(sc, pos < kChunk - 16 ? pos : kChunk - 16, half); };
+            // (the position is made opaque before the clamp: otherwise the
+            // compiler rewrites min(p + c, m) as min(p, m - c) + c, loses track of
+            // which buffer the read touches and waits for the DMA into the other
+            // stream buffer before it)
+            auto ahead = [&](int pos) {
+                asm volatile("" : "+s"(pos));
+                return load_unit<HALF>(sc, pos < kChunk - 16 ? pos : kChunk - 16, half);
+            };
             U qa = ahead(p), qb = ahead(p + 16);
 #pragma unroll
             for (int i = 0; i < MAXRW; ++i) {
