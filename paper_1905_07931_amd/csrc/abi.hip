@@ -240,9 +240,11 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, pw.seg,
                                      pw.counts, stream);
     if (e == hipSuccess) e = launch_exclusive_scan(pw.counts, pw.off, (int)n_slabs, nullptr, stream);
-    if (e == hipSuccess) e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
     if (e != hipSuccess) return L1CSR_EHIP;
     if (capacity < total) {
+        // the host needs the output size before the fill: row pointers now
+        e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
         int32_t h = 0;
         e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
         if (e == hipSuccess) e = hipStreamSynchronize(stream);
@@ -253,7 +255,7 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
         *h_nnz_required = -1;
     }
     return hip_status(launch_prox_fill(n_rows, n_cols, pw.seg, col_idx, vals, G, ldg, eta, t, pw.off,
-                                       col_idx_out, vals_out, capacity, stream));
+                                       col_idx_out, vals_out, capacity, row_ptr_out, d_nnz_out, stream));
 }
 
 int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,

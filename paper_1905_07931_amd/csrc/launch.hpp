@@ -85,10 +85,11 @@ hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *
                              int *seg, int *counts, hipStream_t s);
 hipError_t launch_prox_row_ptr(int n_rows, int n_cols, const int *off, int *row_ptr, int *nnz_out,
                                hipStream_t s);
+// (also writes row_ptr and *nnz_out, nullable, from off[])
 hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *idx,
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
                             const int *off, int *col_out, float *val_out, int64_t capacity,
-                            hipStream_t s);
+                            int *row_ptr, int *nnz_out, hipStream_t s);
 
 // recompress.hip -----------------------------------------------------------
 hipError_t launch_count_rows(int n_rows, int n_cols, const float *Z, int64_t ldz, float t,

@@ -116,7 +116,8 @@ __global__ __launch_bounds__(kProxThreads) void prox_slab_kernel(
     int n_cols, int slabs, const int *__restrict__ seg, const int *__restrict__ idx,
     const float *__restrict__ vals, const float *__restrict__ G, int64_t ldg, double eta, double t,
     int *__restrict__ counts, const int *__restrict__ off, int *__restrict__ col_out,
-    float *__restrict__ val_out, int64_t capacity) {
+    float *__restrict__ val_out, int64_t capacity, int *__restrict__ row_ptr,
+    int *__restrict__ nnz_out) {
     __shared__ __attribute__((aligned(16))) float wrow[kSlab];
     __shared__ int wave_tot[kProxThreads / kWave];
     const int64_t blk = blockIdx.x;
@@ -162,6 +163,16 @@ __global__ __launch_bounds__(kProxThreads) void prox_slab_kernel(
     }
     __syncthreads();
     int64_t out = FILL ? off[blk] : 0;
+    if (FILL && threadIdx.x == 0) {
+        // row pointers: a row starts where its first slab does; the last slab
+        // also closes the last row
+        if (sl == 0) row_ptr[row] = (int)out;
+        if (blk == (int64_t)gridDim.x - 1) {
+            const int total = off[blk + 1];
+            row_ptr[row + 1] = total;
+            if (nnz_out) *nnz_out = total;
+        }
+    }
     int cnt = 0;
 #pragma unroll
     for (int c = 0; c < kSlabChunks; ++c) {
@@ -297,10 +308,12 @@ hipError_t launch_prox_count(int n_rows, int n_cols, const int *ptr, const int *
     const unsigned grid = (unsigned)((int64_t)n_rows * slabs);
     if (v4)
         prox_slab_kernel<true, false><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0,
+            nullptr, nullptr);
     else
         prox_slab_kernel<false, false><<<grid, kProxThreads, 0, s>>>(
-            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0);
+            n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, counts, nullptr, nullptr, nullptr, 0,
+            nullptr, nullptr);
     return hipGetLastError();
 }
 
@@ -315,7 +328,7 @@ hipError_t launch_prox_row_ptr(int n_rows, int n_cols, const int *off, int *row_
 hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *idx,
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
                             const int *off, int *col_out, float *val_out, int64_t capacity,
-                            hipStream_t s) {
+                            int *row_ptr, int *nnz_out, hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     const bool v4 = (ldg % 4 == 0) && aligned16(G);
     const int slabs = prox_slabs(n_cols);
@@ -323,11 +336,11 @@ hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *i
     if (v4)
         prox_slab_kernel<true, true><<<grid, kProxThreads, 0, s>>>(
             n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
-            capacity);
+            capacity, row_ptr, nnz_out);
     else
         prox_slab_kernel<false, true><<<grid, kProxThreads, 0, s>>>(
             n_cols, slabs, seg, idx, vals, G, ldg, (double)eta, t, nullptr, off, col_out, val_out,
-            capacity);
+            capacity, row_ptr, nnz_out);
     return hipGetLastError();
 }
 

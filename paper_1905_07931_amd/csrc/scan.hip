@@ -1,9 +1,10 @@
 // Exclusive prefix sum of int32 counts (row or column pointers) and fills.
 //
-// The counts scanned here have one entry per matrix row or column (a few
+// The counts scanned here have one entry per matrix row, column or slab (a few
 // thousand to a few hundred thousand), so a single 1024-thread workgroup walks
-// the array in tiles of 4096 with a carried running total; every wave scans
-// its lanes with shuffles and the 16 wave totals are scanned through LDS.
+// the array in tiles of 4096 with a carried running total (the next tile's
+// loads are issued before the current tile is scanned); every wave scans its
+// lanes' sums with shuffles and the 16 wave totals are scanned through LDS.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -25,15 +26,24 @@ __global__ __launch_bounds__(kScanThreads) void exclusive_scan_kernel(const int 
     const int wave = tid >> 6;
     if (tid == 0) carry_s = 0;
     __syncthreads();
+    int nv[kScanPerThread];
+    auto load = [&](int base) {
+#pragma unroll
+        for (int e = 0; e < kScanPerThread; ++e) {
+            const int j = base + tid * kScanPerThread + e;
+            nv[e] = j < n ? in[j] : 0;
+        }
+    };
+    load(0);
     for (int base = 0; base < n; base += kScanTile) {
         int v[kScanPerThread];
         int local = 0;
 #pragma unroll
         for (int e = 0; e < kScanPerThread; ++e) {
-            const int j = base + tid * kScanPerThread + e;
-            v[e] = j < n ? in[j] : 0;
+            v[e] = nv[e];
             local += v[e];
         }
+        if (base + kScanTile < n) load(base + kScanTile);
         const int incl = wave_incl_scan(local);
         if (lane == 63) wave_tot[wave] = incl;
         __syncthreads();
