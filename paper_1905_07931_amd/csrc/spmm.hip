@@ -833,6 +833,11 @@ bool shape_plan(spmm_plan &p, int n_rows, int n_cols, int64_t nnz, int B) {
 spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
     spmm_plan p{};
     if (!x4 || B < 128 || n_rows < kNW || n_cols <= 0) return p;
+    // The tiled path costs about 20 us of planning and then runs ~1e7
+    // (entry, batch column) products per us; the rows kernel starts at once and
+    // streams ~5e6 per us out of L2.  Below ~1.7e8 products the rows kernel
+    // finishes first.
+    if ((double)nnz * (double)B < 1.7e8) return p;
     if (B >= 256) {
         // half-wave units halve the number of tiles; they pay off while a
         // wave's chunk of a tile (about nnz / (waves * tiles) pairs) still

@@ -54,14 +54,16 @@ def test_spmm_fwd(shape):
 
 
 # Shapes that drive the LDS-tiled kernel through each vector width (the width
-# follows from the batch: 64*VEC columns per workgroup), several 64-row X
-# tiles, a ragged batch tail, ragged row blocks and both rows-per-wave plans.
+# follows from the batch: 64*VEC columns per workgroup), several X tiles, a
+# ragged batch tail, ragged row blocks and both rows-per-wave plans.  The tiled
+# kernel is chosen from nnz*B >= 1.7e8 products on (smaller products take the
+# rows kernel, covered by SHAPES).
 TILED = [  # (N, K, B, nnz, seed)
-    (300, 784, 64, 23520, 20),      # VEC 1
-    (2000, 300, 128, 30000, 21),    # VEC 2
-    (4096, 300, 1024, 61440, 22),   # VEC 4, 4 rows per wave
-    (4096, 300, 1020, 61440, 23),   # VEC 4, ragged last batch chunk
-    (9000, 333, 1024, 150000, 24),  # VEC 4, 8 rows per wave, ragged tile and row block
+    (300, 784, 64, 23520, 20),        # B < 128: the rows kernel, VEC 1
+    (8000, 1000, 128, 1400000, 21),   # VEC 2
+    (4096, 300, 1024, 200000, 22),    # VEC 4
+    (4096, 300, 1020, 200000, 23),    # VEC 4, ragged last batch chunk
+    (9000, 333, 1024, 200000, 24),    # VEC 4, ragged tile and row block
 ]
 
 
@@ -74,7 +76,7 @@ def test_spmm_fwd_tiled_widths(shape):
     assert_scaled_close(Y, ref, m, what="Y")
 
 
-@pytest.mark.parametrize("shape", [(300, 4096, 1024, 61440, 25), (64, 8192, 1024, 30000, 26)],
+@pytest.mark.parametrize("shape", [(300, 4096, 1024, 200000, 25), (64, 8192, 1024, 200000, 26)],
                          ids=_ids)
 def test_spmm_bwd_tiled_widths(shape):
     L = _layer(shape)
@@ -90,8 +92,8 @@ def test_spmm_power_law_rows_dyadic_bit_exact():
     # kernel on the dyadic grid: every sum is exact, so the bits must match
     import numpy as np_
     rng = np_.random.default_rng(27)
-    N, K, B = 4096, 512, 256
-    rp, ci = synth.zipf_pattern(rng, N, K, 90000, 1.1)
+    N, K, B = 4096, 512, 512
+    rp, ci = synth.zipf_pattern(rng, N, K, 400000, 1.1)
     vals = (rng.integers(1, 17, ci.shape[0]) * rng.choice([-1.0, 1.0], ci.shape[0]) / 16).astype(np_.float32)
     X = (rng.integers(0, 17, (K, B)) / 16).astype(np_.float32)
     W = L1.CSR.from_host(rp, ci, vals, K, device=cuda())
