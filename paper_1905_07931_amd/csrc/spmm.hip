@@ -569,12 +569,23 @@ __global__ __launch_bounds__(1024, 1) void spmm_stream_kernel(
                 if (i < rw) {  // (a guard, not a break: keeps every acc[i] statically indexed)
                     const int pe = p + 8 * nlen[i];
                     const int pl = pe < kChunk ? pe : kChunk;  // part of the run staged in LDS
-                    for (; p + 32 <= pl; p += 32) {
+                    for (; p + 64 <= pl; p += 64) {  // four units per step
+                        const U c0 = qa, c1 = qb;
+                        const U c2 = ahead(p + 32), c3 = ahead(p + 48);
+                        qa = ahead(p + 64);
+                        qb = ahead(p + 80);
+                        fma_unit<VEC, HALF>(xb, c0, acc[i]);
+                        fma_unit<VEC, HALF>(xb, c1, acc[i]);
+                        fma_unit<VEC, HALF>(xb, c2, acc[i]);
+                        fma_unit<VEC, HALF>(xb, c3, acc[i]);
+                    }
+                    if (p + 32 <= pl) {
                         const U c0 = qa, c1 = qb;
                         qa = ahead(p + 32);
                         qb = ahead(p + 48);
                         fma_unit<VEC, HALF>(xb, c0, acc[i]);
                         fma_unit<VEC, HALF>(xb, c1, acc[i]);
+                        p += 32;
                     }
                     if (p < pl) {
                         const U c0 = qa;
