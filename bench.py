@@ -236,12 +236,12 @@ def main():
 def cpu_baseline(Lr, min_seconds):
     """The oracle timed on the host cores on the same step: the whole layer
     (fwd, bwd, dense dW, prox, recompression), repeated until at least
-    `min_seconds` have elapsed (at most 5 runs); the median run is reported."""
+    `min_seconds` have elapsed (at most 12 runs); the median run is reported."""
     import oracle
 
     N, K, B = Lr.N, Lr.K, Lr.B
     times = []
-    while len(times) < 5 and (sum(times) < min_seconds or len(times) < 1):
+    while len(times) < 12 and (sum(times) < min_seconds or len(times) < 1):
         t0 = time.perf_counter()
         oracle.spmm_fwd(Lr.row_ptr, Lr.col_idx, Lr.vals, Lr.X)
         oracle.spmm_bwd_t(Lr.row_ptr, Lr.col_idx, Lr.vals, Lr.dY, K)
