@@ -87,8 +87,7 @@ int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_pt
     if (n_rows > 0 && n_cols > 0 &&
         (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols, nnz)))
         return L1CSR_EINVAL;
-    if (ceil_div(n_rows, 128) > INT32_MAX || ceil_div(n_cols, 1024) > kMaxGridY)
-        return L1CSR_EUNSUPPORTED;
+    if (!csc_grid_fits(n_rows, n_cols)) return L1CSR_EUNSUPPORTED;
     return hip_status(launch_csc_build(n_rows, n_cols, nnz, row_ptr, col_idx, vals, col_ptr, row_idx, perm,
                                        vals_t, ws, stream));
 }

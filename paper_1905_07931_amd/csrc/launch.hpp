@@ -26,6 +26,8 @@ hipError_t launch_seg(int n_rows, int ntiles, int shift, const int *ptr, const i
 
 // csc.hip ------------------------------------------------------------------
 size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz);
+// the (row chunk, column tile) grid of the build fits the launch limits
+bool csc_grid_fits(int n_rows, int n_cols);
 hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
                             const float *vals, int *col_ptr, int *row_idx, int *perm,
                             float *vals_t, void *ws, hipStream_t s);
