@@ -100,13 +100,18 @@ __device__ __forceinline__ int piece_len(int len, int j, int k) {
     return len > j ? (len - j + k - 1) / k : 0;
 }
 
-constexpr int kBuckets = 129;  // 4 buckets per octave of the piece length, plus empty
+// 16 buckets per octave of the piece length, plus empty: fine enough that the
+// lengths of one matrix spread over many buckets (the planner's bucket
+// counters are LDS atomics, and pieces of equal key serialise on one address)
+constexpr int kBucketBits = 4;
+constexpr int kBuckets = 1 + 31 * (1 << kBucketBits);
 
 __device__ __forceinline__ int length_key(int len) {
     if (len <= 0) return 0;
     const int b = 31 - __clz(len);
-    const int sub = b >= 2 ? (len >> (b - 2)) & 3 : (len << (2 - b)) & 3;
-    return 1 + b * 4 + sub;
+    const int sub = b >= kBucketBits ? (len >> (b - kBucketBits)) & ((1 << kBucketBits) - 1)
+                                     : (len << (kBucketBits - b)) & ((1 << kBucketBits) - 1);
+    return 1 + b * (1 << kBucketBits) + sub;
 }
 
 constexpr int kPlanThreads = 1024;
@@ -194,19 +199,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const in
     const int n_pieces = carry;
     if (tid == 0) pbeg[n_rows] = n_pieces;
     __syncthreads();
-    // bucket starts, largest bucket first (one wave, three buckets per lane)
+    // bucket starts, largest bucket first (one wave, kBPL buckets per lane)
+    constexpr int kBPL = (kBuckets + kWave - 1) / kWave;
     if (wave == 0) {
-        int h[3], sum = 0;
+        int h[kBPL], sum = 0;
 #pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            const int b = kBuckets - 1 - (lane * 3 + q);
+        for (int q = 0; q < kBPL; ++q) {
+            const int b = kBuckets - 1 - (lane * kBPL + q);
             h[q] = b >= 0 ? hist[b] : 0;
             sum += h[q];
         }
         int run = wave_incl_scan(sum) - sum;
 #pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            const int b = kBuckets - 1 - (lane * 3 + q);
+        for (int q = 0; q < kBPL; ++q) {
+            const int b = kBuckets - 1 - (lane * kBPL + q);
             if (b >= 0) start[b] = run;
             run += h[q];
         }
