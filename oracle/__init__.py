@@ -62,6 +62,11 @@ def lib():
         L.orc_prox_dense.argtypes = [i32, i32, _i32p, _i32p, _f32p, _f32p, i64, f32, f32,
                                      _f32p, i64, C.c_void_p]
         L.orc_prox_csr.argtypes = [i32, _f32p, _f32p, f32, f32, _f32p]
+        L.orc_prox_adaptive_dense.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64,
+                                              _f32p, _f32p, i64, f32, f32, f32, f32, f32, i64,
+                                              _f32p, i64, C.c_void_p]
+        L.orc_prox_adaptive_csr.argtypes = [i32, i32, _f32p, _f32p, _f32p, _f32p, f32, f32, f32,
+                                            f32, f32, i64, _f32p]
         L.orc_recompress.argtypes = [i32, i32, _f32p, i64, f32, _i32p, _i32p, _f32p, i64,
                                      C.POINTER(C.c_int64)]
         L.orc_compact.argtypes = [i32, _i32p, _i32p, _f32p, _i32p, _i32p, _f32p,
@@ -189,6 +194,58 @@ def prox_csr(vals, gv, eta, lam):
     out = np.empty_like(v)
     _check(lib().orc_prox_csr(v.shape[0], v, g, eta, lam, out), "prox_csr")
     return out
+
+
+RMSPROP = 1
+ADAM = 2
+
+
+def _state(x, shape):
+    """A fresh float32 copy of a solver state (zeros when x is None)."""
+    if x is None:
+        return np.zeros(shape, np.float32)
+    return np.array(x, dtype=np.float32, copy=True, order="C").reshape(shape)
+
+
+def prox_adaptive_dense(solver, row_ptr, col_idx, vals, G, m, v, eta, lam, eps, beta1, beta2,
+                        t, n_cols):
+    """One Prox-RMSProp (solver=RMSPROP, Algorithm 1) or Prox-ADAM (solver=ADAM,
+    Algorithm 2) step over all N*K weights.  m, v are [N][K] states (None =
+    zeros; m is ignored for RMSProp).  Returns (Z, row_counts, m', v') with Z
+    the new dense weights; the inputs are not modified."""
+    rp, ci, w = _csr(row_ptr, col_idx, vals)
+    G = _c(G, np.float32)
+    N = rp.shape[0] - 1
+    m2 = _state(m, (N, n_cols))
+    v2 = _state(v, (N, n_cols))
+    Z = np.empty((N, n_cols), np.float32)
+    cnt = np.empty(N, np.int32)
+    _check(lib().orc_prox_adaptive_dense(int(solver), N, n_cols, rp, ci, w, G, n_cols, m2, v2,
+                                         n_cols, eta, lam, eps, beta1, beta2, int(t), Z, n_cols,
+                                         cnt.ctypes.data_as(C.c_void_p)), "prox_adaptive_dense")
+    return Z, cnt, m2, v2
+
+
+def prox_adaptive_recompress(solver, row_ptr, col_idx, vals, G, m, v, eta, lam, eps, beta1,
+                             beta2, t, n_cols):
+    """prox_adaptive_dense followed by recompress: returns ((row_ptr', col_idx',
+    vals'), m', v')."""
+    Z, _, m2, v2 = prox_adaptive_dense(solver, row_ptr, col_idx, vals, G, m, v, eta, lam, eps,
+                                       beta1, beta2, t, n_cols)
+    return recompress(Z, 0.0), m2, v2
+
+
+def prox_adaptive_csr(solver, vals, gv, m, v, eta, lam, eps, beta1, beta2, t):
+    """The adaptive step on the stored entries only (state per entry).
+    Returns (vals', m', v')."""
+    w = _c(vals, np.float32)
+    g = _c(gv, np.float32)
+    m2 = _state(m, w.shape)
+    v2 = _state(v, w.shape)
+    out = np.empty_like(w)
+    _check(lib().orc_prox_adaptive_csr(int(solver), w.shape[0], w, g, m2, v2, eta, lam, eps,
+                                       beta1, beta2, int(t), out), "prox_adaptive_csr")
+    return out, m2, v2
 
 
 def recompress(Z, t=0.0):

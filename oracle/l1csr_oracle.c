@@ -271,6 +271,129 @@ int orc_prox_csr(int32_t nnz, const float *vals, const float *gv,
 }
 
 /* ------------------------------------------------------------------------
+ * Adaptive proximal steps: Prox-RMSProp (Algorithm 1) and Prox-ADAM
+ * (Algorithm 2).  Both replace the plain step -eta*g of Eq. (prox) by a
+ * preconditioned one and keep the same prox of eta*lambda*||.||_1.
+ *
+ * The algorithms state the mathematics, not the arithmetic.  Readings:
+ *   - each weight's state (v; and m for ADAM) is kept in float, and a step
+ *     reads the stored values;
+ *   - the arithmetic is double, as for the plain prox (Fig. 4 computes in
+ *     double);
+ *   - a moment update  s <- beta*s + (1-beta)*x  is one rounding of that
+ *     expression (beta*s is a product of two floats, exact in double; the
+ *     fma rounds once), then one rounding to float for storage;
+ *   - ADAM's bias corrections divide by 1 - pow(beta, t), in double;
+ *   - the step argument z = w - eta*u rounds once (fma), and the new weight
+ *     is float(S_{eta*lambda}(z)), as in the plain prox step;
+ *   - RMSProp's beta is its squared-gradient decay; it plays beta2's role.
+ * Solver codes: 1 = Prox-RMSProp, 2 = Prox-ADAM.
+ * ---------------------------------------------------------------------- */
+#define ORC_RMSPROP 1
+#define ORC_ADAM 2
+
+typedef struct {
+    int solver;
+    double eta, thr, eps;
+    double beta1, beta2;
+    double bc1, bc2;  /* 1 - pow(beta1, t), 1 - pow(beta2, t) (ADAM only) */
+} orc_adaptive;
+
+static int orc_adaptive_setup(int32_t solver, float eta, float lambda, float eps,
+                              float beta1, float beta2, int64_t t, orc_adaptive *a) {
+    if (solver != ORC_RMSPROP && solver != ORC_ADAM) return ORC_EINVAL;
+    if (!(eta > 0.0f) || !(lambda >= 0.0f) || !(eps > 0.0f) || !isfinite(eta) ||
+        !isfinite(lambda) || !isfinite(eps))
+        return ORC_EINVAL;
+    if (!(beta2 >= 0.0f && beta2 < 1.0f)) return ORC_EINVAL;
+    if (solver == ORC_ADAM && (!(beta1 >= 0.0f && beta1 < 1.0f) || t < 1)) return ORC_EINVAL;
+    a->solver = solver;
+    a->eta = (double)eta;
+    a->thr = orc_threshold(eta, lambda);
+    a->eps = (double)eps;
+    a->beta1 = (double)beta1;
+    a->beta2 = (double)beta2;
+    a->bc1 = solver == ORC_ADAM ? 1.0 - pow((double)beta1, (double)t) : 1.0;
+    a->bc2 = solver == ORC_ADAM ? 1.0 - pow((double)beta2, (double)t) : 1.0;
+    return ORC_OK;
+}
+
+/* One weight: updates *m (ADAM) and *v in place, returns the new weight. */
+static float orc_adaptive_elem(const orc_adaptive *a, float w, float g, float *m, float *v) {
+    const double gd = (double)g;
+    double u;
+    /* second moment (both algorithms): v_t = beta2*v_{t-1} + (1-beta2)*g_t.g_t */
+    *v = (float)fma(1.0 - a->beta2, gd * gd, a->beta2 * (double)*v);
+    if (a->solver == ORC_ADAM) {
+        /* first moment: m_t = beta1*m_{t-1} + (1-beta1)*g_t */
+        *m = (float)fma(1.0 - a->beta1, gd, a->beta1 * (double)*m);
+        /* bias corrections, then the step m^_t / (sqrt(v^_t) + eps) */
+        const double mhat = (double)*m / a->bc1;
+        const double vhat = (double)*v / a->bc2;
+        u = mhat / (sqrt(vhat) + a->eps);
+    } else {
+        /* RMSProp: g_t / (sqrt(v_t) + eps) */
+        u = gd / (sqrt((double)*v) + a->eps);
+    }
+    const double z = fma(-a->eta, u, (double)w);
+    return (float)orc_soft_threshold(z, a->thr);
+}
+
+/* Dense (l1-phase) form over all N*K weights, like orc_prox_dense: w_ik = 0
+ * where W has no entry.  m (ADAM only; ignored for RMSProp) and v are [N][lds]
+ * and are updated in place; Z[i][k] gets the new weight and row_counts[i]
+ * (optional) the number of nonzero Z[i][.]. */
+int orc_prox_adaptive_dense(int32_t solver, int32_t N, int32_t K,
+                            const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                            const float *G, int64_t ldg, float *m, float *v, int64_t lds,
+                            float eta, float lambda, float eps, float beta1, float beta2,
+                            int64_t t, float *Z, int64_t ldz, int32_t *row_counts) {
+    orc_adaptive a;
+    if (N < 0 || K < 0 || ldg < K || ldz < K || lds < K) return ORC_EINVAL;
+    if (orc_adaptive_setup(solver, eta, lambda, eps, beta1, beta2, t, &a) != ORC_OK)
+        return ORC_EINVAL;
+    #pragma omp parallel
+    {
+        float *wrow = (float *)malloc(sizeof(float) * (size_t)(K > 0 ? K : 1));
+        float m_unused = 0.0f;
+        #pragma omp for schedule(dynamic, 8)
+        for (int32_t i = 0; i < N; ++i) {
+            for (int32_t k = 0; k < K; ++k) wrow[k] = 0.0f;
+            for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) wrow[col_idx[p]] = vals[p];
+            int32_t cnt = 0;
+            for (int32_t k = 0; k < K; ++k) {
+                const int64_t s = (int64_t)i * lds + k;
+                float *mp = solver == ORC_ADAM ? &m[s] : &m_unused;
+                const float o = orc_adaptive_elem(&a, wrow[k], G[(int64_t)i * ldg + k], mp, &v[s]);
+                Z[(int64_t)i * ldz + k] = o;
+                cnt += (o != 0.0f);
+            }
+            if (row_counts) row_counts[i] = cnt;
+        }
+        free(wrow);
+    }
+    return ORC_OK;
+}
+
+/* The same step on W's stored entries only, with one state entry per stored
+ * weight (m[nnz] for ADAM, v[nnz]); lambda = 0 trains the fixed pattern
+ * (debiasing, Section 2.4).  vals_out may alias vals. */
+int orc_prox_adaptive_csr(int32_t solver, int32_t nnz, const float *vals, const float *gv,
+                          float *m, float *v, float eta, float lambda, float eps,
+                          float beta1, float beta2, int64_t t, float *vals_out) {
+    orc_adaptive a;
+    if (nnz < 0) return ORC_EINVAL;
+    if (orc_adaptive_setup(solver, eta, lambda, eps, beta1, beta2, t, &a) != ORC_OK)
+        return ORC_EINVAL;
+    float m_unused = 0.0f;
+    for (int32_t p = 0; p < nnz; ++p) {
+        float *mp = solver == ORC_ADAM ? &m[p] : &m_unused;
+        vals_out[p] = orc_adaptive_elem(&a, vals[p], gv[p], mp, &v[p]);
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
  * Dense -> CSR (Section 3.1: store only the nonzero values; Fig. 1(iii)).
  * Keeps the entries with |Z[i][k]| > t (t = 0 after a prox step) in row-major
  * order.  Writes row_ptr[N+1] and, when nnz <= capacity, col_idx/vals.
