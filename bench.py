@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum host time spent timing the oracle")
     ap.add_argument("--workload", default="fc9216x4096",
-                    choices=["fc9216x4096", "fc784x300", "mlp784", "conv2", "fc4096_sweep", "all"],
+                    choices=["fc9216x4096", "fc784x300", "mlp784", "conv2", "fc4096_sweep",
+                             "fc9216x4096_adaptive", "all"],
                     help="fc9216x4096 (default): the metric's workload, one JSON line; the others "
                          "print one informational JSON line each (no CPU baseline)")
     return ap.parse_args()
@@ -96,7 +97,8 @@ def main():
 
     if args.workload != "fc9216x4096":
         import bench_workloads
-        names = (["fc784x300", "mlp784", "conv2", "fc4096_sweep"] if args.workload == "all"
+        names = (["fc784x300", "mlp784", "conv2", "fc4096_sweep", "fc9216x4096_adaptive"]
+                 if args.workload == "all"
                  else [args.workload])
         for n in names:
             for line in bench_workloads.run(n, args, dev):

@@ -9,6 +9,9 @@ informational JSON line; bench.py's default line is the metric.
                   fwd, CSC, bwd, masked dW (SDDMM), support-restricted prox, compaction
     fc4096_sweep  4096 x 4096, batch 512, densities 1/5/20/50%: 20 alternating
                   l1 / debiasing iterations with the CSR rebuilt after every l1 step
+    fc9216x4096_adaptive
+                  the 9216 -> 4096 l1 step with Prox-ADAM (Algorithm 2) and with
+                  Prox-RMSProp (Algorithm 1) in place of the plain proximal step
 """
 from __future__ import annotations
 
@@ -297,5 +300,56 @@ def fc4096_sweep(args, dev):
                     None, nnz_after_l1_steps=nnz_seq)
 
 
+def fc9216x4096_adaptive(args, dev):
+    """One line per solver: fwd, CSC, bwd, dense dW, then the fused adaptive
+    prox + recompression over all N*K weights with dense m, v state (which
+    advances every step; the work per step is the same).  eta = 1e-3 (the usual
+    ADAM step), lambda = 1e-4 as for the plain step: almost every weight
+    survives, the largest output the step can have."""
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    L = synth.fc9216_4096(seed=0)
+    N, K, B, nnz = L.N, L.K, L.B, L.nnz
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=dev)
+    X, dY = torch.from_numpy(L.X).to(dev), torch.from_numpy(L.dY).to(dev)
+    Y = torch.empty((N, B), dtype=torch.float32, device=dev)
+    dX = torch.empty((K, B), dtype=torch.float32, device=dev)
+    dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+    csc = L1.CSC.empty(K, nnz, dev)
+    Wout = _csr_out(L1, torch, N, K, dev)
+    eta, lam = 1e-3, L.lam
+    for solver, tag in [(L1.SOLVER_ADAM, "adam"), (L1.SOLVER_RMSPROP, "rmsprop")]:
+        st = L1.AdaptiveState.zeros(solver, (N, K), dev)
+        names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", f"prox_{tag}_recompress"]
+
+        def step(ev=None):
+            mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+            mark(0); L1.csr_spmm_fwd(W, X, Y)
+            mark(1); L1.csc_build(W, csc)
+            mark(2); L1.csr_spmm_bwd_t(W, dY, csc, dX)
+            mark(3); L1.dense_wgrad(dY, X, dW)
+            mark(4); L1.prox_adaptive_recompress(W, dW, st, eta, lam, out=Wout)
+            mark(5)
+        ms, per = _timed(torch, step, max(args.steps, 10), max(args.warmup, 3), names)
+        nnz_out = int(Wout.row_ptr[-1].item())
+        state_bytes = (16.0 if solver == L1.SOLVER_ADAM else 8.0) * N * K  # read and write m, v / v
+        alg = 4.0 * N * K + state_bytes + (8.0 * nnz + 4 * (N + 1)) + (8.0 * nnz_out + 4 * (N + 1))
+        # the two-pass kernels also re-read m', v' (ADAM) or G, v' (RMSProp)
+        moved = alg + 8.0 * N * K
+        kms = per[f"prox_{tag}_recompress"]
+        flops = 4.0 * nnz * B + 2.0 * N * K * B
+        yield _line(f"fc9216x4096_b1024_d9_zipf_l1_step_prox_{tag}", flops, ms,
+                    dict(N=N, K=K, B=B, nnz=nnz, density=0.09, solver=tag, eta=eta, lam=lam,
+                         eps=st.eps, beta1=st.beta1 if tag == "adam" else None, beta2=st.beta2), per,
+                    nnz_out=nnz_out,
+                    prox_hbm_algorithmic_bytes=alg, prox_hbm_gbs=round(alg / (kms * 1e-3) / 1e9, 1),
+                    prox_hbm_frac=round(alg / (kms * 1e-3) / 1e9 / 8000.0, 4),
+                    prox_bytes_moved_two_pass=moved,
+                    prox_moved_gbs=round(moved / (kms * 1e-3) / 1e9, 1))
+        del st
+
+
 def run(name, args, dev):
-    return {"fc784x300": fc784x300, "mlp784": mlp784, "conv2": conv2, "fc4096_sweep": fc4096_sweep}[name](args, dev)
+    return {"fc784x300": fc784x300, "mlp784": mlp784, "conv2": conv2, "fc4096_sweep": fc4096_sweep,
+            "fc9216x4096_adaptive": fc9216x4096_adaptive}[name](args, dev)

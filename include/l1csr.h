@@ -11,6 +11,7 @@
  *                      gv = (dY . X^T) on W's pattern (debiasing)  sddmm_masked_wgrad
  *   proximal step      Z  = S_t(W - eta*dW), t = eta*lambda        prox_l1_step
  *   recompression      Z -> CSR                   csr_recompress
+ *   adaptive solvers   Prox-RMSProp / Prox-ADAM   prox_adaptive_step, prox_adaptive_recompress
  *
  * Conventions shared by every call
  *   - CSR: row_ptr[n_rows+1] (row_ptr[0] = 0, non-decreasing), col_idx[nnz]
@@ -66,6 +67,12 @@ enum l1csr_precision {
 enum l1csr_prox_mode {
     L1CSR_PROX_DENSE = 0,    /* every one of the N*K weights, dense gradient */
     L1CSR_PROX_CSR = 1       /* W's stored entries only, gradient per entry  */
+};
+
+/* adaptive solvers of prox_adaptive_step / prox_adaptive_recompress */
+enum l1csr_solver {
+    L1CSR_SOLVER_RMSPROP = 1,  /* Prox-RMSProp, Algorithm 1 */
+    L1CSR_SOLVER_ADAM = 2      /* Prox-ADAM, Algorithm 2    */
 };
 
 /* workspace queries (l1csr_workspace_bytes) */
@@ -237,6 +244,67 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
                        int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
                        int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Adaptive proximal steps: Prox-RMSProp (Algorithm 1) and Prox-ADAM
+ * (Algorithm 2), Section 2.3.  Both keep the prox of eta*lambda*||.||_1 of
+ * Eq. (prox) and precondition the minibatch gradient g with per-weight state:
+ *     v' = beta2*v + (1 - beta2)*g*g                     (both; RMSProp's beta)
+ *     m' = beta1*m + (1 - beta1)*g                       (ADAM only)
+ *     u  = g / (sqrt(v') + eps)                                      (RMSProp)
+ *     u  = (m'/(1 - beta1^t)) / (sqrt(v'/(1 - beta2^t)) + eps)       (ADAM)
+ *     w' = S_t(w - eta*u),   t_thr = eta*lambda,  S_t as in prox_l1_step.
+ * Arithmetic in double: each moment update is one fma rounded to float and
+ * stored; u is computed from the stored floats; w - eta*u rounds once (fma)
+ * and S_t once more to float; zero results are +0.0.  beta^t is pow() in
+ * double on the host.  Hyper-parameters: eta > 0, lambda >= 0, eps > 0 (all
+ * finite), 0 <= beta2 < 1; ADAM also needs 0 <= beta1 < 1 and t >= 1 (the
+ * step number, counted from 1); RMSProp ignores beta1, t and m (may be NULL).
+ * A value out of range returns L1CSR_EINVAL.  The state arrays start at zero
+ * (Algorithms 1-2 initialise m and v to 0) and are owned by the caller.
+ *
+ * prox_adaptive_step, mode L1CSR_PROX_DENSE: every one of the N*K weights
+ *   (w = W's value or 0 where W has no entry), g = G[i][k] ([n_rows][ldg]);
+ *   the states m, v are [n_rows][lds] (lds >= n_cols) and are updated in
+ *   place; writes Z[i][k] ([n_rows][ldz]; Z may be G itself with ldz == ldg,
+ *   but must not overlap m or v) and, if row_counts is not NULL, row_counts[i]
+ *   = number of nonzero Z[i][.].  ws must hold
+ *   l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0).
+ * prox_adaptive_step, mode L1CSR_PROX_CSR: W's stored entries only, with one
+ *   gradient G[p] and one state entry m[p], v[p] per stored weight;
+ *   vals[p] is updated in place for 0 <= p < nnz and the pattern is kept
+ *   (lambda = 0: the debiasing phase of Section 2.4 with an adaptive solver).
+ *   ldg, lds, Z, ldz, row_counts and ws are ignored.
+ * G, m and v must not overlap one another in either mode.
+ */
+int prox_adaptive_step(int mode, int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                       const int32_t *row_ptr, const int32_t *col_idx, float *vals,
+                       const float *G, int64_t ldg, float *m, float *v, int64_t lds,
+                       float eta, float lambda, float eps, float beta1, float beta2, int64_t t,
+                       float *Z, int64_t ldz, int32_t *row_counts,
+                       void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * prox_adaptive_step (dense mode) followed by csr_recompress (t = 0) in one
+ * call, without materialising Z: the l1-phase update of Algorithm 1 or 2 from
+ * the CSR weights W, the dense gradient G and the dense states m, v straight
+ * to the new CSR W'.  m and v are updated in place exactly as by
+ * prox_adaptive_step; the output is bit-identical to the two calls.
+ * row_ptr_out, col_idx_out, vals_out, capacity, d_nnz_out and h_nnz_required
+ * behave as in prox_l1_recompress; when the call returns L1CSR_ECAPACITY it
+ * has left m and v unchanged.  With capacity >= n_rows*n_cols (no wait) G and
+ * the states are read in a counting pass that stores m', v', and m', v' (ADAM)
+ * or G, v' (RMSProp) are read again by the filling pass.  The output arrays
+ * must not overlap W's.  ws as
+ * l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0).
+ */
+int prox_adaptive_recompress(int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                             const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                             const float *G, int64_t ldg, float *m, float *v, int64_t lds,
+                             float eta, float lambda, float eps, float beta1, float beta2, int64_t t,
+                             int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                             int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                             void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * CSR -> CSR without its stored zeros (after a support-restricted prox step in

@@ -18,6 +18,7 @@ __all__ = [
     "csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
     "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "csr_validate", "relu_fwd", "relu_bwd",
     "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16",
+    "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
@@ -25,6 +26,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so
 OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PROX_DENSE, PROX_CSR = 0, 1
 F32, BF16 = 0, 1
+SOLVER_RMSPROP, SOLVER_ADAM = 1, 2
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
 OP_PROX_RECOMPRESS = 7
 
@@ -64,6 +66,11 @@ def lib():
                                      C.POINTER(C.c_int64), vp, sz, vp]
         L.prox_l1_recompress.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp,
                                          i64, vp, C.POINTER(C.c_int64), vp, sz, vp]
+        L.prox_adaptive_step.argtypes = [C.c_int, C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp,
+                                         i64, f32, f32, f32, f32, f32, i64, vp, i64, vp, vp, sz, vp]
+        L.prox_adaptive_recompress.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
+                                               f32, f32, f32, f32, f32, i64, vp, vp, vp, i64, vp,
+                                               C.POINTER(C.c_int64), vp, sz, vp]
         L.csr_compact.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.csr_validate.argtypes = [i32, i32, i64, vp, vp, vp, vp]
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
@@ -71,7 +78,8 @@ def lib():
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
-                     "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent"):
+                     "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent",
+                     "prox_adaptive_step", "prox_adaptive_recompress"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -401,6 +409,117 @@ def prox_l1_recompress(W: CSR, G, eta, lam, capacity=None, out: CSR | None = Non
                                     float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
                                     _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
                                     _stream(stream)), "prox_l1_recompress")
+    out.nnz = need.value if need.value >= 0 else None
+    return out
+
+
+@dataclass
+class AdaptiveState:
+    """Hyper-parameters and per-weight state of Prox-RMSProp / Prox-ADAM
+    (Algorithms 1-2).  m (ADAM only) and v are float32 device tensors: [N][K]
+    (a leading dimension >= K is allowed) for the dense form, [nnz] for the
+    stored-entry form; both start at zero.  t is the step number of the next
+    call (from 1); the binding increments it after each call."""
+    solver: int
+    v: object
+    m: object = None
+    eps: float = 1e-8
+    beta1: float = 0.9
+    beta2: float = 0.999
+    t: int = 1
+
+    @staticmethod
+    def zeros(solver, shape, device, **kw):
+        torch = _torch()
+        v = torch.zeros(shape, dtype=torch.float32, device=device)
+        m = torch.zeros(shape, dtype=torch.float32, device=device) if solver == SOLVER_ADAM else None
+        return AdaptiveState(solver, v, m, **kw)
+
+
+def _state_mat(st: AdaptiveState, N, K):
+    n, k, lds = _mat(st.v, "v")
+    if (n, k) != (N, K):
+        raise ValueError("state v must be [n_rows][n_cols]")
+    if st.solver == SOLVER_ADAM:
+        if st.m is None:
+            raise ValueError("Prox-ADAM needs the first-moment state m")
+        nm, km, ldm = _mat(st.m, "m")
+        if (nm, km, ldm) != (N, K, lds):
+            raise ValueError("m and v must have the same shape and leading dimension")
+    return lds
+
+
+def prox_adaptive_step(mode, W: CSR, G, st: AdaptiveState, eta, lam, Z=None, row_counts=None,
+                       stream=None):
+    """One Prox-RMSProp / Prox-ADAM step (Algorithms 1-2).  Dense mode returns Z
+    (may be G itself) and updates st.m, st.v in place; CSR mode updates W.vals
+    and the per-entry state in place.  st.t advances by one."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    m = st.m if st.solver == SOLVER_ADAM else None
+    if mode == PROX_CSR:
+        _vec(G, torch.float32, "G")
+        _vec(st.v, torch.float32, "v")
+        if m is not None:
+            _vec(m, torch.float32, "m")
+        if G.numel() < nnz or st.v.numel() < nnz or (m is not None and m.numel() < nnz):
+            raise ValueError("G and the state must hold one entry per stored weight")
+        _check(lib().prox_adaptive_step(PROX_CSR, st.solver, W.n_rows, W.n_cols, nnz, _p(W.row_ptr),
+                                        _p(W.col_idx), _p(W.vals), _p(G), 0, _p(m), _p(st.v), 0,
+                                        float(eta), float(lam), float(st.eps), float(st.beta1),
+                                        float(st.beta2), int(st.t), None, 0, None, None, 0,
+                                        _stream(stream)), "prox_adaptive_step")
+        st.t += 1
+        return W
+    N, K, ldg = _mat(G, "G")
+    if (N, K) != (W.n_rows, W.n_cols):
+        raise ValueError("G must be [n_rows][n_cols]")
+    lds = _state_mat(st, N, K)
+    if Z is None:
+        Z = torch.empty((N, K), dtype=torch.float32, device=G.device)
+    Nz, Kz, ldz = _mat(Z, "Z")
+    if (Nz, Kz) != (N, K):
+        raise ValueError("Z must be [n_rows][n_cols]")
+    if row_counts is not None:
+        _vec(row_counts, torch.int32, "row_counts")
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), G.device)
+    _check(lib().prox_adaptive_step(PROX_DENSE, st.solver, N, K, nnz, _p(W.row_ptr), _p(W.col_idx),
+                                    _p(W.vals), _p(G), ldg, _p(m), _p(st.v), lds, float(eta),
+                                    float(lam), float(st.eps), float(st.beta1), float(st.beta2),
+                                    int(st.t), _p(Z), ldz, _p(row_counts), _p(ws), wsb,
+                                    _stream(stream)), "prox_adaptive_step")
+    st.t += 1
+    return Z
+
+
+def prox_adaptive_recompress(W: CSR, G, st: AdaptiveState, eta, lam, capacity=None,
+                             out: CSR | None = None, stream=None):
+    """W' = CSR of the Prox-RMSProp / Prox-ADAM step over all N*K weights, in
+    one call (same bits as prox_adaptive_step + csr_recompress); st.m, st.v are
+    updated in place and st.t advances by one (not on a capacity error)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    N, K, ldg = _mat(G, "G")
+    if (N, K) != (W.n_rows, W.n_cols):
+        raise ValueError("G must be [n_rows][n_cols]")
+    lds = _state_mat(st, N, K)
+    m = st.m if st.solver == SOLVER_ADAM else None
+    dev = G.device
+    if out is None:
+        cap = N * K if capacity is None else int(capacity)
+        out = CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
+    cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev)
+    need = C.c_int64(-1)
+    _check(lib().prox_adaptive_recompress(st.solver, N, K, nnz, _p(W.row_ptr), _p(W.col_idx),
+                                          _p(W.vals), _p(G), ldg, _p(m), _p(st.v), lds, float(eta),
+                                          float(lam), float(st.eps), float(st.beta1),
+                                          float(st.beta2), int(st.t), _p(out.row_ptr),
+                                          _p(out.col_idx), _p(out.vals), cap, None, C.byref(need),
+                                          _p(ws), wsb, _stream(stream)), "prox_adaptive_recompress")
+    st.t += 1
     out.nnz = need.value if need.value >= 0 else None
     return out
 

@@ -37,6 +37,40 @@ bool bad_csr(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr
     return false;
 }
 
+// [rows][ld] float matrices p (cols wide) and q: do their byte ranges overlap?
+bool overlap(const float *p, int64_t ldp, const float *q, int64_t ldq, int64_t rows, int64_t cols) {
+    if (p == nullptr || q == nullptr || rows <= 0 || cols <= 0) return false;
+    const char *p0 = reinterpret_cast<const char *>(p);
+    const char *p1 = p0 + sizeof(float) * ((rows - 1) * ldp + cols);
+    const char *q0 = reinterpret_cast<const char *>(q);
+    const char *q1 = q0 + sizeof(float) * ((rows - 1) * ldq + cols);
+    return p0 < q1 && q0 < p1;
+}
+
+// Prox-RMSProp / Prox-ADAM hyper-parameters -> the kernels' double constants;
+// false if any is out of range (Algorithms 1-2: eta > 0, eps > 0, decay rates
+// in [0, 1), t >= 1 for ADAM's bias corrections; lambda >= 0).
+bool make_adaptive(int solver, float eta, float lambda, float eps, float beta1, float beta2,
+                   int64_t t, adaptive_params *P) {
+    if (solver != L1CSR_SOLVER_RMSPROP && solver != L1CSR_SOLVER_ADAM) return false;
+    if (!finite_f(eta) || !finite_f(lambda) || !finite_f(eps)) return false;
+    if (!(eta > 0.f) || !(lambda >= 0.f) || !(eps > 0.f)) return false;
+    if (!(beta2 >= 0.f && beta2 < 1.f)) return false;
+    const bool adam = solver == L1CSR_SOLVER_ADAM;
+    if (adam && (!(beta1 >= 0.f && beta1 < 1.f) || t < 1)) return false;
+    P->solver = adam ? kSolverAdam : kSolverRms;
+    P->eta = (double)eta;
+    P->thr = (double)eta * (double)lambda;  // exact in double
+    P->eps = (double)eps;
+    P->beta1 = adam ? (double)beta1 : 0.0;
+    P->beta2 = (double)beta2;
+    P->omb1 = 1.0 - P->beta1;
+    P->omb2 = 1.0 - P->beta2;
+    P->bc1 = adam ? 1.0 - pow((double)beta1, (double)t) : 1.0;
+    P->bc2 = adam ? 1.0 - pow((double)beta2, (double)t) : 1.0;
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -255,6 +289,111 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     }
     return hip_status(launch_prox_fill(n_rows, n_cols, pw.seg, col_idx, vals, G, ldg, eta, t, pw.off,
                                        col_idx_out, vals_out, capacity, row_ptr_out, d_nnz_out, stream));
+}
+
+int prox_adaptive_step(int mode, int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                       const int32_t *row_ptr, const int32_t *col_idx, float *vals, const float *G,
+                       int64_t ldg, float *m, float *v, int64_t lds, float eta, float lambda,
+                       float eps, float beta1, float beta2, int64_t t, float *Z, int64_t ldz,
+                       int32_t *row_counts, void *ws, size_t ws_bytes, hipStream_t stream) {
+    adaptive_params P;
+    if (!make_adaptive(solver, eta, lambda, eps, beta1, beta2, t, &P)) return L1CSR_EINVAL;
+    const bool adam = solver == L1CSR_SOLVER_ADAM;
+    if (mode == L1CSR_PROX_CSR) {
+        if (nnz < 0 || nnz > INT32_MAX) return L1CSR_EINVAL;
+        if (nnz > 0 && (vals == nullptr || G == nullptr || v == nullptr || (adam && m == nullptr)))
+            return L1CSR_EINVAL;
+        // state and gradient arrays are distinct, one entry per stored weight
+        if (overlap(G, nnz, v, nnz, 1, nnz) || overlap(vals, nnz, v, nnz, 1, nnz) ||
+            (adam && (overlap(m, nnz, v, nnz, 1, nnz) || overlap(m, nnz, G, nnz, 1, nnz) ||
+                      overlap(m, nnz, vals, nnz, 1, nnz))))
+            return L1CSR_EINVAL;
+        return hip_status(launch_adaptive_csr(nnz, vals, G, adam ? m : nullptr, v, P, stream));
+    }
+    if (mode != L1CSR_PROX_DENSE) return L1CSR_EINVAL;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(G, n_rows, n_cols, ldg) || bad_dense(Z, n_rows, n_cols, ldz) ||
+        bad_dense(v, n_rows, n_cols, lds) || (adam && bad_dense(m, n_rows, n_cols, lds)))
+        return L1CSR_EINVAL;
+    if (Z == G ? ldz != ldg : overlap(Z, ldz, G, ldg, n_rows, n_cols)) return L1CSR_EINVAL;
+    if (overlap(v, lds, G, ldg, n_rows, n_cols) || overlap(v, lds, Z, ldz, n_rows, n_cols))
+        return L1CSR_EINVAL;
+    if (adam && (overlap(m, lds, G, ldg, n_rows, n_cols) || overlap(m, lds, Z, ldz, n_rows, n_cols) ||
+                 overlap(m, lds, v, lds, n_rows, n_cols)))
+        return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
+        return L1CSR_EINVAL;
+    const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
+    if (n_slabs > INT32_MAX) return L1CSR_EUNSUPPORTED;
+    if (n_rows == 0) return L1CSR_OK;
+    if (n_cols == 0)
+        return hip_status(row_counts ? launch_fill_i32(row_counts, n_rows, 0, stream) : hipSuccess);
+    const prox_ws pw = prox_carve(n_rows, n_cols, ws);
+    return hip_status(launch_adaptive_slabs(kStageDense, n_rows, n_cols, row_ptr, col_idx, vals, G,
+                                            ldg, adam ? m : nullptr, v, lds, P, pw.seg, nullptr,
+                                            nullptr, nullptr, nullptr, 0, nullptr, nullptr, Z, ldz,
+                                            row_counts, stream));
+}
+
+int prox_adaptive_recompress(int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                             const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                             const float *G, int64_t ldg, float *m, float *v, int64_t lds,
+                             float eta, float lambda, float eps, float beta1, float beta2, int64_t t,
+                             int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                             int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                             void *ws, size_t ws_bytes, hipStream_t stream) {
+    adaptive_params P;
+    if (!make_adaptive(solver, eta, lambda, eps, beta1, beta2, t, &P)) return L1CSR_EINVAL;
+    const bool adam = solver == L1CSR_SOLVER_ADAM;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(G, n_rows, n_cols, ldg) || bad_dense(v, n_rows, n_cols, lds) ||
+        (adam && bad_dense(m, n_rows, n_cols, lds)) || row_ptr_out == nullptr || capacity < 0)
+        return L1CSR_EINVAL;
+    if (overlap(v, lds, G, ldg, n_rows, n_cols) ||
+        (adam && (overlap(m, lds, G, ldg, n_rows, n_cols) || overlap(m, lds, v, lds, n_rows, n_cols))))
+        return L1CSR_EINVAL;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
+    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
+        return L1CSR_EINVAL;
+    if (row_ptr_out == row_ptr) return L1CSR_EINVAL;  // out of place
+    if (n_rows == 0) {
+        hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
+        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
+        if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
+        return hip_status(e);
+    }
+    const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
+    if (n_slabs > INT32_MAX) return L1CSR_EUNSUPPORTED;
+    float *M = adam ? m : nullptr;
+    const prox_ws pw = prox_carve(n_rows, n_cols, ws);
+    // with room for every weight the count pass stores the new moments and the
+    // fill pass recomputes from them; otherwise the state is only written once
+    // the output is known to fit
+    const bool roomy = capacity >= total;
+    hipError_t e = launch_adaptive_slabs(roomy ? kStageCountWrite : kStageCountKeep, n_rows, n_cols,
+                                         row_ptr, col_idx, vals, G, ldg, M, v, lds, P, pw.seg,
+                                         pw.counts, nullptr, nullptr, nullptr, 0, nullptr, nullptr,
+                                         nullptr, 0, nullptr, stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(pw.counts, pw.off, (int)n_slabs, nullptr, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    if (!roomy) {
+        e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        int32_t h = 0;
+        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        if (h_nnz_required) *h_nnz_required = h;
+        if (h > capacity) return L1CSR_ECAPACITY;
+    } else if (h_nnz_required) {
+        *h_nnz_required = -1;
+    }
+    return hip_status(launch_adaptive_slabs(roomy ? kStageFillStored : kStageFillWrite, n_rows, n_cols,
+                                            row_ptr, col_idx, vals, G, ldg, M, v, lds, P, pw.seg,
+                                            nullptr, pw.off, col_idx_out, vals_out, capacity,
+                                            row_ptr_out, d_nnz_out, nullptr, 0, nullptr, stream));
 }
 
 int csr_compact(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,

@@ -64,6 +64,8 @@ hipError_t launch_sddmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, con
                         void *ws, hipStream_t s);
 
 // prox.hip -----------------------------------------------------------------
+// the fused prox kernels work on slabs of 1 << kProxSlabShift columns of a row
+constexpr int kProxSlabShift = 11;
 hipError_t launch_prox_dense(int n_rows, int n_cols, const int *ptr, const int *idx,
                              const float *vals, const float *G, int64_t ldg, float eta, double t,
                              float *Z, int64_t ldz, int *row_counts, hipStream_t s);
@@ -92,6 +94,36 @@ hipError_t launch_prox_fill(int n_rows, int n_cols, const int *seg, const int *i
                             const float *vals, const float *G, int64_t ldg, float eta, double t,
                             const int *off, int *col_out, float *val_out, int64_t capacity,
                             int *row_ptr, int *nnz_out, hipStream_t s);
+
+// prox_adaptive.hip --------------------------------------------------------
+// Prox-RMSProp / Prox-ADAM parameters, prepared on the host in double
+constexpr int kSolverRms = 1;
+constexpr int kSolverAdam = 2;
+struct adaptive_params {
+    int solver;
+    double eta, thr, eps;       // step, threshold eta*lambda, safeguard
+    double beta1, beta2;        // decay rates (RMSProp: beta2 is its beta)
+    double omb1, omb2;          // 1 - beta1, 1 - beta2
+    double bc1, bc2;            // ADAM: 1 - beta^t; RMSProp: unused
+};
+// slab passes of the adaptive step (stages of one call)
+enum {
+    kStageCountWrite = 0,   // count the new weights per slab, store m', v'
+    kStageCountKeep = 1,    // count only (state untouched)
+    kStageFillStored = 2,   // compact, recomputing from the stored m', v'
+    kStageFillWrite = 3,    // compact and store m', v'
+    kStageDense = 4         // write Z and row counts, store m', v'
+};
+// seg and counts are the prox_carve() parts; the count and dense stages also
+// compute seg.  Arguments a stage does not use may be null.
+hipError_t launch_adaptive_slabs(int stage, int n_rows, int n_cols, const int *ptr, const int *idx,
+                                 const float *vals, const float *G, int64_t ldg, float *M, float *V,
+                                 int64_t lds, const adaptive_params &P, int *seg, int *counts,
+                                 const int *off, int *col_out, float *val_out, int64_t capacity,
+                                 int *row_ptr, int *nnz_out, float *Z, int64_t ldz, int *row_counts,
+                                 hipStream_t s);
+hipError_t launch_adaptive_csr(int64_t nnz, float *vals, const float *g, float *M, float *V,
+                               const adaptive_params &P, hipStream_t s);
 
 // recompress.hip -----------------------------------------------------------
 hipError_t launch_count_rows(int n_rows, int n_cols, const float *Z, int64_t ldz, float t,

@@ -107,7 +107,7 @@ __global__ void prox_csr_kernel(int64_t nnz, float *__restrict__ vals, const flo
 // exactly the CSR layout of the result, and row_ptr[row] = off[row * S].
 // seg[row][j] (j = 0 .. S) = first entry of the row with column >= j * kSlab,
 // so a slab reads only its own entries of W.
-constexpr int kSlabShift = 11;
+constexpr int kSlabShift = kProxSlabShift;
 constexpr int kSlab = 1 << kSlabShift;
 constexpr int kSlabChunks = kSlab / (kProxThreads * 4);
 

@@ -44,7 +44,8 @@ def test_header_declares_the_hot_path_calls():
     names = declared_functions()
     for n in ["csr_spmm_fwd", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad", "prox_l1_step",
               "csr_recompress", "prox_l1_recompress", "csc_build", "csc_update_vals", "csr_compact",
-              "csr_validate", "l1csr_workspace_bytes", "l1csr_status_str"]:
+              "csr_validate", "l1csr_workspace_bytes", "l1csr_status_str", "prox_adaptive_step",
+              "prox_adaptive_recompress"]:
         assert n in names, n
 
 
@@ -162,3 +163,53 @@ def test_invalid_arguments_are_rejected_before_launch(lib):
     assert lib.csc_build(4, 4, 3, P, P, P, P, P, P, P, NUL, 0, S) == EINVAL
     # backward: half a CSC (row_idx without col_ptr)
     assert lib.csr_spmm_bwd_t(4, 4, 3, P, P, P, NUL, P, NUL, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
+
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_adaptive_prox_arguments_are_rejected_before_launch(lib):
+    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    lib.prox_adaptive_step.argtypes = [C.c_int, C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
+                                       f32, f32, f32, f32, f32, i64, vp, i64, vp, vp, C.c_size_t, vp]
+    lib.prox_adaptive_recompress.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
+                                             f32, f32, f32, f32, f32, i64, vp, vp, vp, i64, vp, vp, vp,
+                                             C.c_size_t, vp]
+    # distinct, far-apart placeholder buffers: W arrays, G, m, v, Z, outputs, workspace
+    Wp, G, M, V, Z, O, WS = (C.c_void_p(a << 24) for a in range(1, 8))
+    ws = lib.l1csr_workspace_bytes(7, 4, 4, 3, 0)
+    step, rec = lib.prox_adaptive_step, lib.prox_adaptive_recompress
+    nan, inf = float("nan"), float("inf")
+
+    def dense(solver=2, eta=0.01, lam=0.1, eps=1e-8, b1=0.9, b2=0.999, t=1, m=M, v=V, z=Z, g=G,
+              ldg=4, lds=4, ldz=4, w=WS, wb=None):
+        return step(0, solver, 4, 4, 3, Wp, Wp, Wp, g, ldg, m, v, lds, eta, lam, eps, b1, b2, t, z, ldz,
+                    NUL, w, ws if wb is None else wb, S)
+
+    def fused(solver=2, eta=0.01, lam=0.1, eps=1e-8, b1=0.9, b2=0.999, t=1, m=M, v=V, g=G, out=O,
+              w=WS, wb=None):
+        return rec(solver, 4, 4, 3, Wp, Wp, Wp, g, 4, m, v, 4, eta, lam, eps, b1, b2, t, out, out, out,
+                   16, NUL, NUL, w, ws if wb is None else wb, S)
+
+    for f in (dense, fused):
+        # solver codes, step, threshold and safeguard parameters (Algorithms 1-2)
+        for bad in [dict(solver=0), dict(solver=3), dict(eta=0.0), dict(eta=nan), dict(lam=-1.0),
+                    dict(lam=inf), dict(eps=0.0), dict(eps=-1e-8), dict(eps=nan), dict(b2=1.0),
+                    dict(b2=-0.1), dict(b1=1.0), dict(b1=-0.5), dict(t=0), dict(t=-3)]:
+            assert f(**bad) == EINVAL, (f.__name__, bad)
+        # ADAM needs m; G, m, v must be distinct buffers; a short workspace
+        assert f(m=NUL) == EINVAL
+        assert f(m=V) == EINVAL and f(v=G) == EINVAL and f(m=G) == EINVAL
+        assert f(w=NUL) == EINVAL and f(wb=1) == EINVAL
+    # dense form: Z over the state, short leading dimensions
+    assert dense(z=V) == EINVAL and dense(solver=1, m=NUL, z=V) == EINVAL
+    assert dense(ldg=3) == EINVAL and dense(lds=3) == EINVAL and dense(ldz=3) == EINVAL
+    # fused: the output CSR must not be W's
+    assert fused(out=Wp) == EINVAL
+    # stored-entry form: missing state, state over the gradient or the values
+    assert step(1, 2, 4, 4, 3, Wp, Wp, Wp, G, 0, NUL, V, 0, 0.01, 0.0, 1e-8, 0.9, 0.999, 1, NUL, 0,
+                NUL, NUL, 0, S) == EINVAL
+    assert step(1, 1, 4, 4, 3, Wp, Wp, Wp, G, 0, NUL, G, 0, 0.01, 0.0, 1e-8, 0.9, 0.999, 1, NUL, 0,
+                NUL, NUL, 0, S) == EINVAL
+    assert step(1, 1, 4, 4, 3, Wp, Wp, V, G, 0, NUL, V, 0, 0.01, 0.0, 1e-8, 0.9, 0.999, 1, NUL, 0,
+                NUL, NUL, 0, S) == EINVAL
+    assert step(5, 1, 4, 4, 3, Wp, Wp, Wp, G, 4, NUL, V, 4, 0.01, 0.0, 1e-8, 0.9, 0.999, 1, Z, 4,
+                NUL, WS, ws, S) == EINVAL
