@@ -372,6 +372,30 @@ def test_prox_l1_recompress_fused_bit_exact(NK):
         assert bits_equal(h(out.col_idx)[:n], ci) and bits_equal(h(out.vals)[:n], v)
 
 
+@pytest.mark.parametrize("NK", [(9000, 333), (2000, 9217), (4096, 4096), (700, 20001), (1, 1)])
+def test_prox_l1_recompress_large_shapes_both_capacity_paths(NK):
+    # thousands of slabs (ragged last slab when K % 2048 != 0): the no-wait call
+    # (capacity N*K) and the checked call (capacity N*K - 1: count, wait, fill)
+    # must both equal the oracle bit for bit
+    N, K = NK
+    L = synth.fc_layer(N, K, 4, int(0.05 * N * K), seed=N ^ K)
+    rng = np.random.default_rng(N + K)
+    G = (rng.standard_normal((N, K)) * 0.05).astype(np.float32)
+    eta, lam = 0.5, 0.05
+    one = L1.prox_l1_recompress(_W(L), t(G), eta, lam)
+    Zr, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, G, eta, lam, K)
+    rp, ci, v = oracle.recompress(Zr)
+    n = int(rp[-1])
+    assert 0 < n < N * K or N * K == 1
+    assert bits_equal(h(one.row_ptr), rp)
+    assert bits_equal(h(one.col_idx)[:n], ci) and bits_equal(h(one.vals)[:n], v)
+    if n < N * K:
+        two = L1.prox_l1_recompress(_W(L), t(G), eta, lam, capacity=N * K - 1)
+        assert two.nnz == n
+        assert bits_equal(h(two.row_ptr), rp)
+        assert bits_equal(h(two.col_idx)[:n], ci) and bits_equal(h(two.vals)[:n], v)
+
+
 def test_prox_l1_recompress_capacity():
     L = synth.fc_layer(30, 50, 4, 150, seed=3)
     rng = np.random.default_rng(3)
