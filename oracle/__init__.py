@@ -67,6 +67,11 @@ def lib():
                                               _f32p, i64, C.c_void_p]
         L.orc_prox_adaptive_csr.argtypes = [i32, i32, _f32p, _f32p, _f32p, _f32p, f32, f32, f32,
                                             f32, f32, i64, _f32p]
+        conv = [i32] * 9
+        L.orc_conv_fwd.argtypes = [i32] + conv + [i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
+        L.orc_conv_bwd_data.argtypes = [i32] + conv + [i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
+        L.orc_im2col.argtypes = conv + [i32, _f32p, i64, _f32p, i64]
+        L.orc_maxpool_fwd.argtypes = [i32] * 7 + [i32, _f32p, i64, _f32p, i64]
         L.orc_recompress.argtypes = [i32, i32, _f32p, i64, f32, _i32p, _i32p, _f32p, i64,
                                      C.POINTER(C.c_int64)]
         L.orc_compact.argtypes = [i32, _i32p, _i32p, _f32p, _i32p, _i32p, _f32p,
@@ -246,6 +251,56 @@ def prox_adaptive_csr(solver, vals, gv, m, v, eta, lam, eps, beta1, beta2, t):
     _check(lib().orc_prox_adaptive_csr(int(solver), w.shape[0], w, g, m2, v2, eta, lam, eps,
                                        beta1, beta2, int(t), out), "prox_adaptive_csr")
     return out, m2, v2
+
+
+def conv_out_size(H, Wd, KH, KW, SH=1, SW=1, PH=0, PW=0):
+    """(OH, OW) of a convolution (floor division), as the oracle computes them."""
+    return (H + 2 * PH - KH) // SH + 1, (Wd + 2 * PW - KW) // SW + 1
+
+
+def conv_fwd(row_ptr, col_idx, vals, X, C, H, Wd, KH, KW, SH=1, SW=1, PH=0, PW=0):
+    """Direct sparse convolution: X is [C*H*W][B] maps, W an N x (C*KH*KW) CSR
+    filter bank; returns the [N*OH*OW][B] output maps."""
+    rp, ci, v = _csr(row_ptr, col_idx, vals)
+    X = _c(X, np.float32)
+    B = X.shape[1]
+    N = rp.shape[0] - 1
+    OH, OW = conv_out_size(H, Wd, KH, KW, SH, SW, PH, PW)
+    Y = np.empty((N * OH * OW, B), np.float32)
+    _check(lib().orc_conv_fwd(N, C, H, Wd, KH, KW, SH, SW, PH, PW, B, rp, ci, v, X, B, Y, B), "conv_fwd")
+    return Y
+
+
+def conv_bwd_data(row_ptr, col_idx, vals, dY, C, H, Wd, KH, KW, SH=1, SW=1, PH=0, PW=0):
+    """The adjoint of conv_fwd: [N*OH*OW][B] output gradients -> [C*H*W][B]."""
+    rp, ci, v = _csr(row_ptr, col_idx, vals)
+    dY = _c(dY, np.float32)
+    B = dY.shape[1]
+    N = rp.shape[0] - 1
+    dX = np.empty((C * H * Wd, B), np.float32)
+    _check(lib().orc_conv_bwd_data(N, C, H, Wd, KH, KW, SH, SW, PH, PW, B, rp, ci, v, dY, B, dX, B),
+           "conv_bwd_data")
+    return dX
+
+
+def im2col(X, C, H, Wd, KH, KW, SH=1, SW=1, PH=0, PW=0):
+    """The lowered operand: [C*KH*KW][OH*OW*B]."""
+    X = _c(X, np.float32)
+    B = X.shape[1]
+    OH, OW = conv_out_size(H, Wd, KH, KW, SH, SW, PH, PW)
+    out = np.empty((C * KH * KW, OH * OW * B), np.float32)
+    _check(lib().orc_im2col(C, H, Wd, KH, KW, SH, SW, PH, PW, B, X, B, out, OH * OW * B), "im2col")
+    return out
+
+
+def maxpool_fwd(X, C, H, Wd, KH=2, KW=2, SH=2, SW=2):
+    """Max pooling of [C*H*W][B] maps -> [C*OH*OW][B]."""
+    X = _c(X, np.float32)
+    B = X.shape[1]
+    OH, OW = conv_out_size(H, Wd, KH, KW, SH, SW)
+    Y = np.empty((C * OH * OW, B), np.float32)
+    _check(lib().orc_maxpool_fwd(C, H, Wd, KH, KW, SH, SW, B, X, B, Y, B), "maxpool_fwd")
+    return Y
 
 
 def recompress(Z, t=0.0):

@@ -394,6 +394,161 @@ int orc_prox_adaptive_csr(int32_t solver, int32_t nnz, const float *vals, const 
 }
 
 /* ------------------------------------------------------------------------
+ * Convolution layers with CSR filters (the conv rows of Tables A1-A4; Caffe,
+ * which the paper builds on, lowers a convolution to the products of
+ * Section 3.2 through im2col).  Layout, as for the fully connected layers:
+ * maps are [C][H][W] rows of a batch-contiguous matrix, X[(c*H + h)*Wd + w][b];
+ * the filter bank is a CSR matrix with one row per output channel and column
+ * index (ci*KH + kh)*KW + kw.  Cross-correlation (no filter flip), stride
+ * SH x SW, zero padding PH x PW, output OH = (H + 2 PH - KH)/SH + 1 (floor),
+ * OW likewise.  The output maps are [(co*OH + oh)*OW + ow][b].
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t C, H, Wd, KH, KW, SH, SW, PH, PW, OH, OW;
+} orc_conv_geom;
+
+static int orc_conv_setup(int32_t C, int32_t H, int32_t Wd, int32_t KH, int32_t KW, int32_t SH,
+                          int32_t SW, int32_t PH, int32_t PW, orc_conv_geom *g) {
+    if (C < 1 || H < 1 || Wd < 1 || KH < 1 || KW < 1 || SH < 1 || SW < 1 || PH < 0 || PW < 0)
+        return ORC_EINVAL;
+    if (H + 2 * PH < KH || Wd + 2 * PW < KW) return ORC_EINVAL;
+    g->C = C; g->H = H; g->Wd = Wd; g->KH = KH; g->KW = KW;
+    g->SH = SH; g->SW = SW; g->PH = PH; g->PW = PW;
+    g->OH = (H + 2 * PH - KH) / SH + 1;
+    g->OW = (Wd + 2 * PW - KW) / SW + 1;
+    return ORC_OK;
+}
+
+/* Forward: Y[(co,oh,ow)][b] = sum_{p in row co} vals[p] * X[(ci, oh*SH-PH+kh, ow*SW-PW+kw)][b]
+ * over the entries whose input position lies inside the map (p ascending). */
+int orc_conv_fwd(int32_t N, int32_t C, int32_t H, int32_t Wd, int32_t KH, int32_t KW, int32_t SH,
+                 int32_t SW, int32_t PH, int32_t PW, int32_t B, const int32_t *row_ptr,
+                 const int32_t *col_idx, const float *vals, const float *X, int64_t ldx, float *Y,
+                 int64_t ldy) {
+    orc_conv_geom g;
+    if (N < 0 || B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    if (orc_conv_setup(C, H, Wd, KH, KW, SH, SW, PH, PW, &g) != ORC_OK) return ORC_EINVAL;
+    #pragma omp parallel
+    {
+        double *acc = (double *)malloc(sizeof(double) * (size_t)(B > 0 ? B : 1));
+        #pragma omp for schedule(dynamic, 4)
+        for (int32_t co = 0; co < N; ++co) {
+            for (int32_t oh = 0; oh < g.OH; ++oh)
+                for (int32_t ow = 0; ow < g.OW; ++ow) {
+                    for (int32_t b = 0; b < B; ++b) acc[b] = 0.0;
+                    for (int32_t p = row_ptr[co]; p < row_ptr[co + 1]; ++p) {
+                        const int32_t ci = col_idx[p] / (KH * KW);
+                        const int32_t kh = (col_idx[p] / KW) % KH;
+                        const int32_t kw = col_idx[p] % KW;
+                        const int32_t ih = oh * SH - PH + kh, iw = ow * SW - PW + kw;
+                        if (ih < 0 || ih >= H || iw < 0 || iw >= Wd) continue;
+                        const double w = (double)vals[p];
+                        const float *xr = X + ((int64_t)(ci * H + ih) * Wd + iw) * ldx;
+                        for (int32_t b = 0; b < B; ++b) acc[b] += w * (double)xr[b];
+                    }
+                    float *yr = Y + ((int64_t)(co * g.OH + oh) * g.OW + ow) * ldy;
+                    for (int32_t b = 0; b < B; ++b) yr[b] = (float)acc[b];
+                }
+        }
+        free(acc);
+    }
+    return ORC_OK;
+}
+
+/* Backward for the input maps, the adjoint of orc_conv_fwd:
+ *   dX[(ci,ih,iw)][b] = sum over entries p = (co; ci,kh,kw) and output positions
+ *   (oh, ow) with oh*SH-PH+kh = ih, ow*SW-PW+kw = iw of vals[p] * dY[(co,oh,ow)][b].
+ * Accumulated in double over (co, p, oh, ow) in that order, rounded once. */
+int orc_conv_bwd_data(int32_t N, int32_t C, int32_t H, int32_t Wd, int32_t KH, int32_t KW,
+                      int32_t SH, int32_t SW, int32_t PH, int32_t PW, int32_t B,
+                      const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                      const float *dY, int64_t ldy, float *dX, int64_t ldx) {
+    orc_conv_geom g;
+    if (N < 0 || B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    if (orc_conv_setup(C, H, Wd, KH, KW, SH, SW, PH, PW, &g) != ORC_OK) return ORC_EINVAL;
+    const int64_t rows = (int64_t)C * H * Wd;
+    double *acc = (double *)calloc((size_t)(rows * B > 0 ? rows * B : 1), sizeof(double));
+    if (!acc) return ORC_EINVAL;
+    /* parallel over input channels: every entry p writes only into its own ci */
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t cc = 0; cc < C; ++cc)
+        for (int32_t co = 0; co < N; ++co)
+            for (int32_t p = row_ptr[co]; p < row_ptr[co + 1]; ++p) {
+                const int32_t ci = col_idx[p] / (KH * KW);
+                if (ci != cc) continue;
+                const int32_t kh = (col_idx[p] / KW) % KH;
+                const int32_t kw = col_idx[p] % KW;
+                const double w = (double)vals[p];
+                for (int32_t oh = 0; oh < g.OH; ++oh)
+                    for (int32_t ow = 0; ow < g.OW; ++ow) {
+                        const int32_t ih = oh * SH - PH + kh, iw = ow * SW - PW + kw;
+                        if (ih < 0 || ih >= H || iw < 0 || iw >= Wd) continue;
+                        const float *dyr = dY + ((int64_t)(co * g.OH + oh) * g.OW + ow) * ldy;
+                        double *ar = acc + ((int64_t)(ci * H + ih) * Wd + iw) * B;
+                        for (int32_t b = 0; b < B; ++b) ar[b] += w * (double)dyr[b];
+                    }
+            }
+    for (int64_t r = 0; r < rows; ++r)
+        for (int32_t b = 0; b < B; ++b) dX[r * ldx + b] = (float)acc[r * B + b];
+    free(acc);
+    return ORC_OK;
+}
+
+/* im2col (Caffe's lowering): the matrix whose product with the filter bank is
+ * the convolution,
+ *   Xcol[(ci*KH + kh)*KW + kw][(oh*OW + ow)*B + b] = X[(ci, oh*SH-PH+kh, ow*SW-PW+kw)][b]
+ * (0 where the position falls in the padding); Xcol is [C*KH*KW][ldc],
+ * ldc >= OH*OW*B.  The product W . Xcol is then [N][OH*OW*B], the output maps
+ * in the batch-contiguous layout. */
+int orc_im2col(int32_t C, int32_t H, int32_t Wd, int32_t KH, int32_t KW, int32_t SH, int32_t SW,
+               int32_t PH, int32_t PW, int32_t B, const float *X, int64_t ldx, float *Xcol,
+               int64_t ldc) {
+    orc_conv_geom g;
+    if (B < 0 || ldx < B) return ORC_EINVAL;
+    if (orc_conv_setup(C, H, Wd, KH, KW, SH, SW, PH, PW, &g) != ORC_OK) return ORC_EINVAL;
+    if (ldc < (int64_t)g.OH * g.OW * B) return ORC_EINVAL;
+    #pragma omp parallel for schedule(static)
+    for (int32_t r = 0; r < C * KH * KW; ++r) {
+        const int32_t ci = r / (KH * KW), kh = (r / KW) % KH, kw = r % KW;
+        for (int32_t oh = 0; oh < g.OH; ++oh)
+            for (int32_t ow = 0; ow < g.OW; ++ow) {
+                const int32_t ih = oh * SH - PH + kh, iw = ow * SW - PW + kw;
+                float *dst = Xcol + (int64_t)r * ldc + ((int64_t)oh * g.OW + ow) * B;
+                const int inside = ih >= 0 && ih < H && iw >= 0 && iw < Wd;
+                const float *src = inside ? X + ((int64_t)(ci * H + ih) * Wd + iw) * ldx : NULL;
+                for (int32_t b = 0; b < B; ++b) dst[b] = inside ? src[b] : 0.0f;
+            }
+    }
+    return ORC_OK;
+}
+
+/* Max pooling over KH x KW windows with stride SH x SW, no padding (the
+ * subsampling layers of LeNet-5): Y[(c,oh,ow)][b] = max over the window of
+ * X[(c, oh*SH+i, ow*SW+j)][b]; OH = (H - KH)/SH + 1 (floor). */
+int orc_maxpool_fwd(int32_t C, int32_t H, int32_t Wd, int32_t KH, int32_t KW, int32_t SH, int32_t SW,
+                    int32_t B, const float *X, int64_t ldx, float *Y, int64_t ldy) {
+    orc_conv_geom g;
+    if (B < 0 || ldx < B || ldy < B) return ORC_EINVAL;
+    if (orc_conv_setup(C, H, Wd, KH, KW, SH, SW, 0, 0, &g) != ORC_OK) return ORC_EINVAL;
+    #pragma omp parallel for schedule(static)
+    for (int32_t c = 0; c < C; ++c)
+        for (int32_t oh = 0; oh < g.OH; ++oh)
+            for (int32_t ow = 0; ow < g.OW; ++ow) {
+                float *yr = Y + ((int64_t)(c * g.OH + oh) * g.OW + ow) * ldy;
+                for (int32_t b = 0; b < B; ++b) {
+                    float m = -INFINITY;
+                    for (int32_t i = 0; i < KH; ++i)
+                        for (int32_t j = 0; j < KW; ++j) {
+                            const float v = X[((int64_t)(c * H + oh * SH + i) * Wd + ow * SW + j) * ldx + b];
+                            if (v > m) m = v;
+                        }
+                    yr[b] = m;
+                }
+            }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
  * Dense -> CSR (Section 3.1: store only the nonzero values; Fig. 1(iii)).
  * Keeps the entries with |Z[i][k]| > t (t = 0 after a prox step) in row-major
  * order.  Writes row_ptr[N+1] and, when nnz <= capacity, col_idx/vals.
