@@ -12,6 +12,7 @@
  *   proximal step      Z  = S_t(W - eta*dW), t = eta*lambda        prox_l1_step
  *   recompression      Z -> CSR                   csr_recompress
  *   adaptive solvers   Prox-RMSProp / Prox-ADAM   prox_adaptive_step, prox_adaptive_recompress
+ *   conv layers        direct sparse convolution  csr_conv_fwd, csr_conv_bwd_data, conv_im2col
  *
  * Conventions shared by every call
  *   - CSR: row_ptr[n_rows+1] (row_ptr[0] = 0, non-decreasing), col_idx[nnz]
@@ -328,6 +329,55 @@ int csr_compact(int32_t n_rows, int64_t nnz,
  */
 int csr_validate(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
                  const int32_t *col_idx, int32_t *d_status, hipStream_t stream);
+
+/*
+ * Convolution layers with CSR filter banks (the conv rows of Tables A1-A4; in
+ * Caffe, which the method is built on, a convolution is the product of
+ * Section 3.2 with the im2col-lowered input).  Shared conventions:
+ *   - geom (HOST memory, 9 int32): C, H, W, KH, KW, SH, SW, PH, PW = input
+ *     channels, map height and width, filter height and width, stride, zero
+ *     padding.  Output maps OH = (H + 2 PH - KH)/SH + 1, OW likewise (floor).
+ *     An invalid geometry (a size < 1, negative padding, a filter larger than
+ *     the padded map) returns L1CSR_EINVAL.
+ *   - Maps are batch-contiguous matrices like every other activation here:
+ *     X[(c*H + h)*W + w][b] with leading dimension ldx >= B; outputs
+ *     Y[(co*OH + oh)*OW + ow][b].
+ *   - The filter bank is an n_out x (C*KH*KW) CSR matrix, column
+ *     (ci*KH + kh)*KW + kw (Caffe's im2col row order); cross-correlation, no
+ *     flip.
+ *
+ * csr_conv_fwd: the forward product computed directly on the maps,
+ *     Y[(co,oh,ow)][b] = sum_{p in row co} vals[p] * X[(ci, oh*SH-PH+kh, ow*SW-PW+kw)][b]
+ *   over the entries whose input position lies inside the map (padding
+ *   contributes zero), summed in CSR order by one thread per output element.
+ *   Equal to csr_spmm_fwd on conv_im2col(X) without forming the lowered
+ *   operand.
+ * csr_conv_bwd_data: the backward product for the input maps (the adjoint of
+ *   csr_conv_fwd), from the CSC copy of the filter bank (csc_build with
+ *   n_rows = n_out, n_cols = C*KH*KW):
+ *     dX[(ci,ih,iw)][b] = sum over the entries (co; ci,kh,kw) and the output
+ *     positions with oh*SH-PH+kh = ih, ow*SW-PW+kw = iw of w * dY[(co,oh,ow)][b],
+ *   summed by one thread per element in (kh, kw, CSC) order, reproducible.
+ * conv_im2col: the lowered input, Xcol[(ci*KH + kh)*KW + kw][(oh*OW + ow)*B + b]
+ *   (0 in the padding), Xcol [C*KH*KW][ldc], ldc >= OH*OW*B.  With dY
+ *   stored with ldy == B, dY is the [n_out][OH*OW*B] matrix of the lowered
+ *   product, so dense_wgrad(dY, Xcol) and sddmm_masked_wgrad(W, dY, Xcol) give
+ *   the filter gradient of the l1 and the debiasing phase.
+ * l1csr_maxpool_fwd: max over KH x KW windows with stride SH x SW (the
+ *   subsampling layers of LeNet-5), Y[(c,oh,ow)][b]; geom's padding must be 0
+ *   (else L1CSR_EUNSUPPORTED).  Values must be finite.
+ */
+int csr_conv_fwd(const int32_t *geom, int32_t n_out, int64_t nnz,
+                 const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                 const float *X, int64_t ldx, int32_t B, float *Y, int64_t ldy, hipStream_t stream);
+int csr_conv_bwd_data(const int32_t *geom, int32_t n_out, int64_t nnz,
+                      const int32_t *col_ptr, const int32_t *row_idx, const float *vals_t,
+                      const float *dY, int64_t ldy, int32_t B, float *dX, int64_t ldx,
+                      hipStream_t stream);
+int conv_im2col(const int32_t *geom, const float *X, int64_t ldx, int32_t B,
+                float *Xcol, int64_t ldc, hipStream_t stream);
+int l1csr_maxpool_fwd(const int32_t *geom, const float *X, int64_t ldx, int32_t B,
+                      float *Y, int64_t ldy, hipStream_t stream);
 
 /*
  * Layer glue of the fully connected ReLU networks the method trains (their

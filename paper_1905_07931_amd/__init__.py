@@ -19,6 +19,7 @@ __all__ = [
     "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "csr_validate", "relu_fwd", "relu_bwd",
     "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16",
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
+    "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
@@ -72,6 +73,10 @@ def lib():
                                                f32, f32, f32, f32, f32, i64, vp, vp, vp, i64, vp,
                                                C.POINTER(C.c_int64), vp, sz, vp]
         L.csr_compact.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csr_conv_fwd.argtypes = [vp, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp]
+        L.csr_conv_bwd_data.argtypes = [vp, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp]
+        L.conv_im2col.argtypes = [vp, vp, i64, i32, vp, i64, vp]
+        L.l1csr_maxpool_fwd.argtypes = [vp, vp, i64, i32, vp, i64, vp]
         L.csr_validate.argtypes = [i32, i32, i64, vp, vp, vp, vp]
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
         L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
@@ -79,7 +84,8 @@ def lib():
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
                      "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent",
-                     "prox_adaptive_step", "prox_adaptive_recompress"):
+                     "prox_adaptive_step", "prox_adaptive_recompress", "csr_conv_fwd",
+                     "csr_conv_bwd_data", "conv_im2col", "l1csr_maxpool_fwd"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -522,6 +528,108 @@ def prox_adaptive_recompress(W: CSR, G, st: AdaptiveState, eta, lam, capacity=No
     st.t += 1
     out.nnz = need.value if need.value >= 0 else None
     return out
+
+
+@dataclass
+class ConvGeom:
+    """Convolution geometry: input channels C, maps H x W, filters KH x KW,
+    stride SH x SW, zero padding PH x PW."""
+    C: int
+    H: int
+    W: int
+    KH: int
+    KW: int
+    SH: int = 1
+    SW: int = 1
+    PH: int = 0
+    PW: int = 0
+
+    @property
+    def out_hw(self):
+        return ((self.H + 2 * self.PH - self.KH) // self.SH + 1,
+                (self.W + 2 * self.PW - self.KW) // self.SW + 1)
+
+    @property
+    def in_rows(self):
+        return self.C * self.H * self.W
+
+    @property
+    def filter_cols(self):
+        return self.C * self.KH * self.KW
+
+    def _arr(self):
+        return (C.c_int32 * 9)(self.C, self.H, self.W, self.KH, self.KW, self.SH, self.SW, self.PH, self.PW)
+
+
+def csr_conv_fwd(g: ConvGeom, W: CSR, X, Y=None, stream=None):
+    """Output maps [n_out*OH*OW][B] of the CSR filter bank W on maps X [C*H*W][B]."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    rows, B, ldx = _mat(X, "X")
+    if rows != g.in_rows or W.n_cols != g.filter_cols:
+        raise ValueError("X must be [C*H*W][B] and W must have C*KH*KW columns")
+    OH, OW = g.out_hw
+    if Y is None:
+        Y = torch.empty((W.n_rows * OH * OW, B), dtype=torch.float32, device=X.device)
+    ry, by, ldy = _mat(Y, "Y")
+    if (ry, by) != (W.n_rows * OH * OW, B):
+        raise ValueError("Y must be [n_out*OH*OW][B]")
+    _check(lib().csr_conv_fwd(g._arr(), W.n_rows, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(X), ldx,
+                              B, _p(Y), ldy, _stream(stream)), "csr_conv_fwd")
+    return Y
+
+
+def csr_conv_bwd_data(g: ConvGeom, n_out: int, csc: CSC, dY, dX=None, nnz=None, stream=None):
+    """Input-map gradient [C*H*W][B] from dY [n_out*OH*OW][B] and the CSC copy
+    of the filter bank (csc_build of the n_out x C*KH*KW CSR)."""
+    torch = _torch()
+    rows, B, ldy = _mat(dY, "dY")
+    OH, OW = g.out_hw
+    if rows != n_out * OH * OW:
+        raise ValueError("dY must be [n_out*OH*OW][B]")
+    if csc.col_ptr.numel() != g.filter_cols + 1:
+        raise ValueError("the CSC must have C*KH*KW columns")
+    n = csc.row_idx.numel() if nnz is None else int(nnz)
+    if dX is None:
+        dX = torch.empty((g.in_rows, B), dtype=torch.float32, device=dY.device)
+    rx, bx, ldx = _mat(dX, "dX")
+    if (rx, bx) != (g.in_rows, B):
+        raise ValueError("dX must be [C*H*W][B]")
+    _check(lib().csr_conv_bwd_data(g._arr(), n_out, n, _p(csc.col_ptr), _p(csc.row_idx), _p(csc.vals_t),
+                                   _p(dY), ldy, B, _p(dX), ldx, _stream(stream)), "csr_conv_bwd_data")
+    return dX
+
+
+def conv_im2col(g: ConvGeom, X, Xcol=None, stream=None):
+    """The lowered operand [C*KH*KW][OH*OW*B] of maps X [C*H*W][B]."""
+    torch = _torch()
+    rows, B, ldx = _mat(X, "X")
+    if rows != g.in_rows:
+        raise ValueError("X must be [C*H*W][B]")
+    OH, OW = g.out_hw
+    if Xcol is None:
+        Xcol = torch.empty((g.filter_cols, OH * OW * B), dtype=torch.float32, device=X.device)
+    rc, cc, ldc = _mat(Xcol, "Xcol")
+    if (rc, cc) != (g.filter_cols, OH * OW * B):
+        raise ValueError("Xcol must be [C*KH*KW][OH*OW*B]")
+    _check(lib().conv_im2col(g._arr(), _p(X), ldx, B, _p(Xcol), ldc, _stream(stream)), "conv_im2col")
+    return Xcol
+
+
+def maxpool_fwd(g: ConvGeom, X, Y=None, stream=None):
+    """Max pooling (KH x KW windows, stride SH x SW, no padding) of [C*H*W][B] maps."""
+    torch = _torch()
+    rows, B, ldx = _mat(X, "X")
+    if rows != g.in_rows:
+        raise ValueError("X must be [C*H*W][B]")
+    OH, OW = g.out_hw
+    if Y is None:
+        Y = torch.empty((g.C * OH * OW, B), dtype=torch.float32, device=X.device)
+    ry, by, ldy = _mat(Y, "Y")
+    if (ry, by) != (g.C * OH * OW, B):
+        raise ValueError("Y must be [C*OH*OW][B]")
+    _check(lib().l1csr_maxpool_fwd(g._arr(), _p(X), ldx, B, _p(Y), ldy, _stream(stream)), "l1csr_maxpool_fwd")
+    return Y
 
 
 def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:

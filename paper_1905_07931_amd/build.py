@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libl1csr.so")
 
 SOURCES = ["abi.hip", "spmm.hip", "csc.hip", "scan.hip", "gemm.hip", "wgrad_bf16.hip", "sddmm.hip",
-           "prox.hip", "prox_adaptive.hip", "recompress.hip", "glue.hip"]
+           "prox.hip", "prox_adaptive.hip", "recompress.hip", "conv.hip", "glue.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -71,6 +71,17 @@ bool make_adaptive(int solver, float eta, float lambda, float eps, float beta1, 
     return true;
 }
 
+// the geometry array of the conv calls: C, H, W, KH, KW, SH, SW, PH, PW (host)
+bool read_geom(const int32_t *geom, conv_geom *g, int *OH, int *OW) {
+    if (geom == nullptr) return false;
+    g->C = geom[0]; g->H = geom[1]; g->W = geom[2]; g->KH = geom[3]; g->KW = geom[4];
+    g->SH = geom[5]; g->SW = geom[6]; g->PH = geom[7]; g->PW = geom[8];
+    if (!conv_out_dims(*g, OH, OW)) return false;
+    // every flattened map and filter index fits int32
+    const int64_t in = (int64_t)g->C * g->H * g->W, kk = (int64_t)g->C * g->KH * g->KW;
+    return in <= INT32_MAX && kk <= INT32_MAX && (int64_t)*OH * *OW <= INT32_MAX;
+}
+
 }  // namespace
 
 extern "C" {
@@ -426,6 +437,57 @@ int csr_validate(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row
     if (row_ptr == nullptr || d_status == nullptr || (nnz > 0 && col_idx == nullptr))
         return L1CSR_EINVAL;
     return hip_status(launch_csr_validate(n_rows, n_cols, nnz, row_ptr, col_idx, d_status, stream));
+}
+
+int csr_conv_fwd(const int32_t *geom, int32_t n_out, int64_t nnz, const int32_t *row_ptr,
+                 const int32_t *col_idx, const float *vals, const float *X, int64_t ldx, int32_t B,
+                 float *Y, int64_t ldy, hipStream_t stream) {
+    conv_geom g;
+    int OH, OW;
+    if (!read_geom(geom, &g, &OH, &OW) || B < 0) return L1CSR_EINVAL;
+    const int64_t K = (int64_t)g.C * g.KH * g.KW;
+    if (bad_csr(n_out, (int32_t)K, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if ((int64_t)n_out * OH * OW > INT32_MAX) return L1CSR_EUNSUPPORTED;
+    if (bad_dense(X, (int64_t)g.C * g.H * g.W, B, ldx) || bad_dense(Y, (int64_t)n_out * OH * OW, B, ldy))
+        return L1CSR_EINVAL;
+    return hip_status(launch_conv_fwd(g, n_out, B, row_ptr, col_idx, vals, X, ldx, Y, ldy, stream));
+}
+
+int csr_conv_bwd_data(const int32_t *geom, int32_t n_out, int64_t nnz, const int32_t *col_ptr,
+                      const int32_t *row_idx, const float *vals_t, const float *dY, int64_t ldy, int32_t B,
+                      float *dX, int64_t ldx, hipStream_t stream) {
+    conv_geom g;
+    int OH, OW;
+    if (!read_geom(geom, &g, &OH, &OW) || B < 0 || n_out < 0 || nnz < 0) return L1CSR_EINVAL;
+    const int64_t K = (int64_t)g.C * g.KH * g.KW;
+    if (nnz > (int64_t)n_out * K || nnz > INT32_MAX || col_ptr == nullptr) return L1CSR_EINVAL;
+    if (nnz > 0 && (row_idx == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
+    if ((int64_t)n_out * OH * OW > INT32_MAX) return L1CSR_EUNSUPPORTED;
+    if (bad_dense(dY, (int64_t)n_out * OH * OW, B, ldy) || bad_dense(dX, (int64_t)g.C * g.H * g.W, B, ldx))
+        return L1CSR_EINVAL;
+    return hip_status(launch_conv_bwd_data(g, n_out, B, col_ptr, row_idx, vals_t, dY, ldy, dX, ldx, stream));
+}
+
+int conv_im2col(const int32_t *geom, const float *X, int64_t ldx, int32_t B, float *Xcol, int64_t ldc,
+                hipStream_t stream) {
+    conv_geom g;
+    int OH, OW;
+    if (!read_geom(geom, &g, &OH, &OW) || B < 0) return L1CSR_EINVAL;
+    const int64_t cols = (int64_t)OH * OW * B;
+    if (bad_dense(X, (int64_t)g.C * g.H * g.W, B, ldx) || bad_dense(Xcol, (int64_t)g.C * g.KH * g.KW, cols, ldc))
+        return L1CSR_EINVAL;
+    return hip_status(launch_im2col(g, B, X, ldx, Xcol, ldc, stream));
+}
+
+int l1csr_maxpool_fwd(const int32_t *geom, const float *X, int64_t ldx, int32_t B, float *Y, int64_t ldy,
+                      hipStream_t stream) {
+    conv_geom g;
+    int OH, OW;
+    if (!read_geom(geom, &g, &OH, &OW) || B < 0) return L1CSR_EINVAL;
+    if (g.PH != 0 || g.PW != 0) return L1CSR_EUNSUPPORTED;
+    if (bad_dense(X, (int64_t)g.C * g.H * g.W, B, ldx) || bad_dense(Y, (int64_t)g.C * OH * OW, B, ldy))
+        return L1CSR_EINVAL;
+    return hip_status(launch_maxpool_fwd(g, B, X, ldx, Y, ldy, stream));
 }
 
 int l1csr_relu_fwd(int64_t n, const float *x, float *y, hipStream_t stream) {

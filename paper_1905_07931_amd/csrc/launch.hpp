@@ -139,6 +139,25 @@ hipError_t launch_csr_validate(int n_rows, int n_cols, int64_t nnz, const int *p
 hipError_t launch_compact_fill(int n_rows, const int *ptr, const int *idx, const float *vals,
                                const int *ptr_out, int *idx_out, float *vals_out, hipStream_t s);
 
+// conv.hip -----------------------------------------------------------------
+// convolution geometry: input channels C, map H x W, filter KH x KW, stride
+// SH x SW, zero padding PH x PW
+struct conv_geom {
+    int C, H, W, KH, KW, SH, SW, PH, PW;
+};
+// output map size (floor); false if the geometry is invalid
+bool conv_out_dims(const conv_geom &g, int *OH, int *OW);
+hipError_t launch_conv_fwd(const conv_geom &g, int N, int B, const int *ptr, const int *idx,
+                           const float *vals, const float *X, int64_t ldx, float *Y, int64_t ldy,
+                           hipStream_t s);
+hipError_t launch_conv_bwd_data(const conv_geom &g, int N, int B, const int *col_ptr, const int *row_idx,
+                                const float *vals_t, const float *dY, int64_t ldy, float *dX, int64_t ldx,
+                                hipStream_t s);
+hipError_t launch_im2col(const conv_geom &g, int B, const float *X, int64_t ldx, float *Xc, int64_t ldc,
+                         hipStream_t s);
+hipError_t launch_maxpool_fwd(const conv_geom &g, int B, const float *X, int64_t ldx, float *Y, int64_t ldy,
+                              hipStream_t s);
+
 // glue.hip -----------------------------------------------------------------
 hipError_t launch_relu_fwd(int64_t n, const float *x, float *y, hipStream_t s);
 hipError_t launch_relu_bwd(int64_t n, const float *x, const float *dy, float *dx, hipStream_t s);

@@ -217,3 +217,106 @@ def fc4096_batch(t, seed=0, K=4096, N=4096, B=512):
     X = rng.random((K, B)).astype(np.float32)
     dY = (rng.standard_normal((N, B)) / B).astype(np.float32)
     return X, dY
+
+
+# ---------------------------------------------------------------------------
+# Convolution layers (the conv rows of the paper's networks)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class ConvLayer:
+    """A CSR filter bank (n_out x C*KH*KW, column (ci*KH + kh)*KW + kw) with a
+    batch of input maps X [C*H*W][B] and output-map gradients dY [n_out*OH*OW][B]."""
+    n_out: int
+    C: int
+    H: int
+    W: int
+    KH: int
+    KW: int
+    SH: int
+    SW: int
+    PH: int
+    PW: int
+    B: int
+    row_ptr: np.ndarray
+    col_idx: np.ndarray
+    vals: np.ndarray
+    X: np.ndarray
+    dY: np.ndarray
+    eta: float = 0.01
+    lam: float = 1e-4
+    name: str = ""
+
+    @property
+    def OH(self) -> int:
+        return (self.H + 2 * self.PH - self.KH) // self.SH + 1
+
+    @property
+    def OW(self) -> int:
+        return (self.W + 2 * self.PW - self.KW) // self.SW + 1
+
+    @property
+    def K(self) -> int:
+        return self.C * self.KH * self.KW
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1])
+
+    @property
+    def geom(self):
+        """(C, H, W, KH, KW, SH, SW, PH, PW)"""
+        return (self.C, self.H, self.W, self.KH, self.KW, self.SH, self.SW, self.PH, self.PW)
+
+
+def conv_layer(n_out, C, H, W, KH, KW, B, nnz, seed=0, SH=1, SW=1, PH=0, PW=0, w_std=0.05,
+               dyadic=False, name="") -> ConvLayer:
+    """Uniform random filter pattern with exactly nnz entries; values
+    N(0, w_std), maps U[0,1), dY N(0,1) -- or, with dyadic=True, values
+    +-k/16, maps j/16 and dY +-k/16 (every fp32 partial sum exact)."""
+    rp_rng, v_rng, x_rng, dy_rng = streams(seed)
+    K = C * KH * KW
+    row_ptr, col_idx = uniform_pattern(rp_rng, n_out, K, nnz)
+    OH = (H + 2 * PH - KH) // SH + 1
+    OW = (W + 2 * PW - KW) // SW + 1
+    n = col_idx.shape[0]
+    if dyadic:
+        sign = np.where(v_rng.random(n) < 0.5, -1.0, 1.0)
+        vals = (sign * v_rng.integers(1, 17, size=n) / 16.0).astype(np.float32)
+        X = (x_rng.integers(0, 17, size=(C * H * W, B)) / 16.0).astype(np.float32)
+        dY = (dy_rng.integers(-16, 17, size=(n_out * OH * OW, B)) / 16.0).astype(np.float32)
+    else:
+        vals = (v_rng.standard_normal(n) * w_std).astype(np.float32)
+        X = x_rng.random((C * H * W, B)).astype(np.float32)
+        dY = dy_rng.standard_normal((n_out * OH * OW, B)).astype(np.float32)
+    return ConvLayer(n_out, C, H, W, KH, KW, SH, SW, PH, PW, B, row_ptr, col_idx, vals, X, dY,
+                     name=name or f"conv{n_out}x{C}x{KH}x{KW}_{H}x{W}_b{B}")
+
+
+def lenet5_conv2(seed=0, B=256, density=0.10) -> ConvLayer:
+    """LeNet-5 conv2: 20 -> 50 channels, 5x5 filters on 12x12 maps, batch 256
+    (the lowered shape is the 50 x 500 by 500 x (256*64) product)."""
+    return conv_layer(50, 20, 12, 12, 5, 5, B, nnz_for(50, 500, density), seed=seed, w_std=0.05,
+                      name=f"lenet5_conv2_b{B}_d{int(round(density * 100))}")
+
+
+# LeNet-5 layer shapes and the nonzeros kept after compression and retraining
+# (Table A1, SpC(Retrain) column): conv1 142/500, conv2 1750/25000,
+# fc1 10045/400000, fc2 280/5000.
+LENET5_NNZ = {"conv1": 142, "conv2": 1750, "fc1": 10045, "fc2": 280}
+
+
+def lenet5_compressed(seed=0, B=256):
+    """Synthetic compressed LeNet-5 for inference: uniform random patterns with
+    the Table A1 nonzero counts, He-initialised values N(0, sqrt(2/fan_in)),
+    inputs X [784][B] ~ U[0,1) (28 x 28 single-channel maps).  Returns a dict
+    name -> (n_out, fan_in, row_ptr, col_idx, vals) and X."""
+    rp_rng, v_rng, x_rng, _ = streams(seed)
+    shapes = {"conv1": (20, 25), "conv2": (50, 500), "fc1": (500, 800), "fc2": (10, 500)}
+    layers = {}
+    for name, (n_out, fan_in) in shapes.items():
+        row_ptr, col_idx = uniform_pattern(rp_rng, n_out, fan_in, LENET5_NNZ[name])
+        vals = (v_rng.standard_normal(col_idx.shape[0]) * np.sqrt(2.0 / fan_in)).astype(np.float32)
+        layers[name] = (n_out, fan_in, row_ptr, col_idx, vals)
+    X = x_rng.random((784, B)).astype(np.float32)
+    return layers, X
