@@ -47,7 +47,7 @@ def parse():
                     help="minimum host time spent timing the oracle")
     ap.add_argument("--workload", default="fc9216x4096",
                     choices=["fc9216x4096", "fc784x300", "mlp784", "conv2", "fc4096_sweep",
-                             "fc9216x4096_adaptive", "all"],
+                             "fc9216x4096_adaptive", "lenet5_inference", "conv2_direct", "all"],
                     help="fc9216x4096 (default): the metric's workload, one JSON line; the others "
                          "print one informational JSON line each (no CPU baseline)")
     return ap.parse_args()
@@ -97,7 +97,8 @@ def main():
 
     if args.workload != "fc9216x4096":
         import bench_workloads
-        names = (["fc784x300", "mlp784", "conv2", "fc4096_sweep", "fc9216x4096_adaptive"]
+        names = (["fc784x300", "mlp784", "conv2", "conv2_direct", "fc4096_sweep", "fc9216x4096_adaptive",
+                  "lenet5_inference"]
                  if args.workload == "all"
                  else [args.workload])
         for n in names:

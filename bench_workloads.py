@@ -12,6 +12,12 @@ informational JSON line; bench.py's default line is the metric.
     fc9216x4096_adaptive
                   the 9216 -> 4096 l1 step with Prox-ADAM (Algorithm 2) and with
                   Prox-RMSProp (Algorithm 1) in place of the plain proximal step
+    lenet5_inference
+                  forward-only compressed LeNet-5 (Table A1 nonzero counts),
+                  batch sweep, beside the same network with every weight stored
+    conv2_direct  LeNet-5 conv2 from real 20 x 12 x 12 maps, batch 256: direct
+                  sparse conv forward and input gradient, im2col + filter
+                  gradient (dense and pattern-sampled), prox + recompression
 """
 from __future__ import annotations
 
@@ -350,6 +356,126 @@ def fc9216x4096_adaptive(args, dev):
         del st
 
 
+LENET_G1 = (1, 28, 28, 5, 5, 1, 1, 0, 0)
+LENET_P1 = (20, 24, 24, 2, 2, 2, 2, 0, 0)
+LENET_G2 = (20, 12, 12, 5, 5, 1, 1, 0, 0)
+LENET_P2 = (50, 8, 8, 2, 2, 2, 2, 0, 0)
+
+
+def _dense_lenet(layers):
+    """The same network with every weight stored (the uncompressed model)."""
+    out = {}
+    rng = np.random.default_rng(123)
+    for k, (n_out, fan_in, _, _, _) in layers.items():
+        rp = (np.arange(n_out + 1) * fan_in).astype(np.int32)
+        ci = np.tile(np.arange(fan_in, dtype=np.int32), n_out)
+        v = (rng.standard_normal(n_out * fan_in) * np.sqrt(2.0 / fan_in)).astype(np.float32)
+        v[v == 0] = 1e-3
+        out[k] = (n_out, fan_in, rp, ci, v)
+    return out
+
+
+def lenet5_inference(args, dev):
+    """Forward-only LeNet-5: conv1 20@5x5 -> max pool 2 -> conv2 50@5x5 -> max
+    pool 2 -> fc1 500 -> ReLU -> fc2 10, weights with the Table A1 SpC(Retrain)
+    nonzero counts (12,217 of 430,500), inputs 28 x 28 maps, batch-contiguous.
+    One line per batch size: images/s eager and replayed from a HIP graph, the
+    per-layer times, and the same network with all weights stored."""
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    g1, p1, g2, p2 = (L1.ConvGeom(*x) for x in (LENET_G1, LENET_P1, LENET_G2, LENET_P2))
+    names = ["conv1", "pool1", "conv2", "pool2", "fc1", "relu", "fc2"]
+    for B in (1, 64, 256, 1024, 10000):
+        layers, Xh = synth.lenet5_compressed(seed=0, B=B)
+        X = torch.from_numpy(Xh).to(dev)
+        res = {}
+        for tag, ls in (("compressed", layers), ("all_weights", _dense_lenet(layers))):
+            W = {k: L1.CSR.from_host(v[2], v[3], v[4], v[1], device=dev) for k, v in ls.items()}
+            y1 = torch.empty((20 * 576, B), dtype=torch.float32, device=dev)
+            q1 = torch.empty((20 * 144, B), dtype=torch.float32, device=dev)
+            y2 = torch.empty((50 * 64, B), dtype=torch.float32, device=dev)
+            q2 = torch.empty((800, B), dtype=torch.float32, device=dev)
+            h1 = torch.empty((500, B), dtype=torch.float32, device=dev)
+            r1 = torch.empty_like(h1)
+            z = torch.empty((10, B), dtype=torch.float32, device=dev)
+
+            def step(ev=None):
+                mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+                mark(0); L1.csr_conv_fwd(g1, W["conv1"], X, y1)
+                mark(1); L1.maxpool_fwd(p1, y1, q1)
+                mark(2); L1.csr_conv_fwd(g2, W["conv2"], q1, y2)
+                mark(3); L1.maxpool_fwd(p2, y2, q2)
+                mark(4); L1.csr_spmm_fwd(W["fc1"], q2, h1)
+                mark(5); L1.relu_fwd(h1, r1)
+                mark(6); L1.csr_spmm_fwd(W["fc2"], r1, z)
+                mark(7)
+            ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+            ms_graph = _graph_timed(torch, step, max(args.steps, 20))
+            nnz = {k: int(v[2][-1]) for k, v in ls.items()}
+            macs = nnz["conv1"] * 576 + nnz["conv2"] * 64 + nnz["fc1"] + nnz["fc2"]
+            res[tag] = dict(ms=ms, ms_graph=ms_graph, per=per, nnz=sum(nnz.values()), macs=macs)
+            del W, y1, q1, y2, q2, h1, r1, z
+        c, d = res["compressed"], res["all_weights"]
+        best = min(c["ms"], c["ms_graph"])
+        yield _line(f"lenet5_inference_b{B}", 2.0 * c["macs"] * B, best,
+                    dict(model="LeNet-5 (Table A1 SpC(Retrain) nonzeros)", B=B, nnz=c["nnz"],
+                         weights=430500), c["per"],
+                    images_per_s=round(B / (best * 1e-3), 1),
+                    ms_per_batch_eager=round(c["ms"], 4), ms_per_batch_graph=round(c["ms_graph"], 4),
+                    all_weights_ms=round(min(d["ms"], d["ms_graph"]), 4),
+                    all_weights_kernels_ms=d["per"],
+                    speedup_vs_all_weights=round(min(d["ms"], d["ms_graph"]) / best, 2),
+                    note="value = 2 * (nonzero MACs per image) * B / time")
+
+
+def conv2_direct(args, dev):
+    """LeNet-5 conv2 (20 -> 50 channels, 5x5, 12x12 maps, batch 256, 10%
+    density) from the maps: the l1-phase step with the direct sparse products."""
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    L = synth.lenet5_conv2(seed=0)
+    g = L1.ConvGeom(*L.geom)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = torch.from_numpy(L.X).to(dev), torch.from_numpy(L.dY).to(dev)
+    F = L.OH * L.OW * L.B
+    Y = torch.empty((L.n_out * L.OH * L.OW, L.B), dtype=torch.float32, device=dev)
+    dX = torch.empty_like(X)
+    Xc = torch.empty((L.K, F), dtype=torch.float32, device=dev)
+    dW = torch.empty((L.n_out, L.K), dtype=torch.float32, device=dev)
+    gv = torch.empty(max(L.nnz, 1), dtype=torch.float32, device=dev)
+    dYm = dY.view(L.n_out, F)
+    csc = L1.CSC.empty(L.K, L.nnz, dev)
+    Wout = _csr_out(L1, torch, L.n_out, L.K, dev)
+    names = ["csr_conv_fwd", "csc_build", "csr_conv_bwd_data", "conv_im2col", "dense_wgrad",
+             "prox_l1_recompress", "sddmm_masked_wgrad"]
+
+    def step(ev=None):
+        mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
+        mark(0); L1.csr_conv_fwd(g, W, X, Y)
+        mark(1); L1.csc_build(W, csc)
+        mark(2); L1.csr_conv_bwd_data(g, L.n_out, csc, dY, dX, nnz=L.nnz)
+        mark(3); L1.conv_im2col(g, X, Xc)
+        mark(4); L1.dense_wgrad(dYm, Xc, dW)
+        mark(5); L1.prox_l1_recompress(W, dW, L.eta, L.lam, out=Wout)
+        mark(6); L1.sddmm_masked_wgrad(W, dYm, Xc, gv)
+        mark(7)
+    ms, per = _timed(torch, step, max(args.steps, 20), max(args.warmup, 5), names)
+    ms_graph = _graph_timed(torch, step, max(args.steps, 20))
+    # the l1 step proper (fwd, CSC, input gradient, im2col, dense filter
+    # gradient, prox); the sampled gradient of the debiasing phase is timed beside it
+    l1_ms = sum(v for k, v in per.items() if k != "sddmm_masked_wgrad")
+    flops = 2.0 * L.nnz * F * 2 + 2.0 * L.n_out * L.K * F
+    im2col_bytes = 4.0 * L.K * F + 4.0 * L.C * L.H * L.W * L.B
+    yield _line("lenet5_conv2_direct_b256_d10_l1_step", flops, l1_ms,
+                dict(n_out=L.n_out, C=L.C, H=L.H, W=L.W, KH=L.KH, KW=L.KW, B=L.B, nnz=L.nnz, density=0.10),
+                per, ms_all_calls_eager=round(ms, 4), ms_all_calls_graph=round(ms_graph, 4),
+                im2col_hbm_gbs=round(im2col_bytes / (per["conv_im2col"] * 1e-3) / 1e9, 1),
+                note="value over the l1-step calls; the sampled filter gradient is the debiasing phase's")
+
+
 def run(name, args, dev):
     return {"fc784x300": fc784x300, "mlp784": mlp784, "conv2": conv2, "fc4096_sweep": fc4096_sweep,
-            "fc9216x4096_adaptive": fc9216x4096_adaptive}[name](args, dev)
+            "fc9216x4096_adaptive": fc9216x4096_adaptive, "lenet5_inference": lenet5_inference,
+            "conv2_direct": conv2_direct}[name](args, dev)
