@@ -84,7 +84,8 @@ enum l1csr_op {
     L1CSR_OP_SPMM = 4,
     L1CSR_OP_COMPACT = 5,
     L1CSR_OP_SOFTMAX_XENT = 6,
-    L1CSR_OP_PROX_RECOMPRESS = 7
+    L1CSR_OP_PROX_RECOMPRESS = 7,
+    L1CSR_OP_DENSE_WGRAD = 8
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -166,10 +167,16 @@ int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz,
  *   (2^-7 + 2^-16) sum_b |dY X| plus the fp32 summation error:
  *   outside the fp32 accuracy contract, reported separately.
  * Any other precision value returns L1CSR_EINVAL.
+ * ws (nullable) with l1csr_workspace_bytes(L1CSR_OP_DENSE_WGRAD, N, K, 0, B)
+ * bytes lets an fp32 product with few 128 x 128 output tiles and a long batch
+ * (conv filter banks over batch x positions) split its reduction into ranges
+ * whose partial sums are added in a fixed order afterwards; the size is 0
+ * when no split is planned.  Results are reproducible either way.
  */
 int dense_wgrad(int32_t N, int32_t K, int32_t B,
                 const float *dY, int64_t ldy, const float *X, int64_t ldx,
-                float *dW, int64_t ldw, int precision, hipStream_t stream);
+                float *dW, int64_t ldw, int precision, void *ws, size_t ws_bytes,
+                hipStream_t stream);
 
 /*
  * Weight gradient of the debiasing phase (Section 2.4: retrain without the
@@ -338,7 +345,8 @@ int csr_validate(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row
  *     channels, map height and width, filter height and width, stride, zero
  *     padding.  Output maps OH = (H + 2 PH - KH)/SH + 1, OW likewise (floor).
  *     An invalid geometry (a size < 1, negative padding, a filter larger than
- *     the padded map) returns L1CSR_EINVAL.
+ *     the padded map, more than 1024 filter positions KH*KW) returns
+ *     L1CSR_EINVAL.
  *   - Maps are batch-contiguous matrices like every other activation here:
  *     X[(c*H + h)*W + w][b] with leading dimension ldx >= B; outputs
  *     Y[(co*OH + oh)*OW + ow][b].

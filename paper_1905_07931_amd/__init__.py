@@ -30,6 +30,7 @@ F32, BF16 = 0, 1
 SOLVER_RMSPROP, SOLVER_ADAM = 1, 2
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
 OP_PROX_RECOMPRESS = 7
+OP_DENSE_WGRAD = 8
 
 
 class L1CSRError(RuntimeError):
@@ -59,7 +60,7 @@ def lib():
         L.csc_update_vals.argtypes = [i32, i64, vp, vp, vp, vp, vp]
         L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
                                      vp, sz, vp]
-        L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, C.c_int, vp]
+        L.dense_wgrad.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, C.c_int, vp, sz, vp]
         L.sddmm_masked_wgrad.argtypes = [i32, i32, i64, vp, vp, vp, i64, vp, i64, i32, vp, vp, sz, vp]
         L.prox_l1_step.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, i64,
                                    vp, vp]
@@ -320,7 +321,8 @@ def dense_wgrad(dY, X, dW=None, precision=F32, stream=None):
     Nw, Kw, ldw = _mat(dW, "dW")
     if (Nw, Kw) != (N, K):
         raise ValueError("dW must be [N][K]")
-    _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, int(precision),
+    ws, wsb = _workspace(workspace_bytes(OP_DENSE_WGRAD, N, K, 0, B), dY.device)
+    _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, int(precision), _p(ws), wsb,
                              _stream(stream)), "dense_wgrad")
     return dW
 

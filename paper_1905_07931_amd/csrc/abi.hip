@@ -107,6 +107,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
         case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_PROX_RECOMPRESS: return round_up(prox_recompress_workspace_bytes(n_rows, n_cols));
+        case L1CSR_OP_DENSE_WGRAD: return round_up(wgrad_workspace_bytes(n_rows, n_cols, B));
         case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
         default: return 0;
     }
@@ -170,15 +171,17 @@ int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *r
 }
 
 int dense_wgrad(int32_t N, int32_t K, int32_t B, const float *dY, int64_t ldy, const float *X,
-                int64_t ldx, float *dW, int64_t ldw, int precision, hipStream_t stream) {
+                int64_t ldx, float *dW, int64_t ldw, int precision, void *ws, size_t ws_bytes,
+                hipStream_t stream) {
     if (N < 0 || K < 0 || B < 0) return L1CSR_EINVAL;
     if (precision != L1CSR_F32 && precision != L1CSR_BF16) return L1CSR_EINVAL;
     if (bad_dense(dY, N, B, ldy) || bad_dense(X, K, B, ldx) || bad_dense(dW, N, K, ldw))
         return L1CSR_EINVAL;
+    if (ws != nullptr && ws_bytes < wgrad_workspace_bytes(N, K, B)) return L1CSR_EINVAL;
     if (ceil_div(N, 128) > kMaxGridY) return L1CSR_EUNSUPPORTED;
     if (precision == L1CSR_BF16)
         return hip_status(launch_wgrad_bf16(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
-    return hip_status(launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
+    return hip_status(launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, dW, ldw, ws, stream));
 }
 
 int sddmm_masked_wgrad(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,

@@ -24,6 +24,8 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kStage = 2048;  // filter entries staged in LDS per pass
+constexpr int kBatch = 8;     // entries whose loads are in flight together
+constexpr int kMaxKK = 1024;  // filter positions KH*KW per channel (backward)
 
 struct geom_t {
     int C, H, W, KH, KW, SH, SW, PH, PW, OH, OW;
@@ -84,20 +86,11 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_kernel(geom_t g, int B, con
     __shared__ int off_s[kStage];
     __shared__ int khw_s[kStage];
     __shared__ float w_s[kStage];
-    const int co = blockIdx.x / slices;
-    const int slice = blockIdx.x - co * slices;
+    const int co = blockIdx.x;
     const int64_t F = (int64_t)g.OH * g.OW * B;
-    const int64_t f = ((int64_t)slice * kThreads + threadIdx.x) * VEC;
-    const bool active = f < F;
-    const int pos = active ? (int)(f / B) : 0;
-    const int b = active ? (int)(f - (int64_t)pos * B) : 0;
-    const int oh = pos / g.OW, ow = pos - oh * g.OW;
-    const int ih0 = oh * g.SH - g.PH, iw0 = ow * g.SW - g.PW;
     const int s = ptr[co], e = ptr[co + 1];
-    typename V::T acc = V::zero();
-    for (int p0 = s; p0 < e; p0 += kStage) {
-        const int n = min(kStage, e - p0);
-        __syncthreads();  // the previous pass's entries are consumed
+    auto stage = [&](int p0, int n) {
+        __syncthreads();  // the previous entries are consumed
         for (int i = threadIdx.x; i < n; i += kThreads) {
             const int col = idx[p0 + i];
             const int ci = col / (g.KH * g.KW);
@@ -108,18 +101,43 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_kernel(geom_t g, int B, con
             w_s[i] = vals[p0 + i];
         }
         __syncthreads();
-        if (active) {
-            const int64_t base = (int64_t)(ih0 * g.W + iw0);
-            for (int i = 0; i < n; ++i) {
-                const int kh = khw_s[i] >> 16, kw = khw_s[i] & 0xffff;
-                const int ih = ih0 + kh, iw = iw0 + kw;
-                if (ih < 0 || ih >= g.H || iw < 0 || iw >= g.W) continue;
-                const typename V::T x = V::load(X + (base + off_s[i]) * ldx + b);
-                V::fma(acc, w_s[i], x);
+    };
+    const bool one_pass = e - s <= kStage;
+    if (one_pass) stage(s, e - s);  // once for every slice of this block
+    // the block walks slices blockIdx.y, blockIdx.y + gridDim.y, ... of channel co
+    for (int slice = blockIdx.y; slice < slices; slice += gridDim.y) {
+        const int64_t f = ((int64_t)slice * kThreads + threadIdx.x) * VEC;
+        const bool active = f < F;
+        const int pos = active ? (int)(f / B) : 0;
+        const int b = active ? (int)(f - (int64_t)pos * B) : 0;
+        const int oh = pos / g.OW, ow = pos - oh * g.OW;
+        const int ih0 = oh * g.SH - g.PH, iw0 = ow * g.SW - g.PW;
+        const int64_t base = (int64_t)(ih0 * g.W + iw0);
+        typename V::T acc = V::zero();
+        for (int p0 = s; p0 < e; p0 += kStage) {
+            const int n = min(kStage, e - p0);
+            if (!one_pass) stage(p0, n);
+            if (!active) continue;
+            // kBatch entries' loads in flight at a time; an entry whose input
+            // position is outside the map loads row 0 instead and is skipped
+            for (int i0 = 0; i0 < n; i0 += kBatch) {
+                typename V::T x[kBatch];
+                bool ok[kBatch];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int i = i0 + u < n ? i0 + u : n - 1;
+                    const int kh = khw_s[i] >> 16, kw = khw_s[i] & 0xffff;
+                    const int ih = ih0 + kh, iw = iw0 + kw;
+                    ok[u] = i0 + u < n && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W;
+                    x[u] = V::load(X + (ok[u] ? (base + off_s[i]) * ldx : 0) + b);
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u)
+                    if (ok[u]) V::fma(acc, w_s[i0 + u], x[u]);
             }
         }
+        if (active) V::store(Y + ((int64_t)co * g.OH * g.OW + pos) * ldy + b, acc);
     }
-    if (active) V::store(Y + ((int64_t)co * g.OH * g.OW + pos) * ldy + b, acc);
 }
 
 // Backward for the input maps.  Block (ci, slice) over the flattened
@@ -135,27 +153,23 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_kernel(geom_t g, int B, con
     __shared__ int co_s[kStage];
     __shared__ int khw_s[kStage];
     __shared__ float w_s[kStage];
-    const int ci = blockIdx.x / slices;
-    const int slice = blockIdx.x - ci * slices;
+    __shared__ int cp_s[kMaxKK + 1];
+    const int ci = blockIdx.x;
     const int64_t F = (int64_t)g.H * g.W * B;
-    const int64_t f = ((int64_t)slice * kThreads + threadIdx.x) * VEC;
-    const bool active = f < F;
-    const int pos = active ? (int)(f / B) : 0;
-    const int b = active ? (int)(f - (int64_t)pos * B) : 0;
-    const int ih = pos / g.W, iw = pos - ih * g.W;
     const int kk = g.KH * g.KW;
-    const int s = col_ptr[ci * kk], e = col_ptr[(ci + 1) * kk];
-    typename V::T acc = V::zero();
-    for (int q0 = s; q0 < e; q0 += kStage) {
-        const int n = min(kStage, e - q0);
+    // the column pointers of this channel's KH*KW filter columns (kk <= kMaxKK)
+    for (int c = threadIdx.x; c <= kk; c += kThreads) cp_s[c] = col_ptr[ci * kk + c];
+    __syncthreads();
+    const int s = cp_s[0], e = cp_s[kk];
+    auto stage = [&](int q0, int n) {
         __syncthreads();
         for (int i = threadIdx.x; i < n; i += kThreads) {
-            // the filter column of CSC entry q0 + i: last c with col_ptr[ci*kk + c] <= q0 + i
+            // the filter column of CSC entry q0 + i: last c with cp_s[c] <= q0 + i
             const int q = q0 + i;
             int lo = 0, hi = kk - 1;
             while (lo < hi) {
                 const int mid = (lo + hi + 1) >> 1;
-                if (col_ptr[ci * kk + mid] <= q) lo = mid; else hi = mid - 1;
+                if (cp_s[mid] <= q) lo = mid; else hi = mid - 1;
             }
             const int kh = lo / g.KW, kw = lo - kh * g.KW;
             co_s[i] = row_idx[q];
@@ -163,19 +177,41 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_kernel(geom_t g, int B, con
             w_s[i] = vals_t[q];
         }
         __syncthreads();
-        if (active) {
-            for (int i = 0; i < n; ++i) {
-                const int kh = khw_s[i] >> 16, kw = khw_s[i] & 0xffff;
-                const int th = ih + g.PH - kh, tw = iw + g.PW - kw;  // oh*SH, ow*SW
-                if (th < 0 || tw < 0) continue;
-                const int oh = th / g.SH, ow = tw / g.SW;
-                if (oh * g.SH != th || ow * g.SW != tw || oh >= g.OH || ow >= g.OW) continue;
-                const typename V::T y = V::load(dY + ((int64_t)(co_s[i] * g.OH + oh) * g.OW + ow) * ldy + b);
-                V::fma(acc, w_s[i], y);
+    };
+    const bool one_pass = e - s <= kStage;
+    if (one_pass) stage(s, e - s);
+    for (int slice = blockIdx.y; slice < slices; slice += gridDim.y) {
+        const int64_t f = ((int64_t)slice * kThreads + threadIdx.x) * VEC;
+        const bool active = f < F;
+        const int pos = active ? (int)(f / B) : 0;
+        const int b = active ? (int)(f - (int64_t)pos * B) : 0;
+        const int ih = pos / g.W, iw = pos - ih * g.W;
+        typename V::T acc = V::zero();
+        for (int q0 = s; q0 < e; q0 += kStage) {
+            const int n = min(kStage, e - q0);
+            if (!one_pass) stage(q0, n);
+            if (!active) continue;
+            for (int i0 = 0; i0 < n; i0 += kBatch) {
+                typename V::T y[kBatch];
+                bool ok[kBatch];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int i = i0 + u < n ? i0 + u : n - 1;
+                    const int kh = khw_s[i] >> 16, kw = khw_s[i] & 0xffff;
+                    const int th = ih + g.PH - kh, tw = iw + g.PW - kw;  // oh*SH, ow*SW
+                    const int oh = th >= 0 ? th / g.SH : -1, ow = tw >= 0 ? tw / g.SW : -1;
+                    ok[u] = i0 + u < n && oh >= 0 && ow >= 0 && oh * g.SH == th && ow * g.SW == tw &&
+                            oh < g.OH && ow < g.OW;
+                    const int64_t row = ok[u] ? (int64_t)(co_s[i] * g.OH + oh) * g.OW + ow : 0;
+                    y[u] = V::load(dY + row * ldy + b);
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u)
+                    if (ok[u]) V::fma(acc, w_s[i0 + u], y[u]);
             }
         }
+        if (active) V::store(dX + ((int64_t)ci * g.H * g.W + pos) * ldx + b, acc);
     }
-    if (active) V::store(dX + ((int64_t)ci * g.H * g.W + pos) * ldx + b, acc);
 }
 
 // im2col: row r = (ci, kh, kw) of the lowered operand, flattened columns
@@ -227,12 +263,22 @@ bool vec4_ok(int B, int64_t lda, const void *a, int64_t ldb, const void *b) {
 
 int64_t slices_of(int64_t F, int vec) { return ceil_div(F, (int64_t)kThreads * vec); }
 
+constexpr int64_t kMaxGridX = 0x7fffffff;
+// blocks per channel: one per slice (many short blocks keep the most gathers in
+// flight; fewer blocks walking several slices each measured slower), at most
+// 65535, the rest walked by the blocks' slice loop
+int64_t slice_blocks(int64_t slices, int64_t channels) {
+    (void)channels;
+    return slices < 65535 ? (slices < 1 ? 1 : slices) : 65535;
+}
+
 }  // namespace
 
 bool conv_out_dims(const conv_geom &g, int *OH, int *OW) {
     if (g.C < 1 || g.H < 1 || g.W < 1 || g.KH < 1 || g.KW < 1 || g.SH < 1 || g.SW < 1 || g.PH < 0 || g.PW < 0)
         return false;
     if (g.KH > 0xffff || g.KW > 0xffff) return false;
+    if ((int64_t)g.KH * g.KW > kMaxKK) return false;
     if (g.H + 2 * g.PH < g.KH || g.W + 2 * g.PW < g.KW) return false;
     const geom_t t = to_geom(g);
     *OH = t.OH;
@@ -248,8 +294,8 @@ hipError_t launch_conv_fwd(const conv_geom &cg, int N, int B, const int *ptr, co
     if (N == 0 || F == 0) return hipSuccess;
     const bool v4 = vec4_ok(B, ldx, X, ldy, Y);
     const int64_t sl = slices_of(F, v4 ? 4 : 1);
-    if (sl * N > INT32_MAX) return hipErrorInvalidConfiguration;
-    const unsigned grid = (unsigned)(sl * N);
+    if (sl > INT32_MAX || N > kMaxGridX) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)N, (unsigned)slice_blocks(sl, N));
     if (v4)
         conv_fwd_kernel<4><<<grid, kThreads, 0, s>>>(g, B, ptr, idx, vals, X, ldx, Y, ldy, (int)sl);
     else
@@ -266,8 +312,8 @@ hipError_t launch_conv_bwd_data(const conv_geom &cg, int N, int B, const int *co
     (void)N;
     const bool v4 = vec4_ok(B, ldy, dY, ldx, dX);
     const int64_t sl = slices_of(F, v4 ? 4 : 1);
-    if (sl * g.C > INT32_MAX) return hipErrorInvalidConfiguration;
-    const unsigned grid = (unsigned)(sl * g.C);
+    if (sl > INT32_MAX || g.C > kMaxGridX) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)g.C, (unsigned)slice_blocks(sl, g.C));
     if (v4)
         conv_bwd_kernel<4><<<grid, kThreads, 0, s>>>(g, B, col_ptr, row_idx, vals_t, dY, ldy, dX, ldx, (int)sl);
     else

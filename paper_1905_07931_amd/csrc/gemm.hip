@@ -169,6 +169,48 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_mfma_kernel(
         }
 }
 
+// Split reduction for outputs too small to fill the chip (conv filter banks:
+// a few 128 x 128 tiles, batch x positions in the tens of thousands): split s
+// reduces batch indices [s*chunk, (s+1)*chunk) of every tile into its own
+// partial P[s][M][Nn]; wgrad_reduce_kernel then adds the partials in split
+// order, so the result is deterministic.
+template <bool V4>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_split_kernel(
+    int M, int Nn, int Kr, int chunk, const float *__restrict__ A, int64_t lda,
+    const float *__restrict__ Bt, int64_t ldb, float *__restrict__ P) {
+    __shared__ __attribute__((aligned(16))) tile_smem sm;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    const int k0 = blockIdx.z * chunk;
+    const int kr = min(chunk, Kr - k0);
+    floatx16 acc[2][2];
+    mfma_tile<V4>(M, Nn, kr, A + k0, lda, Bt + k0, ldb, m0, n0, sm, acc);
+    float *Ps = P + (int64_t)blockIdx.z * M * Nn;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int col = n0 + acc_col(b);
+            if (col >= Nn) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + acc_row(a, r);
+                if (row < M) Ps[(int64_t)row * Nn + col] = acc[a][b][r];
+            }
+        }
+}
+
+__global__ void wgrad_reduce_kernel(int M, int Nn, int S, const float *__restrict__ P,
+                                    float *__restrict__ C, int64_t ldc) {
+    const int64_t n = (int64_t)M * Nn;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        float acc = P[i];
+        for (int s = 1; s < S; ++s) acc += P[(int64_t)s * n + i];
+        const int64_t row = i / Nn;
+        C[row * ldc + (i - row * Nn)] = acc;
+    }
+}
+
 // Masked variant: the tile is staged through LDS and only the entries of the
 // CSR pattern are written, gv[p] = C[row(p)][col(p)].  seg[row][t] = first
 // entry of the row with column >= t * 128 (t = 0 .. ceil(Nn / 128)).
@@ -202,11 +244,45 @@ __global__ __launch_bounds__(kThreads, 2) void sddmm_mfma_kernel(
 
 }  // namespace
 
+wgrad_split wgrad_plan(int N, int K, int B) {
+    wgrad_split p{1, B};
+    const int64_t tiles = ceil_div(N, BM) * ceil_div(K, BN);
+    if (N == 0 || K == 0 || B == 0 || tiles >= 256) return p;
+    int64_t s = ceil_div(512, tiles);                  // about 512 workgroups
+    s = s < B / 256 ? s : B / 256;                      // at least 256 batch entries each
+    s = s < 64 ? s : 64;
+    if (s < 2) return p;
+    const int64_t chunk = ceil_div(ceil_div(B, s), BK) * BK;  // whole K-steps, 16-byte aligned
+    p.splits = (int)ceil_div(B, chunk);
+    p.chunk = (int)chunk;
+    return p;
+}
+
+size_t wgrad_workspace_bytes(int N, int K, int B) {
+    const wgrad_split p = wgrad_plan(N, K, B);
+    return p.splits > 1 ? sizeof(float) * (size_t)p.splits * N * K : 0;
+}
+
 hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
-                            int64_t ldx, float *dW, int64_t ldw, hipStream_t s) {
+                            int64_t ldx, float *dW, int64_t ldw, void *ws, hipStream_t s) {
     if (N == 0 || K == 0) return hipSuccess;
-    dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
     const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
+    const wgrad_split p = wgrad_plan(N, K, B);
+    if (ws != nullptr && p.splits > 1) {
+        float *P = static_cast<float *>(ws);
+        dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM), (unsigned)p.splits);
+        if (v4)
+            wgrad_split_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, p.chunk, dY, ldy, X, ldx, P);
+        else
+            wgrad_split_kernel<false><<<grid, kThreads, 0, s>>>(N, K, B, p.chunk, dY, ldy, X, ldx, P);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t n = (int64_t)N * K;
+        const unsigned rgrid = (unsigned)(ceil_div(n, 256) < 4096 ? ceil_div(n, 256) : 4096);
+        wgrad_reduce_kernel<<<rgrid, 256, 0, s>>>(N, K, p.splits, P, dW, ldw);
+        return hipGetLastError();
+    }
+    dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
     if (v4)
         wgrad_f32_mfma_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
     else

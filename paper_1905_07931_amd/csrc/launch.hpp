@@ -45,8 +45,16 @@ hipError_t launch_fill_rows_f32(float *p, int64_t rows, int64_t cols, int64_t ld
                                 hipStream_t s);
 
 // gemm.hip -----------------------------------------------------------------
+// dense dW with the batch reduction split over `splits` ranges of `chunk`
+// (partials in ws, added in split order) when the output has few tiles
+struct wgrad_split {
+    int splits, chunk;
+};
+wgrad_split wgrad_plan(int N, int K, int B);
+size_t wgrad_workspace_bytes(int N, int K, int B);
+// ws (nullable) holds wgrad_workspace_bytes(); without it no split is made
 hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
-                            int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
+                            int64_t ldx, float *dW, int64_t ldw, void *ws, hipStream_t s);
 // the same with operands rounded to bf16 (wgrad_bf16.hip)
 hipError_t launch_wgrad_bf16(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                              int64_t ldx, float *dW, int64_t ldw, hipStream_t s);

@@ -68,7 +68,7 @@ def test_workspace_sizes(lib):
     ws = lib.l1csr_workspace_bytes
     assert ws(99, 10, 10, 10, 10) == 0                 # unknown op
     assert ws(1, -1, 10, 10, 10) == 0                  # negative size
-    for op in range(1, 8):
+    for op in range(1, 9):
         for dims in [(1, 1, 1, 1), (300, 784, 23520, 64), (4096, 9216, 3397386, 1024)]:
             b = ws(op, *dims)
             assert b % 256 == 0, (op, dims, b)
@@ -94,7 +94,8 @@ def _setup(lib):
                                  C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
                                  C.c_size_t, C.c_void_p]
     lib.dense_wgrad.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
-                                C.c_int64, C.c_void_p, C.c_int64, C.c_int, C.c_void_p]
+                                C.c_int64, C.c_void_p, C.c_int64, C.c_int, C.c_void_p, C.c_size_t,
+                                C.c_void_p]
     lib.csr_validate.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
                                  C.c_void_p]
     lib.prox_l1_step.argtypes = [C.c_int, C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
@@ -131,11 +132,15 @@ def test_invalid_arguments_are_rejected_before_launch(lib):
     assert lib.l1csr_workspace_bytes(4, 4096, 300, 200000, 1024) > 1
     assert lib.csr_spmm_fwd(4096, 300, 200000, P, P, P, P, 1024, 1024, P, 1024, P, 1, S) == EINVAL
     # dense dW: short ld, missing output, unknown precision
-    assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, 0, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, 0, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, 1, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, 2, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, -1, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, 0, NUL, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, 0, NUL, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, 1, NUL, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, 2, NUL, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, -1, NUL, 0, S) == EINVAL
+    # a workspace shorter than the split reduction of a skinny product needs
+    need = lib.l1csr_workspace_bytes(8, 50, 500, 0, 16384)
+    assert need >= 4 * 50 * 500 * 2
+    assert lib.dense_wgrad(50, 500, 16384, P, 16384, P, 16384, P, 500, 0, P, need - 4096, S) == EINVAL
     # CSR check: negative sizes, missing status or columns
     assert lib.csr_validate(-1, 4, 0, P, P, P, S) == EINVAL
     assert lib.csr_validate(4, 4, 3, P, P, NUL, S) == EINVAL

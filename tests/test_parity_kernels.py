@@ -216,6 +216,28 @@ def test_dense_wgrad_batch_one_bit_exact_and_padded():
     assert np.all(h(dWp)[:, 66:] == 3.0)
 
 
+@pytest.mark.parametrize("NKB", [(50, 500, 16384), (7, 130, 9001), (20, 25, 147456), (129, 257, 2080),
+                                 (300, 784, 256 * 8)])
+def test_dense_wgrad_split_reduction(NKB):
+    # few output tiles and a long batch: the reduction is split into ranges
+    # (ragged last range when B is not a multiple of the range length) and the
+    # partials are added in a fixed order
+    N, K, B = NKB
+    assert L1.workspace_bytes(L1.OP_DENSE_WGRAD, N, K, 0, B) > 0
+    rng = np.random.default_rng(N + K + B)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    X = rng.random((K, B)).astype(np.float32)
+    dW1 = h(L1.dense_wgrad(t(dY), t(X)))
+    assert_scaled_close(dW1, oracle.dense_wgrad(dY, X), oracle.dense_wgrad(np.abs(dY), X), what="dW split")
+    assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), dW1)  # reproducible
+
+
+def test_dense_wgrad_split_reduction_dyadic_bit_exact():
+    L = synth.dyadic_layer(50, 500, 16384, 10, seed=6)
+    assert L1.workspace_bytes(L1.OP_DENSE_WGRAD, 50, 500, 0, 16384) > 0
+    assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
+
+
 def test_dense_wgrad_dyadic_bit_exact():
     L = synth.dyadic_layer(200, 300, 256, 10, seed=5)
     assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
