@@ -232,6 +232,26 @@ def test_dense_wgrad_split_reduction(NKB):
     assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), dW1)  # reproducible
 
 
+@pytest.mark.parametrize("NKB", [(257, 10999, 370), (130, 38400, 300), (200, 32768, 96)])
+def test_dense_wgrad_many_tiles(NKB):
+    # at least 256 output tiles (no split of the reduction): 258 ragged tiles
+    # with scalar loads (B % 4 != 0), 600 tiles, 512 tiles (whole rounds of
+    # two workgroups per CU)
+    N, K, B = NKB
+    assert L1.workspace_bytes(L1.OP_DENSE_WGRAD, N, K, 0, B) == 0
+    rng = np.random.default_rng(N + K + B)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    X = rng.random((K, B)).astype(np.float32)
+    dW1 = h(L1.dense_wgrad(t(dY), t(X)))
+    assert_scaled_close(dW1, oracle.dense_wgrad(dY, X), oracle.dense_wgrad(np.abs(dY), X), what="dW")
+    assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), dW1)  # reproducible
+
+
+def test_dense_wgrad_many_tiles_dyadic_bit_exact():
+    L = synth.dyadic_layer(257, 10999, 370, 10, seed=7)
+    assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
+
+
 def test_dense_wgrad_split_reduction_dyadic_bit_exact():
     L = synth.dyadic_layer(50, 500, 16384, 10, seed=6)
     assert L1.workspace_bytes(L1.OP_DENSE_WGRAD, 50, 500, 0, 16384) > 0
