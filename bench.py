@@ -125,7 +125,7 @@ def main():
 
     names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_recompress"]
 
-    def step(ev=None, wg=None):
+    def step(ev=None, wg=None, prec=L1.F32):
         def mark(i):
             if ev is not None:
                 ev[i].record()
@@ -138,7 +138,7 @@ def main():
         mark(3)
         if wg is not None:
             wg[0].record()
-        L1.dense_wgrad(dY, X, dW)
+        L1.dense_wgrad(dY, X, dW, precision=prec)
         if wg is not None:
             wg[1].record()
         mark(4)
@@ -172,6 +172,7 @@ def main():
     torch.cuda.synchronize()
     per = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
            for i, n in enumerate(names)}
+    nnz_out = int(Wout.row_ptr[-1].item())  # of the fp32 step (the lines below reuse Wout)
 
     # dense dW with bf16 operands: reported beside the step, not part of it
     dWb = torch.empty_like(dW)
@@ -186,7 +187,22 @@ def main():
     bf16_ms = float(np.mean([evb[s].elapsed_time(evb[s + 1]) for s in range(args.steps)]))
     del dWb
 
-    nnz_out = int(Wout.row_ptr[-1].item())
+    # the same step with the weight gradient split into bf16 hi + lo on the
+    # bf16 matrix cores (BF16X3: inside the 1e-4 contract)
+    for _ in range(2):
+        step(prec=L1.BF16X3)
+    x3_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(args.steps)]
+    start3, end3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start3.record()
+    for s in range(args.steps):
+        step(wg=x3_ev[s], prec=L1.BF16X3)
+    end3.record()
+    torch.cuda.synchronize()
+    ms_x3 = start3.elapsed_time(end3) / args.steps
+    wg_x3_ms = float(np.mean([a.elapsed_time(b) for a, b in x3_ev]))
+
     flops_step = 2.0 * nnz * B * 2 + 2.0 * N * K * B          # fwd + bwd + dense dW
     flops_nnz_only = 6.0 * nnz * B
     gflops = flops_step / (ms_per_step * 1e-3) / 1e9
@@ -239,6 +255,15 @@ def main():
                              "frac": round(wg_flops / (bf16_ms * 1e-3) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 4),
                              "note": "operands rounded to bf16, exact products, fp32 sums; outside the "
                                      "1e-4 fp32 contract and not part of the step"},
+        "step_bf16x3": {"ms_per_step": round(ms_x3, 4),
+                        "value": round(flops_step / (ms_x3 * 1e-3) / 1e9, 1),
+                        "dense_wgrad_ms": round(wg_x3_ms, 4),
+                        "dense_wgrad_tflops": round(wg_flops / (wg_x3_ms * 1e-3) / 1e12, 1),
+                        "bf16_mfma_frac": round(3 * wg_flops / (wg_x3_ms * 1e-3) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 4),
+                        "note": "the same step with dense_wgrad precision BF16X3: operands split into bf16 "
+                                "hi + lo, hi.hi + hi.lo + lo.hi exact on the bf16 matrix cores, fp32 sums; "
+                                "within the 1e-4 contract (per-product error < 4.7e-5); tflops counts the "
+                                "2NKB fp32-equivalent flops, bf16_mfma_frac the 3x executed ones"},
         "input_gen_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)

@@ -61,7 +61,8 @@ enum l1csr_status {
 /* dense_wgrad operand precision */
 enum l1csr_precision {
     L1CSR_F32 = 0,           /* fp32 operands, fp32 matrix cores: the 1e-4 contract */
-    L1CSR_BF16 = 1           /* operands rounded to bf16 (nearest even), exact products, fp32 sums */
+    L1CSR_BF16 = 1,          /* operands rounded to bf16 (nearest even), exact products, fp32 sums */
+    L1CSR_BF16X3 = 2         /* operands split into bf16 hi + lo, three exact products, fp32 sums */
 };
 
 /* prox_l1_step modes */
@@ -166,6 +167,14 @@ int csr_spmm_bwd_t(int32_t n_rows, int32_t n_cols, int64_t nnz,
  *   fp32: each operand rounds by at most 2^-8 relative, so |dW - exact| <=
  *   (2^-7 + 2^-16) sum_b |dY X| plus the fp32 summation error:
  *   outside the fp32 accuracy contract, reported separately.
+ * precision L1CSR_BF16X3: every dY and X element x is split into
+ *   hi = bf16(x) and lo = bf16(x - hi) (nearest even; x - hi is exact), and
+ *   each product is taken as hi_a hi_b + hi_a lo_b + lo_a hi_b on the bf16
+ *   matrix cores, all exact, summed in fp32.  Per product the error is at most
+ *   3 (1 + 2^-7) 2^-16 |ab| < 4.7e-5 |ab| (the dropped lo_a lo_b and the
+ *   parts' rounding), so |dW - exact| <= 4.7e-5 sum_b |dY X| plus the fp32
+ *   summation error: inside the 1e-4 contract, at about twice the speed of
+ *   L1CSR_F32.
  * Any other precision value returns L1CSR_EINVAL.
  * ws (nullable) with l1csr_workspace_bytes(L1CSR_OP_DENSE_WGRAD, N, K, 0, B)
  * bytes lets an fp32 product with few 128 x 128 output tiles and a long batch

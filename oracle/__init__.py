@@ -50,6 +50,7 @@ def lib():
         L.orc_spmm_bwd_t.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
         L.orc_dense_wgrad.argtypes = [i32, i32, i32, _f32p, i64, _f32p, i64, _f32p, i64]
         L.orc_dense_wgrad_bf16.argtypes = [i32, i32, i32, _f32p, i64, _f32p, i64, _f32p, i64]
+        L.orc_dense_wgrad_bf16x3.argtypes = [i32, i32, i32, _f32p, i64, _f32p, i64, _f32p, i64]
         L.orc_bf16_round.argtypes = [f32]
         L.orc_bf16_round.restype = f32
         L.orc_sddmm.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, i64, _f32p, i64, _f32p]
@@ -156,6 +157,18 @@ def dense_wgrad_bf16(dY, X):
     K = X.shape[0]
     dW = np.empty((N, K), np.float32)
     _check(lib().orc_dense_wgrad_bf16(N, K, B, dY, B, X, B, dW, K), "dense_wgrad_bf16")
+    return dW
+
+
+def dense_wgrad_bf16x3(dY, X):
+    """dW with each operand split into bf16 hi = bf16(x), lo = bf16(x - hi) and
+    each product taken as hi hi + hi lo + lo hi, exact products summed in double."""
+    dY = _c(dY, np.float32)
+    X = _c(X, np.float32)
+    N, B = dY.shape
+    K = X.shape[0]
+    dW = np.empty((N, K), np.float32)
+    _check(lib().orc_dense_wgrad_bf16x3(N, K, B, dY, B, X, B, dW, K), "dense_wgrad_bf16x3")
     return dW
 
 

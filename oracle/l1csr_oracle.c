@@ -175,6 +175,54 @@ int orc_dense_wgrad_bf16(int32_t N, int32_t K, int32_t B,
     return rc;
 }
 
+/* Dense weight gradient with each operand split into two bf16 parts:
+ * hi = bf16(x), lo = bf16(x - hi) (x - hi is exact in float), and each product
+ * taken as hi_a hi_b + hi_a lo_b + lo_a hi_b (the lo_a lo_b term is dropped);
+ * every product is exact, the three are added in that order and summed over
+ * b ascending in double. */
+int orc_dense_wgrad_bf16x3(int32_t N, int32_t K, int32_t B,
+                           const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                           float *dW, int64_t ldw) {
+    if (N < 0 || K < 0 || B < 0 || ldx < B || ldy < B || ldw < K) return ORC_EINVAL;
+    const size_t ny = (size_t)N * B + 1, nx = (size_t)K * B + 1;
+    float *hy = (float *)malloc(sizeof(float) * ny), *ly = (float *)malloc(sizeof(float) * ny);
+    float *hx = (float *)malloc(sizeof(float) * nx), *lx = (float *)malloc(sizeof(float) * nx);
+    if (!hy || !ly || !hx || !lx) {
+        free(hy);
+        free(ly);
+        free(hx);
+        free(lx);
+        return ORC_EINVAL;
+    }
+    for (int32_t i = 0; i < N; ++i)
+        for (int32_t b = 0; b < B; ++b) {
+            const float v = dY[(int64_t)i * ldy + b];
+            hy[(int64_t)i * B + b] = orc_bf16_round(v);
+            ly[(int64_t)i * B + b] = orc_bf16_round(v - hy[(int64_t)i * B + b]);
+        }
+    for (int32_t k = 0; k < K; ++k)
+        for (int32_t b = 0; b < B; ++b) {
+            const float v = X[(int64_t)k * ldx + b];
+            hx[(int64_t)k * B + b] = orc_bf16_round(v);
+            lx[(int64_t)k * B + b] = orc_bf16_round(v - hx[(int64_t)k * B + b]);
+        }
+    for (int32_t i = 0; i < N; ++i)
+        for (int32_t k = 0; k < K; ++k) {
+            double acc = 0.0;
+            for (int32_t b = 0; b < B; ++b) {
+                const double ha = hy[(int64_t)i * B + b], la = ly[(int64_t)i * B + b];
+                const double hb = hx[(int64_t)k * B + b], lb = lx[(int64_t)k * B + b];
+                acc += ha * hb + ha * lb + la * hb;
+            }
+            dW[(int64_t)i * ldw + k] = (float)acc;
+        }
+    free(hy);
+    free(ly);
+    free(hx);
+    free(lx);
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------------------
  * Weight gradient of the debiasing phase (Section 2.4: retraining without the
  * regulariser, zero-valued weights excluded from training).  The gradient is

@@ -17,7 +17,7 @@ __all__ = [
     "CSR", "CSC", "L1CSRError", "lib", "status_str", "workspace_bytes",
     "csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad",
     "prox_l1_step", "csr_recompress", "prox_l1_recompress", "csr_compact", "csr_validate", "relu_fwd", "relu_bwd",
-    "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16",
+    "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16", "BF16X3",
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
     "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
 ]
@@ -26,7 +26,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so
 
 OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 PROX_DENSE, PROX_CSR = 0, 1
-F32, BF16 = 0, 1
+F32, BF16, BF16X3 = 0, 1, 2
 SOLVER_RMSPROP, SOLVER_ADAM = 1, 2
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
 OP_PROX_RECOMPRESS = 7
@@ -309,8 +309,10 @@ def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
 
 
 def dense_wgrad(dY, X, dW=None, precision=F32, stream=None):
-    """dW = dY . X^T on the matrix cores: fp32 operands (F32), or operands
-    rounded to bf16 with exact products and fp32 sums (BF16)."""
+    """dW = dY . X^T on the matrix cores: fp32 operands (F32); operands
+    rounded to bf16 with exact products and fp32 sums (BF16); or operands split
+    into bf16 hi + lo with three exact products per pair and fp32 sums (BF16X3,
+    inside the fp32 contract)."""
     torch = _torch()
     N, B, ldy = _mat(dY, "dY")
     K, Bx, ldx = _mat(X, "X")

@@ -174,13 +174,16 @@ int dense_wgrad(int32_t N, int32_t K, int32_t B, const float *dY, int64_t ldy, c
                 int64_t ldx, float *dW, int64_t ldw, int precision, void *ws, size_t ws_bytes,
                 hipStream_t stream) {
     if (N < 0 || K < 0 || B < 0) return L1CSR_EINVAL;
-    if (precision != L1CSR_F32 && precision != L1CSR_BF16) return L1CSR_EINVAL;
+    if (precision != L1CSR_F32 && precision != L1CSR_BF16 && precision != L1CSR_BF16X3)
+        return L1CSR_EINVAL;
     if (bad_dense(dY, N, B, ldy) || bad_dense(X, K, B, ldx) || bad_dense(dW, N, K, ldw))
         return L1CSR_EINVAL;
     if (ws != nullptr && ws_bytes < wgrad_workspace_bytes(N, K, B)) return L1CSR_EINVAL;
     if (ceil_div(N, 128) > kMaxGridY) return L1CSR_EUNSUPPORTED;
     if (precision == L1CSR_BF16)
         return hip_status(launch_wgrad_bf16(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
+    if (precision == L1CSR_BF16X3)
+        return hip_status(launch_wgrad_bf16x3(N, K, B, dY, ldy, X, ldx, dW, ldw, stream));
     return hip_status(launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, dW, ldw, ws, stream));
 }
 

@@ -135,7 +135,7 @@ def test_invalid_arguments_are_rejected_before_launch(lib):
     assert lib.dense_wgrad(4, 4, 8, P, 7, P, 8, P, 4, 0, NUL, 0, S) == EINVAL
     assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 3, 0, NUL, 0, S) == EINVAL
     assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, NUL, 4, 1, NUL, 0, S) == EINVAL
-    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, 2, NUL, 0, S) == EINVAL
+    assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, 3, NUL, 0, S) == EINVAL
     assert lib.dense_wgrad(4, 4, 8, P, 8, P, 8, P, 4, -1, NUL, 0, S) == EINVAL
     # a workspace shorter than the split reduction of a skinny product needs
     need = lib.l1csr_workspace_bytes(8, 50, 500, 0, 16384)

@@ -253,6 +253,61 @@ def test_dense_wgrad_bf16_pins():
     assert np.max(d / m) > 2.0 ** -14  # and the rounding does show
 
 
+def _bf16_bits(x):
+    """bf16 rounding by integer arithmetic on the float32 bit pattern (add half
+    an ulp of the 16 dropped bits, plus the kept lsb for ties to even, then
+    truncate): independent of the oracle's frexp-based definition."""
+    u = np.asarray(x, np.float32).reshape(-1).view(np.uint32).astype(np.uint64)
+    r = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return r.astype(np.uint32).view(np.float32)
+
+
+def test_bf16_rounding_matches_bit_arithmetic():
+    rng = np.random.default_rng(21)
+    x = (rng.standard_normal(4000) * np.exp2(rng.integers(-60, 60, 4000))).astype(np.float32)
+    # exact ties: the 16 dropped bits are 0x8000, kept lsb even and odd
+    t = rng.integers(0x3F000000, 0x4F000000, 400, dtype=np.uint64) & 0xFFFF0000
+    ties = np.concatenate([(t | 0x8000), (t | 0x18000)]).astype(np.uint32).view(np.float32)
+    x = np.concatenate([x, ties, -ties])
+    assert np.array_equal(oracle.bf16_round(x), _bf16_bits(x))
+
+
+def test_dense_wgrad_bf16x3_pins():
+    rng = np.random.default_rng(12)
+    # the split: hi + lo is within 2^-16 |x| of x, both parts on the bf16 grid
+    x = rng.standard_normal(3000).astype(np.float32)
+    hi = _bf16_bits(x)
+    lo = _bf16_bits(x - hi)
+    assert np.all(np.abs(x.astype(np.float64) - hi - lo) <= 2.0 ** -16 * np.abs(x))
+    assert np.array_equal(_bf16_bits(lo), lo)
+    # B = 1: hi hi + hi lo + lo hi of the independently split operands, exact in
+    # double, rounded once
+    dy = rng.standard_normal((29, 1)).astype(np.float32)
+    xx = rng.standard_normal((31, 1)).astype(np.float32)
+    ha, hb = _bf16_bits(dy).astype(np.float64), _bf16_bits(xx).astype(np.float64)
+    la = _bf16_bits(dy.reshape(-1) - ha.astype(np.float32)).astype(np.float64)
+    lb = _bf16_bits(xx.reshape(-1) - hb.astype(np.float32)).astype(np.float64)
+    want = (np.outer(ha, hb) + np.outer(ha, lb) + np.outer(la, hb)).astype(np.float32)
+    assert np.array_equal(oracle.dense_wgrad_bf16x3(dy, xx), want)
+    # the lo lo term is dropped: x = 1 + 2^-8 + 2^-9 splits into hi = 1 + 2^-7,
+    # lo = -2^-9, so x x comes out 2^-18 short (visible in float32 at 1)
+    v = np.array([[1.0 + 2.0 ** -8 + 2.0 ** -9]], np.float32)
+    got = float(oracle.dense_wgrad_bf16x3(v, v)[0, 0])
+    assert got == float(np.float32(float(v[0, 0]) ** 2 - 2.0 ** -18)) and got != float(np.float32(float(v[0, 0]) ** 2))
+    # operands on the bf16 grid: lo = 0, the fp32 definition itself
+    dY = oracle.bf16_round(rng.standard_normal(37 * 19)).reshape(37, 19)
+    X = oracle.bf16_round(rng.random(23 * 19)).reshape(23, 19)
+    assert np.array_equal(oracle.dense_wgrad_bf16x3(dY, X), oracle.dense_wgrad(dY, X))
+    # within 3 (1 + 2^-7) 2^-16 of sum |dY X| of the exact product (plus the two
+    # float32 output roundings), and the dropped terms do show
+    dY = rng.standard_normal((40, 300)).astype(np.float32)
+    X = rng.random((50, 300)).astype(np.float32)
+    m = np.abs(dY.astype(np.float64)) @ np.abs(X.T.astype(np.float64))
+    d = np.abs(oracle.dense_wgrad_bf16x3(dY, X).astype(np.float64) - oracle.dense_wgrad(dY, X))
+    assert np.all(d <= 3 * (1 + 2.0 ** -7) * 2.0 ** -16 * m + 2.0 ** -23 * m)
+    assert np.max(d / m) > 2.0 ** -22
+
+
 def test_dyadic_exact_integer_brute_force():
     L = synth.dyadic_layer(23, 41, 19, 300, seed=9, empty_rows=(2,), full_rows=(5,))
     Wi = np.rint(_dense(L) * 16).astype(np.int64)

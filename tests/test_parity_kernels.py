@@ -301,6 +301,62 @@ def test_dense_wgrad_bf16_batch_one_bit_exact_and_padded():
     assert np.all(h(dWp)[:, 66:] == 3.0)
 
 
+# bf16 hi + lo split, three products: against the oracle of the same split
+# (exact products, so only fp32 summation separates the two), and against the
+# exact fp32 definition within the 1e-4 contract itself
+@pytest.mark.parametrize("NKB", [(1, 1, 1), (7, 5, 3), (129, 130, 33), (300, 784, 64),
+                                 (257, 1000, 100), (64, 300, 256), (256, 384, 1024), (130, 2600, 300),
+                                 (5, 9, 0)])
+def test_dense_wgrad_bf16x3(NKB):
+    N, K, B = NKB
+    rng = np.random.default_rng(N * 13 + K)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    X = rng.random((K, B)).astype(np.float32)
+    dW = h(L1.dense_wgrad(t(dY), t(X), precision=L1.BF16X3))
+    m = oracle.dense_wgrad(np.abs(dY), X)
+    assert_scaled_close(dW, oracle.dense_wgrad_bf16x3(dY, X), m, what="dW bf16x3 vs its split")
+    assert_scaled_close(dW, oracle.dense_wgrad(dY, X), m, what="dW bf16x3 vs fp32")
+    assert bits_equal(h(L1.dense_wgrad(t(dY), t(X), precision=L1.BF16X3)), dW)  # reproducible
+
+
+def test_dense_wgrad_bf16x3_batch_one_dyadic_and_padded():
+    rng = np.random.default_rng(3)
+    # B = 1: three exact products added in fp32 (two roundings at most)
+    dY = rng.standard_normal((70, 1)).astype(np.float32)
+    X = rng.standard_normal((150, 1)).astype(np.float32)
+    m = np.abs(dY.astype(np.float64)) @ np.abs(X.T.astype(np.float64))
+    assert_scaled_close(h(L1.dense_wgrad(t(dY), t(X), precision=L1.BF16X3)), oracle.dense_wgrad_bf16x3(dY, X),
+                        m, tol=2.0 ** -22, what="dW bf16x3, B = 1")
+    # dyadic operands sit on the bf16 grid (lo = 0) and every sum is exact
+    L = synth.dyadic_layer(200, 300, 256, 10, seed=5)
+    assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X), precision=L1.BF16X3)), oracle.dense_wgrad(L.dY, L.X))
+    # leading dimensions not a multiple of 4 (scalar loads), ragged tiles
+    import torch
+    dY2 = rng.standard_normal((33, 45)).astype(np.float32)
+    X2 = rng.random((66, 45)).astype(np.float32)
+    dYp = torch.zeros((33, 47), device=cuda()); dYp[:, :45] = t(dY2)
+    Xp = torch.zeros((66, 51), device=cuda()); Xp[:, :45] = t(X2)
+    dWp = torch.full((33, 70), 3.0, device=cuda())
+    L1.dense_wgrad(dYp[:, :45], Xp[:, :45], dWp[:, :66], precision=L1.BF16X3)
+    assert_scaled_close(h(dWp)[:, :66], oracle.dense_wgrad(dY2, X2), oracle.dense_wgrad(np.abs(dY2), X2),
+                        what="dW bf16x3, padded")
+    assert np.all(h(dWp)[:, 66:] == 3.0)
+
+
+def test_dense_wgrad_bf16x3_full_size_sampled():
+    # the 9216 -> 4096 layer's gradient at batch 1024, in the launch the step
+    # uses; sampled rows and columns against the exact fp32 definition
+    L = synth.fc9216_4096(seed=0)
+    dW = L1.dense_wgrad(t(L.dY), t(L.X), precision=L1.BF16X3)
+    rng = np.random.default_rng(94)
+    rows = np.sort(rng.choice(L.N, 48, replace=False))
+    cols = np.sort(rng.choice(L.K, 64, replace=False))
+    got = h(dW)[np.ix_(rows, cols)]
+    ref = oracle.dense_wgrad(L.dY[rows], L.X[cols])
+    m = oracle.dense_wgrad(np.abs(L.dY[rows]), np.abs(L.X[cols]))
+    assert_scaled_close(got, ref, m, what="dW bf16x3 full size")
+
+
 # ----------------------------------------------------------------------------
 # CSR well-formedness check
 # ----------------------------------------------------------------------------
