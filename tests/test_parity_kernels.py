@@ -306,7 +306,9 @@ def test_dense_wgrad_bf16_batch_one_bit_exact_and_padded():
 # exact fp32 definition within the 1e-4 contract itself
 @pytest.mark.parametrize("NKB", [(1, 1, 1), (7, 5, 3), (129, 130, 33), (300, 784, 64),
                                  (257, 1000, 100), (64, 300, 256), (256, 384, 1024), (130, 2600, 300),
-                                 (5, 9, 0)])
+                                 (5, 9, 0),
+                                 # many tiles: the 256 x 288 shape (ragged, scalar loads; whole float4)
+                                 (1000, 12700, 70), (1024, 12800, 64)])
 def test_dense_wgrad_bf16x3(NKB):
     N, K, B = NKB
     rng = np.random.default_rng(N * 13 + K)
