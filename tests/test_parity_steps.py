@@ -152,14 +152,14 @@ def independent_band_check(W, dY, X, eta, lam, K, new_W):
 # single-layer l1 steps
 # ----------------------------------------------------------------------------
 
-def l1_step(L, W, host, rows=None, cols=None, band=True):
+def l1_step(L, W, host, rows=None, cols=None, band=True, precision=L1.F32):
     """fwd, CSC, bwd, dense dW, prox + recompress; every stage checked."""
     X, dY = L.X, L.dY
     Xg, dYg = t(X), t(dY)
     Y = L1.csr_spmm_fwd(W, Xg)
     csc = L1.csc_build(W)
     dX = L1.csr_spmm_bwd_t(W, dYg, csc)
-    dW = L1.dense_wgrad(dYg, Xg)
+    dW = L1.dense_wgrad(dYg, Xg, precision=precision)
     out = L1.prox_l1_recompress(W, dW, L.eta, L.lam)
     dWh = h(dW)
     check_fwd(host, X, h(Y), rows)
@@ -194,6 +194,26 @@ def test_fc9216x4096_zipf_l1_step_full_size():
     cols = rng.choice(L.K, 64, replace=False)
     out, new, n_band = l1_step(L, W, (L.row_ptr, L.col_idx, L.vals), rows=rows, cols=cols)
     assert n_band <= 1e-5 * L.N * L.K
+
+
+@pytest.mark.parametrize("which", ["fc784x300", "fc9216x4096"])
+def test_l1_step_with_split_bf16_gradient(which):
+    # the same steps with the weight gradient in BF16X3 (inside the contract):
+    # dW within 1e-4 of the exact product, the prox + recompression of the
+    # GPU's dW bit for bit, and every mask difference from the fully
+    # independent oracle step inside the rounding band of the threshold
+    if which == "fc784x300":
+        L = synth.fc784_300(seed=0)
+        rows = cols = None
+    else:
+        L = synth.fc9216_4096(seed=0)
+        rng = np.random.default_rng(91)
+        rows = np.sort(rng.choice(L.N, 48, replace=False))
+        cols = rng.choice(L.K, 64, replace=False)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+    out, new, n_band = l1_step(L, W, (L.row_ptr, L.col_idx, L.vals), rows=rows, cols=cols,
+                               precision=L1.BF16X3)
+    assert n_band <= 1e-4 * L.N * L.K
 
 
 def test_empty_layer_regrows_then_empties():
@@ -369,12 +389,14 @@ def test_fc4096_density_sweep_alternating_steps(pct):
         assert abs(b - a) <= 0.25 * max(a, 1)
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3])
+def test_graph_replays_match_eager(precision):
     """The l1 step of the 784 -> 300 layer followed by a debiasing step on its
     output, captured once into a HIP graph (torch.cuda.CUDAGraph) and replayed
     three times with eager work and host waits in between: every replay gives
     the eager result bit for bit (all the kernels are deterministic), after
-    the outputs were overwritten with garbage."""
+    the outputs were overwritten with garbage.  With the fp32 and the split
+    bf16 weight gradient."""
     import torch
     L = synth.fc784_300(seed=0)
     dev = cuda()
@@ -393,7 +415,7 @@ def test_graph_replays_match_eager():
         L1.csr_spmm_fwd(W, x, Y)
         L1.csc_build(W, csc)
         L1.csr_spmm_bwd_t(W, dY, csc, dX)
-        L1.dense_wgrad(dY, x, dW)
+        L1.dense_wgrad(dY, x, dW, precision=precision)
         L1.prox_l1_recompress(W, dW, L.eta, L.lam, out=W1)
         W1.nnz = nnz1  # None: the binding reads it from the device (a host wait)
         L1.sddmm_masked_wgrad(W1, dY, x, gv)
