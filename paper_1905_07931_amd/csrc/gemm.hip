@@ -13,6 +13,15 @@
 // use the same one; lane half h takes batch indices [16h, 16h + 16) of the
 // chunk, step s index 16h + s, so each lane reads its fragments as contiguous
 // float4s from LDS.
+//
+// Outputs with many tiles also have a 256x288 shape: 4x3 waves of 64x96 (2x3
+// MFMA tiles each), K-step 32, one 12-wave workgroup per CU (153 KB of LDS).
+// Per MFMA it stages fewer bytes and spends fewer barriers, and 4096 x 9216
+// is 512 tiles, two whole rounds of the 256 CUs.  The host takes the shape
+// with the shorter modelled time: the tiles per CU, ceil(tiles / 256), times
+// the tile's flops at the shape's measured rate.
+#include <cmath>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -169,6 +178,138 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_mfma_kernel(
         }
 }
 
+// The 256x288 shape (see the file comment); load and stage helpers generic in
+// the tile height, the tile loop as in mfma_tile.
+constexpr int LBM = 256, LBN = 288, LWM = 4, LWN = 3;
+constexpr int kLargeThreads = 64 * LWM * LWN;
+
+template <bool V4, int ROWS>
+__device__ __forceinline__ void load_rows(const float *__restrict__ src, int64_t ld, int rows, int kred, int row0,
+                                          int k0, float4 (&r)[(ROWS * BK / 4 + kLargeThreads - 1) / kLargeThreads]) {
+    constexpr int LPT = (ROWS * BK / 4 + kLargeThreads - 1) / kLargeThreads;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+        const int f = threadIdx.x + i * kLargeThreads;  // float4 index inside the tile
+        const int rr = f >> 3;                           // 8 float4 per tile row
+        const int kk = (f & 7) * 4;
+        const int grow = row0 + rr, gk = k0 + kk;
+        const bool rv = rr < ROWS && grow < rows;
+        if (V4 && rv && gk + 3 < kred) {
+            r[i] = *reinterpret_cast<const float4 *>(src + (int64_t)grow * ld + gk);
+        } else {
+            const float *p = src + (int64_t)grow * ld + gk;
+            r[i].x = (rv && gk + 0 < kred) ? p[0] : 0.f;
+            r[i].y = (rv && gk + 1 < kred) ? p[1] : 0.f;
+            r[i].z = (rv && gk + 2 < kred) ? p[2] : 0.f;
+            r[i].w = (rv && gk + 3 < kred) ? p[3] : 0.f;
+        }
+    }
+}
+
+template <int ROWS>
+__device__ __forceinline__ void store_rows(float *lds, const float4 (&r)[(ROWS * BK / 4 + kLargeThreads - 1) / kLargeThreads]) {
+    constexpr int LPT = (ROWS * BK / 4 + kLargeThreads - 1) / kLargeThreads;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+        const int f = threadIdx.x + i * kLargeThreads;
+        const int rr = f >> 3;
+        const int kk = (f & 7) * 4;
+        if (rr < ROWS) *reinterpret_cast<float4 *>(lds + rr * LDS_STRIDE + kk) = r[i];
+    }
+}
+
+template <bool V4>
+__global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_large_kernel(
+    int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
+    int64_t ldb, float *__restrict__ C, int64_t ldc) {
+    constexpr int TM = LBM / LWM / 32, TN = LBN / LWN / 32;
+    constexpr int LA = (LBM * BK / 4 + kLargeThreads - 1) / kLargeThreads;
+    constexpr int LB = (LBN * BK / 4 + kLargeThreads - 1) / kLargeThreads;
+    __shared__ __attribute__((aligned(16))) float As[2][LBM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) float Bs[2][LBN * LDS_STRIDE];
+    const int m0 = blockIdx.y * LBM, n0 = blockIdx.x * LBN;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wm = (wave / LWN) * (LBM / LWM), wn = (wave % LWN) * (LBN / LWN);
+    const int lr = lane & 31;
+    const int lh = lane >> 5;
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    const int nchunks = (Kr + BK - 1) / BK;
+    float4 ra[LA], rb[LB];
+    load_rows<V4, LBM>(A, lda, M, Kr, m0, 0, ra);
+    load_rows<V4, LBN>(Bt, ldb, Nn, Kr, n0, 0, rb);
+    store_rows<LBM>(As[0], ra);
+    store_rows<LBN>(Bs[0], rb);
+    __syncthreads();
+
+    const int oa = (wm + lr) * LDS_STRIDE + lh * 16, ob = (wn + lr) * LDS_STRIDE + lh * 16;
+    for (int c = 0; c < nchunks; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < nchunks) {
+            load_rows<V4, LBM>(A, lda, M, Kr, m0, (c + 1) * BK, ra);
+            load_rows<V4, LBN>(Bt, ldb, Nn, Kr, n0, (c + 1) * BK, rb);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            float av[TM][4], bv[TN][4];
+#pragma unroll
+            for (int a = 0; a < TM; ++a) {
+                const float4 x = *reinterpret_cast<const float4 *>(As[buf] + oa + a * 32 * LDS_STRIDE + 4 * q);
+                av[a][0] = x.x; av[a][1] = x.y; av[a][2] = x.z; av[a][3] = x.w;
+            }
+#pragma unroll
+            for (int b = 0; b < TN; ++b) {
+                const float4 x = *reinterpret_cast<const float4 *>(Bs[buf] + ob + b * 32 * LDS_STRIDE + 4 * q);
+                bv[b][0] = x.x; bv[b][1] = x.y; bv[b][2] = x.z; bv[b][3] = x.w;
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int a = 0; a < TM; ++a)
+#pragma unroll
+                    for (int b = 0; b < TN; ++b)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][s], bv[b][s], acc[a][b], 0, 0, 0);
+        }
+        if (c + 1 < nchunks) {
+            store_rows<LBM>(As[buf ^ 1], ra);
+            store_rows<LBN>(Bs[buf ^ 1], rb);
+        }
+        __syncthreads();
+    }
+    // D layout of the 32x32 MFMA (acc_row / acc_col for this wave grid)
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+            const int col = n0 + wn + b * 32 + lr;
+            if (col >= Nn) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                if (row < M) C[(int64_t)row * ldc + col] = acc[a][b][r];
+            }
+        }
+}
+
+// measured rates of the two shapes (whole chip, TFLOP/s) and the per-CU round
+// model the host chooses by
+constexpr int kCUs = 256;
+constexpr double kSmallRate = 121.7, kLargeRate = 131.3;
+
+double tile_model_us(int N, int K, int B, int bm, int bn, double rate) {
+    const double tiles = (double)ceil_div(N, bm) * (double)ceil_div(K, bn);
+    const double per_cu = std::ceil(tiles / kCUs);
+    return per_cu * 2.0 * bm * bn * (double)(B > 0 ? B : 1) / (rate * 1e6 / kCUs);
+}
+
 // Split reduction for outputs too small to fill the chip (conv filter banks:
 // a few 128 x 128 tiles, batch x positions in the tens of thousands): split s
 // reduces batch indices [s*chunk, (s+1)*chunk) of every tile into its own
@@ -280,6 +421,14 @@ hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, c
         const int64_t n = (int64_t)N * K;
         const unsigned rgrid = (unsigned)(ceil_div(n, 256) < 4096 ? ceil_div(n, 256) : 4096);
         wgrad_reduce_kernel<<<rgrid, 256, 0, s>>>(N, K, p.splits, P, dW, ldw);
+        return hipGetLastError();
+    }
+    if (tile_model_us(N, K, B, LBM, LBN, kLargeRate) < tile_model_us(N, K, B, BM, BN, kSmallRate)) {
+        dim3 grid((unsigned)ceil_div(K, LBN), (unsigned)ceil_div(N, LBM));
+        if (v4)
+            wgrad_f32_large_kernel<true><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
+        else
+            wgrad_f32_large_kernel<false><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
         return hipGetLastError();
     }
     dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));

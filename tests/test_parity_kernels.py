@@ -232,11 +232,13 @@ def test_dense_wgrad_split_reduction(NKB):
     assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), dW1)  # reproducible
 
 
-@pytest.mark.parametrize("NKB", [(257, 10999, 370), (130, 38400, 300), (200, 32768, 96)])
+@pytest.mark.parametrize("NKB", [(257, 10999, 370), (130, 38400, 300), (200, 32768, 96),
+                                 (2048, 9216, 64), (2000, 9000, 70)])
 def test_dense_wgrad_many_tiles(NKB):
     # at least 256 output tiles (no split of the reduction): 258 ragged tiles
     # with scalar loads (B % 4 != 0), 600 tiles, 512 tiles (whole rounds of
-    # two workgroups per CU)
+    # two workgroups per CU); the last two take the 256 x 288 shape (whole
+    # float4 loads, then ragged tiles with scalar loads)
     N, K, B = NKB
     assert L1.workspace_bytes(L1.OP_DENSE_WGRAD, N, K, 0, B) == 0
     rng = np.random.default_rng(N + K + B)
