@@ -384,6 +384,7 @@ def lenet5_inference(args, dev):
     import torch
     import paper_1905_07931_amd as L1
     from paper_1905_07931_amd import synth
+    from paper_1905_07931_amd.metrics import compression_label
     g1, p1, g2, p2 = (L1.ConvGeom(*x) for x in (LENET_G1, LENET_P1, LENET_G2, LENET_P2))
     names = ["conv1", "pool1", "conv2", "pool2", "fc1", "relu", "fc2"]
     for B in (1, 64, 256, 1024, 10000):
@@ -426,6 +427,7 @@ def lenet5_inference(args, dev):
                     all_weights_ms=round(min(d["ms"], d["ms_graph"]), 4),
                     all_weights_kernels_ms=d["per"],
                     speedup_vs_all_weights=round(min(d["ms"], d["ms_graph"]) / best, 2),
+                    compression=compression_label(c["nnz"], 430500),
                     note="value = 2 * (nonzero MACs per image) * B / time")
 
 
