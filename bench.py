@@ -173,6 +173,8 @@ def main():
     per = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
            for i, n in enumerate(names)}
     nnz_out = int(Wout.row_ptr[-1].item())  # of the fp32 step (the lines below reuse Wout)
+    step_each = [evs[s][0].elapsed_time(evs[s][len(names)]) for s in range(args.steps)]
+    step_pct = [round(float(np.percentile(step_each, q)), 4) for q in (10, 50, 90)]
 
     # dense dW with bf16 operands: reported beside the step, not part of it
     dWb = torch.empty_like(dW)
@@ -251,6 +253,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "ms_per_step_p10_p50_p90": step_pct,
         "ms_per_step_graph": round(ms_graph, 4),
         "value_graph": round(flops_step / (ms_graph * 1e-3) / 1e9, 1),
         "gflops_nnz_only": round(flops_nnz_only / (ms_per_step * 1e-3) / 1e9, 1),

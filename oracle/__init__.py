@@ -39,12 +39,24 @@ def build(force: bool = False) -> str:
 _lib = None
 
 
+def build_sanitized(out_path: str) -> str:
+    """The same source built with AddressSanitizer and UndefinedBehaviorSanitizer
+    (any report aborts), for the sanitizer run of the oracle's pins."""
+    cmd = ["gcc", "-O1", "-g", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
+           "-fopenmp", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", _SRC, "-o", out_path, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out_path
+
+
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        # ORACLE_LIB names another build of the same source (the sanitizer run)
+        path = os.environ.get("ORACLE_LIB") or LIB_PATH
+        if path == LIB_PATH and not os.path.exists(LIB_PATH):
             build()
-        L = C.CDLL(LIB_PATH)
+        L = C.CDLL(path)
         i32, i64, f32 = C.c_int32, C.c_int64, C.c_float
         L.orc_spmm_fwd.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
         L.orc_spmm_bwd_t.argtypes = [i32, i32, i32, _i32p, _i32p, _f32p, _f32p, i64, _f32p, i64]
