@@ -329,16 +329,19 @@ def fc9216x4096_adaptive(args, dev):
         st = L1.AdaptiveState.zeros(solver, (N, K), dev)
         names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", f"prox_{tag}_recompress"]
 
-        def step(ev=None):
+        def step(ev=None, prec=L1.F32):
             mark = (lambda i: ev[i].record()) if ev else (lambda i: None)
             mark(0); L1.csr_spmm_fwd(W, X, Y)
             mark(1); L1.csc_build(W, csc)
             mark(2); L1.csr_spmm_bwd_t(W, dY, csc, dX)
-            mark(3); L1.dense_wgrad(dY, X, dW)
+            mark(3); L1.dense_wgrad(dY, X, dW, precision=prec)
             mark(4); L1.prox_adaptive_recompress(W, dW, st, eta, lam, out=Wout)
             mark(5)
         ms, per = _timed(torch, step, max(args.steps, 10), max(args.warmup, 3), names)
         nnz_out = int(Wout.row_ptr[-1].item())
+        # the same step with the split-bf16 weight gradient (inside the 1e-4 contract)
+        ms_x3, _ = _timed(torch, lambda ev=None: step(ev, prec=L1.BF16X3), max(args.steps, 10),
+                          max(args.warmup, 3), names)
         state_bytes = (16.0 if solver == L1.SOLVER_ADAM else 8.0) * N * K  # read and write m, v / v
         alg = 4.0 * N * K + state_bytes + (8.0 * nnz + 4 * (N + 1)) + (8.0 * nnz_out + 4 * (N + 1))
         # the two-pass kernels also re-read m', v' (ADAM) or G, v' (RMSProp)
@@ -352,7 +355,9 @@ def fc9216x4096_adaptive(args, dev):
                     prox_hbm_algorithmic_bytes=alg, prox_hbm_gbs=round(alg / (kms * 1e-3) / 1e9, 1),
                     prox_hbm_frac=round(alg / (kms * 1e-3) / 1e9 / 8000.0, 4),
                     prox_bytes_moved_two_pass=moved,
-                    prox_moved_gbs=round(moved / (kms * 1e-3) / 1e9, 1))
+                    prox_moved_gbs=round(moved / (kms * 1e-3) / 1e9, 1),
+                    ms_per_step_bf16x3=round(ms_x3, 4),
+                    value_bf16x3=round(flops / (ms_x3 * 1e-3) / 1e9, 1))
         del st
 
 
