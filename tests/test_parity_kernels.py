@@ -249,6 +249,19 @@ def test_dense_wgrad_many_tiles(NKB):
     assert bits_equal(h(L1.dense_wgrad(t(dY), t(X))), dW1)  # reproducible
 
 
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3])
+def test_dense_wgrad_empty_batch_large_shape(precision):
+    # B = 0 on a shape that takes the 256 x 288 tiles: no reduction step at
+    # all, every entry of dW written as an exact zero (padded ld, garbage before)
+    import torch
+    dY = torch.zeros((2048, 0), device=cuda())
+    X = torch.zeros((9216, 0), device=cuda())
+    dW = torch.full((2048, 9220), 5.0, device=cuda())
+    L1.dense_wgrad(dY, X, dW[:, :9216], precision=precision)
+    out = h(dW)
+    assert not out[:, :9216].any() and np.all(out[:, 9216:] == 5.0)
+
+
 def test_dense_wgrad_many_tiles_dyadic_bit_exact():
     L = synth.dyadic_layer(257, 10999, 370, 10, seed=7)
     assert bits_equal(h(L1.dense_wgrad(t(L.dY), t(L.X))), oracle.dense_wgrad(L.dY, L.X))
