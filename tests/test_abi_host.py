@@ -121,6 +121,24 @@ def _setup(lib):
 
 
 @pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_sizes_beyond_the_int32_layout_are_unsupported(lib):
+    # row pointers are int32: an N x K output above 2^31 - 1 entries cannot be
+    # addressed; grid limits bound the batch and the row tiles
+    _setup(lib)
+    big = 65536  # 65536 * 65536 = 2^32 entries
+    assert lib.csr_recompress(big, big, P, big, 0.0, NUL, P, P, P, 16, NUL, NUL, P, 1 << 30, S) == EUNSUPPORTED
+    Q = C.c_void_p(8192)  # an output CSR distinct from the input
+    assert lib.prox_l1_recompress(big, big, 0, P, P, P, P, big, 0.1, 0.1, Q, Q, Q, 16, NUL, NUL, P, 1 << 30,
+                                  S) == EUNSUPPORTED
+    assert lib.dense_wgrad(128 * 65536 + 1, 4, 8, P, 8, P, 8, P, 4, 0, NUL, 0, S) == EUNSUPPORTED
+    assert lib.csr_spmm_fwd(4, 4, 3, P, P, P, P, 64 * 65536 + 64, 64 * 65536 + 64, P, 64 * 65536 + 64,
+                            NUL, 0, S) == EUNSUPPORTED
+    # the largest supported N x K passes the size check (it fails later only on the missing workspace)
+    n = 46340  # 46340^2 = 2,147,395,600 < 2^31
+    assert lib.csr_recompress(n, n, P, n, 0.0, NUL, P, P, P, 16, NUL, NUL, NUL, 0, S) == EINVAL
+
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
 def test_invalid_arguments_are_rejected_before_launch(lib):
     _setup(lib)
     # SpMM: negative size, missing pointer, short leading dimension, nnz > N*K, short workspace
