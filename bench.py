@@ -11,8 +11,12 @@ row lengths, batch 1024, fp32):
     dW = dY.X^T                   dense_wgrad     (fp32 matrix cores)
     W' = CSR(S_t(W - eta*dW))     prox_l1_recompress (prox + recompression in one call)
 
-Every step reads the same resident inputs and writes W' to its own buffers,
-so all timed steps do identical work.  Prints ONE JSON line.
+The timed step is L1.l1_step: the same five calls with the dependencies of a
+training loop on two streams (the CSC build beside the forward product, the
+backward product beside the prox once dense_wgrad is done).  The serial
+schedule is timed beside it and gives the per-call split.  Every step reads
+the same resident inputs and writes W' to its own buffers, so all timed steps
+do identical work.  Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
 """
@@ -125,7 +129,16 @@ def main():
 
     names = ["csr_spmm_fwd", "csc_build", "csr_spmm_bwd_t", "dense_wgrad", "prox_l1_recompress"]
 
-    def step(ev=None, wg=None, prec=L1.F32):
+    def step(wg=None, prec=L1.F32):
+        """The step as a training loop runs it: the two-stream schedule of
+        L1.l1_step (CSC build beside the forward product, backward product
+        beside the prox), all outputs ready on the current stream at the end."""
+        L1.l1_step(W, X, dY, eta, lam, Y=Y, dX=dX, dW=dW, csc=csc, out=Wout, precision=prec,
+                   events=None if wg is None else {"dense_wgrad": wg})
+
+    def serial_step(ev=None, prec=L1.F32, wg=None):
+        """The same calls one after another on one stream (events between them
+        give the per-call split)."""
         def mark(i):
             if ev is not None:
                 ev[i].record()
@@ -145,36 +158,43 @@ def main():
         L1.prox_l1_recompress(W, dW, eta, lam, out=Wout)
         mark(5)
 
+    def timed_steps(fn):
+        """K back-to-back steps; an event on the current stream between steps
+        gives each step's time, events around dense_wgrad its live duration."""
+        bound = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        wg = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        bound[0].record()
+        for s in range(args.steps):
+            fn(wg[s])
+            bound[s + 1].record()
+        torch.cuda.synchronize()
+        each = [bound[s].elapsed_time(bound[s + 1]) for s in range(args.steps)]
+        return (bound[0].elapsed_time(bound[-1]) / args.steps, each,
+                float(np.mean([a.elapsed_time(b) for a, b in wg])))
+
     for _ in range(args.warmup):
         step()
+        serial_step()
     torch.cuda.synchronize()
 
-    # whole-step timing: K back-to-back steps; inside them, events around the
-    # dominant launch (dense_wgrad, same stream) give its live duration
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    wg_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    start.record()
-    for s in range(args.steps):
-        step(wg=wg_ev[s])
-    end.record()
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
-    wg_live_ms = float(np.mean([a.elapsed_time(b) for a, b in wg_ev]))
+    # whole-step timing of the two-stream step; dense_wgrad (the dominant
+    # launch, alone on its stream while it runs) timed live inside it
+    ms_per_step, step_each, wg_live_ms = timed_steps(lambda wg: step(wg))
+    step_pct = [round(float(np.percentile(step_each, q)), 4) for q in (10, 50, 90)]
 
-    # per-kernel durations with events between the calls (same stream)
+    # the serial schedule, and per-call durations from events between its calls
+    ms_serial, _, _ = timed_steps(lambda wg: serial_step(wg=wg))
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
     for s in range(args.steps):
-        step(evs[s])
+        serial_step(evs[s])
     torch.cuda.synchronize()
     per = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
            for i, n in enumerate(names)}
     nnz_out = int(Wout.row_ptr[-1].item())  # of the fp32 step (the lines below reuse Wout)
-    step_each = [evs[s][0].elapsed_time(evs[s][len(names)]) for s in range(args.steps)]
-    step_pct = [round(float(np.percentile(step_each, q)), 4) for q in (10, 50, 90)]
 
     # dense dW with bf16 operands: reported beside the step, not part of it
     dWb = torch.empty_like(dW)
@@ -193,17 +213,7 @@ def main():
     # bf16 matrix cores (BF16X3: inside the 1e-4 contract)
     for _ in range(2):
         step(prec=L1.BF16X3)
-    x3_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(args.steps)]
-    start3, end3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start3.record()
-    for s in range(args.steps):
-        step(wg=x3_ev[s], prec=L1.BF16X3)
-    end3.record()
-    torch.cuda.synchronize()
-    ms_x3 = start3.elapsed_time(end3) / args.steps
-    wg_x3_ms = float(np.mean([a.elapsed_time(b) for a, b in x3_ev]))
+    ms_x3, _, wg_x3_ms = timed_steps(lambda wg: step(wg, prec=L1.BF16X3))
 
     # both steps captured once into a HIP graph and replayed: the same kernels
     # without the host's per-launch cost (every call is capture-safe here)
@@ -254,6 +264,9 @@ def main():
         "cpu_baseline": cpu,
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
         "ms_per_step_p10_p50_p90": step_pct,
+        "schedule": "two streams (CSC build beside the forward SpMM; backward SpMM beside the prox, "
+                    "after dense_wgrad); kernels_ms from the serial schedule",
+        "ms_per_step_serial": round(ms_serial, 4),
         "ms_per_step_graph": round(ms_graph, 4),
         "value_graph": round(flops_step / (ms_graph * 1e-3) / 1e9, 1),
         "gflops_nnz_only": round(flops_nnz_only / (ms_per_step * 1e-3) / 1e9, 1),

@@ -20,6 +20,7 @@ __all__ = [
     "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16", "BF16X3",
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
     "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
+    "l1_step", "side_stream",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
@@ -158,14 +159,20 @@ def _mat(t, name):
 _ws_cache: dict = {}
 
 
-def _workspace(nbytes, device):
+def _workspace(nbytes, device, stream=None):
+    """Scratch for one call, cached per (device, stream the call runs on): calls
+    on one stream run in order and may share it, calls on two streams never do.
+    A buffer is allocated with its stream current, so the caching allocator
+    reuses it only in that stream's order once it is replaced."""
     if nbytes == 0:
         return None, 0
     torch = _torch()
-    key = (device.index, torch.cuda.current_stream(device).cuda_stream)
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    key = (device.index, s.cuda_stream)
     buf = _ws_cache.get(key)
     if buf is None or buf.numel() < nbytes:
-        buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.stream(s):
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
         _ws_cache[key] = buf
     return buf, nbytes
 
@@ -257,7 +264,7 @@ def csr_spmm_fwd(W: CSR, X, Y=None, stream=None):
     N, By, ldy = _mat(Y, "Y")
     if N != W.n_rows or By != B:
         raise ValueError("Y must be [n_rows][B]")
-    ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_rows, W.n_cols, nnz, B), X.device)
+    ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_rows, W.n_cols, nnz, B), X.device, stream)
     _check(lib().csr_spmm_fwd(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
                               _p(X), ldx, B, _p(Y), ldy, _p(ws), wsb, _stream(stream)),
            "csr_spmm_fwd")
@@ -270,7 +277,7 @@ def csc_build(W: CSR, out: CSC | None = None, stream=None) -> CSC:
     dev = W.row_ptr.device
     if out is None:
         out = CSC.empty(W.n_cols, W.col_idx.numel(), dev)
-    ws, wsb = _workspace(workspace_bytes(OP_CSC_BUILD, W.n_rows, W.n_cols, nnz, 0), dev)
+    ws, wsb = _workspace(workspace_bytes(OP_CSC_BUILD, W.n_rows, W.n_cols, nnz, 0), dev, stream)
     _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
                            _p(out.col_ptr), _p(out.row_idx), _p(out.perm), _p(out.vals_t), _p(ws),
                            wsb, _stream(stream)), "csc_build")
@@ -301,7 +308,7 @@ def csr_spmm_bwd_t(W: CSR, dY, csc: CSC | None = None, dX=None, stream=None):
     wsb = 0
     if csc is not None:
         cp, ri, vt = csc.col_ptr, csc.row_idx, csc.vals_t
-        ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_cols, W.n_rows, nnz, B), dY.device)
+        ws, wsb = _workspace(workspace_bytes(OP_SPMM, W.n_cols, W.n_rows, nnz, B), dY.device, stream)
     _check(lib().csr_spmm_bwd_t(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
                                 _p(cp), _p(ri), _p(vt), _p(dY), ldy, B, _p(dX), ldx, _p(ws), wsb,
                                 _stream(stream)), "csr_spmm_bwd_t")
@@ -323,7 +330,7 @@ def dense_wgrad(dY, X, dW=None, precision=F32, stream=None):
     Nw, Kw, ldw = _mat(dW, "dW")
     if (Nw, Kw) != (N, K):
         raise ValueError("dW must be [N][K]")
-    ws, wsb = _workspace(workspace_bytes(OP_DENSE_WGRAD, N, K, 0, B), dY.device)
+    ws, wsb = _workspace(workspace_bytes(OP_DENSE_WGRAD, N, K, 0, B), dY.device, stream)
     _check(lib().dense_wgrad(N, K, B, _p(dY), ldy, _p(X), ldx, _p(dW), ldw, int(precision), _p(ws), wsb,
                              _stream(stream)), "dense_wgrad")
     return dW
@@ -339,7 +346,7 @@ def sddmm_masked_wgrad(W: CSR, dY, X, gv=None, stream=None):
         raise ValueError("shape mismatch")
     if gv is None:
         gv = torch.empty(max(nnz, 1), dtype=torch.float32, device=dY.device)
-    ws, wsb = _workspace(workspace_bytes(OP_SDDMM, W.n_rows, W.n_cols, nnz, B), dY.device)
+    ws, wsb = _workspace(workspace_bytes(OP_SDDMM, W.n_rows, W.n_cols, nnz, B), dY.device, stream)
     _check(lib().sddmm_masked_wgrad(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(dY),
                                     ldy, _p(X), ldx, B, _p(gv), _p(ws), wsb, _stream(stream)),
            "sddmm_masked_wgrad")
@@ -390,7 +397,7 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
                   torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
                   torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
     cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
-    ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev)
+    ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev, stream)
     need = C.c_int64(-1)
     _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
                                 _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
@@ -413,7 +420,7 @@ def prox_l1_recompress(W: CSR, G, eta, lam, capacity=None, out: CSR | None = Non
                   torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
                   torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
     cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
-    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev)
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev, stream)
     need = C.c_int64(-1)
     _check(lib().prox_l1_recompress(N, K, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(G), ldg,
                                     float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
@@ -492,7 +499,7 @@ def prox_adaptive_step(mode, W: CSR, G, st: AdaptiveState, eta, lam, Z=None, row
         raise ValueError("Z must be [n_rows][n_cols]")
     if row_counts is not None:
         _vec(row_counts, torch.int32, "row_counts")
-    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), G.device)
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), G.device, stream)
     _check(lib().prox_adaptive_step(PROX_DENSE, st.solver, N, K, nnz, _p(W.row_ptr), _p(W.col_idx),
                                     _p(W.vals), _p(G), ldg, _p(m), _p(st.v), lds, float(eta),
                                     float(lam), float(st.eps), float(st.beta1), float(st.beta2),
@@ -521,7 +528,7 @@ def prox_adaptive_recompress(W: CSR, G, st: AdaptiveState, eta, lam, capacity=No
                   torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
                   torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
     cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
-    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev)
+    ws, wsb = _workspace(workspace_bytes(OP_PROX_RECOMPRESS, N, K, nnz, 0), dev, stream)
     need = C.c_int64(-1)
     _check(lib().prox_adaptive_recompress(st.solver, N, K, nnz, _p(W.row_ptr), _p(W.col_idx),
                                           _p(W.vals), _p(G), ldg, _p(m), _p(st.v), lds, float(eta),
@@ -646,7 +653,7 @@ def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:
         out = CSR(W.n_rows, W.n_cols, torch.empty(W.n_rows + 1, dtype=torch.int32, device=dev),
                   torch.empty(cap, dtype=torch.int32, device=dev),
                   torch.empty(cap, dtype=torch.float32, device=dev), None)
-    ws, wsb = _workspace(workspace_bytes(OP_COMPACT, W.n_rows, 0, nnz, 0), dev)
+    ws, wsb = _workspace(workspace_bytes(OP_COMPACT, W.n_rows, 0, nnz, 0), dev, stream)
     _check(lib().csr_compact(W.n_rows, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(out.row_ptr),
                              _p(out.col_idx), _p(out.vals), None, _p(ws), wsb, _stream(stream)),
            "csr_compact")
@@ -707,7 +714,11 @@ def softmax_xent(logits, labels, dlogits=None, loss=None, stream=None):
         raise ValueError("dlogits must share the leading dimension of logits")
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=logits.device)
-    ws, wsb = _workspace(workspace_bytes(OP_SOFTMAX_XENT, Cn, 0, 0, B), logits.device)
+    ws, wsb = _workspace(workspace_bytes(OP_SOFTMAX_XENT, Cn, 0, 0, B), logits.device, stream)
     _check(lib().l1csr_softmax_xent(Cn, B, _p(logits), ld, _p(labels), _p(dlogits), _p(loss),
                                     _p(ws), wsb, _stream(stream)), "l1csr_softmax_xent")
     return loss, dlogits
+
+
+# the two-stream l1 step over the entry points above
+from .step import l1_step, side_stream  # noqa: E402

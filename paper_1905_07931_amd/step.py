@@ -1,0 +1,89 @@
+"""One l1-phase training step of a CSR layer on two HIP streams.
+
+The step of Sections 2.3 and 3.1-3.2 for a layer Y = W X with W stored
+compressed (CSR) and activations batch-contiguous:
+
+    Y  = W X                      forward product
+    CSC(W)                        column-major copy of W for the transposed product
+    dX = W^T dY                   backward product (gradient to the layer below)
+    G  = dY X^T                   dense weight gradient (every weight, zero or not)
+    W' = prox_{eta*lambda}(W - eta G), recompressed to CSR   (Eq. 5)
+
+Only the forward product has to finish before the rest: dY is the upstream
+gradient of Y.  The five calls keep the dependencies of a training loop and
+run on two streams of equal (default) priority:
+
+    main:  fwd ──── dense dW ──── prox + recompress ───┐
+    side:  CSC build           └──── bwd (W^T dY) ─────┴─ join
+
+The CSC build needs only W, so it fills the gaps of the forward product's
+planning launches.  The backward product is started after the weight gradient
+(a scheduling choice: it needs only dY and the CSC) and runs beside the
+proximal step, an HBM stream that leaves the CUs free for its planning
+launches.  The dense weight gradient, the longest launch,
+runs alone.  Every launch is deterministic, so the outputs equal those of the
+same calls made one after another on one stream, bit for bit.
+
+Each entry point keeps its own workspace per stream, so the two streams never
+share scratch memory.  The function is capture-safe: it forks the side stream
+from the caller's stream and joins it back before returning, so it records
+into a HIP graph (torch.cuda.CUDAGraph) like a single-stream sequence.
+"""
+from __future__ import annotations
+
+from . import CSC, CSR, F32, csc_build, csr_spmm_bwd_t, csr_spmm_fwd, dense_wgrad, prox_l1_recompress
+
+_side_streams: dict = {}
+
+
+def side_stream(device):
+    """The side stream used for `device` (created once, default priority)."""
+    import torch
+    idx = torch.device(device).index
+    if idx is None:
+        idx = torch.cuda.current_device()
+    s = _side_streams.get(idx)
+    if s is None:
+        s = torch.cuda.Stream(device=idx)
+        _side_streams[idx] = s
+    return s
+
+
+def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: CSR,
+            precision: int = F32, side=None, events: dict | None = None) -> CSR:
+    """Run one l1 step on the caller's current stream plus a side stream.
+
+    W is the N x K layer (CSR, nnz known on the host or read from the device),
+    X the K x B input, dY the N x B upstream gradient.  Results go to the
+    caller's buffers: Y (N x B), dX (K x B), dW (N x K dense gradient), csc
+    (the CSC copy of W, capacity >= nnz) and out (W' in CSR, capacity N*K).
+    precision selects the dense weight gradient's arithmetic (F32 or BF16X3).
+    side: the stream to fork onto (default: one per device).  events: optional
+    {call name: (start, end)} torch events, recorded around that call on the
+    stream it runs on.  All outputs are ready on the caller's stream when the
+    call returns (no host wait).  Returns out.
+    """
+    import torch
+    main = torch.cuda.current_stream(X.device)
+    if side is None:
+        side = side_stream(X.device)
+    if side.cuda_stream == main.cuda_stream:
+        raise ValueError("the side stream must differ from the current stream")
+
+    def call(name, stream, fn):
+        ev = events.get(name) if events else None
+        if ev is not None:
+            ev[0].record(stream)
+        fn()
+        if ev is not None:
+            ev[1].record(stream)
+
+    side.wait_stream(main)  # W, X, dY as the caller left them
+    call("csc_build", side, lambda: csc_build(W, csc, stream=side))
+    call("csr_spmm_fwd", main, lambda: csr_spmm_fwd(W, X, Y))
+    call("dense_wgrad", main, lambda: dense_wgrad(dY, X, dW, precision=precision))
+    side.wait_stream(main)  # dY follows Y; the CSC is on side already
+    call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t(W, dY, csc, dX, stream=side))
+    call("prox_l1_recompress", main, lambda: prox_l1_recompress(W, dW, eta, lam, out=out))
+    main.wait_stream(side)
+    return out

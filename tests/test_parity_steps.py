@@ -447,3 +447,119 @@ def test_graph_replays_match_eager(precision):
         for a, b in zip(outs(), ref):
             assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
                                b.view(torch.int32) if b.dtype == torch.float32 else b), r
+
+
+# ----------------------------------------------------------------------------
+# the two-stream step (L1.l1_step) and calls on several streams
+# ----------------------------------------------------------------------------
+
+def _step_buffers(L, dev):
+    import torch
+    return dict(Y=torch.empty((L.N, L.B), device=dev), dX=torch.empty((L.K, L.B), device=dev),
+                dW=torch.empty((L.N, L.K), device=dev), csc=L1.CSC.empty(L.K, L.nnz, dev),
+                out=L1.CSR(L.N, L.K, torch.empty(L.N + 1, dtype=torch.int32, device=dev),
+                           torch.empty(L.N * L.K, dtype=torch.int32, device=dev),
+                           torch.empty(L.N * L.K, dtype=torch.float32, device=dev), None))
+
+
+def _step_outputs(o, nnz_in):
+    n = int(o["out"].row_ptr[-1].item())
+    c = o["csc"]
+    return [o["Y"], o["dX"], o["dW"], c.col_ptr, c.row_idx[:nnz_in], c.perm[:nnz_in], c.vals_t[:nnz_in],
+            o["out"].row_ptr, o["out"].col_idx[:n], o["out"].vals[:n]]
+
+
+def _same_bits(a, b):
+    import torch
+    as_int = lambda x: x.view(torch.int32) if x.dtype == torch.float32 else x
+    return a.shape == b.shape and torch.equal(as_int(a), as_int(b))
+
+
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3])
+@pytest.mark.parametrize("which", ["fc784x300", "fc9216x4096"])
+def test_two_stream_step_matches_serial_calls(which, precision):
+    """L1.l1_step (CSC build and backward product on a side stream) gives the
+    outputs of the five calls made one after another on one stream, bit for
+    bit, on two calls in a row with the outputs overwritten in between; the
+    serial calls are checked against the oracle by the step tests above."""
+    import torch
+    L = synth.fc784_300(seed=0) if which == "fc784x300" else synth.fc9216_4096(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = t(L.X), t(L.dY)
+    a, b = _step_buffers(L, dev), _step_buffers(L, dev)
+    L1.csr_spmm_fwd(W, X, a["Y"])
+    L1.csc_build(W, a["csc"])
+    L1.csr_spmm_bwd_t(W, dY, a["csc"], a["dX"])
+    L1.dense_wgrad(dY, X, a["dW"], precision=precision)
+    L1.prox_l1_recompress(W, a["dW"], L.eta, L.lam, out=a["out"])
+    ref = _step_outputs(a, L.nnz)
+    for r in range(2):
+        for x in (b["Y"], b["dX"], b["dW"], b["out"].vals, b["csc"].vals_t):
+            x.fill_(-7)
+        got = L1.l1_step(W, X, dY, L.eta, L.lam, Y=b["Y"], dX=b["dX"], dW=b["dW"], csc=b["csc"],
+                         out=b["out"], precision=precision)
+        assert got is b["out"]
+        for i, (x, y) in enumerate(zip(_step_outputs(b, L.nnz), ref)):
+            assert _same_bits(x, y), (r, i)
+    torch.cuda.synchronize()
+
+
+def test_two_stream_step_graph_replays_match_eager():
+    """L1.l1_step captured into a HIP graph (the side stream forked from and
+    joined to the capture stream) and replayed three times, with eager steps
+    on other inputs and garbage written to the outputs in between: every
+    replay gives the eager result bit for bit."""
+    import torch
+    L = synth.fc784_300(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = t(L.X), t(L.dY)
+    X2 = t(np.flip(L.X, 1).copy())
+    o = _step_buffers(L, dev)
+    run = lambda x: L1.l1_step(W, x, dY, L.eta, L.lam, Y=o["Y"], dX=o["dX"], dW=o["dW"], csc=o["csc"],
+                               out=o["out"])
+    run(X)
+    torch.cuda.synchronize()
+    ref = [x.clone() for x in _step_outputs(o, L.nnz)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(X)
+    for r in range(3):
+        run(X2)
+        torch.cuda.synchronize()
+        for x in (o["Y"], o["dX"], o["dW"], o["out"].vals, o["csc"].vals_t):
+            x.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (x, y) in enumerate(zip(_step_outputs(o, L.nnz), ref)):
+            assert _same_bits(x, y), (r, i)
+
+
+def test_calls_on_two_streams_use_separate_workspaces():
+    """Tiled forward products (plan, pair stream and partial rows in the
+    call's workspace) issued alternately on two streams with no wait between
+    them: each stream's calls use their own workspace, so every result equals
+    the one-stream result bit for bit."""
+    import torch
+    L = synth.fc9216_4096(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    assert L1.workspace_bytes(L1.OP_SPMM, L.N, L.K, L.nnz, L.B) > 0  # the tiled path
+    rng = np.random.default_rng(5)
+    Xs = [t(L.X), t(rng.standard_normal(L.X.shape).astype(np.float32))]
+    ref = [L1.csr_spmm_fwd(W, x) for x in Xs]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[torch.full_like(ref[0], -7.0) for _ in range(3)] for _ in range(2)]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for r in range(3):
+        for i in range(2):
+            L1.csr_spmm_fwd(W, Xs[i], outs[i][r], stream=streams[i])
+    for s in streams:
+        torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for i in range(2):
+        for r in range(3):
+            assert _same_bits(outs[i][r], ref[i]), (i, r)
