@@ -134,7 +134,7 @@ def main():
         L1.l1_step (CSC build beside the forward product, backward product
         beside the prox), all outputs ready on the current stream at the end."""
         L1.l1_step(W, X, dY, eta, lam, Y=Y, dX=dX, dW=dW, csc=csc, out=Wout, precision=prec,
-                   events=None if wg is None else {"dense_wgrad": wg})
+                   events=None if wg is None else {"dense_wgrad": wg}, schedule="two_stream")
 
     def serial_step(ev=None, prec=L1.F32, wg=None):
         """The same calls one after another on one stream (events between them

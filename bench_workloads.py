@@ -118,11 +118,19 @@ def fc784x300(args, dev):
     nnz_out = int(Wout.row_ptr[-1].item())
     Wout.nnz = nnz_out
     ms_graph = _graph_timed(torch, step, max(args.steps, 20))
+
+    def step2(ev=None):  # the two-stream schedule of L1.l1_step
+        L1.l1_step(W, X, dY, L.eta, L.lam, Y=Y, dX=dX, dW=dW, csc=csc, out=Wout, schedule="two_stream")
+    ms2, _ = _timed(torch, step2, max(args.steps, 20), max(args.warmup, 5), None)
+    ms2_graph = _graph_timed(torch, step2, max(args.steps, 20))
     flops = 4.0 * L.nnz * L.B + 2.0 * L.N * L.K * L.B
     yield _line("fc784x300_b64_d10_l1_step", flops, ms,
                 dict(N=L.N, K=L.K, B=L.B, nnz=L.nnz, density=0.10), per,
                 nnz_out=nnz_out, ms_per_step_graph=round(ms_graph, 4),
-                value_graph=round(flops / (ms_graph * 1e-3) / 1e9, 1))
+                value_graph=round(flops / (ms_graph * 1e-3) / 1e9, 1),
+                ms_per_step_two_stream=round(ms2, 4), ms_per_step_two_stream_graph=round(ms2_graph, 4),
+                note="ms_per_step: the calls one after another on one stream (what L1.l1_step "
+                     "picks for this layer); two_stream: L1.l1_step forced onto two streams")
 
 
 def mlp784(args, dev):

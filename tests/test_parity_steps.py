@@ -478,10 +478,12 @@ def _same_bits(a, b):
 @pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3])
 @pytest.mark.parametrize("which", ["fc784x300", "fc9216x4096"])
 def test_two_stream_step_matches_serial_calls(which, precision):
-    """L1.l1_step (CSC build and backward product on a side stream) gives the
-    outputs of the five calls made one after another on one stream, bit for
-    bit, on two calls in a row with the outputs overwritten in between; the
-    serial calls are checked against the oracle by the step tests above."""
+    """L1.l1_step (CSC build and backward product on a side stream, forced,
+    and its automatic choice: two streams for the tiled 9216 -> 4096 products,
+    one for the 784 -> 300 layer) gives the outputs of the five calls made one
+    after another on one stream, bit for bit, on four calls in a row with the
+    outputs overwritten in between; the serial calls are checked against the
+    oracle by the step tests above."""
     import torch
     L = synth.fc784_300(seed=0) if which == "fc784x300" else synth.fc9216_4096(seed=0)
     dev = cuda()
@@ -494,11 +496,11 @@ def test_two_stream_step_matches_serial_calls(which, precision):
     L1.dense_wgrad(dY, X, a["dW"], precision=precision)
     L1.prox_l1_recompress(W, a["dW"], L.eta, L.lam, out=a["out"])
     ref = _step_outputs(a, L.nnz)
-    for r in range(2):
+    for r, schedule in enumerate(("two_stream", "auto", "two_stream", "serial")):
         for x in (b["Y"], b["dX"], b["dW"], b["out"].vals, b["csc"].vals_t):
             x.fill_(-7)
         got = L1.l1_step(W, X, dY, L.eta, L.lam, Y=b["Y"], dX=b["dX"], dW=b["dW"], csc=b["csc"],
-                         out=b["out"], precision=precision)
+                         out=b["out"], precision=precision, schedule=schedule)
         assert got is b["out"]
         for i, (x, y) in enumerate(zip(_step_outputs(b, L.nnz), ref)):
             assert _same_bits(x, y), (r, i)
@@ -506,7 +508,7 @@ def test_two_stream_step_matches_serial_calls(which, precision):
 
 
 def test_two_stream_step_graph_replays_match_eager():
-    """L1.l1_step captured into a HIP graph (the side stream forked from and
+    """L1.l1_step on two streams captured into a HIP graph (the side stream forked from and
     joined to the capture stream) and replayed three times, with eager steps
     on other inputs and garbage written to the outputs in between: every
     replay gives the eager result bit for bit."""
@@ -518,7 +520,7 @@ def test_two_stream_step_graph_replays_match_eager():
     X2 = t(np.flip(L.X, 1).copy())
     o = _step_buffers(L, dev)
     run = lambda x: L1.l1_step(W, x, dY, L.eta, L.lam, Y=o["Y"], dX=o["dX"], dW=o["dW"], csc=o["csc"],
-                               out=o["out"])
+                               out=o["out"], schedule="two_stream")
     run(X)
     torch.cuda.synchronize()
     ref = [x.clone() for x in _step_outputs(o, L.nnz)]
@@ -563,3 +565,19 @@ def test_calls_on_two_streams_use_separate_workspaces():
     for i in range(2):
         for r in range(3):
             assert _same_bits(outs[i][r], ref[i]), (i, r)
+
+
+def test_l1_step_schedule_choice():
+    """"auto" forks only where a product takes the tiled path, and a bad
+    schedule name is rejected before anything is enqueued."""
+    from paper_1905_07931_amd.step import two_stream_pays
+    dev = cuda()
+    small, big = synth.fc784_300(seed=0), synth.fc9216_4096(seed=0)
+    Ws = L1.CSR.from_host(small.row_ptr, small.col_idx, small.vals, small.K, device=dev)
+    Wb = L1.CSR.from_host(big.row_ptr, big.col_idx, big.vals, big.K, device=dev)
+    assert not two_stream_pays(Ws, small.B)
+    assert two_stream_pays(Wb, big.B)
+    o = _step_buffers(small, dev)
+    with pytest.raises(ValueError):
+        L1.l1_step(Ws, t(small.X), t(small.dY), small.eta, small.lam, Y=o["Y"], dX=o["dX"], dW=o["dW"],
+                   csc=o["csc"], out=o["out"], schedule="parallel")
