@@ -34,7 +34,9 @@ the caller's stream unless one of the two products is tiled.
 Each entry point keeps its own workspace per stream, so the two streams never
 share scratch memory.  The function is capture-safe: it forks the side stream
 from the caller's stream and joins it back before returning, so it records
-into a HIP graph (torch.cuda.CUDAGraph) like a single-stream sequence.
+into a HIP graph (torch.cuda.CUDAGraph) like a single-stream sequence.  As
+for every entry point under capture, W's nnz must be known on the host
+(W.nnz set): reading it from the device is a host wait.
 """
 from __future__ import annotations
 
