@@ -316,7 +316,8 @@ def fc4096_sweep(args, dev):
 
 def fc9216x4096_adaptive(args, dev):
     """One line per solver: fwd, CSC, bwd, dense dW, then the fused adaptive
-    prox + recompression over all N*K weights with dense m, v state (which
+    prox + recompression over all N*K weights (L1.l1_step with the adaptive
+    state, on two streams; the serial calls beside it) with dense m, v state (which
     advances every step; the work per step is the same).  eta = 1e-3 (the usual
     ADAM step), lambda = 1e-4 as for the plain step: almost every weight
     survives, the largest output the step can have."""
@@ -345,11 +346,16 @@ def fc9216x4096_adaptive(args, dev):
             mark(3); L1.dense_wgrad(dY, X, dW, precision=prec)
             mark(4); L1.prox_adaptive_recompress(W, dW, st, eta, lam, out=Wout)
             mark(5)
-        ms, per = _timed(torch, step, max(args.steps, 10), max(args.warmup, 3), names)
+        def step2(ev=None, prec=L1.F32):  # the two-stream schedule of L1.l1_step
+            L1.l1_step(W, X, dY, eta, lam, Y=Y, dX=dX, dW=dW, csc=csc, out=Wout, precision=prec,
+                       schedule="two_stream", adaptive=st)
+        # serial calls (per-call split), then the two-stream step (the line's value)
+        ms_serial, per = _timed(torch, step, max(args.steps, 10), max(args.warmup, 3), names)
+        ms, _ = _timed(torch, step2, max(args.steps, 10), max(args.warmup, 3), None)
         nnz_out = int(Wout.row_ptr[-1].item())
         # the same step with the split-bf16 weight gradient (inside the 1e-4 contract)
-        ms_x3, _ = _timed(torch, lambda ev=None: step(ev, prec=L1.BF16X3), max(args.steps, 10),
-                          max(args.warmup, 3), names)
+        ms_x3, _ = _timed(torch, lambda ev=None: step2(ev, prec=L1.BF16X3), max(args.steps, 10),
+                          max(args.warmup, 3), None)
         state_bytes = (16.0 if solver == L1.SOLVER_ADAM else 8.0) * N * K  # read and write m, v / v
         alg = 4.0 * N * K + state_bytes + (8.0 * nnz + 4 * (N + 1)) + (8.0 * nnz_out + 4 * (N + 1))
         # the two-pass kernels also re-read m', v' (ADAM) or G, v' (RMSProp)
@@ -365,7 +371,10 @@ def fc9216x4096_adaptive(args, dev):
                     prox_bytes_moved_two_pass=moved,
                     prox_moved_gbs=round(moved / (kms * 1e-3) / 1e9, 1),
                     ms_per_step_bf16x3=round(ms_x3, 4),
-                    value_bf16x3=round(flops / (ms_x3 * 1e-3) / 1e9, 1))
+                    value_bf16x3=round(flops / (ms_x3 * 1e-3) / 1e9, 1),
+                    ms_per_step_serial=round(ms_serial, 4),
+                    note="ms_per_step: L1.l1_step on two streams (fp32 and BF16X3 dW); "
+                         "ms_per_step_serial and kernels_ms: the calls one after another on one stream")
         del st
 
 

@@ -9,6 +9,10 @@ compressed (CSR) and activations batch-contiguous:
     G  = dY X^T                   dense weight gradient (every weight, zero or not)
     W' = prox_{eta*lambda}(W - eta G), recompressed to CSR   (Eq. 5)
 
+or, with an adaptive solver (Algorithms 1-2), the same soft threshold after
+the Prox-RMSProp / Prox-ADAM preconditioned step, fused with the
+recompression the same way.
+
 Only the forward product has to finish before the rest: dY is the upstream
 gradient of Y.  The five calls keep the dependencies of a training loop and
 run on two streams of equal (default) priority:
@@ -40,8 +44,8 @@ for every entry point under capture, W's nnz must be known on the host
 """
 from __future__ import annotations
 
-from . import (CSC, CSR, F32, OP_SPMM, csc_build, csr_spmm_bwd_t, csr_spmm_fwd, dense_wgrad,
-               prox_l1_recompress, workspace_bytes)
+from . import (CSC, CSR, F32, OP_SPMM, AdaptiveState, csc_build, csr_spmm_bwd_t, csr_spmm_fwd,
+               dense_wgrad, prox_adaptive_recompress, prox_l1_recompress, workspace_bytes)
 
 _side_streams: dict = {}
 
@@ -68,7 +72,7 @@ def two_stream_pays(W: CSR, B: int) -> bool:
 
 def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: CSR,
             precision: int = F32, side=None, events: dict | None = None,
-            schedule: str = "auto") -> CSR:
+            schedule: str = "auto", adaptive: AdaptiveState | None = None) -> CSR:
     """Run one l1 step on the caller's current stream plus a side stream.
 
     W is the N x K layer (CSR, nnz known on the host or read from the device),
@@ -79,8 +83,11 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
     side: the stream to fork onto (default: one per device).  events: optional
     {call name: (start, end)} torch events, recorded around that call on the
     stream it runs on.  schedule: "two_stream", "serial" (every call on the
-    caller's stream) or "auto" (two_stream where a product is tiled).  All
-    outputs are ready on the caller's stream when the call returns.  Returns out.
+    caller's stream) or "auto" (two_stream where a product is tiled).
+    adaptive: Prox-RMSProp / Prox-ADAM state with dense [N][K] m, v; the step
+    then ends with prox_adaptive_recompress (state updated in place, t
+    advanced) instead of prox_l1_recompress.  All outputs are ready on the
+    caller's stream when the call returns.  Returns out.
     """
     import torch
     if schedule not in ("auto", "two_stream", "serial"):
@@ -112,7 +119,11 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
     if fork:
         side.wait_stream(main)  # dY follows Y; the CSC is on side already
     call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t(W, dY, csc, dX, stream=side))
-    call("prox_l1_recompress", main, lambda: prox_l1_recompress(W, dW, eta, lam, out=out, stream=main))
+    if adaptive is None:
+        call("prox_l1_recompress", main, lambda: prox_l1_recompress(W, dW, eta, lam, out=out, stream=main))
+    else:
+        call("prox_adaptive_recompress", main,
+             lambda: prox_adaptive_recompress(W, dW, adaptive, eta, lam, out=out, stream=main))
     if fork:
         main.wait_stream(side)
     return out

@@ -581,3 +581,39 @@ def test_l1_step_schedule_choice():
     with pytest.raises(ValueError):
         L1.l1_step(Ws, t(small.X), t(small.dY), small.eta, small.lam, Y=o["Y"], dX=o["dX"], dW=o["dW"],
                    csc=o["csc"], out=o["out"], schedule="parallel")
+
+
+@pytest.mark.parametrize("solver", [L1.SOLVER_ADAM, L1.SOLVER_RMSPROP])
+@pytest.mark.parametrize("which,schedule", [("fc784x300", "two_stream"), ("fc9216x4096", "auto")])
+def test_two_stream_adaptive_step_matches_serial_calls(which, schedule, solver):
+    """L1.l1_step with a Prox-ADAM / Prox-RMSProp state (Algorithms 1-2) on two
+    streams gives, over two carried steps, the outputs, the state m, v and the
+    step counter of the same calls made one after another on one stream, bit
+    for bit (the adaptive calls are checked against the oracle in their own
+    tests)."""
+    import torch
+    L = synth.fc784_300(seed=0) if which == "fc784x300" else synth.fc9216_4096(seed=0)
+    dev = cuda()
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    X, dY = t(L.X), t(L.dY)
+    a, b = _step_buffers(L, dev), _step_buffers(L, dev)
+    sa = L1.AdaptiveState.zeros(solver, (L.N, L.K), dev)
+    sb = L1.AdaptiveState.zeros(solver, (L.N, L.K), dev)
+    eta = 1e-3
+    for r in range(2):
+        L1.csr_spmm_fwd(W, X, a["Y"])
+        L1.csc_build(W, a["csc"])
+        L1.csr_spmm_bwd_t(W, dY, a["csc"], a["dX"])
+        L1.dense_wgrad(dY, X, a["dW"])
+        L1.prox_adaptive_recompress(W, a["dW"], sa, eta, L.lam, out=a["out"])
+        for x in (b["Y"], b["dX"], b["dW"], b["out"].vals):
+            x.fill_(-7)
+        L1.l1_step(W, X, dY, eta, L.lam, Y=b["Y"], dX=b["dX"], dW=b["dW"], csc=b["csc"], out=b["out"],
+                   schedule=schedule, adaptive=sb)
+        for i, (x, y) in enumerate(zip(_step_outputs(b, L.nnz), _step_outputs(a, L.nnz))):
+            assert _same_bits(x, y), (r, i)
+        assert _same_bits(sb.v, sa.v), r
+        if solver == L1.SOLVER_ADAM:
+            assert _same_bits(sb.m, sa.m), r
+        assert sb.t == sa.t == r + 2
+    torch.cuda.synchronize()
