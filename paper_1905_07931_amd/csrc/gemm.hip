@@ -69,15 +69,12 @@ __device__ __forceinline__ void store_tile(float *lds, const float4 (&r)[kLoadsP
     }
 }
 
-constexpr int C_STRIDE = BN + 1;  // staged C tile of the masked epilogue
-
-// double-buffered operand tiles; the masked epilogue reuses them for C
+// double-buffered operand tiles
 union tile_smem {
     struct {
         float As[2][BM * LDS_STRIDE];
         float Bs[2][BN * LDS_STRIDE];
     } ab;
-    float C[BM * C_STRIDE];
 };
 
 // acc = the 128x128 tile (m0, n0) of A . Bt^T (A [M][lda], Bt [Nn][ldb], both
@@ -352,37 +349,6 @@ __global__ void wgrad_reduce_kernel(int M, int Nn, int S, const float *__restric
     }
 }
 
-// Masked variant: the tile is staged through LDS and only the entries of the
-// CSR pattern are written, gv[p] = C[row(p)][col(p)].  seg[row][t] = first
-// entry of the row with column >= t * 128 (t = 0 .. ceil(Nn / 128)).
-template <bool V4>
-__global__ __launch_bounds__(kThreads, 2) void sddmm_mfma_kernel(
-    int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
-    int64_t ldb, const int *__restrict__ seg, int ntiles, const int *__restrict__ idx,
-    float *__restrict__ gv) {
-    __shared__ __attribute__((aligned(16))) tile_smem sm;
-    float *smem = sm.C;
-    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-    floatx16 acc[2][2];
-    mfma_tile<V4>(M, Nn, Kr, A, lda, Bt, ldb, m0, n0, sm, acc);
-    // the last chunk ended with a barrier: the operand buffers are free
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) smem[acc_row(a, r) * C_STRIDE + acc_col(b)] = acc[a][b][r];
-    __syncthreads();
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int rr = wave; rr < BM; rr += kThreads / kWave) {
-        const int row = m0 + rr;
-        if (row >= M) break;
-        const int *sr = seg + (int64_t)row * (ntiles + 1) + blockIdx.x;
-        const int lo = sr[0], hi = sr[1];
-        for (int p = lo + lane; p < hi; p += kWave) gv[p] = smem[rr * C_STRIDE + (idx[p] - n0)];
-    }
-}
-
 }  // namespace
 
 wgrad_split wgrad_plan(int N, int K, int B) {
@@ -436,19 +402,6 @@ hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, c
         wgrad_f32_mfma_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
     else
         wgrad_f32_mfma_kernel<false><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
-    return hipGetLastError();
-}
-
-hipError_t launch_sddmm_mfma(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
-                             int64_t ldx, const int *seg, const int *idx, float *gv, hipStream_t s) {
-    if (N == 0 || K == 0) return hipSuccess;
-    const int ntiles = (int)ceil_div(K, BN);
-    dim3 grid((unsigned)ntiles, (unsigned)ceil_div(N, BM));
-    const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
-    if (v4)
-        sddmm_mfma_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, seg, ntiles, idx, gv);
-    else
-        sddmm_mfma_kernel<false><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, seg, ntiles, idx, gv);
     return hipGetLastError();
 }
 

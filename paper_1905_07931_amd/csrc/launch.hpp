@@ -61,12 +61,6 @@ hipError_t launch_wgrad_bf16(int N, int K, int B, const float *dY, int64_t ldy, 
 // the same with operands split into bf16 hi + lo, three products (wgrad_bf16x3.hip)
 hipError_t launch_wgrad_bf16x3(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                                int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
-// gv[p] = (dY . X^T)[row(p)][col(p)] through 128x128 matrix-core tiles of the
-// dense product; seg[row][t] = first entry of the row with column >= 128 t,
-// t = 0 .. ceil(K / 128) (launch_seg with shift 7)
-hipError_t launch_sddmm_mfma(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
-                             int64_t ldx, const int *seg, const int *idx, float *gv, hipStream_t s);
-
 // sddmm.hip ----------------------------------------------------------------
 // gv[p] = sum_b dY[row(p)][b] X[col(p)][b]; ws holds sddmm_workspace_bytes()
 size_t sddmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B);

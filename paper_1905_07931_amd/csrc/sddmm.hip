@@ -256,26 +256,6 @@ __global__ __launch_bounds__(256) void sddmm_reduce_kernel(int64_t nnz, int nseg
     if (wave == 0 && p < nnz) gv[p] = ((acc + red[0][lane]) + red[1][lane]) + red[2][lane];
 }
 
-// Matrix-core path: the dense product in 128x128 tiles with a masked
-// epilogue.  It does N*K*B multiply-adds instead of nnz*B, but at the matrix
-// cores' rate and without streaming an X row per entry through L2; it pays off
-// at high density.  Estimated times (us): the gather path moves about 24 TB/s
-// of X rows out of L2; a 128x128 tile takes about 0.15 us per batch entry with
-// two tiles per CU.
-constexpr int kDenseShift = 7;
-
-bool use_dense(int n_rows, int n_cols, int64_t nnz, int B) {
-    const double gather_us = (double)nnz * B * 4.0 / 24e6 + 5.0;
-    const double tiles = (double)ceil_div(n_rows, 128) * (double)ceil_div(n_cols, 128);
-    const double rounds = (double)ceil_div((int64_t)tiles, 512);
-    const double dense_us = rounds * 0.152 * B + 8.0;
-    return dense_us < gather_us;
-}
-
-size_t dense_ws_bytes(int n_rows, int n_cols) {
-    return sizeof(int) * (size_t)n_rows * (size_t)(ceil_div(n_cols, (int64_t)1 << kDenseShift) + 1);
-}
-
 struct gplan {
     int vec, nch, nbr;
     int shift, R;
@@ -369,7 +349,6 @@ void launch_gather(const gplan &pl, const gwork &w, int n_rows, int64_t nnz, con
 
 size_t sddmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B) {
     if (nnz == 0 || B == 0) return 0;
-    if (use_dense(n_rows, n_cols, nnz, B)) return dense_ws_bytes(n_rows, n_cols);
     // the larger of the vector and scalar plans
     const size_t a = carve(make_plan(n_rows, n_cols, nnz, B, true), n_rows, nnz, nullptr).bytes;
     const size_t b = carve(make_plan(n_rows, n_cols, nnz, B, false), n_rows, nnz, nullptr).bytes;
@@ -382,12 +361,6 @@ hipError_t launch_sddmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, con
     if (nnz == 0) return hipSuccess;
     if (B == 0) return launch_fill_f32(gv, nnz, 0.f, s);
     hipError_t e;
-    if (use_dense(n_rows, n_cols, nnz, B)) {
-        int *seg = static_cast<int *>(ws);
-        const int ntiles = (int)ceil_div(n_cols, (int64_t)1 << kDenseShift);
-        if ((e = launch_seg(n_rows, ntiles, kDenseShift, ptr, idx, seg, s)) != hipSuccess) return e;
-        return launch_sddmm_mfma(n_rows, n_cols, B, dY, ldy, X, ldx, seg, idx, gv, s);
-    }
     const bool v4 = (B % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) && aligned16(dY);
     const gplan pl = make_plan(n_rows, n_cols, nnz, B, v4);
     const gwork w = carve(pl, n_rows, nnz, ws);

@@ -125,15 +125,26 @@ def fc_layer(N, K, B, nnz, seed=0, w_std=0.05, pattern="uniform", zipf_s=1.1,
     return Layer(N, K, B, row_ptr, col_idx, vals, X, dY, eta, lam, name)
 
 
-def dyadic_layer(N, K, B, nnz, seed=0, empty_rows=(), full_rows=()) -> Layer:
+def dyadic_layer(N, K, B, nnz, seed=0, empty_rows=(), full_rows=(), pattern="uniform",
+                 zipf_s=1.1) -> Layer:
     """Inputs on a coarse dyadic grid: every float32 product and partial sum of
     the hot path is then exact, so any summation order gives the same bits.
 
     vals = +-k/16 (k in 1..16), X = j/16 (j in 0..16), dY = +-k/16; eta = 2^-7.
-    Rows listed in ``empty_rows`` get no entries, rows in ``full_rows`` all K.
+    ``pattern`` is "uniform", "zipf" (power-law row lengths, as fc_layer) or
+    an explicit (row_ptr, col_idx) pair (nnz is then ignored).  Rows listed in
+    ``empty_rows`` get no entries, rows in ``full_rows`` all K.
     """
     rp_rng, v_rng, x_rng, dy_rng = streams(seed)
-    row_ptr, col_idx = uniform_pattern(rp_rng, N, K, nnz)
+    if isinstance(pattern, tuple):
+        row_ptr = np.asarray(pattern[0], np.int32)
+        col_idx = np.asarray(pattern[1], np.int32)
+    elif pattern == "zipf":
+        row_ptr, col_idx = zipf_pattern(rp_rng, N, K, nnz, zipf_s)
+    elif pattern == "uniform":
+        row_ptr, col_idx = uniform_pattern(rp_rng, N, K, nnz)
+    else:
+        raise ValueError(pattern)
     if len(empty_rows) or len(full_rows):
         dense = np.zeros((N, K), bool)
         rows = np.repeat(np.arange(N), np.diff(row_ptr))

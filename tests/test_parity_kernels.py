@@ -100,6 +100,36 @@ def test_spmm_power_law_rows_dyadic_bit_exact():
     assert bits_equal(h(L1.csr_spmm_fwd(W, t(X))), oracle.spmm_fwd(rp, ci, vals, X))
 
 
+def _banded_dyadic(seed):
+    """4096 x 9216 at batch 1024 with every row dense over the first 128
+    columns, two fully dense rows, and uniform entries elsewhere (~2.9 M in
+    all), on the dyadic grid.  The mean load per (wave, X tile) keeps the
+    forward product on the tiled path with half-wave units (B >= 256 and a
+    mean chunk below 0.75 of the 1 KB LDS slot), while the first X tile holds
+    about 1000 pairs per wave, far beyond the slot, so the loop's reads of a
+    run from the stream in global memory are exercised; the full rows are cut
+    into strided pieces (a split row summed by the fix-up pass)."""
+    N, K, B = 4096, 9216, 1024
+    rng = np.random.default_rng(seed)
+    dense = np.zeros((N, K), bool)
+    dense[:, :128] = True
+    flat = rng.choice(N * (K - 128), 2_400_000, replace=False)
+    dense[flat // (K - 128), 128 + flat % (K - 128)] = True
+    dense[[17, 3001], :] = True
+    rp, ci = synth.pattern_from_positions(N, K, np.flatnonzero(dense.reshape(-1)))
+    return synth.dyadic_layer(N, K, B, 0, seed=seed, pattern=(rp, ci))
+
+
+def test_spmm_chunks_beyond_lds_slot_dyadic_bit_exact():
+    L = _banded_dyadic(41)
+    W = _W(L)
+    assert L1.workspace_bytes(L1.OP_SPMM, L.N, L.K, L.nnz, L.B) > 0  # the tiled path
+    Y = h(L1.csr_spmm_fwd(W, t(L.X)))
+    assert bits_equal(Y, oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)), "Y"
+    dX = h(L1.csr_spmm_bwd_t(W, t(L.dY), L1.csc_build(W)))
+    assert bits_equal(dX, oracle.spmm_bwd_t(L.row_ptr, L.col_idx, L.vals, L.dY, L.K)), "dX"
+
+
 def test_spmm_fwd_padded_leading_dimension():
     L = synth.fc_layer(50, 70, 37, 900, seed=11)
     import torch
@@ -427,11 +457,11 @@ def test_sddmm(shape):
     assert_scaled_close(gv, ref, m, what="gv")
 
 
-# large and dense enough that the matrix-core tile path is taken (vector and
-# scalar operand loads; ragged 128-tiles in both dimensions)
+# dense patterns (50 % and 93 % of the entries stored) through the gather
+# kernel, with vector and scalar operand loads and ragged column ranges
 @pytest.mark.parametrize("shape", [(2048, 2048, 256, 2097152, 11), (1100, 1030, 333, 1050000, 12)],
                          ids=_ids)
-def test_sddmm_dense_tiles(shape):
+def test_sddmm_dense_patterns(shape):
     L = _layer(shape)
     gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
     ref = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
