@@ -252,7 +252,7 @@ int csr_recompress(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz, 
  * output is bit-identical to the two calls.  G is read twice (a counting pass
  * and a filling pass); row_ptr_out, col_idx_out, vals_out, capacity,
  * d_nnz_out and h_nnz_required behave as in csr_recompress.  The output arrays
- * must not overlap W's.  ws as
+ * must not overlap W's arrays, G or one another (L1CSR_EINVAL).  ws as
  * l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0).
  */
 int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
@@ -312,7 +312,7 @@ int prox_adaptive_step(int mode, int solver, int32_t n_rows, int32_t n_cols, int
  * has left m and v unchanged.  With capacity >= n_rows*n_cols (no wait) G and
  * the states are read in a counting pass that stores m', v', and m', v' (ADAM)
  * or G, v' (RMSProp) are read again by the filling pass.  The output arrays
- * must not overlap W's.  ws as
+ * must not overlap W's arrays, G, m, v or one another (L1CSR_EINVAL).  ws as
  * l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0).
  */
 int prox_adaptive_recompress(int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,

@@ -119,6 +119,15 @@ def _p(t):
     return None if t is None else C.c_void_p(t.data_ptr())
 
 
+def _set_nnz(out, need, stream):
+    """The host count a call returned (>= 0), else the queued pinned copy."""
+    if need >= 0:
+        out.nnz = int(need)
+        out._pending = None
+    else:
+        out.track_nnz(stream)
+
+
 def _stream(stream=None):
     torch = _torch()
     s = torch.cuda.current_stream() if stream is None else stream
@@ -181,8 +190,13 @@ def _workspace(nbytes, device, stream=None):
 class CSR:
     """An N x K CSR matrix in device memory (int32 indices, float32 values).
 
-    ``nnz`` is the host-side count when known; after :func:`csr_recompress`
-    without a host wait it is ``None`` and ``row_ptr[-1]`` holds it on device.
+    ``nnz`` is the host-side count when known.  A call that writes a CSR
+    without waiting (:func:`csr_recompress`, :func:`prox_l1_recompress`, ...
+    at full capacity) leaves it ``None``: ``row_ptr[-1]`` holds it on the
+    device, and the call has queued a copy of it into pinned host memory
+    behind its last kernel.  The first use of the matrix then waits for that
+    copy only (an event), not for the whole device; set ``nnz`` beforehand
+    (e.g. under graph capture) to avoid the wait.
     ``col_idx``/``vals`` may be longer than nnz (capacity).
     """
     n_rows: int
@@ -191,11 +205,34 @@ class CSR:
     col_idx: "object"
     vals: "object"
     nnz: int | None = None
+    _pending: "object" = None  # (pinned int32 copy of row_ptr[-1], its event)
 
     def host_nnz(self) -> int:
         if self.nnz is None:
-            self.nnz = int(self.row_ptr[-1].item())
+            if self._pending is not None:
+                host, ev = self._pending
+                ev.synchronize()
+                self.nnz = int(host[0])
+            else:
+                self.nnz = int(self.row_ptr[-1].item())
+        self._pending = None
         return self.nnz
+
+    def track_nnz(self, stream=None):
+        """Queue the copy of row_ptr[-1] to pinned host memory on `stream`
+        (after the kernels that wrote it) and forget the host count."""
+        torch = _torch()
+        s = torch.cuda.current_stream(self.row_ptr.device) if stream is None else stream
+        self.nnz = None
+        self._pending = None
+        if torch.cuda.is_current_stream_capturing():
+            return  # a captured graph has no host copy to wait for: the caller sets nnz
+        host = torch.empty(1, dtype=torch.int32, pin_memory=True)
+        with torch.cuda.stream(s):
+            host.copy_(self.row_ptr[-1:], non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(s)
+        self._pending = (host, ev)
 
     def validate_shapes(self):
         torch = _torch()
@@ -204,7 +241,8 @@ class CSR:
         _vec(self.vals, torch.float32, "vals")
         if self.row_ptr.numel() != self.n_rows + 1:
             raise ValueError("row_ptr must have n_rows + 1 entries")
-        nnz = self.nnz if self.nnz is not None else self.col_idx.numel()
+        # the stored count sizes plans and workspaces: never guess it from the capacity
+        nnz = self.host_nnz()
         if self.col_idx.numel() < nnz or self.vals.numel() < nnz:
             raise ValueError("col_idx/vals shorter than nnz")
         return nnz
@@ -402,7 +440,7 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
     _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
                                 _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
                                 _stream(stream)), "csr_recompress")
-    out.nnz = need.value if need.value >= 0 else None
+    _set_nnz(out, need.value, stream)
     return out
 
 
@@ -426,7 +464,7 @@ def prox_l1_recompress(W: CSR, G, eta, lam, capacity=None, out: CSR | None = Non
                                     float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
                                     _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
                                     _stream(stream)), "prox_l1_recompress")
-    out.nnz = need.value if need.value >= 0 else None
+    _set_nnz(out, need.value, stream)
     return out
 
 
@@ -537,7 +575,7 @@ def prox_adaptive_recompress(W: CSR, G, st: AdaptiveState, eta, lam, capacity=No
                                           _p(out.col_idx), _p(out.vals), cap, None, C.byref(need),
                                           _p(ws), wsb, _stream(stream)), "prox_adaptive_recompress")
     st.t += 1
-    out.nnz = need.value if need.value >= 0 else None
+    _set_nnz(out, need.value, stream)
     return out
 
 
@@ -657,7 +695,7 @@ def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:
     _check(lib().csr_compact(W.n_rows, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(out.row_ptr),
                              _p(out.col_idx), _p(out.vals), None, _p(ws), wsb, _stream(stream)),
            "csr_compact")
-    out.nnz = None
+    out.track_nnz(stream)
     return out
 
 

@@ -4,6 +4,7 @@
 // stream (csr_recompress with a short capacity is the one documented wait).
 #include <math.h>
 
+
 #include "../../include/l1csr.h"
 #include "common.hpp"
 #include "launch.hpp"
@@ -47,6 +48,43 @@ bool overlap(const float *p, int64_t ldp, const float *q, int64_t ldq, int64_t r
     return p0 < q1 && q0 < p1;
 }
 
+// byte ranges [a, a + na) and [b, b + nb) intersect (null or empty never does)
+bool bytes_overlap(const void *a, size_t na, const void *b, size_t nb) {
+    if (a == nullptr || b == nullptr || na == 0 || nb == 0) return false;
+    const char *a0 = static_cast<const char *>(a), *b0 = static_cast<const char *>(b);
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// extent in bytes of a [rows][ld] float matrix with `cols` columns used
+size_t dense_bytes(int64_t rows, int64_t cols, int64_t ld) {
+    return rows > 0 && cols > 0 ? sizeof(float) * (size_t)((rows - 1) * ld + cols) : 0;
+}
+
+// The output CSR of an out-of-place update (row_ptr_out [n_rows + 1],
+// col_idx_out / vals_out [capacity]) must not share memory with any input the
+// kernels still read while it is written (W's arrays, the gradient, states).
+bool outputs_overlap(int32_t n_rows, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,
+                     const float *vals, const int32_t *row_ptr_out, const int32_t *col_idx_out,
+                     const float *vals_out, int64_t capacity, const void *const *dense_in,
+                     const size_t *dense_in_bytes, int n_dense) {
+    const size_t rp = sizeof(int32_t) * ((size_t)n_rows + 1);
+    const size_t cap = sizeof(int32_t) * (size_t)capacity;  // int32 and float alike
+    const size_t in = sizeof(int32_t) * (size_t)nnz;
+    const void *outs[3] = {row_ptr_out, col_idx_out, vals_out};
+    const size_t out_b[3] = {rp, cap, cap};
+    const void *ins[3] = {row_ptr, col_idx, vals};
+    const size_t in_b[3] = {rp, in, in};
+    for (int o = 0; o < 3; ++o) {
+        for (int q = o + 1; q < 3; ++q)
+            if (bytes_overlap(outs[o], out_b[o], outs[q], out_b[q])) return true;
+        for (int i = 0; i < 3; ++i)
+            if (bytes_overlap(outs[o], out_b[o], ins[i], in_b[i])) return true;
+        for (int d = 0; d < n_dense; ++d)
+            if (bytes_overlap(outs[o], out_b[o], dense_in[d], dense_in_bytes[d])) return true;
+    }
+    return false;
+}
+
 // Prox-RMSProp / Prox-ADAM hyper-parameters -> the kernels' double constants;
 // false if any is out of range (Algorithms 1-2: eta > 0, eps > 0, decay rates
 // in [0, 1), t >= 1 for ADAM's bias corrections; lambda >= 0).
@@ -82,9 +120,73 @@ bool read_geom(const int32_t *geom, conv_geom *g, int *OH, int *OW) {
     return in <= INT32_MAX && kk <= INT32_MAX && (int64_t)*OH * *OW <= INT32_MAX;
 }
 
+// argument checks of prox_l1_recompress (every one but the workspace)
+int prox_recompress_check(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                          const int32_t *col_idx, const float *vals, const float *G, int64_t ldg,
+                          float eta, float lambda, const int32_t *row_ptr_out, const int32_t *col_idx_out,
+                          const float *vals_out, int64_t capacity) {
+    if (!finite_f(eta) || !finite_f(lambda) || eta <= 0.f || lambda < 0.f) return L1CSR_EINVAL;
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(G, n_rows, n_cols, ldg) || row_ptr_out == nullptr || capacity < 0)
+        return L1CSR_EINVAL;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
+    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    if ((int64_t)n_rows * prox_slabs(n_cols) > INT32_MAX) return L1CSR_EUNSUPPORTED;
+    // out of place: no output array may share memory with W or G
+    const void *din[1] = {G};
+    const size_t dinb[1] = {dense_bytes(n_rows, n_cols, ldg)};
+    if (outputs_overlap(n_rows, nnz, row_ptr, col_idx, vals, row_ptr_out, col_idx_out, vals_out, capacity,
+                        din, dinb, 1))
+        return L1CSR_EINVAL;
+    return L1CSR_OK;
+}
+
+// the launches of prox_l1_recompress on checked arguments, with ws holding
+// prox_recompress_workspace_bytes(n_rows, n_cols) bytes
+int prox_recompress_run(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                        const int32_t *col_idx, const float *vals, const float *G, int64_t ldg,
+                        float eta, float lambda, int32_t *row_ptr_out, int32_t *col_idx_out,
+                        float *vals_out, int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                        void *ws, hipStream_t stream) {
+    (void)nnz;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (n_rows == 0) {
+        hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
+        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
+        if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
+        return hip_status(e);
+    }
+    const double t = (double)eta * (double)lambda;     // exact in double
+    // scratch: per-slab entry bounds and counts, then the counts' exclusive
+    // scan (the output layout)
+    const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
+    const prox_ws pw = prox_carve(n_rows, n_cols, ws);
+    hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, pw.seg,
+                                     pw.counts, stream);
+    if (e == hipSuccess) e = launch_exclusive_scan(pw.counts, pw.off, (int)n_slabs, nullptr, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    if (capacity < total) {
+        // the host needs the output size before the fill: row pointers now
+        e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        int32_t h = 0;
+        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        if (h_nnz_required) *h_nnz_required = h;
+        if (h > capacity) return L1CSR_ECAPACITY;
+    } else if (h_nnz_required) {
+        *h_nnz_required = -1;
+    }
+    return hip_status(launch_prox_fill(n_rows, n_cols, pw.seg, col_idx, vals, G, ldg, eta, t, pw.off,
+                                       col_idx_out, vals_out, capacity, row_ptr_out, d_nnz_out, stream));
+}
+
 }  // namespace
 
 extern "C" {
+
 
 const char *l1csr_status_str(int status) {
     switch (status) {
@@ -265,47 +367,14 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
                        float eta, float lambda, int32_t *row_ptr_out, int32_t *col_idx_out,
                        float *vals_out, int64_t capacity, int32_t *d_nnz_out,
                        int64_t *h_nnz_required, void *ws, size_t ws_bytes, hipStream_t stream) {
-    if (!finite_f(eta) || !finite_f(lambda) || eta <= 0.f || lambda < 0.f) return L1CSR_EINVAL;
-    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
-    if (bad_dense(G, n_rows, n_cols, ldg) || row_ptr_out == nullptr || capacity < 0)
-        return L1CSR_EINVAL;
-    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
-    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
-    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    const int v = prox_recompress_check(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
+                                        row_ptr_out, col_idx_out, vals_out, capacity);
+    if (v != L1CSR_OK) return v;
     if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
         return L1CSR_EINVAL;
-    if (row_ptr_out == row_ptr) return L1CSR_EINVAL;  // out of place
-    if (n_rows == 0) {
-        hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
-        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
-        if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
-        return hip_status(e);
-    }
-    const double t = (double)eta * (double)lambda;     // exact in double
-    // scratch: per-slab entry bounds and counts, then the counts' exclusive
-    // scan (the output layout)
-    const int64_t n_slabs = (int64_t)n_rows * prox_slabs(n_cols);
-    if (n_slabs > INT32_MAX) return L1CSR_EUNSUPPORTED;
-    const prox_ws pw = prox_carve(n_rows, n_cols, ws);
-    hipError_t e = launch_prox_count(n_rows, n_cols, row_ptr, col_idx, vals, G, ldg, eta, t, pw.seg,
-                                     pw.counts, stream);
-    if (e == hipSuccess) e = launch_exclusive_scan(pw.counts, pw.off, (int)n_slabs, nullptr, stream);
-    if (e != hipSuccess) return L1CSR_EHIP;
-    if (capacity < total) {
-        // the host needs the output size before the fill: row pointers now
-        e = launch_prox_row_ptr(n_rows, n_cols, pw.off, row_ptr_out, d_nnz_out, stream);
-        if (e != hipSuccess) return L1CSR_EHIP;
-        int32_t h = 0;
-        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
-        if (e == hipSuccess) e = hipStreamSynchronize(stream);
-        if (e != hipSuccess) return L1CSR_EHIP;
-        if (h_nnz_required) *h_nnz_required = h;
-        if (h > capacity) return L1CSR_ECAPACITY;
-    } else if (h_nnz_required) {
-        *h_nnz_required = -1;
-    }
-    return hip_status(launch_prox_fill(n_rows, n_cols, pw.seg, col_idx, vals, G, ldg, eta, t, pw.off,
-                                       col_idx_out, vals_out, capacity, row_ptr_out, d_nnz_out, stream));
+    return prox_recompress_run(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
+                               row_ptr_out, col_idx_out, vals_out, capacity, d_nnz_out, h_nnz_required, ws,
+                               stream);
 }
 
 int prox_adaptive_step(int mode, int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,
@@ -374,7 +443,14 @@ int prox_adaptive_recompress(int solver, int32_t n_rows, int32_t n_cols, int64_t
     if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
     if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
         return L1CSR_EINVAL;
-    if (row_ptr_out == row_ptr) return L1CSR_EINVAL;  // out of place
+    {  // out of place: no output array may share memory with W, G or the states
+        const void *din[3] = {G, v, adam ? m : nullptr};
+        const size_t dinb[3] = {dense_bytes(n_rows, n_cols, ldg), dense_bytes(n_rows, n_cols, lds),
+                                adam ? dense_bytes(n_rows, n_cols, lds) : 0};
+        if (outputs_overlap(n_rows, nnz, row_ptr, col_idx, vals, row_ptr_out, col_idx_out, vals_out,
+                            capacity, din, dinb, 3))
+            return L1CSR_EINVAL;
+    }
     if (n_rows == 0) {
         hipError_t e = launch_fill_i32(row_ptr_out, 1, 0, stream);
         if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);

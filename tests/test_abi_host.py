@@ -236,3 +236,49 @@ def test_adaptive_prox_arguments_are_rejected_before_launch(lib):
                 NUL, NUL, 0, S) == EINVAL
     assert step(5, 1, 4, 4, 3, Wp, Wp, Wp, G, 4, NUL, V, 4, 0.01, 0.0, 1e-8, 0.9, 0.999, 1, Z, 4,
                 NUL, WS, ws, S) == EINVAL
+
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_fused_updates_reject_outputs_overlapping_inputs(lib):
+    """prox_l1_recompress / prox_adaptive_recompress write W' while other
+    workgroups still read W, G and the states: any byte overlap between an
+    output array (row_ptr_out [N+1], col_idx_out / vals_out [capacity]) and
+    an input, or between two outputs, is rejected before launch.  With every
+    buffer distinct the same calls get past validation (and, with no GPU,
+    fail only at the launch)."""
+    _setup(lib)
+    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    lib.prox_adaptive_recompress.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
+                                             f32, f32, f32, f32, f32, i64, vp, vp, vp, i64, vp, vp, vp,
+                                             C.c_size_t, vp]
+    N = K = 64
+    nnz, cap = 100, N * K
+    base = {n: (i + 1) << 24 for i, n in enumerate(["rp", "ci", "v", "G", "m", "vv", "rpo", "cio", "vo", "ws"])}
+    ws = lib.l1csr_workspace_bytes(7, N, K, nnz, 0)
+
+    def plain(**o):
+        a = dict(base, **o)
+        p = {k: C.c_void_p(x) for k, x in a.items()}
+        return lib.prox_l1_recompress(N, K, nnz, p["rp"], p["ci"], p["v"], p["G"], K, 0.1, 0.1, p["rpo"],
+                                      p["cio"], p["vo"], cap, NUL, NUL, p["ws"], ws, S)
+
+    def adam(**o):
+        a = dict(base, **o)
+        p = {k: C.c_void_p(x) for k, x in a.items()}
+        return lib.prox_adaptive_recompress(2, N, K, nnz, p["rp"], p["ci"], p["v"], p["G"], K, p["m"],
+                                            p["vv"], K, 0.01, 0.1, 1e-8, 0.9, 0.999, 1, p["rpo"], p["cio"],
+                                            p["vo"], cap, NUL, NUL, p["ws"], ws, S)
+
+    for f in (plain, adam):
+        assert f() == EHIP  # valid arguments: only the launch fails here
+        inside = lambda name, off=64: base[name] + off
+        for bad in [dict(cio=inside("v")), dict(vo=inside("ci")), dict(vo=inside("G", 4 * (N * K - 1))),
+                    dict(rpo=inside("ci", 4 * (nnz - 1))), dict(cio=inside("rp", -4 * cap + 8)),
+                    dict(vo=inside("cio", 4 * (cap - 1))), dict(rpo=inside("vo"))]:
+            assert f(**bad) == EINVAL, (f.__name__, bad)
+        # just past the end of an input is fine
+        assert f(cio=base["v"] + 4 * nnz) == EHIP
+    for bad in [dict(vo=inside("m")), dict(cio=inside("vv", 4 * (N * K - 1)))]:
+        assert adam(**bad) == EINVAL, bad
+    assert plain(vo=inside("m")) == EHIP  # the plain update has no state
+

@@ -665,3 +665,56 @@ def test_two_stream_adaptive_step_matches_serial_calls(which, schedule, solver):
             assert _same_bits(sb.m, sa.m), r
         assert sb.t == sa.t == r + 2
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("which", ["fc784x300", "fc4096_d5"])
+def test_l1_step_loop_carries_W_forward(which):
+    """A training loop feeds each step's new CSR back in as the next W
+    (ping-pong buffers) without ever setting nnz itself.  Each output's count
+    is queued to pinned host memory behind the call that wrote it, and the
+    next step takes it from there (a wait on that copy alone), so products,
+    CSC and plans are sized for the stored entries, never for the N*K
+    capacity.  Three steps through l1_step (auto schedule) equal the same
+    calls made one after another on one stream, bit for bit."""
+    import torch
+    dev = cuda()
+    if which == "fc784x300":
+        L = synth.fc784_300(seed=0)
+        lam = L.lam
+        batches = [(L.X, L.dY)] * 3
+    else:
+        L = synth.fc4096_sweep(0.05)
+        lam = json.load(open(os.path.join(GOLDEN, "fc4096_lambda.json")))["lambda"]["5"]
+        batches = [synth.fc4096_batch(2 * it) for it in range(3)]
+    N, K, eta = L.N, L.K, L.eta
+    Wa = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=dev)
+    Wb = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=dev)
+    bufs_a = [_step_buffers(L, dev)["out"] for _ in range(2)]
+    bufs_b = [_step_buffers(L, dev)["out"] for _ in range(2)]
+    Y, dX = torch.empty((N, L.B), device=dev), torch.empty((K, L.B), device=dev)
+    Yb, dXb = torch.empty_like(Y), torch.empty_like(dX)
+    dW, dWb = torch.empty((N, K), device=dev), torch.empty((N, K), device=dev)
+    csc_a, csc_b = L1.CSC.empty(K, N * K, dev), L1.CSC.empty(K, N * K, dev)
+    for it, (Xh, dYh) in enumerate(batches):
+        X, dY = t(Xh), t(dYh)
+        if it > 0:
+            assert Wb.nnz is None and Wb._pending is not None  # count still on its way to the host
+        outa, outb = bufs_a[it % 2], bufs_b[it % 2]
+        L1.csr_spmm_fwd(Wa, X, Y)
+        L1.csc_build(Wa, csc_a)
+        L1.csr_spmm_bwd_t(Wa, dY, csc_a, dX)
+        L1.dense_wgrad(dY, X, dW)
+        L1.prox_l1_recompress(Wa, dW, eta, lam, out=outa)
+        L1.l1_step(Wb, X, dY, eta, lam, Y=Yb, dX=dXb, dW=dWb, csc=csc_b, out=outb, schedule="auto")
+        n_in = Wb.host_nnz()
+        assert n_in == int(Wb.row_ptr[-1].item())
+        n = outb.host_nnz()
+        assert n == outa.host_nnz() == int(outb.row_ptr[-1].item())
+        for x, y in ((Yb, Y), (dXb, dX), (dWb, dW), (outb.row_ptr, outa.row_ptr),
+                     (outb.col_idx[:n], outa.col_idx[:n]), (outb.vals[:n], outa.vals[:n]),
+                     (csc_b.col_ptr, csc_a.col_ptr), (csc_b.row_idx[:n_in], csc_a.row_idx[:n_in])):
+            assert _same_bits(x, y), it
+        outb.nnz = None  # as the step left it: the count comes from the queued copy
+        outb.track_nnz()
+        Wa, Wb = outa, outb
+    torch.cuda.synchronize()
