@@ -55,7 +55,8 @@ enum l1csr_status {
     L1CSR_ECAPACITY = -2,    /* output capacity too small (csr_recompress) */
     L1CSR_EBADCSR = -3,      /* malformed CSR (csr_validate, via its device status) */
     L1CSR_EHIP = -4,         /* a HIP runtime or launch error */
-    L1CSR_EUNSUPPORTED = -5  /* valid but unsupported combination */
+    L1CSR_EUNSUPPORTED = -5, /* valid but unsupported combination */
+    L1CSR_ESCRATCH = -6      /* a no-allocation call needs more than its static scratch */
 };
 
 /* dense_wgrad operand precision */
@@ -261,6 +262,30 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
                        int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
                        int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * prox_l1_recompress for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments without (ws, ws_bytes), the same kernels and bit-identical
+ * results.  Its scratch (per-slab entry bounds, counts and offsets,
+ * l1csr_workspace_bytes(L1CSR_OP_PROX_RECOMPRESS, n_rows, n_cols, nnz, 0)
+ * bytes) lives in a static device array of L1CSR_NOALLOC_SCRATCH_BYTES
+ * (16 MiB) that each GPU the library runs on holds until the process ends;
+ * a larger need returns L1CSR_ESCRATCH before anything is launched.  The
+ * call allocates and frees nothing.  Every call of this entry point on one
+ * GPU shares that GPU's array (the last call's contents stay in it; nothing
+ * in it needs to start at zero), so such calls that overlap in time on one
+ * GPU, on different streams or from different threads, race: the caller
+ * orders them.  The first call on a device looks up the array's device
+ * address (a runtime call that does not enqueue work).
+ */
+#define L1CSR_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int prox_l1_recompress_noalloc(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                               const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                               const float *G, int64_t ldg, float eta, float lambda,
+                               int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
+                               int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                               hipStream_t stream);
 
 /*
  * Adaptive proximal steps: Prox-RMSProp (Algorithm 1) and Prox-ADAM

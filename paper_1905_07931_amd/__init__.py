@@ -20,12 +20,13 @@ __all__ = [
     "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16", "BF16X3",
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
     "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
-    "l1_step", "side_stream",
+    "l1_step", "side_stream", "prox_l1_recompress_noalloc",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
 
-OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED, ESCRATCH = 0, -1, -2, -3, -4, -5, -6
+NOALLOC_SCRATCH_BYTES = 16 << 20  # L1CSR_NOALLOC_SCRATCH_BYTES
 PROX_DENSE, PROX_CSR = 0, 1
 F32, BF16, BF16X3 = 0, 1, 2
 SOLVER_RMSPROP, SOLVER_ADAM = 1, 2
@@ -69,6 +70,8 @@ def lib():
                                      C.POINTER(C.c_int64), vp, sz, vp]
         L.prox_l1_recompress.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp,
                                          i64, vp, C.POINTER(C.c_int64), vp, sz, vp]
+        L.prox_l1_recompress_noalloc.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp,
+                                                 vp, i64, vp, C.POINTER(C.c_int64), vp]
         L.prox_adaptive_step.argtypes = [C.c_int, C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp,
                                          i64, f32, f32, f32, f32, f32, i64, vp, i64, vp, vp, sz, vp]
         L.prox_adaptive_recompress.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
@@ -85,6 +88,7 @@ def lib():
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
+                     "prox_l1_recompress_noalloc",
                      "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent",
                      "prox_adaptive_step", "prox_adaptive_recompress", "csr_conv_fwd",
                      "csr_conv_bwd_data", "conv_im2col", "l1csr_maxpool_fwd"):
@@ -440,6 +444,24 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
     _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
                                 _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
                                 _stream(stream)), "csr_recompress")
+    _set_nnz(out, need.value, stream)
+    return out
+
+
+def prox_l1_recompress_noalloc(W: CSR, G, eta, lam, out: CSR, capacity=None, stream=None):
+    """prox_l1_recompress without a workspace: the library's static per-device
+    scratch (L1CSR_NOALLOC_SCRATCH_BYTES) serves the call, which allocates
+    nothing; `out` must be given.  Calls of it that overlap on one GPU race."""
+    nnz = W.validate_shapes()
+    N, K, ldg = _mat(G, "G")
+    if (N, K) != (W.n_rows, W.n_cols):
+        raise ValueError("G must be [n_rows][n_cols]")
+    cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
+    need = C.c_int64(-1)
+    _check(lib().prox_l1_recompress_noalloc(N, K, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(G),
+                                            ldg, float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
+                                            _p(out.vals), cap, None, C.byref(need), _stream(stream)),
+           "prox_l1_recompress_noalloc")
     _set_nnz(out, need.value, stream)
     return out
 

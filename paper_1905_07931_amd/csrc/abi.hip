@@ -4,6 +4,7 @@
 // stream (csr_recompress with a short capacity is the one documented wait).
 #include <math.h>
 
+#include <mutex>
 
 #include "../../include/l1csr.h"
 #include "common.hpp"
@@ -183,6 +184,43 @@ int prox_recompress_run(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                                        col_idx_out, vals_out, capacity, row_ptr_out, d_nnz_out, stream));
 }
 
+// Static scratch of the entry points that allocate nothing (callers that
+// cannot call hipMalloc: graph capture, serving loops).  Each GPU the library
+// runs on holds its own copy until the process ends; every such call on one
+// GPU shares it, so calls that overlap on one GPU race.  Host code never
+// passes the array's name to a kernel: the name is a host-side stand-in, and
+// the device address is looked up once per device (scratch_ptr).
+constexpr size_t kScratchBytes = L1CSR_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxDevices] = {};
+
+// device address of `scratch` on the device `stream` belongs to (the current
+// device for the null stream), looked up with that device current on first use
+hipError_t scratch_ptr(hipStream_t stream, void **out) {
+    int dev = 0;
+    hipError_t e = stream != nullptr ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[dev] == nullptr) {
+        int cur = 0;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        const hipError_t e2 = cur != dev ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess) return e;
+        if (e2 != hipSuccess) return e2;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -196,6 +234,7 @@ const char *l1csr_status_str(int status) {
         case L1CSR_EBADCSR: return "malformed CSR";
         case L1CSR_EHIP: return "HIP runtime or launch error";
         case L1CSR_EUNSUPPORTED: return "unsupported size or combination";
+        case L1CSR_ESCRATCH: return "needs more scratch than the library's static buffer holds";
         default: return "unknown status";
     }
 }
@@ -372,6 +411,23 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_
     if (v != L1CSR_OK) return v;
     if (n_rows > 0 && (ws == nullptr || ws_bytes < prox_recompress_workspace_bytes(n_rows, n_cols)))
         return L1CSR_EINVAL;
+    return prox_recompress_run(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
+                               row_ptr_out, col_idx_out, vals_out, capacity, d_nnz_out, h_nnz_required, ws,
+                               stream);
+}
+
+int prox_l1_recompress_noalloc(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                               const int32_t *col_idx, const float *vals, const float *G, int64_t ldg,
+                               float eta, float lambda, int32_t *row_ptr_out, int32_t *col_idx_out,
+                               float *vals_out, int64_t capacity, int32_t *d_nnz_out,
+                               int64_t *h_nnz_required, hipStream_t stream) {
+    const int v = prox_recompress_check(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
+                                        row_ptr_out, col_idx_out, vals_out, capacity);
+    if (v != L1CSR_OK) return v;
+    if (n_rows > 0 && prox_recompress_workspace_bytes(n_rows, n_cols) > kScratchBytes)
+        return L1CSR_ESCRATCH;
+    void *ws = nullptr;
+    if (n_rows > 0 && scratch_ptr(stream, &ws) != hipSuccess) return L1CSR_EHIP;
     return prox_recompress_run(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
                                row_ptr_out, col_idx_out, vals_out, capacity, d_nnz_out, h_nnz_required, ws,
                                stream);

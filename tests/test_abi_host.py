@@ -16,7 +16,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "l1csr.h")
 LIB = os.path.join(ROOT, "paper_1905_07931_amd", "libl1csr.so")
 
-OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED, ESCRATCH = 0, -1, -2, -3, -4, -5, -6
 NO_GPU = not os.path.exists("/dev/kfd")
 
 
@@ -45,7 +45,7 @@ def test_header_declares_the_hot_path_calls():
     for n in ["csr_spmm_fwd", "csr_spmm_bwd_t", "dense_wgrad", "sddmm_masked_wgrad", "prox_l1_step",
               "csr_recompress", "prox_l1_recompress", "csc_build", "csc_update_vals", "csr_compact",
               "csr_validate", "l1csr_workspace_bytes", "l1csr_status_str", "prox_adaptive_step",
-              "prox_adaptive_recompress"]:
+              "prox_adaptive_recompress", "prox_l1_recompress_noalloc"]:
         assert n in names, n
 
 
@@ -56,11 +56,11 @@ def test_library_exports_every_declared_function(lib):
 
 def test_status_strings(lib):
     seen = set()
-    for code in (OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED):
+    for code in (OK, EINVAL, ECAPACITY, EBADCSR, EHIP, EUNSUPPORTED, ESCRATCH):
         s = lib.l1csr_status_str(code).decode()
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == 6
+    assert len(seen) == 7
     assert lib.l1csr_status_str(12345).decode() == "unknown status"
 
 
@@ -282,3 +282,26 @@ def test_fused_updates_reject_outputs_overlapping_inputs(lib):
         assert adam(**bad) == EINVAL, bad
     assert plain(vo=inside("m")) == EHIP  # the plain update has no state
 
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_noalloc_prox_checks_its_arguments_and_scratch_before_launch(lib):
+    """prox_l1_recompress_noalloc validates like prox_l1_recompress and
+    rejects a layer whose slab scratch exceeds the 16 MiB static array with
+    L1CSR_ESCRATCH, before any runtime call."""
+    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    f = lib.prox_l1_recompress_noalloc
+    f.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, i64, vp, vp, vp]
+    a = {n: C.c_void_p((i + 1) << 28) for i, n in enumerate(["rp", "ci", "v", "G", "rpo", "cio", "vo"])}
+
+    def call(N, K, nnz=0, eta=0.01, lam=1e-4, ldg=None, rpo=None, cap=None):
+        return f(N, K, nnz, a["rp"], a["ci"], a["v"], a["G"], K if ldg is None else ldg, eta, lam,
+                 a["rpo"] if rpo is None else rpo, a["cio"], a["vo"], N * K if cap is None else cap, NUL,
+                 NUL, S)
+
+    assert lib.l1csr_workspace_bytes(7, 2_000_000, 1, 0, 0) > 16 << 20
+    assert call(2_000_000, 1) == ESCRATCH
+    assert call(64, 64, eta=float("nan")) == EINVAL
+    assert call(64, 64, ldg=63) == EINVAL
+    assert call(64, 64, rpo=C.c_void_p(0)) == EINVAL  # no row pointers
+    assert call(64, 64, nnz=10, rpo=a["ci"]) == EINVAL   # output over W's columns
+    assert call(65536, 65536) == EUNSUPPORTED            # beyond the int32 layout
