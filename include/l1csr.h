@@ -87,7 +87,8 @@ enum l1csr_op {
     L1CSR_OP_COMPACT = 5,
     L1CSR_OP_SOFTMAX_XENT = 6,
     L1CSR_OP_PROX_RECOMPRESS = 7,
-    L1CSR_OP_DENSE_WGRAD = 8
+    L1CSR_OP_DENSE_WGRAD = 8,
+    L1CSR_OP_WGRAD_PROX = 9    /* dense_wgrad_prox, fp32 (other precisions need none) */
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -262,6 +263,57 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
                        int32_t *row_ptr_out, int32_t *col_idx_out, float *vals_out,
                        int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The l1-phase weight update of Eq. (prox) with the layer's minibatch
+ * gradient, without storing the gradient:
+ *     dW = dY . X^T                      (as dense_wgrad with `precision`)
+ *     Z  = S_t(W - eta * dW),  t = eta * lambda   (as prox_l1_step, dense mode)
+ * The GEMM's epilogue applies the soft threshold to its own result, reading W
+ * through its bitmap index (csr_bitmap_build: mask, pos), and also writes
+ * word_counts[i][w] = the number of nonzero Z[i][32w .. 32w + 32), the input
+ * of csr_recompress_counted (so the recompression reads Z once and never W).
+ * Z is bit-identical to dense_wgrad + prox_l1_step.
+ * dY [N][ldy], X [K][ldx], W (N x K CSR with nnz entries), mask / pos
+ * [N][ceil(K/32)] (read), Z [N][ldz] (ldz >= K) and word_counts
+ * [N][ceil(K/32)] (written); the outputs must be disjoint from each other
+ * and from every input (L1CSR_EINVAL).  ws as
+ * l1csr_workspace_bytes(L1CSR_OP_WGRAD_PROX, N, K, nnz, B) for fp32 (0 unless
+ * the product splits its reduction: few output tiles, a long batch).
+ */
+int dense_wgrad_prox(int32_t N, int32_t K, int32_t B,
+                     const float *dY, int64_t ldy, const float *X, int64_t ldx, int precision,
+                     int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                     const uint32_t *mask, const int32_t *pos, float eta, float lambda,
+                     float *Z, int64_t ldz, int32_t *word_counts, void *ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/*
+ * Dense -> CSR (Section 3.1) from the per-word nonzero counts that
+ * dense_wgrad_prox wrote with Z: keeps the nonzero Z entries (|Z| > 0) in
+ * row-major order, bit-identical to csr_recompress(Z, t = 0).  Row pointers
+ * come from the counts (row sums and their exclusive scan), so Z is read once.
+ * row_ptr_out [n_rows+1], col_idx_out / vals_out [capacity]; capacity,
+ * d_nnz_out and h_nnz_required behave as in csr_recompress.  The outputs
+ * must not overlap each other, Z, the counts or ws.  ws holds
+ * l1csr_workspace_bytes(L1CSR_OP_RECOMPRESS, n_rows, n_cols, 0, 0) bytes.
+ */
+int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz,
+                           const int32_t *word_counts, int32_t *row_ptr_out, int32_t *col_idx_out,
+                           float *vals_out, int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                           void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Bitmap index of W's pattern (the CSR of Section 3.1 seen by 32-column
+ * words), read by dense_wgrad_prox to find w_ik for every (i, k):
+ *     mask[i][w] bit c = 1 iff W stores (i, 32w + c)
+ *     pos[i][w]  = CSR position of row i's first entry with column >= 32w
+ *                  (row_ptr[i + 1] if there is none)
+ * for 0 <= w < ceil(n_cols / 32); both [n_rows][ceil(n_cols / 32)],
+ * caller-owned, disjoint.  Deterministic; depends only on the pattern.
+ */
+int csr_bitmap_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                     const int32_t *col_idx, uint32_t *mask, int32_t *pos, hipStream_t stream);
 
 /*
  * prox_l1_recompress for callers that cannot allocate memory (code under HIP

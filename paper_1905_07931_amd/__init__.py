@@ -20,7 +20,8 @@ __all__ = [
     "softmax_xent", "PROX_DENSE", "PROX_CSR", "F32", "BF16", "BF16X3",
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
     "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
-    "l1_step", "side_stream", "prox_l1_recompress_noalloc",
+    "l1_step", "side_stream", "prox_l1_recompress_noalloc", "dense_wgrad_prox", "csr_recompress_counted",
+    "dense_wgrad_prox_recompress", "csr_bitmap_build", "Bitmap",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
@@ -33,6 +34,7 @@ SOLVER_RMSPROP, SOLVER_ADAM = 1, 2
 OP_CSC_BUILD, OP_RECOMPRESS, OP_SDDMM, OP_SPMM, OP_COMPACT, OP_SOFTMAX_XENT = 1, 2, 3, 4, 5, 6
 OP_PROX_RECOMPRESS = 7
 OP_DENSE_WGRAD = 8
+OP_WGRAD_PROX = 9
 
 
 class L1CSRError(RuntimeError):
@@ -72,6 +74,11 @@ def lib():
                                          i64, vp, C.POINTER(C.c_int64), vp, sz, vp]
         L.prox_l1_recompress_noalloc.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, f32, f32, vp, vp,
                                                  vp, i64, vp, C.POINTER(C.c_int64), vp]
+        L.dense_wgrad_prox.argtypes = [i32, i32, i32, vp, i64, vp, i64, C.c_int, i64, vp, vp, vp, vp, vp, f32, f32,
+                                       vp, i64, vp, vp, sz, vp]
+        L.csr_recompress_counted.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, i64, vp, C.POINTER(C.c_int64),
+                                             vp, sz, vp]
+        L.csr_bitmap_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp]
         L.prox_adaptive_step.argtypes = [C.c_int, C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp,
                                          i64, f32, f32, f32, f32, f32, i64, vp, i64, vp, vp, sz, vp]
         L.prox_adaptive_recompress.argtypes = [C.c_int, i32, i32, i64, vp, vp, vp, vp, i64, vp, vp, i64,
@@ -88,7 +95,7 @@ def lib():
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
         for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
-                     "prox_l1_recompress_noalloc",
+                     "prox_l1_recompress_noalloc", "dense_wgrad_prox", "csr_recompress_counted", "csr_bitmap_build",
                      "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent",
                      "prox_adaptive_step", "prox_adaptive_recompress", "csr_conv_fwd",
                      "csr_conv_bwd_data", "conv_im2col", "l1csr_maxpool_fwd"):
@@ -446,6 +453,99 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
                                 _stream(stream)), "csr_recompress")
     _set_nnz(out, need.value, stream)
     return out
+
+
+@dataclass
+class Bitmap:
+    """Bitmap index of a CSR pattern: mask / pos [n_rows][ceil(n_cols / 32)]
+    (csr_bitmap_build)."""
+    mask: "object"
+    pos: "object"
+
+    @staticmethod
+    def empty(n_rows, n_cols, device):
+        torch = _torch()
+        kw = max((n_cols + 31) // 32, 1)
+        return Bitmap(torch.empty((max(n_rows, 1), kw), dtype=torch.int32, device=device),
+                      torch.empty((max(n_rows, 1), kw), dtype=torch.int32, device=device))
+
+
+def csr_bitmap_build(W: CSR, bm: Bitmap | None = None, stream=None) -> Bitmap:
+    """W's bitmap index for dense_wgrad_prox_recompress (depends on the pattern only)."""
+    nnz = W.validate_shapes()
+    if bm is None:
+        bm = Bitmap.empty(W.n_rows, W.n_cols, W.row_ptr.device)
+    kw = (W.n_cols + 31) // 32
+    for t_ in (bm.mask, bm.pos):
+        if not t_.is_contiguous() or t_.numel() < W.n_rows * kw:
+            raise ValueError("bitmap arrays must be contiguous with n_rows * ceil(n_cols / 32) entries")
+    _check(lib().csr_bitmap_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(bm.mask),
+                                  _p(bm.pos), _stream(stream)), "csr_bitmap_build")
+    return bm
+
+
+def dense_wgrad_prox(W: CSR, dY, X, eta, lam, bitmap: Bitmap, Z=None, word_counts=None, precision=F32,
+                     stream=None):
+    """Z = S_{eta*lam}(W - eta * dY.X^T) ([N][K], dW never stored) and the
+    nonzero count of every 32-column word of Z's rows ([N][ceil(K/32)]), one
+    GEMM launch; W read through its bitmap index.  Returns (Z, word_counts)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    N, B, ldy = _mat(dY, "dY")
+    K, Bx, ldx = _mat(X, "X")
+    if (N, K) != (W.n_rows, W.n_cols) or Bx != B:
+        raise ValueError("dY must be [N][B] and X [K][B] for an N x K layer")
+    dev = dY.device
+    if Z is None:
+        Z = torch.empty((N, K), dtype=torch.float32, device=dev)
+    rz, cz, ldz = _mat(Z, "Z")
+    if (rz, cz) != (N, K):
+        raise ValueError("Z must be [N][K]")
+    kw = (K + 31) // 32
+    if word_counts is None:
+        word_counts = torch.empty((max(N, 1), max(kw, 1)), dtype=torch.int32, device=dev)
+    if not word_counts.is_contiguous() or word_counts.numel() < N * kw:
+        raise ValueError("word_counts must be contiguous with N * ceil(K/32) entries")
+    ws, wsb = (None, 0)
+    if precision == F32:
+        ws, wsb = _workspace(workspace_bytes(OP_WGRAD_PROX, N, K, nnz, B), dev, stream)
+    _check(lib().dense_wgrad_prox(N, K, B, _p(dY), ldy, _p(X), ldx, int(precision), nnz, _p(W.row_ptr),
+                                  _p(W.col_idx), _p(W.vals), _p(bitmap.mask), _p(bitmap.pos), float(eta), float(lam),
+                                  _p(Z), ldz, _p(word_counts), _p(ws), wsb, _stream(stream)), "dense_wgrad_prox")
+    return Z, word_counts
+
+
+def csr_recompress_counted(Z, word_counts, out: CSR | None = None, capacity=None, stream=None) -> CSR:
+    """Z -> CSR of its nonzeros using dense_wgrad_prox's word counts (Z read once)."""
+    torch = _torch()
+    N, K, ldz = _mat(Z, "Z")
+    dev = Z.device
+    if out is None:
+        cap = N * K if capacity is None else int(capacity)
+        out = CSR(N, K, torch.empty(N + 1, dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.int32, device=dev),
+                  torch.empty(max(cap, 1), dtype=torch.float32, device=dev), None)
+    cap = min(out.col_idx.numel(), out.vals.numel()) if capacity is None else int(capacity)
+    ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev, stream)
+    need = C.c_int64(-1)
+    _check(lib().csr_recompress_counted(N, K, _p(Z), ldz, _p(word_counts), _p(out.row_ptr), _p(out.col_idx),
+                                        _p(out.vals), cap, None, C.byref(need), _p(ws), wsb, _stream(stream)),
+           "csr_recompress_counted")
+    _set_nnz(out, need.value, stream)
+    return out
+
+
+def dense_wgrad_prox_recompress(W: CSR, dY, X, eta, lam, Z=None, out: CSR | None = None,
+                                precision=F32, capacity=None, bitmap: Bitmap | None = None, stream=None):
+    """The whole l1 update: csr_bitmap_build (unless `bitmap` is given),
+    dense_wgrad_prox and csr_recompress_counted, in that order on `stream`.
+    Z = S_{eta*lam}(W - eta * dY.X^T) and W' = CSR(Z), bit for bit as
+    dense_wgrad + prox_l1_step + csr_recompress.  Returns (Z, out)."""
+    if bitmap is None:
+        bitmap = csr_bitmap_build(W, stream=stream)
+    Z, wc = dense_wgrad_prox(W, dY, X, eta, lam, bitmap, Z=Z, precision=precision, stream=stream)
+    out = csr_recompress_counted(Z, wc, out=out, capacity=capacity, stream=stream)
+    return Z, out
 
 
 def prox_l1_recompress_noalloc(W: CSR, G, eta, lam, out: CSR, capacity=None, stream=None):

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libl1csr.so")
 
-SOURCES = ["abi.hip", "spmm.hip", "csc.hip", "scan.hip", "gemm.hip", "wgrad_bf16.hip", "wgrad_bf16x3.hip", "sddmm.hip",
+SOURCES = ["abi.hip", "spmm.hip", "csc.hip", "scan.hip", "gemm.hip", "wgrad_bf16.hip", "wgrad_bf16x3.hip", "wgrad_prox.hip", "sddmm.hip",
            "prox.hip", "prox_adaptive.hip", "recompress.hip", "conv.hip", "glue.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

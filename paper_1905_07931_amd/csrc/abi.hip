@@ -249,6 +249,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
         case L1CSR_OP_PROX_RECOMPRESS: return round_up(prox_recompress_workspace_bytes(n_rows, n_cols));
         case L1CSR_OP_DENSE_WGRAD: return round_up(wgrad_workspace_bytes(n_rows, n_cols, B));
+        case L1CSR_OP_WGRAD_PROX: return round_up(wgrad_prox_split_bytes(n_rows, n_cols, B, L1CSR_F32));
         case L1CSR_OP_SOFTMAX_XENT: return round_up(sizeof(float) * (size_t)(ceil_div(B, 256) + 1));
         default: return 0;
     }
@@ -431,6 +432,98 @@ int prox_l1_recompress_noalloc(int32_t n_rows, int32_t n_cols, int64_t nnz, cons
     return prox_recompress_run(n_rows, n_cols, nnz, row_ptr, col_idx, vals, G, ldg, eta, lambda,
                                row_ptr_out, col_idx_out, vals_out, capacity, d_nnz_out, h_nnz_required, ws,
                                stream);
+}
+
+int dense_wgrad_prox(int32_t N, int32_t K, int32_t B, const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                     int precision, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                     const uint32_t *mask, const int32_t *pos, float eta, float lambda, float *Z, int64_t ldz,
+                     int32_t *word_counts, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (N < 0 || K < 0 || B < 0) return L1CSR_EINVAL;
+    if (precision != L1CSR_F32 && precision != L1CSR_BF16 && precision != L1CSR_BF16X3) return L1CSR_EINVAL;
+    if (!finite_f(eta) || !finite_f(lambda) || eta <= 0.f || lambda < 0.f) return L1CSR_EINVAL;
+    if (bad_csr(N, K, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
+    if (bad_dense(dY, N, B, ldy) || bad_dense(X, K, B, ldx) || bad_dense(Z, N, K, ldz)) return L1CSR_EINVAL;
+    if ((int64_t)N * K > 0 && (mask == nullptr || pos == nullptr || word_counts == nullptr)) return L1CSR_EINVAL;
+    if ((int64_t)N * K > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 positions in the bitmap index
+    if (ceil_div(N, 128) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    const size_t split = wgrad_prox_split_bytes(N, K, B, precision);
+    if (split > 0 && (ws == nullptr || ws_bytes < split)) return L1CSR_EINVAL;
+    {  // the outputs Z and word_counts apart from each other and from every input
+        const size_t wc = word_counts_bytes(N, K), in = sizeof(int32_t) * (size_t)nnz;
+        const void *outs[2] = {Z, word_counts};
+        const size_t ob[2] = {dense_bytes(N, K, ldz), wc};
+        const void *ins[7] = {dY, X, row_ptr, col_idx, vals, mask, pos};
+        const size_t ib[7] = {dense_bytes(N, B, ldy), dense_bytes(K, B, ldx), sizeof(int32_t) * ((size_t)N + 1), in,
+                              in, wc, wc};
+        if (bytes_overlap(outs[0], ob[0], outs[1], ob[1])) return L1CSR_EINVAL;
+        for (int o = 0; o < 2; ++o)
+            for (int i = 0; i < 7; ++i)
+                if (bytes_overlap(outs[o], ob[o], ins[i], ib[i])) return L1CSR_EINVAL;
+    }
+    const double t = (double)eta * (double)lambda;  // exact in double
+    return hip_status(launch_wgrad_prox(N, K, B, dY, ldy, X, ldx, precision, vals,
+                                        reinterpret_cast<const unsigned *>(mask), pos, eta, t, Z, ldz, word_counts,
+                                        split > 0 ? ws : nullptr, stream));
+}
+
+int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64_t ldz,
+                           const int32_t *word_counts, int32_t *row_ptr_out, int32_t *col_idx_out,
+                           float *vals_out, int64_t capacity, int32_t *d_nnz_out, int64_t *h_nnz_required,
+                           void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n_rows < 0 || n_cols < 0 || capacity < 0) return L1CSR_EINVAL;
+    const int64_t total = (int64_t)n_rows * (int64_t)n_cols;
+    if (total > INT32_MAX) return L1CSR_EUNSUPPORTED;  // int32 row pointers
+    if (bad_dense(Z, n_rows, n_cols, ldz) || row_ptr_out == nullptr) return L1CSR_EINVAL;
+    if (total > 0 && word_counts == nullptr) return L1CSR_EINVAL;
+    if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < sizeof(int) * ((size_t)n_rows + 1))) return L1CSR_EINVAL;
+    {  // outputs apart from each other and from Z and the counts
+        const size_t cap = sizeof(int32_t) * (size_t)capacity, rp = sizeof(int32_t) * ((size_t)n_rows + 1);
+        const void *outs[3] = {row_ptr_out, col_idx_out, vals_out};
+        const size_t ob[3] = {rp, cap, cap};
+        const void *ins[3] = {Z, word_counts, ws};
+        const size_t ib[3] = {dense_bytes(n_rows, n_cols, ldz), word_counts_bytes(n_rows, n_cols), rp};
+        for (int o = 0; o < 3; ++o) {
+            for (int q = o + 1; q < 3; ++q)
+                if (bytes_overlap(outs[o], ob[o], outs[q], ob[q])) return L1CSR_EINVAL;
+            for (int i = 0; i < 3; ++i)
+                if (bytes_overlap(outs[o], ob[o], ins[i], ib[i])) return L1CSR_EINVAL;
+        }
+    }
+    hipError_t e;
+    if (total == 0) {  // no weights: an empty CSR
+        e = launch_fill_i32(row_ptr_out, (int64_t)n_rows + 1, 0, stream);
+        if (e == hipSuccess && d_nnz_out) e = launch_fill_i32(d_nnz_out, 1, 0, stream);
+        if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
+        return hip_status(e);
+    }
+    e = launch_counted_row_ptr(n_rows, n_cols, word_counts, static_cast<int *>(ws), row_ptr_out, stream);
+    if (e != hipSuccess) return L1CSR_EHIP;
+    if (capacity < total) {
+        int32_t h = 0;
+        e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+        if (h_nnz_required) *h_nnz_required = h;
+        if (h > capacity) {
+            if (d_nnz_out) launch_copy_i32(row_ptr_out + n_rows, d_nnz_out, stream);
+            return L1CSR_ECAPACITY;
+        }
+    } else if (h_nnz_required) {
+        *h_nnz_required = -1;
+    }
+    return hip_status(launch_counted_compact(n_rows, n_cols, Z, ldz, word_counts, row_ptr_out, col_idx_out, vals_out,
+                                             capacity, d_nnz_out, stream));
+}
+
+int csr_bitmap_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
+                     const int32_t *col_idx, uint32_t *mask, int32_t *pos, hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, nullptr, false)) return L1CSR_EINVAL;
+    if ((int64_t)n_rows * n_cols > 0 && (mask == nullptr || pos == nullptr)) return L1CSR_EINVAL;
+    const size_t bm = sizeof(int32_t) * (size_t)n_rows * (size_t)ceil_div(n_cols, 32);
+    if (bytes_overlap(mask, bm, pos, bm)) return L1CSR_EINVAL;
+    return hip_status(launch_bitmap(n_rows, n_cols, row_ptr, col_idx, reinterpret_cast<unsigned *>(mask), pos,
+                                    stream));
 }
 
 int prox_adaptive_step(int mode, int solver, int32_t n_rows, int32_t n_cols, int64_t nnz,

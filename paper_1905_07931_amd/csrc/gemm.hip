@@ -24,12 +24,11 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "prox_epilogue.hpp"
 
 namespace l1csr {
 
 namespace {
-
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 32;
 constexpr int LDS_STRIDE = BK + 4;  // 36 floats: conflict-free 16-byte fragment reads
@@ -153,14 +152,28 @@ __device__ __forceinline__ int acc_col(int b) {
     return (wave & 1) * 64 + b * 32 + (lane & 31);
 }
 
-template <bool V4>
+// PROX: the epilogue writes Z = S_t(W - eta*dW) and the per-(row, 64-column
+// slab) counts instead of dW (prox_epilogue.hpp)
+template <bool V4, bool PROX>
 __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_mfma_kernel(
     int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
-    int64_t ldb, float *__restrict__ C, int64_t ldc) {
+    int64_t ldb, float *__restrict__ C, int64_t ldc, prox_epi P) {
     __shared__ __attribute__((aligned(16))) tile_smem sm;
     const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
     floatx16 acc[2][2];
     mfma_tile<V4>(M, Nn, Kr, A, lda, Bt, ldb, m0, n0, sm, acc);
+    if constexpr (PROX) {
+        // the tile loop ended with a barrier: the operand buffers are free
+        static_assert(sizeof(sm.ab.As) >= sizeof(int2) * BM * (BN / 32), "staging space");
+        int2 *stage = reinterpret_cast<int2 *>(sm.ab.As);
+        prox_stage<BM, BN, kThreads>(P, M, m0, n0, stage);
+        const int wave = threadIdx.x >> 6;
+        constexpr int TPB = 2;  // MFMA tiles per gather batch: 8 KB of LDS per wave
+        static_assert(sizeof(sm.ab.Bs) >= sizeof(float) * 16 * TPB * kThreads, "gather space");
+        float *gbuf = &sm.ab.Bs[0][0] + wave * 16 * TPB * kWave;
+        prox_store<2, BN, TPB>(acc, M, Nn, m0, n0, (wave >> 1) * 64, (wave & 1) * 64, stage, gbuf, C, ldc, P);
+        return;
+    }
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -215,10 +228,10 @@ __device__ __forceinline__ void store_rows(float *lds, const float4 (&r)[(ROWS *
     }
 }
 
-template <bool V4>
+template <bool V4, bool PROX>
 __global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_large_kernel(
     int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
-    int64_t ldb, float *__restrict__ C, int64_t ldc) {
+    int64_t ldb, float *__restrict__ C, int64_t ldc, prox_epi P) {
     constexpr int TM = LBM / LWM / 32, TN = LBN / LWN / 32;
     constexpr int LA = (LBM * BK / 4 + kLargeThreads - 1) / kLargeThreads;
     constexpr int LB = (LBN * BK / 4 + kLargeThreads - 1) / kLargeThreads;
@@ -280,6 +293,21 @@ __global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_large_kernel(
             store_rows<LBN>(Bs[buf ^ 1], rb);
         }
         __syncthreads();
+    }
+    if constexpr (PROX) {
+        // the last chunk ended with a barrier: the operand buffers are free
+        static_assert(TM == 2 && sizeof(As) >= sizeof(int2) * LBM * (LBN / 32), "staging space");
+        int2 *stage = reinterpret_cast<int2 *>(&As[0][0]);
+        prox_stage<LBM, LBN, kLargeThreads>(P, M, m0, n0, stage);
+        // gather buffers of 2 MFMA tiles (8 KB) per wave: waves 0-5 in the A
+        // buffers after the staged words, waves 6-11 in the B buffers
+        constexpr int TPB = 2, GBF = 16 * TPB * kWave;  // floats per wave
+        constexpr int kStageFloats = 2 * LBM * (LBN / 32);
+        static_assert(sizeof(As) >= sizeof(float) * (kStageFloats + 6 * GBF) && sizeof(Bs) >= sizeof(float) * 6 * GBF &&
+                      LWM * LWN == 12, "gather space");
+        float *gbuf = wave < 6 ? &As[0][0] + kStageFloats + wave * GBF : &Bs[0][0] + (wave - 6) * GBF;
+        prox_store<TN, LBN, TPB>(acc, M, Nn, m0, n0, wm, wn, stage, gbuf, C, ldc, P);
+        return;
     }
     // D layout of the 32x32 MFMA (acc_row / acc_col for this wave grid)
 #pragma unroll
@@ -349,6 +377,30 @@ __global__ void wgrad_reduce_kernel(int M, int Nn, int S, const float *__restric
     }
 }
 
+// the 256x288 shape where its modelled time is shorter
+bool f32_large(int N, int K, int B) {
+    return tile_model_us(N, K, B, LBM, LBN, kLargeRate) < tile_model_us(N, K, B, BM, BN, kSmallRate);
+}
+
+template <bool PROX>
+hipError_t launch_f32_tiles(int N, int K, int B, const float *dY, int64_t ldy, const float *X, int64_t ldx,
+                            float *C, int64_t ldc, bool v4, const prox_epi &P, hipStream_t s) {
+    if (f32_large(N, K, B)) {
+        dim3 grid((unsigned)ceil_div(K, LBN), (unsigned)ceil_div(N, LBM));
+        if (v4)
+            wgrad_f32_large_kernel<true, PROX><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
+        else
+            wgrad_f32_large_kernel<false, PROX><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
+        return hipGetLastError();
+    }
+    dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
+    if (v4)
+        wgrad_f32_mfma_kernel<true, PROX><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
+    else
+        wgrad_f32_mfma_kernel<false, PROX><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 wgrad_split wgrad_plan(int N, int K, int B) {
@@ -389,20 +441,19 @@ hipError_t launch_wgrad_f32(int N, int K, int B, const float *dY, int64_t ldy, c
         wgrad_reduce_kernel<<<rgrid, 256, 0, s>>>(N, K, p.splits, P, dW, ldw);
         return hipGetLastError();
     }
-    if (tile_model_us(N, K, B, LBM, LBN, kLargeRate) < tile_model_us(N, K, B, BM, BN, kSmallRate)) {
-        dim3 grid((unsigned)ceil_div(K, LBN), (unsigned)ceil_div(N, LBM));
-        if (v4)
-            wgrad_f32_large_kernel<true><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
-        else
-            wgrad_f32_large_kernel<false><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
-        return hipGetLastError();
-    }
-    dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
-    if (v4)
-        wgrad_f32_mfma_kernel<true><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
-    else
-        wgrad_f32_mfma_kernel<false><<<grid, kThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, dW, ldw);
-    return hipGetLastError();
+    return launch_f32_tiles<false>(N, K, B, dY, ldy, X, ldx, dW, ldw, v4, prox_epi{}, s);
+}
+
+int wgrad_f32_prox_slab(int N, int K, int B) {
+    if (wgrad_plan(N, K, B).splits > 1) return 0;
+    return f32_large(N, K, B) ? LBN / LWN : BN / 2;
+}
+
+hipError_t launch_wgrad_f32_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                                 int64_t ldx, float *Z, int64_t ldz, const prox_epi &P, hipStream_t s) {
+    if (N == 0 || K == 0) return hipSuccess;
+    const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
+    return launch_f32_tiles<true>(N, K, B, dY, ldy, X, ldx, Z, ldz, v4, P, s);
 }
 
 }  // namespace l1csr

@@ -40,6 +40,8 @@ hipError_t launch_csc_gather_vals(int n_cols, int64_t nnz_bound, const int *col_
 // optionally also writes the total to *total_out.
 hipError_t launch_exclusive_scan(const int *in, int *out, int n, int *total_out, hipStream_t s);
 hipError_t launch_fill_i32(int *p, int64_t n, int v, hipStream_t s);
+// *dst = *src in stream order (one device int; capture-safe, no memcpy node)
+hipError_t launch_copy_i32(const int *src, int *dst, hipStream_t s);
 hipError_t launch_fill_f32(float *p, int64_t n, float v, hipStream_t s);
 hipError_t launch_fill_rows_f32(float *p, int64_t rows, int64_t cols, int64_t ld, float v,
                                 hipStream_t s);
@@ -61,6 +63,42 @@ hipError_t launch_wgrad_bf16(int N, int K, int B, const float *dY, int64_t ldy, 
 // the same with operands split into bf16 hi + lo, three products (wgrad_bf16x3.hip)
 hipError_t launch_wgrad_bf16x3(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                                int64_t ldx, float *dW, int64_t ldw, hipStream_t s);
+
+// wgrad_prox.hip / the GEMMs' prox epilogue (prox_epilogue.hpp) ------------
+struct prox_epi;
+// columns per counted slab of the fp32 / split-bf16 GEMM with the prox
+// epilogue at this shape (0: the fp32 product would split its reduction,
+// which has no such epilogue)
+int wgrad_f32_prox_slab(int N, int K, int B);
+int wgrad_bf16x3_prox_slab(int N, int K, int B);
+// dense_wgrad precision codes (the ABI's l1csr_precision)
+constexpr int kPrecF32 = 0, kPrecBF16 = 1, kPrecBF16X3 = 2;
+// Z = S_t(W - eta * dY.X^T) and P.counts, in one GEMM launch
+hipError_t launch_wgrad_f32_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                                 int64_t ldx, float *Z, int64_t ldz, const prox_epi &P, hipStream_t s);
+hipError_t launch_wgrad_bf16x3_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                                    int64_t ldx, float *Z, int64_t ldz, const prox_epi &P, hipStream_t s);
+// the l1 update in two calls (wgrad_prox.hip):
+//   launch_wgrad_prox: Z and the per-(row, 32-column word) nonzero counts
+//     (counts [N][ceil(K / 32)]) from W's bitmap index (mask / pos); split_ws
+//     holds wgrad_prox_split_bytes() (fp32 products that split their batch);
+//   launch_counted_row_ptr: row_ptr_out (row_ptr_out[N] = nnz') from the
+//     counts, row_counts holding N + 1 ints;
+//   launch_counted_compact: col_out / val_out (< capacity), nnz' to d_nnz_out.
+size_t word_counts_bytes(int N, int K);
+size_t wgrad_prox_split_bytes(int N, int K, int B, int precision);
+hipError_t launch_wgrad_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                             int64_t ldx, int precision, const float *vals, const unsigned *mask, const int *pos,
+                             float eta, double t, float *Z, int64_t ldz, int *counts, void *split_ws,
+                             hipStream_t s);
+hipError_t launch_counted_row_ptr(int N, int K, const int *counts, int *row_counts, int *row_ptr_out,
+                                  hipStream_t s);
+hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts,
+                                  const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
+                                  int *d_nnz_out, hipStream_t s);
+// bitmap index of a CSR pattern: mask / pos [n_rows][ceil(n_cols / 32)]
+hipError_t launch_bitmap(int n_rows, int n_cols, const int *ptr, const int *idx, unsigned *mask, int *pos,
+                         hipStream_t s);
 // sddmm.hip ----------------------------------------------------------------
 // gv[p] = sum_b dY[row(p)][b] X[col(p)][b]; ws holds sddmm_workspace_bytes()
 size_t sddmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B);

@@ -10,6 +10,7 @@
 // loads; Z is written and the nonzeros of the row are counted.
 #include "common.hpp"
 #include "launch.hpp"
+#include "prox_epilogue.hpp"
 
 namespace l1csr {
 
@@ -17,12 +18,6 @@ namespace {
 
 constexpr int kProxThreads = 256;
 constexpr int kProxTile = 8192;  // columns per LDS pass (32 KB)
-
-__device__ __forceinline__ float soft_threshold(float w, float g, double eta, double t) {
-    const double z = (double)w - eta * (double)g;
-    const double s = z > t ? z - t : (z < -t ? z + t : 0.0);
-    return (float)s;
-}
 
 template <bool V4>
 __global__ __launch_bounds__(kProxThreads) void prox_dense_kernel(

@@ -1,0 +1,122 @@
+// The proximal step of Eq. (prox) applied in a weight-gradient GEMM's
+// epilogue: instead of dW the kernel writes
+//     Z[i][k] = S_t(w_ik - eta * dW[i][k]),  t = eta * lambda,
+// and the number of nonzero Z entries of every 32-column word of every row,
+// so that the recompression that follows reads Z once and never W.
+//
+// W's value at (i, k) comes from a bitmap index of its CSR built before the
+// GEMM: for every row and 32-column word, mask (bit c set iff column 32w + c
+// is stored) and pos (CSR position of the row's first entry with column >=
+// 32w), so w_ik = vals[pos + popcount(mask & below(c))] if the bit is set,
+// else 0.  The tile's mask/pos words are staged in LDS once the reduction is
+// done, and the stored values are gathered straight into LDS.
+//
+// The arithmetic is that of the prox kernels (prox.hip): double, eta*g exact,
+// z rounds once, S_t(z) once more to float; zero results are +0.0; an entry
+// is kept iff its float result is nonzero.
+#pragma once
+
+#include "common.hpp"
+
+namespace l1csr {
+
+__device__ __forceinline__ float soft_threshold(float w, float g, double eta, double t) {
+    const double z = (double)w - eta * (double)g;
+    const double s = z > t ? z - t : (z < -t ? z + t : 0.0);
+    return (float)s;
+}
+
+// kernel argument of a GEMM with the prox epilogue
+struct prox_epi {
+    const unsigned *mask;  // [M][kw]
+    const int *pos;        // [M][kw]
+    const float *vals;     // W's values (CSR order)
+    double eta, t;
+    int kw;                // 32-column words per row, ceil(Nn / 32)
+    int *counts;           // [M][kw] nonzero Z entries per (row, word)
+};
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// Stage the tile's mask/pos words (rows m0 .. m0+BM, words n0/32 .. n0/32 +
+// BN/32) into LDS; all NT threads of the workgroup call it (it ends with a
+// barrier).  stage holds BM * BN / 32 int2.
+template <int BM, int BN, int NT>
+__device__ __forceinline__ void prox_stage(const prox_epi &P, int M, int m0, int n0, int2 *stage) {
+    constexpr int WPT = BN / 32;
+    const int w0 = n0 >> 5;
+    for (int i = threadIdx.x; i < BM * WPT; i += NT) {
+        const int r = i / WPT, w = i - r * WPT;
+        const int row = m0 + r, gw = w0 + w;
+        int2 v = make_int2(0, 0);
+        if (row < M && gw < P.kw) {
+            const int64_t o = (int64_t)row * P.kw + gw;
+            v = make_int2((int)P.mask[o], P.pos[o]);
+        }
+        stage[i] = v;
+    }
+    __syncthreads();
+}
+
+typedef __attribute__((address_space(3))) void prox_lds_void;
+
+// The epilogue of one wave holding a (2*32) x (TN*32) block of the tile at
+// (m0 + wm, n0 + wn) in the D layout of the 32x32 MFMAs: lane l, register r
+// of MFMA tile (a, b) holds row 32a + 8(r/4) + 4(l/32) + r%4, column
+// 32b + l%32.  W's values are gathered TPB MFMA tiles (16*TPB registers) at a
+// time with direct global->LDS loads into this wave's buffer gbuf (lane l's
+// value of register j of the batch at gbuf[j*64 + l]), so a batch costs one
+// memory round trip and no registers; then the batch is thresholded, stored
+// and counted (ballots over the lanes of each row half; lane l accumulates
+// the counts of the wave's row l, one per 32-column word).
+template <int TN, int BN, int TPB>
+__device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, int Nn, int m0, int n0,
+                                           int wm, int wn, const int2 *stage, float *gbuf,
+                                           float *__restrict__ C, int64_t ldc, const prox_epi &P) {
+    constexpr int WPT = BN / 32, NTILE = 2 * TN;
+    static_assert(NTILE % TPB == 0, "batches of whole MFMA tiles");
+    const int lane = threadIdx.x & 63;
+    const int lr = lane & 31, lh = lane >> 5;
+    const unsigned below = (1u << lr) - 1u;
+    int mine[TN] = {};  // this lane's counts (wave row `lane`) per word of the block
+#pragma unroll
+    for (int q0 = 0; q0 < NTILE; q0 += TPB) {
+        uint64_t smask = 0;  // bit j: register j of the batch holds a stored weight
+#pragma unroll
+        for (int j = 0; j < 16 * TPB; ++j) {
+            const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
+            const int rt = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+            const int2 mp = stage[(wm + rt) * WPT + ((wn >> 5) + b)];
+            const unsigned m = (unsigned)mp.x;
+            if ((m >> lr) & 1u) {
+                smask |= 1ull << j;
+                __builtin_amdgcn_global_load_lds((const void *)(P.vals + mp.y + __popc(m & below)),
+                                                 (prox_lds_void *)(gbuf + j * kWave), 4, 0, 0);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the gathered values are in LDS
+#pragma unroll
+        for (int j = 0; j < 16 * TPB; ++j) {
+            const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
+            const int col = n0 + wn + b * 32 + lr;
+            const int rt = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // row inside the wave block
+            const int row = m0 + wm + rt;
+            const float w = (smask >> j) & 1u ? gbuf[j * kWave + lane] : 0.f;
+            const float o = soft_threshold(w, acc[a][b][r], P.eta, P.t);
+            const bool valid = row < M && col < Nn;
+            if (valid) C[(int64_t)row * ldc + col] = o;
+            const uint64_t k = __ballot(valid && o != 0.f);
+            // wave rows rt(lh = 0) = rt0 and rt(lh = 1) = rt0 + 4
+            const int rt0 = a * 32 + 8 * (r >> 2) + (r & 3);
+            mine[b] += lane == rt0 ? __popcll(k & 0xffffffffull) : (lane == rt0 + 4 ? __popcll(k >> 32) : 0);
+        }
+    }
+    const int row = m0 + wm + lane;
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+        const int word = ((n0 + wn) >> 5) + b;
+        if (row < M && word < P.kw) P.counts[(int64_t)row * P.kw + word] = mine[b];
+    }
+}
+
+}  // namespace l1csr

@@ -92,6 +92,10 @@ __global__ void fill_rows_f32_kernel(float *p, int64_t rows, int64_t cols, int64
     }
 }
 
+__global__ void copy_i32_kernel(const int *src, int *dst) {
+    if (threadIdx.x == 0) *dst = *src;
+}
+
 unsigned fill_grid(int64_t n) {
     int64_t g = ceil_div(n, 256);
     if (g > 65536) g = 65536;
@@ -109,6 +113,11 @@ hipError_t launch_exclusive_scan(const int *in, int *out, int n, int *total_out,
 hipError_t launch_fill_i32(int *p, int64_t n, int v, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     fill_i32_kernel<<<fill_grid(n), 256, 0, s>>>(p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_i32(const int *src, int *dst, hipStream_t s) {
+    copy_i32_kernel<<<1, 64, 0, s>>>(src, dst);
     return hipGetLastError();
 }
 

@@ -27,12 +27,12 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "prox_epilogue.hpp"
 
 namespace l1csr {
 
 namespace {
 
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
@@ -85,10 +85,12 @@ __device__ __forceinline__ floatx16 mfma(bf16x8 a, bf16x8 b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-template <bool V4, int BM, int BN, int WM, int WN, int BK, int MINB>
+// PROX: the epilogue writes Z = S_t(W - eta*dW) and the per-(row, slab)
+// counts instead of dW (prox_epilogue.hpp)
+template <bool V4, int BM, int BN, int WM, int WN, int BK, int MINB, bool PROX>
 __global__ __launch_bounds__(64 * WM * WN, MINB) void wgrad_bf16x3_mfma_kernel(
     int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
-    int64_t ldb, float *__restrict__ C, int64_t ldc) {
+    int64_t ldb, float *__restrict__ C, int64_t ldc, prox_epi P) {
     constexpr int NT = 64 * WM * WN, TM = BM / WM / 32, TN = BN / WN / 32, STR = BK + 8;
     constexpr int LA = (BM * BK / 4 + NT - 1) / NT, LB = (BN * BK / 4 + NT - 1) / NT;
     static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN && BK % 16 == 0, "tile shape");
@@ -161,6 +163,22 @@ __global__ __launch_bounds__(64 * WM * WN, MINB) void wgrad_bf16x3_mfma_kernel(
         __syncthreads();
     }
 
+    if constexpr (PROX) {
+        // the last chunk ended with a barrier: the operand buffers are free
+        static_assert(TM == 2 && sizeof(Ah) >= sizeof(int2) * BM * (BN / 32), "staging space");
+        int2 *stage = reinterpret_cast<int2 *>(&Ah[0][0]);
+        prox_stage<BM, BN, NT>(P, M, m0, n0, stage);
+        // gather buffers of one MFMA tile (4 KB) per wave: half the waves in
+        // the bf16 hi tiles of B, half in the lo tiles
+        constexpr int GBF = 16 * kWave;
+        static_assert(sizeof(Bh) >= sizeof(float) * GBF * (NT / 128) && sizeof(Bl) >= sizeof(float) * GBF * (NT / 128),
+                      "gather space");
+        const int hw = wave % (NT / 128);
+        float *gbuf = (wave < NT / 128 ? reinterpret_cast<float *>(&Bh[0][0]) : reinterpret_cast<float *>(&Bl[0][0])) +
+                      hw * GBF;
+        prox_store<TN, BN, 1>(acc, M, Nn, m0, n0, wm, wn, stage, gbuf, C, ldc, P);
+        return;
+    }
     // D layout of the 32x32 MFMA: lane l, register r holds
     // row 8*(r/4) + 4*(l/32) + r%4, column l%32 of the 32x32 tile.
 #pragma unroll
@@ -186,15 +204,17 @@ struct x3_shape {
         const double tile_flops = 2.0 * BM * BN * (double)(B > 0 ? B : 1);
         return per_cu * tile_flops / (rate_tflops * 1e6 / kCUs);
     }
+    static constexpr int kSlab = 32 * (BN / WN / 32);  // a wave's columns
+    template <bool PROX>
     static hipError_t launch(int N, int K, int B, const float *dY, int64_t ldy, const float *X, int64_t ldx,
-                             float *dW, int64_t ldw, bool v4, hipStream_t s) {
+                             float *dW, int64_t ldw, bool v4, const prox_epi &P, hipStream_t s) {
         dim3 grid((unsigned)ceil_div(K, BN), (unsigned)ceil_div(N, BM));
         if (v4)
-            wgrad_bf16x3_mfma_kernel<true, BM, BN, WM, WN, BK, MINB><<<grid, 64 * WM * WN, 0, s>>>(
-                N, K, B, dY, ldy, X, ldx, dW, ldw);
+            wgrad_bf16x3_mfma_kernel<true, BM, BN, WM, WN, BK, MINB, PROX><<<grid, 64 * WM * WN, 0, s>>>(
+                N, K, B, dY, ldy, X, ldx, dW, ldw, P);
         else
-            wgrad_bf16x3_mfma_kernel<false, BM, BN, WM, WN, BK, MINB><<<grid, 64 * WM * WN, 0, s>>>(
-                N, K, B, dY, ldy, X, ldx, dW, ldw);
+            wgrad_bf16x3_mfma_kernel<false, BM, BN, WM, WN, BK, MINB, PROX><<<grid, 64 * WM * WN, 0, s>>>(
+                N, K, B, dY, ldy, X, ldx, dW, ldw, P);
         return hipGetLastError();
     }
 };
@@ -202,15 +222,31 @@ using x3_small = x3_shape<128, 128, 2, 2, 32, 2>;
 using x3_large = x3_shape<256, 288, 4, 3, 16, 1>;
 constexpr double kSmallRate = 283.0, kLargeRate = 355.0;
 
+bool x3_large_shape(int N, int K, int B) {
+    return x3_large::model_us(N, K, B, kLargeRate) < x3_small::model_us(N, K, B, kSmallRate);
+}
+
 }  // namespace
 
 hipError_t launch_wgrad_bf16x3(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                                int64_t ldx, float *dW, int64_t ldw, hipStream_t s) {
     if (N == 0 || K == 0) return hipSuccess;
     const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
-    if (x3_large::model_us(N, K, B, kLargeRate) < x3_small::model_us(N, K, B, kSmallRate))
-        return x3_large::launch(N, K, B, dY, ldy, X, ldx, dW, ldw, v4, s);
-    return x3_small::launch(N, K, B, dY, ldy, X, ldx, dW, ldw, v4, s);
+    if (x3_large_shape(N, K, B))
+        return x3_large::launch<false>(N, K, B, dY, ldy, X, ldx, dW, ldw, v4, prox_epi{}, s);
+    return x3_small::launch<false>(N, K, B, dY, ldy, X, ldx, dW, ldw, v4, prox_epi{}, s);
+}
+
+int wgrad_bf16x3_prox_slab(int N, int K, int B) {
+    return x3_large_shape(N, K, B) ? x3_large::kSlab : x3_small::kSlab;
+}
+
+hipError_t launch_wgrad_bf16x3_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                                    int64_t ldx, float *Z, int64_t ldz, const prox_epi &P, hipStream_t s) {
+    if (N == 0 || K == 0) return hipSuccess;
+    const bool v4 = (ldy % 4 == 0) && (ldx % 4 == 0) && aligned16(dY) && aligned16(X);
+    if (x3_large_shape(N, K, B)) return x3_large::launch<true>(N, K, B, dY, ldy, X, ldx, Z, ldz, v4, P, s);
+    return x3_small::launch<true>(N, K, B, dY, ldy, X, ldx, Z, ldz, v4, P, s);
 }
 
 }  // namespace l1csr

@@ -1,0 +1,330 @@
+// The l1-phase weight update of Eq. (prox) from the layer's activations
+// straight to the new CSR, reading the dense gradient's result once:
+//
+//   1. bitmap index of W (bitmap_kernel): per row and 32-column word, the
+//      stored-column mask and the CSR position of the word's first entry;
+//   2. the weight-gradient GEMM with the prox epilogue (prox_epilogue.hpp):
+//      Z = S_t(W - eta * dY.X^T) and the nonzero count of every 32-column
+//      word of every row;
+//   3. row totals of the word counts, their exclusive scan = row_ptr';
+//   4. compaction of Z into col_idx', vals' (compact_kernel): a workgroup per
+//      (row, 3072-column chunk) starts at row_ptr'[row] plus the counts of
+//      the row's words before the chunk, so no second pass over the gradient.
+//
+// Shapes whose GEMM has no prox epilogue (bf16 operands, or an fp32 product
+// that splits its reduction) write dW into Z first and run the same prox in
+// place (prox_words_kernel); the rest is shared.  Every value is the one
+// prox_l1_step would compute from dense_wgrad's dW, and every structure the
+// canonical CSR, so the result equals dense_wgrad + prox_l1_recompress bit
+// for bit.
+#include "common.hpp"
+#include "launch.hpp"
+#include "prox_epilogue.hpp"
+
+namespace l1csr {
+
+namespace {
+
+constexpr int kCompactCols = 3072;  // columns per compaction workgroup (whole 32-column words)
+constexpr int kCompactThreads = 256;
+constexpr int kCompactVecs = kCompactCols / (4 * kCompactThreads);  // float4 per thread: 3
+
+// mask[row][w] bit c: column 32w + c is stored; pos[row][w]: CSR position of
+// the row's first entry with column >= 32w (row_ptr[row + 1] past the last).
+// A wave takes kBitmapSpan consecutive entries of one row (grid: rows x
+// spans; waves past their row's end only handle an empty row), 64 at a time.
+// Entries of one word sit in consecutive positions (columns are sorted), so a
+// segmented OR scan across the lanes, carried from one 64-entry chunk to the
+// next and seeded with the up to 31 entries before the span, gives each word's
+// mask in the lane of its last entry in the row, which alone writes it.  The
+// first entry of a word writes its pos and the pos of the empty words before
+// it; the wave holding the row's last entry writes the words after it.  Every
+// word is written exactly once, by one lane; no atomics.
+constexpr int kBitmapSpan = 512;
+
+__global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spans, const int *__restrict__ ptr,
+                                                     const int *__restrict__ idx, unsigned *__restrict__ mask,
+                                                     int *__restrict__ pos) {
+    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int row = (int)(item / spans), span = (int)(item - (int64_t)row * spans);
+    if (row >= n_rows) return;
+    const int lane = threadIdx.x & 63;
+    const int s = ptr[row], e = ptr[row + 1];
+    unsigned *mr = mask + (int64_t)row * kw;
+    int *pr = pos + (int64_t)row * kw;
+    const int b0 = s + span * kBitmapSpan;
+    if (s == e) {  // an empty row: every word empty, pos = the row's start
+        if (span == 0)
+            for (int x = lane; x < kw; x += kWave) {
+                mr[x] = 0u;
+                pr[x] = s;
+            }
+        return;
+    }
+    if (b0 >= e) return;
+    const int b1 = min(e, b0 + kBitmapSpan);
+    // the entry before the span and the bits its word already has
+    int prevw = -1;
+    unsigned carry = 0u;
+    if (b0 > s) {
+        const int q = b0 - 32 + (lane & 31);
+        const int cq = q >= s ? idx[q] : -1;
+        prevw = lane_bcast(cq, 31) >> 5;
+        const bool same = lane < 32 && cq >= 0 && (cq >> 5) == prevw;
+        unsigned bit = same ? 1u << (cq & 31) : 0u;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) bit |= __shfl_xor(bit, d, kWave);
+        carry = bit;
+    }
+    // the span's entries, plus the entry after it (to tell a word's last entry)
+    constexpr int U = kBitmapSpan / kWave;
+    int cu[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int q = b0 + u * kWave + lane;
+        cu[u] = q < b1 ? idx[q] : 0;
+    }
+    const int after = b1 < e ? idx[b1] >> 5 : 0x7fffffff;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int base = b0 + u * kWave;
+        if (base >= b1) break;
+        const int p = base + lane;
+        const bool valid = p < b1;
+        const int c = cu[u];
+        const int w = valid ? c >> 5 : 0x7fffffff;
+        unsigned v = valid ? 1u << (c & 31) : 0u;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const unsigned vu = __shfl_up(v, d, kWave);
+            const int wu = __shfl_up(w, d, kWave);
+            if (lane >= d && wu == w) v |= vu;
+        }
+        if (w == prevw) v |= carry;
+        const int n = min(kWave, b1 - base);
+        int wn = __shfl_down(w, 1, kWave);
+        if (lane == n - 1) wn = base + n < b1 ? lane_bcast(cu[u + 1 < U ? u + 1 : u], 0) >> 5 : after;
+        if (valid && wn != w) mr[w] = v;  // the word's last entry in the row
+        int pw = __shfl_up(w, 1, kWave);
+        if (lane == 0) pw = prevw;
+        if (valid && w != pw) {
+            for (int x = pw + 1; x < w; ++x) {  // empty words before this one
+                mr[x] = 0u;
+                pr[x] = p;
+            }
+            pr[w] = p;
+        }
+        prevw = lane_bcast(w, n - 1);
+        carry = (unsigned)lane_bcast((int)v, n - 1);
+    }
+    if (b1 == e)
+        for (int x = prevw + 1 + lane; x < kw; x += kWave) {  // words past the row's last entry
+            mr[x] = 0u;
+            pr[x] = e;
+        }
+}
+
+// Z <- S_t(W - eta * Z) in place (Z holds dW), counts per 32-column word:
+// one wave per (row, pair of words), lane = column.
+__global__ __launch_bounds__(256) void prox_words_kernel(int n_rows, int n_cols, prox_epi P,
+                                                         float *__restrict__ Z, int64_t ldz) {
+    const int pairs = (P.kw + 1) / 2;
+    const int64_t total = (int64_t)n_rows * pairs;
+    const int lane = threadIdx.x & 63;
+    const unsigned below = (1u << (lane & 31)) - 1u;
+    for (int64_t it = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); it < total; it += (int64_t)gridDim.x * 4) {
+        const int row = (int)(it / pairs), pr = (int)(it - (int64_t)row * pairs);
+        const int col = pr * 64 + lane;
+        const bool valid = col < n_cols;
+        float o = 0.f;
+        if (valid) {
+            const int64_t wo = (int64_t)row * P.kw + (col >> 5);
+            const unsigned m = P.mask[wo];
+            const bool stored = (m >> (lane & 31)) & 1u;
+            const float w = stored ? P.vals[P.pos[wo] + __popc(m & below)] : 0.f;
+            float *z = Z + (int64_t)row * ldz + col;
+            o = soft_threshold(w, *z, P.eta, P.t);
+            *z = o;
+        }
+        const uint64_t k = __ballot(valid && o != 0.f);
+        if (lane == 0) P.counts[(int64_t)row * P.kw + 2 * pr] = __popcll(k & 0xffffffffull);
+        if (lane == 32 && 2 * pr + 1 < P.kw) P.counts[(int64_t)row * P.kw + 2 * pr + 1] = __popcll(k >> 32);
+    }
+}
+
+// row_counts[row] = sum of the row's word counts (one wave per row)
+__global__ __launch_bounds__(256) void slab_rowsum_kernel(int n_rows, int slabs, const int *__restrict__ counts,
+                                                          int *__restrict__ row_counts) {
+    // (slabs: the counts per row)
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= n_rows) return;
+    const int lane = threadIdx.x & 63;
+    const int *c = counts + (int64_t)row * slabs;
+    int v = 0;
+    for (int j = lane; j < slabs; j += kWave) v += c[j];
+    v = wave_sum_int(v);
+    if (lane == 0) row_counts[row] = v;
+}
+
+// Z -> col_idx', vals' for columns [c0, c0 + 3072) of one row, nonzeros in
+// column order.  Thread t holds the float4s t, t + 256, t + 512 of the chunk;
+// ranks come from four ballots per float4 slot and the wave totals of all
+// three slots are exchanged through LDS in one barrier.  The chunk's output
+// is assembled in LDS and then written with every store instruction covering
+// 64 consecutive positions (scattered per-lane stores measured 1.5x slower).
+template <bool V4>
+__global__ __launch_bounds__(kCompactThreads) void compact_kernel(
+    int n_cols, int chunks, const float *__restrict__ Z, int64_t ldz, int kw,
+    const int *__restrict__ counts, const int *__restrict__ row_ptr, int *__restrict__ col_out,
+    float *__restrict__ val_out, int64_t capacity) {
+    __shared__ int red[kCompactThreads / kWave];
+    __shared__ int tot[kCompactVecs][kCompactThreads / kWave];
+    const int row = blockIdx.x / chunks, ch = blockIdx.x - row * chunks;
+    const int c0 = ch * kCompactCols;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float *z = Z + (int64_t)row * ldz;
+    float v[kCompactVecs][4];
+#pragma unroll
+    for (int u = 0; u < kCompactVecs; ++u) {
+        const int c = c0 + 4 * (tid + u * kCompactThreads);
+        if (V4 && c + 3 < n_cols) {
+            const float4 t = *reinterpret_cast<const float4 *>(z + c);
+            v[u][0] = t.x; v[u][1] = t.y; v[u][2] = t.z; v[u][3] = t.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[u][e] = c + e < n_cols ? z[c + e] : 0.f;
+        }
+    }
+    // the row's output before this chunk: row_ptr' plus the earlier words
+    const int s0 = c0 / 32;
+    int before = 0;
+    for (int j = tid; j < s0; j += kCompactThreads) before += counts[(int64_t)row * kw + j];
+    before = wave_sum_int(before);
+    if (lane == 0) red[wave] = before;
+    int below_lane[kCompactVecs];
+#pragma unroll
+    for (int u = 0; u < kCompactVecs; ++u) {
+        int sum = 0, mine = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint64_t b = __ballot(v[u][e] != 0.f);
+            sum += __popcll(b);
+            mine += popc_below(b);
+        }
+        below_lane[u] = mine;
+        if (lane == 0) tot[u][wave] = sum;
+    }
+    __syncthreads();
+    int64_t base = row_ptr[row];
+#pragma unroll
+    for (int w = 0; w < kCompactThreads / kWave; ++w) base += red[w];
+    __shared__ int lcol[kCompactCols];
+    __shared__ float lval[kCompactCols];
+    int lo = 0;  // position inside the chunk's output
+#pragma unroll
+    for (int u = 0; u < kCompactVecs; ++u) {
+        int o = lo + below_lane[u];
+#pragma unroll
+        for (int w = 0; w < kCompactThreads / kWave; ++w) o += w < wave ? tot[u][w] : 0;
+        const int c = c0 + 4 * (tid + u * kCompactThreads);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (v[u][e] != 0.f) {
+                lcol[o] = c + e;
+                lval[o] = v[u][e];
+                ++o;
+            }
+        }
+#pragma unroll
+        for (int w = 0; w < kCompactThreads / kWave; ++w) lo += tot[u][w];
+    }
+    __syncthreads();
+    for (int i = tid; i < lo; i += kCompactThreads) {
+        if (base + i < capacity) {
+            col_out[base + i] = lcol[i];
+            val_out[base + i] = lval[i];
+        }
+    }
+}
+
+}  // namespace
+
+size_t word_counts_bytes(int N, int K) { return sizeof(int) * (size_t)N * (size_t)ceil_div(K, 32); }
+
+hipError_t launch_bitmap(int n_rows, int n_cols, const int *ptr, const int *idx, unsigned *mask, int *pos,
+                         hipStream_t s) {
+    if (n_rows == 0 || n_cols == 0) return hipSuccess;
+    const int kw = (int)ceil_div(n_cols, 32);
+    const int spans = (int)ceil_div(n_cols, kBitmapSpan);  // a row holds at most n_cols entries
+    const int64_t blocks = ceil_div((int64_t)n_rows * spans, 4);
+    if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+    bitmap_kernel<<<(unsigned)blocks, 256, 0, s>>>(n_rows, kw, spans, ptr, idx, mask, pos);
+    return hipGetLastError();
+}
+
+size_t wgrad_prox_split_bytes(int N, int K, int B, int precision) {
+    const bool fused = precision == kPrecF32 ? wgrad_f32_prox_slab(N, K, B) > 0 : precision == kPrecBF16X3;
+    return fused || precision != kPrecF32 ? 0 : wgrad_workspace_bytes(N, K, B);
+}
+
+hipError_t launch_wgrad_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
+                             int64_t ldx, int precision, const float *vals, const unsigned *mask, const int *pos,
+                             float eta, double t, float *Z, int64_t ldz, int *counts, void *split_ws,
+                             hipStream_t s) {
+    if (N == 0 || K == 0) return hipSuccess;
+    prox_epi P{};
+    P.mask = mask;
+    P.pos = pos;
+    P.vals = vals;
+    P.eta = (double)eta;
+    P.t = t;
+    P.kw = (int)ceil_div(K, 32);
+    P.counts = counts;
+    if (precision == kPrecF32 && wgrad_f32_prox_slab(N, K, B) > 0)
+        return launch_wgrad_f32_prox(N, K, B, dY, ldy, X, ldx, Z, ldz, P, s);
+    if (precision == kPrecBF16X3) return launch_wgrad_bf16x3_prox(N, K, B, dY, ldy, X, ldx, Z, ldz, P, s);
+    // dW into Z, then the prox in place
+    hipError_t e;
+    if (precision == kPrecF32)
+        e = launch_wgrad_f32(N, K, B, dY, ldy, X, ldx, Z, ldz, split_ws, s);
+    else
+        e = launch_wgrad_bf16(N, K, B, dY, ldy, X, ldx, Z, ldz, s);
+    if (e != hipSuccess) return e;
+    const int64_t items = (int64_t)N * ((P.kw + 1) / 2);
+    const int64_t grid = ceil_div(items, 4) < 8192 ? ceil_div(items, 4) : 8192;
+    prox_words_kernel<<<(unsigned)grid, 256, 0, s>>>(N, K, P, Z, ldz);
+    return hipGetLastError();
+}
+
+hipError_t launch_counted_row_ptr(int N, int K, const int *counts, int *row_counts, int *row_ptr_out,
+                                  hipStream_t s) {
+    const int kw = (int)ceil_div(K, 32);
+    slab_rowsum_kernel<<<(unsigned)ceil_div(N, 4), 256, 0, s>>>(N, kw, counts, row_counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_exclusive_scan(row_counts, row_ptr_out, N, nullptr, s);  // row_ptr_out[N] = nnz'
+}
+
+hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts,
+                                  const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
+                                  int *d_nnz_out, hipStream_t s) {
+    const int kw = (int)ceil_div(K, 32);
+    const int chunks = (int)ceil_div(K, kCompactCols);
+    const int64_t blocks = (int64_t)N * chunks;
+    if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+    hipError_t e = hipSuccess;
+    if (blocks > 0) {
+        const bool v4 = (ldz % 4 == 0) && aligned16(Z);
+        if (v4)
+            compact_kernel<true><<<(unsigned)blocks, kCompactThreads, 0, s>>>(K, chunks, Z, ldz, kw, counts,
+                                                                              row_ptr_out, col_out, val_out, capacity);
+        else
+            compact_kernel<false><<<(unsigned)blocks, kCompactThreads, 0, s>>>(K, chunks, Z, ldz, kw, counts,
+                                                                               row_ptr_out, col_out, val_out, capacity);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess && d_nnz_out) e = launch_copy_i32(row_ptr_out + N, d_nnz_out, s);
+    return e;
+}
+
+}  // namespace l1csr

@@ -7,26 +7,27 @@ compressed (CSR) and activations batch-contiguous:
     CSC(W)                        column-major copy of W for the transposed product
     dX = W^T dY                   backward product (gradient to the layer below)
     G  = dY X^T                   dense weight gradient (every weight, zero or not)
-    W' = prox_{eta*lambda}(W - eta G), recompressed to CSR   (Eq. 5)
+    W' = prox_{eta*lambda}(W - eta G), recompressed to CSR   (Eq. (prox))
 
-or, with an adaptive solver (Algorithms 1-2), the same soft threshold after
-the Prox-RMSProp / Prox-ADAM preconditioned step, fused with the
-recompression the same way.
+The last two run as dense_wgrad_prox (the GEMM's epilogue applies the soft
+threshold to its own result and counts the survivors per 32-column word) and
+csr_recompress_counted, so the dense Z = S_t(W - eta G) is written once and
+read once by the recompression, and G itself is never stored.  With an adaptive solver
+(Algorithms 1-2) G is stored and the preconditioned step is fused with the
+recompression instead (prox_adaptive_recompress).
 
 Only the forward product has to finish before the rest: dY is the upstream
-gradient of Y.  The five calls keep the dependencies of a training loop and
-run on two streams of equal (default) priority:
+gradient of Y.  The calls keep the dependencies of a training loop and run on
+two streams of equal (default) priority:
 
-    main:  fwd ──── dense dW ──── prox + recompress ───┐
-    side:  CSC build           └──── bwd (W^T dY) ─────┴─ join
+    main:  fwd ──────────┬── dW GEMM + prox ──── recompress ───┐
+    side:  CSC, bitmap ──┴─────── bwd (W^T dY) ────────────────┴─ join
 
-The CSC build needs only W, so it fills the gaps of the forward product's
-planning launches.  The backward product is started after the weight gradient
-(a scheduling choice: it needs only dY and the CSC) and runs beside the
-proximal step, an HBM stream that leaves the CUs free for its planning
-launches.  The dense weight gradient, the longest launch,
-runs alone.  Every launch is deterministic, so the outputs equal those of the
-same calls made one after another on one stream, bit for bit.
+The CSC copy and the bitmap index that the GEMM's prox epilogue reads W
+through depend on W only, so they fill the gaps of the forward product's
+planning launches; the backward product needs dY and the CSC and runs beside
+the weight update.  Every launch is deterministic, so the outputs equal those
+of the same calls made one after another on one stream, bit for bit.
 
 The overlap pays where a product takes the tiled path (a workspace for its
 plan and pair stream).  Small layers run the rows kernel, a few short launches
@@ -44,8 +45,9 @@ for every entry point under capture, W's nnz must be known on the host
 """
 from __future__ import annotations
 
-from . import (CSC, CSR, F32, OP_SPMM, AdaptiveState, csc_build, csr_spmm_bwd_t, csr_spmm_fwd,
-               dense_wgrad, prox_adaptive_recompress, prox_l1_recompress, workspace_bytes)
+from . import (CSC, CSR, F32, OP_SPMM, AdaptiveState, Bitmap, csc_build, csr_bitmap_build, csr_recompress_counted,
+               csr_spmm_bwd_t, csr_spmm_fwd, dense_wgrad, dense_wgrad_prox, prox_adaptive_recompress,
+               workspace_bytes)
 
 _side_streams: dict = {}
 
@@ -72,21 +74,28 @@ def two_stream_pays(W: CSR, B: int) -> bool:
 
 def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: CSR,
             precision: int = F32, side=None, events: dict | None = None,
-            schedule: str = "auto", adaptive: AdaptiveState | None = None) -> CSR:
+            schedule: str = "auto", adaptive: AdaptiveState | None = None,
+            bitmap: Bitmap | None = None) -> CSR:
     """Run one l1 step on the caller's current stream plus a side stream.
 
     W is the N x K layer (CSR, nnz known on the host or read from the device),
     X the K x B input, dY the N x B upstream gradient.  Results go to the
-    caller's buffers: Y (N x B), dX (K x B), dW (N x K dense gradient), csc
-    (the CSC copy of W, capacity >= nnz) and out (W' in CSR, capacity N*K).
+    caller's buffers: Y (N x B), dX (K x B), dW (N x K: the dense prox result
+    Z = S_t(W - eta G) of the plain step, the gradient G of an adaptive one),
+    csc (the CSC copy of W, capacity >= nnz) and out (W' in CSR, capacity N*K).
     precision selects the dense weight gradient's arithmetic (F32 or BF16X3).
     side: the stream to fork onto (default: one per device).  events: optional
     {call name: (start, end)} torch events, recorded around that call on the
-    stream it runs on.  schedule: "two_stream", "serial" (every call on the
+    stream it runs on ("csc_build", "csr_bitmap_build", "csr_spmm_fwd",
+    "csr_spmm_bwd_t", "dense_wgrad_prox", "csr_recompress_counted"; adaptive:
+    "dense_wgrad",
+    "prox_adaptive_recompress").  schedule: "two_stream", "serial" (every call on the
     caller's stream) or "auto" (two_stream where a product is tiled).
     adaptive: Prox-RMSProp / Prox-ADAM state with dense [N][K] m, v; the step
     then ends with prox_adaptive_recompress (state updated in place, t
-    advanced) instead of prox_l1_recompress.  All outputs are ready on the
+    advanced) instead of dense_wgrad_prox + csr_recompress_counted.  bitmap: buffers for
+    W's bitmap index (Bitmap.empty(N, K)); allocated per call if None.  All
+    outputs are ready on the
     caller's stream when the call returns.  Returns out.
     """
     import torch
@@ -111,17 +120,30 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
             ev[1].record(stream)
 
     fork = side is not main
+    if adaptive is None and bitmap is None:
+        bitmap = Bitmap.empty(W.n_rows, W.n_cols, X.device)  # on the caller's stream
     if fork:
         side.wait_stream(main)  # W, X, dY as the caller left them
     call("csc_build", side, lambda: csc_build(W, csc, stream=side))
+    if adaptive is None:
+        call("csr_bitmap_build", side, lambda: csr_bitmap_build(W, bitmap, stream=side))
+        if fork:
+            indexed = torch.cuda.Event()
+            indexed.record(side)
     call("csr_spmm_fwd", main, lambda: csr_spmm_fwd(W, X, Y, stream=main))
-    call("dense_wgrad", main, lambda: dense_wgrad(dY, X, dW, precision=precision, stream=main))
     if fork:
         side.wait_stream(main)  # dY follows Y; the CSC is on side already
     call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t(W, dY, csc, dX, stream=side))
     if adaptive is None:
-        call("prox_l1_recompress", main, lambda: prox_l1_recompress(W, dW, eta, lam, out=out, stream=main))
+        if fork:
+            main.wait_event(indexed)
+        counts = {}
+        call("dense_wgrad_prox", main,
+             lambda: counts.setdefault("wc", dense_wgrad_prox(W, dY, X, eta, lam, bitmap, Z=dW, precision=precision,
+                                                              stream=main)[1]))
+        call("csr_recompress_counted", main, lambda: csr_recompress_counted(dW, counts["wc"], out=out, stream=main))
     else:
+        call("dense_wgrad", main, lambda: dense_wgrad(dY, X, dW, precision=precision, stream=main))
         call("prox_adaptive_recompress", main,
              lambda: prox_adaptive_recompress(W, dW, adaptive, eta, lam, out=out, stream=main))
     if fork:

@@ -305,3 +305,54 @@ def test_noalloc_prox_checks_its_arguments_and_scratch_before_launch(lib):
     assert call(64, 64, rpo=C.c_void_p(0)) == EINVAL  # no row pointers
     assert call(64, 64, nnz=10, rpo=a["ci"]) == EINVAL   # output over W's columns
     assert call(65536, 65536) == EUNSUPPORTED            # beyond the int32 layout
+
+
+@pytest.mark.skipif(not NO_GPU, reason="validation calls use placeholder pointers; run without a GPU")
+def test_fused_weight_update_arguments_are_rejected_before_launch(lib):
+    """dense_wgrad_prox, csr_recompress_counted and csr_bitmap_build check
+    their arguments on the host: sizes, precision, eta / lambda, a missing
+    bitmap or counts array, leading dimensions, a short workspace, and every
+    output apart from every input."""
+    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    f = lib.dense_wgrad_prox
+    f.argtypes = [i32, i32, i32, vp, i64, vp, i64, C.c_int, i64, vp, vp, vp, vp, vp, f32, f32, vp, i64, vp, vp,
+                  C.c_size_t, vp]
+    g = lib.csr_recompress_counted
+    g.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, i64, vp, vp, vp, C.c_size_t, vp]
+    bb = lib.csr_bitmap_build
+    bb.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp]
+    N, K, B, nnz = 64, 100, 16, 300
+    names = ["dY", "X", "rp", "ci", "v", "Z", "wc", "mk", "ps", "rpo", "cio", "vo", "ws"]
+    base = {n: (i + 1) << 26 for i, n in enumerate(names)}
+
+    def prox(**o):
+        a = dict(base)
+        a.update({k: v for k, v in o.items() if k in a})
+        p = {k: (None if x is None else C.c_void_p(x)) for k, x in a.items()}
+        return f(o.get("N", N), o.get("K", K), B, p["dY"], o.get("ldy", B), p["X"], B, o.get("prec", 0), nnz,
+                 p["rp"], p["ci"], p["v"], p["mk"], p["ps"], o.get("eta", 0.01), o.get("lam", 1e-4), p["Z"],
+                 o.get("ldz", K), p["wc"], p["ws"], 0, S)
+
+    def rec(**o):
+        a = dict(base)
+        a.update({k: v for k, v in o.items() if k in a})
+        p = {k: (None if x is None else C.c_void_p(x)) for k, x in a.items()}
+        return g(o.get("N", N), o.get("K", K), p["Z"], o.get("ldz", K), p["wc"], p["rpo"], p["cio"], p["vo"],
+                 N * K, None, None, p["ws"], o.get("wsb", 4 * (N + 1)), S)
+
+    assert lib.l1csr_workspace_bytes(9, N, K, nnz, B) == 0  # no split at this shape
+    assert prox() == EHIP and rec() == EHIP  # valid: only the launch fails without a GPU
+    for bad in [dict(prec=3), dict(N=-1), dict(eta=0.0), dict(lam=float("nan")), dict(ldy=B - 1), dict(ldz=K - 1),
+                dict(mk=None), dict(ps=None), dict(wc=None), dict(Z=base["dY"] + 8), dict(wc=base["Z"] + 4),
+                dict(Z=base["mk"] + 4), dict(wc=base["ci"])]:
+        assert prox(**bad) == EINVAL, bad
+    assert prox(N=65536, K=65536, ldz=65536) == EUNSUPPORTED
+    for bad in [dict(N=-1), dict(ldz=K - 1), dict(wc=None), dict(rpo=None), dict(wsb=4 * N), dict(ws=None),
+                dict(cio=base["Z"] + 4), dict(vo=base["wc"]), dict(rpo=base["cio"] + 4 * (N * K - 1)),
+                dict(vo=base["ws"])]:
+        assert rec(**bad) == EINVAL, bad
+    assert rec(N=65536, K=65536, ldz=65536) == EUNSUPPORTED
+    P, Q = C.c_void_p(1 << 26), C.c_void_p(2 << 26)
+    assert bb(-1, 4, 0, P, P, P, Q, S) == EINVAL
+    assert bb(4, 4, 3, P, P, None, Q, S) == EINVAL
+    assert bb(4, 64, 3, P, P, P, C.c_void_p((1 << 26) + 8), S) == EINVAL  # mask and pos overlap

@@ -224,8 +224,7 @@ def test_fc9216x4096_zipf_dyadic_two_stream_step_bit_exact():
     torch.cuda.synchronize()
     assert bits_equal(h(o["Y"]), oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)), "Y"
     assert bits_equal(h(o["dX"]), oracle.spmm_bwd_t(L.row_ptr, L.col_idx, L.vals, L.dY, L.K)), "dX"
-    dWr = oracle.dense_wgrad(L.dY, L.X)
-    assert bits_equal(h(o["dW"]), dWr), "dW"
+    dWr = oracle.dense_wgrad(L.dY, L.X)  # exact on the grid: the step's products must give it
     col_ptr, row_idx, perm = csc_reference(L.row_ptr, L.col_idx, L.K)
     c = o["csc"]
     assert bits_equal(h(c.col_ptr), col_ptr), "col_ptr"
@@ -233,6 +232,7 @@ def test_fc9216x4096_zipf_dyadic_two_stream_step_bit_exact():
     assert bits_equal(h(c.perm)[:L.nnz], perm), "perm"
     assert bits_equal(h(c.vals_t)[:L.nnz], L.vals[perm]), "vals_t"
     Z, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, dWr, L.eta, L.lam, L.K)
+    assert bits_equal(h(o["dW"]), Z), "Z = S_t(W - eta dW)"  # the step's dense buffer holds Z
     rpn, cin, vn = oracle.recompress(Z)
     n = int(rpn[-1])
     # the grid produces exact ties |z| == t (deleted) as well as survivors
@@ -528,10 +528,12 @@ def _same_bits(a, b):
 def test_two_stream_step_matches_serial_calls(which, precision):
     """L1.l1_step (CSC build and backward product on a side stream, forced,
     and its automatic choice: two streams for the tiled 9216 -> 4096 products,
-    one for the 784 -> 300 layer) gives the outputs of the five calls made one
-    after another on one stream, bit for bit, on four calls in a row with the
-    outputs overwritten in between; the serial calls are checked against the
-    oracle by the step tests above."""
+    one for the 784 -> 300 layer; the weight update as the fused
+    dense_wgrad_prox_recompress) gives the outputs of the unfused calls made
+    one after another on one stream, bit for bit (its dense buffer holds Z =
+    S_t(W - eta dW)), on four calls in a row with the outputs overwritten in
+    between; the serial calls are checked against the oracle by the step
+    tests above."""
     import torch
     L = synth.fc784_300(seed=0) if which == "fc784x300" else synth.fc9216_4096(seed=0)
     dev = cuda()
@@ -543,6 +545,7 @@ def test_two_stream_step_matches_serial_calls(which, precision):
     L1.csr_spmm_bwd_t(W, dY, a["csc"], a["dX"])
     L1.dense_wgrad(dY, X, a["dW"], precision=precision)
     L1.prox_l1_recompress(W, a["dW"], L.eta, L.lam, out=a["out"])
+    L1.prox_l1_step(L1.PROX_DENSE, W, a["dW"], L.eta, L.lam, Z=a["dW"])  # the step leaves Z in dW
     ref = _step_outputs(a, L.nnz)
     for r, schedule in enumerate(("two_stream", "auto", "two_stream", "serial")):
         for x in (b["Y"], b["dX"], b["dW"], b["out"].vals, b["csc"].vals_t):
@@ -705,6 +708,7 @@ def test_l1_step_loop_carries_W_forward(which):
         L1.csr_spmm_bwd_t(Wa, dY, csc_a, dX)
         L1.dense_wgrad(dY, X, dW)
         L1.prox_l1_recompress(Wa, dW, eta, lam, out=outa)
+        L1.prox_l1_step(L1.PROX_DENSE, Wa, dW, eta, lam, Z=dW)  # as the step leaves its dense buffer
         L1.l1_step(Wb, X, dY, eta, lam, Y=Yb, dX=dXb, dW=dWb, csc=csc_b, out=outb, schedule="auto")
         n_in = Wb.host_nnz()
         assert n_in == int(Wb.row_ptr[-1].item())

@@ -1,0 +1,249 @@
+"""The fused l1 update dense_wgrad_prox_recompress on the GPU.
+
+Z = S_t(W - eta * dY.X^T) (Eq. (prox) with the minibatch gradient, the
+closed form of Section 2.2) and W' = CSR(Z) (Section 3.1) must equal, bit for
+bit:
+  - the unfused calls dense_wgrad (same precision) + prox_l1_step (dense
+    mode) + prox_l1_recompress, and
+  - the oracle's prox and recompression applied to that dense_wgrad result
+    (the products themselves are checked against the oracle by the
+    dense_wgrad tests; on the dyadic grid the whole update is compared with
+    the fully independent oracle step).
+Shapes cover both GEMM tile shapes (256 x 288 and 128 x 128), ragged tiles in
+both dimensions, the split-reduction and bf16-operand fallbacks, empty
+layers, rows and batches, and the capacity paths.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1905_07931_amd as L1
+from paper_1905_07931_amd import synth
+
+from _helpers import bits_equal, cuda, h, t
+
+pytestmark = pytest.mark.gpu
+
+
+def _W(L):
+    return L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=cuda())
+
+
+def _fused_vs_unfused(L, precision, lam=None, eta=None):
+    import torch
+    lam = L.lam if lam is None else lam
+    eta = L.eta if eta is None else eta
+    W = _W(L)
+    X, dY = t(L.X), t(L.dY)
+    Z, out = L1.dense_wgrad_prox_recompress(W, dY, X, eta, lam, precision=precision)
+    dW = L1.dense_wgrad(dY, X, precision=precision)
+    dWh = h(dW)
+    ref_out = L1.prox_l1_recompress(W, dW, eta, lam)
+    Zr = L1.prox_l1_step(L1.PROX_DENSE, W, dW.clone(), eta, lam)
+    torch.cuda.synchronize()
+    assert bits_equal(h(Z), h(Zr)), "Z vs prox_l1_step"
+    n = out.host_nnz()
+    assert n == ref_out.host_nnz()
+    assert bits_equal(h(out.row_ptr), h(ref_out.row_ptr)), "row_ptr"
+    assert bits_equal(h(out.col_idx)[:n], h(ref_out.col_idx)[:n]), "col_idx"
+    assert bits_equal(h(out.vals)[:n], h(ref_out.vals)[:n]), "vals"
+    # and the oracle's prox + recompression of the same gradient
+    Zo, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, dWh, eta, lam, L.K)
+    assert bits_equal(h(Z), Zo), "Z vs oracle"
+    rp, ci, v = oracle.recompress(Zo)
+    assert int(rp[-1]) == n
+    assert bits_equal(h(out.row_ptr), rp) and bits_equal(h(out.col_idx)[:n], ci) and bits_equal(h(out.vals)[:n], v)
+    return n
+
+
+SHAPES = [  # (N, K, B, nnz, seed): tile shapes and ragged edges
+    (300, 784, 64, 23520, 0),        # the 784 -> 300 layer
+    (1000, 1000, 100, 90000, 1),     # ragged 128- and 288-wide tiles
+    (257, 10999, 37, 200000, 2),     # ragged rows, many column tiles
+    (64, 33, 5, 300, 3),             # narrower than one 32-column word
+    (1, 1, 1, 1, 4), (1, 700, 3, 10, 5), (700, 1, 3, 10, 6),
+    (130, 257, 65, 0, 7),            # empty layer: only regrowth
+]
+
+
+def _ids(s):
+    return "N{}K{}B{}nnz{}".format(*s[:4])
+
+
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3, L1.BF16])
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+def test_fused_update_equals_unfused_calls(shape, precision):
+    N, K, B, nnz, seed = shape
+    L = synth.fc_layer(N, K, B, nnz, seed=seed)
+    _fused_vs_unfused(L, precision)
+
+
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3])
+def test_fused_update_full_size_9216x4096(precision):
+    # the 256 x 288 tiles (two rounds of the chip), Zipf rows; a lambda that
+    # deletes part of the layer as well as regrowing it
+    L = synth.fc9216_4096(seed=0)
+    n = _fused_vs_unfused(L, precision, lam=0.5)
+    assert 0 < n < L.N * L.K
+
+
+def test_fused_update_split_reduction_fallback():
+    # 50 x 500 with a reduction of 16384: the fp32 product splits its batch
+    # (no fused epilogue there), so dW goes through Z and the prox runs after
+    L = synth.conv2_im2col(seed=0)
+    _fused_vs_unfused(L, L1.F32)
+
+
+def test_fused_update_dyadic_full_size_bit_exact_with_independent_oracle():
+    # every fp32 sum of dW is exact on the dyadic grid, so the update must
+    # equal the fully independent oracle step (its own dW) bit for bit
+    import torch
+    L = synth.dyadic_layer(4096, 9216, 1024, synth.nnz_for(4096, 9216, 0.09), seed=1, pattern="zipf")
+    W = _W(L)
+    Z, out = L1.dense_wgrad_prox_recompress(W, t(L.dY), t(L.X), L.eta, L.lam)
+    torch.cuda.synchronize()
+    dWr = oracle.dense_wgrad(L.dY, L.X)
+    Zo, _ = oracle.prox_dense(L.row_ptr, L.col_idx, L.vals, dWr, L.eta, L.lam, L.K)
+    assert bits_equal(h(Z), Zo)
+    rp, ci, v = oracle.recompress(Zo)
+    n = int(rp[-1])
+    assert 0 < n < L.N * L.K  # the grid makes exact ties |z| == t, deleted
+    assert bits_equal(h(out.row_ptr), rp) and bits_equal(h(out.col_idx)[:n], ci) and bits_equal(h(out.vals)[:n], v)
+
+
+def test_fused_update_empty_batch_and_huge_threshold():
+    # B = 0: dW = 0, so Z = S_t(W) (stored weights shrink by t); then a
+    # threshold above every |w - eta g| deletes the whole layer
+    L = synth.fc_layer(300, 784, 0, 23520, seed=8)
+    _fused_vs_unfused(L, L1.F32)
+    L2 = synth.fc_layer(300, 784, 16, 23520, seed=9)
+    assert _fused_vs_unfused(L2, L1.F32, lam=1e6) == 0
+
+
+def test_fused_update_capacity_paths():
+    import torch
+    L = synth.fc_layer(200, 300, 32, 6000, seed=10)
+    W = _W(L)
+    X, dY = t(L.X), t(L.dY)
+    Z, full = L1.dense_wgrad_prox_recompress(W, dY, X, L.eta, 0.05)
+    n = full.host_nnz()
+    assert 0 < n < L.N * L.K
+    # exactly enough room: the call waits, fills and reports the count on the host
+    Z2, exact = L1.dense_wgrad_prox_recompress(W, dY, X, L.eta, 0.05, capacity=n)
+    assert exact.nnz == n
+    assert bits_equal(h(exact.row_ptr), h(full.row_ptr)) and bits_equal(h(exact.vals)[:n], h(full.vals)[:n])
+    # one short: L1CSR_ECAPACITY, row pointers valid, nothing else written
+    out = L1.CSR(L.N, L.K, torch.empty(L.N + 1, dtype=torch.int32, device=cuda()),
+                 torch.full((n - 1,), -7, dtype=torch.int32, device=cuda()),
+                 torch.full((n - 1,), -7.0, dtype=torch.float32, device=cuda()), None)
+    with pytest.raises(L1.L1CSRError) as ei:
+        L1.dense_wgrad_prox_recompress(W, dY, X, L.eta, 0.05, out=out, capacity=n - 1)
+    assert ei.value.status == L1.ECAPACITY
+    torch.cuda.synchronize()
+    assert bits_equal(h(out.row_ptr), h(full.row_ptr))
+    assert bool((out.col_idx == -7).all()) and bool((out.vals == -7.0).all())
+
+
+def test_fused_update_padded_leading_dimensions():
+    import torch
+    L = synth.fc_layer(130, 300, 40, 4000, seed=11)
+    W = _W(L)
+    dev = cuda()
+    Xp = torch.zeros((L.K, 44), device=dev)
+    Xp[:, :40] = t(L.X)
+    dYp = torch.zeros((L.N, 48), device=dev)
+    dYp[:, :40] = t(L.dY)
+    Zp = torch.full((L.N, 304), 5.0, device=dev)
+    Z, out = L1.dense_wgrad_prox_recompress(W, dYp[:, :40], Xp[:, :40], L.eta, L.lam, Z=Zp[:, :300])
+    Zr, ref = L1.dense_wgrad_prox_recompress(W, t(L.dY), t(L.X), L.eta, L.lam)
+    torch.cuda.synchronize()
+    assert bits_equal(h(Zp)[:, :300], h(Zr)) and np.all(h(Zp)[:, 300:] == 5.0)
+    n = ref.host_nnz()
+    assert out.host_nnz() == n and bits_equal(h(out.col_idx)[:n], h(ref.col_idx)[:n])
+
+
+def _bitmap_reference(row_ptr, col_idx, N, K):
+    """mask[i][w] bit c = (i, 32w + c) stored; pos[i][w] = first CSR position
+    of row i with column >= 32w (numpy: bit arithmetic and a sorted search)."""
+    kw = (K + 31) // 32
+    rp = np.asarray(row_ptr, np.int64)
+    ci = np.asarray(col_idx, np.int64)
+    rows = np.repeat(np.arange(N), np.diff(rp))
+    mask = np.zeros((N, kw), np.uint64)
+    np.bitwise_or.at(mask, (rows, ci >> 5), np.left_shift(np.uint64(1), (ci & 31).astype(np.uint64)))
+    pos = np.empty((N, kw), np.int64)
+    for i in range(N):
+        seg = ci[rp[i]:rp[i + 1]]
+        pos[i] = rp[i] + np.searchsorted(seg, 32 * np.arange(kw), side="left")
+    return mask.astype(np.uint32).view(np.int32), pos.astype(np.int32)
+
+
+@pytest.mark.parametrize("case", ["zipf", "banded", "narrow", "empty_rows"])
+def test_bitmap_index_bit_exact(case):
+    # long rows cross the 512-entry spans of the build (words straddling a
+    # span boundary), dense rows fill every word, empty rows and columns that
+    # are not a multiple of 32
+    rng = np.random.default_rng(61)
+    if case == "zipf":
+        N, K = 700, 9216
+        rp, ci = synth.zipf_pattern(rng, N, K, 600000, 1.1)
+    elif case == "banded":
+        N, K = 300, 2000
+        dense = np.zeros((N, K), bool)
+        dense[:, 500:1700] = rng.random((N, 1200)) < 0.7
+        dense[[3, 77], :] = True
+        rp, ci = synth.pattern_from_positions(N, K, np.flatnonzero(dense.reshape(-1)))
+    elif case == "narrow":
+        N, K = 1000, 45
+        rp, ci = synth.uniform_pattern(rng, N, K, 20000)
+    else:
+        N, K = 200, 1001
+        dense = rng.random((N, K)) < 0.3
+        dense[::3] = False
+        rp, ci = synth.pattern_from_positions(N, K, np.flatnonzero(dense.reshape(-1)))
+    vals = np.ones(len(ci), np.float32)
+    W = L1.CSR.from_host(rp, ci, vals, K, device=cuda())
+    bm = L1.csr_bitmap_build(W)
+    mask, pos = _bitmap_reference(rp, ci, N, K)
+    kw = (K + 31) // 32
+    assert bits_equal(h(bm.mask).reshape(-1)[: N * kw].reshape(N, kw), mask)
+    assert bits_equal(h(bm.pos).reshape(-1)[: N * kw].reshape(N, kw), pos)
+
+
+def test_fused_update_with_prebuilt_bitmap():
+    # the bitmap built by the caller (as l1_step does on its side stream)
+    # gives the same result as the one the call builds itself
+    import torch
+    L = synth.fc_layer(1000, 1000, 100, 90000, seed=12)
+    W = _W(L)
+    bm = L1.csr_bitmap_build(W)
+    Z1, o1 = L1.dense_wgrad_prox_recompress(W, t(L.dY), t(L.X), L.eta, L.lam, bitmap=bm)
+    Z2, o2 = L1.dense_wgrad_prox_recompress(W, t(L.dY), t(L.X), L.eta, L.lam)
+    torch.cuda.synchronize()
+    n = o2.host_nnz()
+    assert bits_equal(h(Z1), h(Z2)) and o1.host_nnz() == n
+    assert bits_equal(h(o1.col_idx)[:n], h(o2.col_idx)[:n]) and bits_equal(h(o1.vals)[:n], h(o2.vals)[:n])
+
+
+@pytest.mark.parametrize("precision", [L1.F32, L1.BF16X3, L1.BF16])
+def test_word_counts_and_counted_recompress(precision):
+    # the two calls the step makes: dense_wgrad_prox's per-word counts are the
+    # nonzeros of Z per 32 columns, and csr_recompress_counted gives the
+    # canonical CSR of Z (as csr_recompress with t = 0)
+    import torch
+    L = synth.fc_layer(257, 1000, 70, 30000, seed=13)
+    W = _W(L)
+    bm = L1.csr_bitmap_build(W)
+    Z, wc = L1.dense_wgrad_prox(W, t(L.dY), t(L.X), L.eta, 0.02, bm, precision=precision)
+    out = L1.csr_recompress_counted(Z, wc)
+    ref = L1.csr_recompress(Z.clone(), 0.0)
+    torch.cuda.synchronize()
+    Zh = h(Z)
+    kw = (L.K + 31) // 32
+    pad = np.zeros((L.N, kw * 32), bool)
+    pad[:, :L.K] = Zh != 0
+    assert bits_equal(h(wc).reshape(-1)[: L.N * kw].reshape(L.N, kw), pad.reshape(L.N, kw, 32).sum(2).astype(np.int32))
+    n = ref.host_nnz()
+    assert out.host_nnz() == n and 0 < n < L.N * L.K
+    assert bits_equal(h(out.row_ptr), h(ref.row_ptr))
+    assert bits_equal(h(out.col_idx)[:n], h(ref.col_idx)[:n]) and bits_equal(h(out.vals)[:n], h(ref.vals)[:n])
