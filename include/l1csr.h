@@ -122,11 +122,15 @@ int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
  *     col_ptr[n_cols+1], row_idx[nnz], perm[nnz], vals_t[nnz]
  * with row_idx strictly increasing inside each column (the unique canonical
  * CSC), perm[q] = the CSR position of CSC entry q and vals_t[q] = vals[perm[q]].
+ * It is built from W's bitmap index (csr_bitmap_build): mask / pos given by
+ * the caller (both, e.g. shared with dense_wgrad_prox), or both NULL and the
+ * call builds them in ws.  nnz is row_ptr[n_rows] or an upper bound on it.
  * Deterministic.  ws must hold
  * l1csr_workspace_bytes(L1CSR_OP_CSC_BUILD, n_rows, n_cols, nnz, 0) bytes.
  */
 int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz,
               const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+              const uint32_t *mask, const int32_t *pos,
               int32_t *col_ptr, int32_t *row_idx, int32_t *perm, float *vals_t,
               void *ws, size_t ws_bytes, hipStream_t stream);
 
@@ -275,7 +279,7 @@ int prox_l1_recompress(int32_t n_rows, int32_t n_cols, int64_t nnz,
  * of csr_recompress_counted (so the recompression reads Z once and never W).
  * Z is bit-identical to dense_wgrad + prox_l1_step.
  * dY [N][ldy], X [K][ldx], W (N x K CSR with nnz entries), mask / pos
- * [N][ceil(K/32)] (read), Z [N][ldz] (ldz >= K) and word_counts
+ * [ceil(K/32)][N] (read), Z [N][ldz] (ldz >= K) and word_counts
  * [N][ceil(K/32)] (written); the outputs must be disjoint from each other
  * and from every input (L1CSR_EINVAL).  ws as
  * l1csr_workspace_bytes(L1CSR_OP_WGRAD_PROX, N, K, nnz, B) for fp32 (0 unless
@@ -306,11 +310,12 @@ int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64
 /*
  * Bitmap index of W's pattern (the CSR of Section 3.1 seen by 32-column
  * words), read by dense_wgrad_prox to find w_ik for every (i, k):
- *     mask[i][w] bit c = 1 iff W stores (i, 32w + c)
- *     pos[i][w]  = CSR position of row i's first entry with column >= 32w
+ *     mask[w][i] bit c = 1 iff W stores (i, 32w + c)
+ *     pos[w][i]  = CSR position of row i's first entry with column >= 32w
  *                  (row_ptr[i + 1] if there is none)
- * for 0 <= w < ceil(n_cols / 32); both [n_rows][ceil(n_cols / 32)],
- * caller-owned, disjoint.  Deterministic; depends only on the pattern.
+ * for 0 <= w < ceil(n_cols / 32), word-major: both
+ * [ceil(n_cols / 32)][n_rows], caller-owned, disjoint.  Deterministic; depends
+ * only on the pattern (also the input of csc_build).
  */
 int csr_bitmap_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
                      const int32_t *col_idx, uint32_t *mask, int32_t *pos, hipStream_t stream);

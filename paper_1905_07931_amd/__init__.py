@@ -60,7 +60,7 @@ def lib():
         L.l1csr_workspace_bytes.argtypes = [C.c_int, i32, i32, i64, i32]
         L.l1csr_workspace_bytes.restype = sz
         L.csr_spmm_fwd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
-        L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.csc_update_vals.argtypes = [i32, i64, vp, vp, vp, vp, vp]
         L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
                                      vp, sz, vp]
@@ -320,14 +320,17 @@ def csr_spmm_fwd(W: CSR, X, Y=None, stream=None):
     return Y
 
 
-def csc_build(W: CSR, out: CSC | None = None, stream=None) -> CSC:
-    """Deterministic CSC copy of W (col_ptr, row_idx, perm, vals_t)."""
+def csc_build(W: CSR, out: CSC | None = None, bitmap: "Bitmap | None" = None, stream=None) -> CSC:
+    """Deterministic CSC copy of W (col_ptr, row_idx, perm, vals_t), built from
+    W's bitmap index (given, or built by the call)."""
     nnz = W.validate_shapes()
     dev = W.row_ptr.device
     if out is None:
-        out = CSC.empty(W.n_cols, W.col_idx.numel(), dev)
+        out = CSC.empty(W.n_cols, max(nnz, 1), dev)
     ws, wsb = _workspace(workspace_bytes(OP_CSC_BUILD, W.n_rows, W.n_cols, nnz, 0), dev, stream)
-    _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals),
+    mask = None if bitmap is None else _p(bitmap.mask)
+    pos = None if bitmap is None else _p(bitmap.pos)
+    _check(lib().csc_build(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), mask, pos,
                            _p(out.col_ptr), _p(out.row_idx), _p(out.perm), _p(out.vals_t), _p(ws),
                            wsb, _stream(stream)), "csc_build")
     return out
@@ -457,17 +460,17 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
 
 @dataclass
 class Bitmap:
-    """Bitmap index of a CSR pattern: mask / pos [n_rows][ceil(n_cols / 32)]
-    (csr_bitmap_build)."""
+    """Bitmap index of a CSR pattern, word-major: mask / pos
+    [ceil(n_cols / 32)][n_rows] (csr_bitmap_build)."""
     mask: "object"
     pos: "object"
 
     @staticmethod
     def empty(n_rows, n_cols, device):
         torch = _torch()
-        kw = max((n_cols + 31) // 32, 1)
-        return Bitmap(torch.empty((max(n_rows, 1), kw), dtype=torch.int32, device=device),
-                      torch.empty((max(n_rows, 1), kw), dtype=torch.int32, device=device))
+        kw = max((n_cols + 31) // 32, 1)  # word-major: [kw][n_rows]
+        return Bitmap(torch.empty((kw, max(n_rows, 1)), dtype=torch.int32, device=device),
+                      torch.empty((kw, max(n_rows, 1)), dtype=torch.int32, device=device))
 
 
 def csr_bitmap_build(W: CSR, bm: Bitmap | None = None, stream=None) -> Bitmap:

@@ -267,16 +267,19 @@ int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row
 }
 
 int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
-              const int32_t *col_idx, const float *vals, int32_t *col_ptr, int32_t *row_idx,
-              int32_t *perm, float *vals_t, void *ws, size_t ws_bytes, hipStream_t stream) {
+              const int32_t *col_idx, const float *vals, const uint32_t *mask, const int32_t *pos,
+              int32_t *col_ptr, int32_t *row_idx, int32_t *perm, float *vals_t, void *ws, size_t ws_bytes,
+              hipStream_t stream) {
     if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true)) return L1CSR_EINVAL;
     if (col_ptr == nullptr) return L1CSR_EINVAL;
+    if ((mask == nullptr) != (pos == nullptr)) return L1CSR_EINVAL;  // both or neither
     if (nnz > 0 && (row_idx == nullptr || perm == nullptr || vals_t == nullptr)) return L1CSR_EINVAL;
     if (n_rows > 0 && n_cols > 0 &&
         (ws == nullptr || ws_bytes < csc_workspace_bytes(n_rows, n_cols, nnz)))
         return L1CSR_EINVAL;
     if (!csc_grid_fits(n_rows, n_cols)) return L1CSR_EUNSUPPORTED;
-    return hip_status(launch_csc_build(n_rows, n_cols, nnz, row_ptr, col_idx, vals, col_ptr, row_idx, perm,
+    return hip_status(launch_csc_build(n_rows, n_cols, nnz, row_ptr, col_idx, vals,
+                                       reinterpret_cast<const unsigned *>(mask), pos, col_ptr, row_idx, perm,
                                        vals_t, ws, stream));
 }
 

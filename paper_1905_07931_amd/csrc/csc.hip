@@ -1,22 +1,17 @@
 // Deterministic CSR -> CSC for the backward product: column pointers, the row
 // of every entry, its CSR position (perm) and its value in CSC order.
 //
-// Rows are taken in chunks of 256 and columns in tiles of up to 512 (segment
-// pointers per (row, tile) come from the same planning pass as the products).
-// For one (chunk, tile) a workgroup builds in LDS a 256-bit mask per column
-// (eight 32-bit words) whose bit r says "row r of the chunk has an entry in
-// this column" (atomicOr, so the result does not depend on order).  An entry
-// (row r of chunk c, column k) then goes to
-//     col_ptr[k]                              entries of earlier columns
-//   + sum_{c' < c} popcount(mask_{c'}[k])     same column, earlier chunks
-//   + popcount(mask_c[k] & ((1 << r) - 1))    same column, earlier rows of c
-// which orders every column by row (the canonical CSC) without sorting and
-// without order-dependent atomics.  A chunk's entries of one column land in
-// one run (~23 entries at 9% density), so the scattered 8-byte stores mostly
-// fill whole cache lines.  (128 x 1024 measured 62 us for the scatter at
-// 4096 x 9216, 256 x 512 54 us, 512 x 256 114 us.)
-// Passes: segment pointers -> counts -> per-column chunk scan -> column
-// pointer scan -> scatter (rebuilds the masks, bases staged in LDS).
+// Built from the bitmap index of W (launch_bitmap, word-major: mask[w][row]
+// has bit c set iff (row, 32w + c) is stored, pos[w][row] is the CSR position
+// of the row's first entry at a column >= 32w).  A workgroup takes one
+// 32-column word and a block of up to 1024 rows; its 4 waves take 256 rows
+// each (one row per lane, four groups) and hold the rows' mask and pos words
+// in registers.  For every column of the word a ballot of the column's bit
+// ranks the stored rows, so the column's entries come out in row order (the
+// canonical CSC) and are written as contiguous runs, with no sorting and no
+// atomics.  The entry's CSR position is pos + popcount(mask &
+// below(c)).  Passes: counts per (row block, column) -> per-column scan over
+// the blocks -> column pointer scan -> emit.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -24,62 +19,45 @@ namespace l1csr {
 
 namespace {
 
-constexpr int kChunkRows = 256;
-constexpr int kMaskWords = kChunkRows / 32;
-constexpr int kTileShift = 9;
-constexpr int kTileCols = 1 << kTileShift;
-constexpr int kCscThreads = 1024;
+constexpr int kRowBlock = 1024;  // rows per workgroup (256 threads, 4 waves of 256 rows)
+constexpr int kCscThreads = 256;
 
-__device__ __forceinline__ void build_masks(int n_rows, const int *__restrict__ seg, int ntc,
-                                            const int *__restrict__ idx, int chunk, int t, int k0,
-                                            int ncols_tile, uint32_t (*M)[kTileCols]) {
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int nwaves = blockDim.x >> 6;
-    constexpr int kRowsPerWave = kChunkRows / (kCscThreads / kWave);
-    // bounds of this wave's rows, then their first entries, before any use
-    int sb[kRowsPerWave], eb[kRowsPerWave], k1st[kRowsPerWave];
-#pragma unroll
-    for (int u = 0; u < kRowsPerWave; ++u) {
-        const int row = chunk * kChunkRows + wave + u * nwaves;
-        sb[u] = eb[u] = 0;
-        if (row < n_rows) {
-            const int *sr = seg + (int64_t)row * (ntc + 1) + t;
-            sb[u] = sr[0];
-            eb[u] = sr[1];
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < kRowsPerWave; ++u) k1st[u] = sb[u] + lane < eb[u] ? idx[sb[u] + lane] - k0 : -1;
-    for (int k = threadIdx.x; k < kMaskWords * kTileCols; k += blockDim.x) M[k / kTileCols][k % kTileCols] = 0u;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kRowsPerWave; ++u) {
-        const int r = wave + u * nwaves;
-        if (k1st[u] >= 0 && k1st[u] < ncols_tile) atomicOr(&M[r >> 5][k1st[u]], 1u << (r & 31));
-        for (int p = sb[u] + kWave + lane; p < eb[u]; p += kWave) {
-            const int k = idx[p] - k0;
-            if (k >= 0 && k < ncols_tile) atomicOr(&M[r >> 5][k], 1u << (r & 31));
-        }
-    }
-    __syncthreads();
-}
+// Each of the 4 waves takes 256 consecutive rows of the block (four groups of
+// 64, one row per lane) and evaluates all 32 columns of the word per mask
+// read: 32 ballots per group, no dependent chain through LDS.
+constexpr int kWaveRows = kRowBlock / (kCscThreads / kWave);  // 256
 
-__global__ __launch_bounds__(kCscThreads) void csc_count_kernel(int n_rows, int n_cols, int ntc,
-                                                                const int *__restrict__ seg,
-                                                                const int *__restrict__ idx,
+// cnt[rb][c] = stored entries of column c in row block rb
+__global__ __launch_bounds__(kCscThreads) void csc_count_kernel(int n_rows, int n_cols,
+                                                                const unsigned *__restrict__ mask,
                                                                 int *__restrict__ cnt) {
-    __shared__ uint32_t M[kMaskWords][kTileCols];
-    const int chunk = blockIdx.x, t = blockIdx.y;
-    const int k0 = t * kTileCols;
-    const int nct = min(kTileCols, n_cols - k0);
-    build_masks(n_rows, seg, ntc, idx, chunk, t, k0, nct, M);
-    int *c = cnt + (int64_t)chunk * n_cols + k0;
-    for (int k = threadIdx.x; k < nct; k += blockDim.x) {
+    __shared__ int part[kCscThreads / kWave][32];
+    const int w = blockIdx.x, rb = blockIdx.y;
+    const int r0 = rb * kRowBlock, r1 = min(n_rows, r0 + kRowBlock);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t o = (int64_t)w * n_rows;
+    unsigned m[kWaveRows / kWave];
+#pragma unroll
+    for (int g = 0; g < kWaveRows / kWave; ++g) {
+        const int i = r0 + wave * kWaveRows + g * kWave + lane;
+        m[g] = i < r1 ? mask[o + i] : 0u;
+    }
+    int mine = 0;  // lane c < 32: this wave's count of column 32w + c
+#pragma unroll
+    for (int c = 0; c < 32; ++c) {
         int n = 0;
 #pragma unroll
-        for (int w = 0; w < kMaskWords; ++w) n += __popc(M[w][k]);
-        c[k] = n;
+        for (int g = 0; g < kWaveRows / kWave; ++g) n += __popcll(__ballot((m[g] >> c) & 1u));
+        mine = lane == c ? n : mine;
+    }
+    if (lane < 32) part[wave][lane] = mine;
+    __syncthreads();
+    if (threadIdx.x < 32) {
+        const int c = 32 * w + threadIdx.x;
+        int n = 0;
+#pragma unroll
+        for (int j = 0; j < kCscThreads / kWave; ++j) n += part[j][threadIdx.x];
+        if (c < n_cols) cnt[(int64_t)rb * n_cols + c] = n;
     }
 }
 
@@ -110,56 +88,107 @@ __global__ __launch_bounds__(256) void csc_colscan_kernel(int n_chunks, int n_co
     tot[k] = run;
 }
 
-// one scattered 8-byte store per entry, (row, CSR position), into a staging
-// array; csc_finish_kernel then writes row_idx, perm and vals_t coalesced
-__global__ __launch_bounds__(kCscThreads) void csc_scatter_kernel(
-    int n_rows, int n_cols, int ntc, const int *__restrict__ seg, const int *__restrict__ idx,
-    const int *__restrict__ cnt, const int *__restrict__ col_ptr, int2 *__restrict__ pairs) {
-    __shared__ uint32_t M[kMaskWords][kTileCols];
-    __shared__ int base[kTileCols];
-    const int chunk = blockIdx.x, t = blockIdx.y;
-    const int k0 = t * kTileCols;
-    const int nct = min(kTileCols, n_cols - k0);
-    const int *c = cnt + (int64_t)chunk * n_cols + k0;
-    for (int k = threadIdx.x; k < nct; k += blockDim.x) base[k] = col_ptr[k0 + k] + c[k];
-    build_masks(n_rows, seg, ntc, idx, chunk, t, k0, nct, M);  // ends with a barrier
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int nwaves = blockDim.x >> 6;
-    for (int r = wave; r < kChunkRows; r += nwaves) {
-        const int row = chunk * kChunkRows + r;
-        if (row >= n_rows) break;
-        const int *sr = seg + (int64_t)row * (ntc + 1) + t;
-        const int s = sr[0], e = sr[1];
-        const int rw = r >> 5;
-        const uint32_t below = (1u << (r & 31)) - 1u;
-        for (int p = s + lane; p < e; p += kWave) {
-            const int k = idx[p] - k0;
-            if (k >= 0 && k < nct) {
-                int rank = __popc(M[rw][k] & below);
+// row_idx, perm and vals_t of every (column, row block): the column's entries
+// of the block at col_ptr[c] + cnt[rb][c] onwards, in row order.  Wave j's
+// rows of column c start after the column's entries in the block's earlier
+// waves (per-wave counts exchanged through LDS); inside a 64-row group a
+// ballot ranks them.  Columns are taken eight at a time: every entry goes to
+// an LDS run of its column (the first kRunCap of the block's entries of that
+// column; any further ones, only in very dense columns, are stored directly),
+// and the runs are then written with consecutive lanes on consecutive
+// positions, the values gathered there.
+constexpr int kRunCols = 8;
+constexpr int kRunCap = 256;
+
+__global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n_cols,
+                                                               const unsigned *__restrict__ mask,
+                                                               const int *__restrict__ pos,
+                                                               const float *__restrict__ vals,
+                                                               const int *__restrict__ cnt,
+                                                               const int *__restrict__ col_ptr,
+                                                               int *__restrict__ row_idx,
+                                                               int *__restrict__ perm,
+                                                               float *__restrict__ vals_t) {
+    constexpr int NW = kCscThreads / kWave, G = kWaveRows / kWave;
+    __shared__ int start[NW + 1][32];  // [j][c]: column c's entries of waves < j (row NW: block total)
+    __shared__ int run_row[kRunCols][kRunCap];
+    __shared__ int run_p[kRunCols][kRunCap];
+    const int w = blockIdx.x, rb = blockIdx.y;
+    const int r0 = rb * kRowBlock, r1 = min(n_rows, r0 + kRowBlock);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t o = (int64_t)w * n_rows;
+    unsigned m[G];
+    int ps[G];
 #pragma unroll
-                for (int w = 0; w < kMaskWords; ++w) rank += w < rw ? __popc(M[w][k]) : 0;
-                pairs[base[k] + rank] = make_int2(row, p);
+    for (int g = 0; g < G; ++g) {
+        const int i = r0 + wave * kWaveRows + g * kWave + lane;
+        m[g] = i < r1 ? mask[o + i] : 0u;
+        ps[g] = i < r1 ? pos[o + i] : 0;
+    }
+    int mine = 0;
+#pragma unroll
+    for (int c = 0; c < 32; ++c) {
+        int n = 0;
+#pragma unroll
+        for (int g = 0; g < G; ++g) n += __popcll(__ballot((m[g] >> c) & 1u));
+        mine = lane == c ? n : mine;
+    }
+    if (lane < 32) start[wave][lane] = mine;
+    __syncthreads();
+    if (threadIdx.x < 32) {  // exclusive scan over the waves (relative to the block's run)
+        int run = 0;
+#pragma unroll
+        for (int j = 0; j < NW; ++j) {
+            const int v = start[j][threadIdx.x];
+            start[j][threadIdx.x] = run;
+            run += v;
+        }
+        start[NW][threadIdx.x] = run;
+    }
+    __syncthreads();
+    const int nc = min(32, n_cols - 32 * w);
+    for (int c0 = 0; c0 < nc; c0 += kRunCols) {
+#pragma unroll
+        for (int cc = 0; cc < kRunCols; ++cc) {
+            const int c = c0 + cc;
+            if (c >= nc) break;  // uniform
+            const unsigned below = (1u << c) - 1u;
+            int q0 = start[wave][c];
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const bool set = (m[g] >> c) & 1u;
+                const uint64_t b = __ballot(set);
+                if (set) {
+                    const int q = q0 + popc_below(b);
+                    const int row = r0 + wave * kWaveRows + g * kWave + lane;
+                    const int p = ps[g] + __popc(m[g] & below);
+                    if (q < kRunCap) {
+                        run_row[cc][q] = row;
+                        run_p[cc][q] = p;
+                    } else {  // beyond the staged run: straight to the output
+                        const int64_t d = (int64_t)col_ptr[32 * w + c] + cnt[(int64_t)rb * n_cols + 32 * w + c] + q;
+                        row_idx[d] = row;
+                        perm[d] = p;
+                        vals_t[d] = vals[p];
+                    }
+                }
+                q0 += __popcll(b);
             }
         }
-    }
-}
-
-// row_idx[q], perm[q] from the staged pairs; vals_t[q] = vals[perm[q]]
-__global__ __launch_bounds__(256) void csc_finish_kernel(int n_rows, int64_t nnz,
-                                                         const int *__restrict__ ptr,
-                                                         const int2 *__restrict__ pairs,
-                                                         const float *__restrict__ vals,
-                                                         int *__restrict__ row_idx,
-                                                         int *__restrict__ perm,
-                                                         float *__restrict__ vals_t) {
-    const int64_t n = min(nnz, (int64_t)ptr[n_rows]);  // nnz may be a capacity bound
-    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n;
-         q += (int64_t)gridDim.x * blockDim.x) {
-        const int2 rp = pairs[q];
-        row_idx[q] = rp.x;
-        perm[q] = rp.y;
-        vals_t[q] = vals[rp.y];
+        __syncthreads();
+        // the staged runs, consecutive threads on consecutive positions
+        for (int cc = 0; cc < kRunCols && c0 + cc < nc; ++cc) {
+            const int c = 32 * w + c0 + cc;
+            const int n = min(kRunCap, start[NW][c0 + cc]);
+            const int64_t d0 = (int64_t)col_ptr[c] + cnt[(int64_t)rb * n_cols + c];
+            for (int q = threadIdx.x; q < n; q += kCscThreads) {
+                const int p = run_p[cc][q];
+                row_idx[d0 + q] = run_row[cc][q];
+                perm[d0 + q] = p;
+                vals_t[d0 + q] = vals[p];
+            }
+        }
+        __syncthreads();  // the runs are refilled by the next columns
     }
 }
 
@@ -173,57 +202,58 @@ __global__ void gather_vals_kernel(int n_cols, const int *__restrict__ col_ptr,
 }
 
 struct csc_layout {
-    int n_chunks, ntc;
-    int64_t seg_ints, cnt_ints, tot_ints, pair_ints;  // pairs start 8-byte aligned
+    int n_blocks, kw;
+    int64_t bm_ints, cnt_ints, tot_ints;
 };
 
-csc_layout layout(int n_rows, int n_cols, int64_t nnz) {
+csc_layout layout(int n_rows, int n_cols) {
     csc_layout l;
-    l.n_chunks = (int)ceil_div(n_rows, kChunkRows);
-    l.ntc = (int)ceil_div(n_cols, kTileCols);
-    l.seg_ints = (int64_t)n_rows * (l.ntc + 1);
-    l.cnt_ints = (int64_t)l.n_chunks * n_cols;
-    l.tot_ints = ((int64_t)n_cols + 2) & ~(int64_t)1;
-    if ((l.seg_ints + l.cnt_ints) & 1) l.tot_ints += 1;
-    l.pair_ints = 2 * nnz;
+    l.n_blocks = (int)ceil_div(n_rows, kRowBlock);
+    l.kw = (int)ceil_div(n_cols, 32);
+    l.bm_ints = (int64_t)n_rows * l.kw;
+    l.cnt_ints = (int64_t)l.n_blocks * n_cols;
+    l.tot_ints = (int64_t)n_cols + 1;
     return l;
 }
 
 }  // namespace
 
 bool csc_grid_fits(int n_rows, int n_cols) {
-    return ceil_div(n_rows, kChunkRows) <= INT32_MAX && ceil_div(n_cols, kTileCols) <= 65535;
+    return ceil_div(n_cols, 32) <= INT32_MAX && ceil_div(n_rows, kRowBlock) <= 65535;
 }
 
 size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz) {
-    const csc_layout l = layout(n_rows, n_cols, nnz);
-    return sizeof(int) * (size_t)(l.seg_ints + l.cnt_ints + l.tot_ints + l.pair_ints);
+    (void)nnz;
+    const csc_layout l = layout(n_rows, n_cols);
+    return sizeof(int) * (size_t)(2 * l.bm_ints + l.cnt_ints + l.tot_ints);
 }
 
 hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
-                            const float *vals, int *col_ptr, int *row_idx, int *perm,
-                            float *vals_t, void *ws, hipStream_t s) {
+                            const float *vals, const unsigned *mask, const int *pos, int *col_ptr, int *row_idx,
+                            int *perm, float *vals_t, void *ws, hipStream_t s) {
     if (n_cols == 0) return launch_fill_i32(col_ptr, 1, 0, s);
     if (n_rows == 0) return launch_fill_i32(col_ptr, (int64_t)n_cols + 1, 0, s);
-    const csc_layout l = layout(n_rows, n_cols, nnz);
-    int *seg = static_cast<int *>(ws);
-    int *cnt = seg + l.seg_ints;
+    const csc_layout l = layout(n_rows, n_cols);
+    int *bm = static_cast<int *>(ws);
+    int *cnt = bm + 2 * l.bm_ints;
     int *tot = cnt + l.cnt_ints;
-    int2 *pairs = reinterpret_cast<int2 *>(tot + l.tot_ints);
-    hipError_t e = launch_seg(n_rows, l.ntc, kTileShift, ptr, idx, seg, s);
-    if (e != hipSuccess) return e;
-    dim3 grid(l.n_chunks, l.ntc);
-    csc_count_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt);
+    hipError_t e;
+    if (mask == nullptr) {  // no bitmap index from the caller: build it here
+        unsigned *m = reinterpret_cast<unsigned *>(bm);
+        int *p = bm + l.bm_ints;
+        if ((e = launch_bitmap(n_rows, n_cols, ptr, idx, m, p, s)) != hipSuccess) return e;
+        mask = m;
+        pos = p;
+    }
+    dim3 grid(l.kw, l.n_blocks);
+    csc_count_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, mask, cnt);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    csc_colscan_kernel<<<(unsigned)ceil_div(n_cols, 256), 256, 0, s>>>(l.n_chunks, n_cols, cnt, tot);
+    csc_colscan_kernel<<<(unsigned)ceil_div(n_cols, 256), 256, 0, s>>>(l.n_blocks, n_cols, cnt, tot);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(tot, col_ptr, n_cols, nullptr, s)) != hipSuccess) return e;
-    csc_scatter_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, l.ntc, seg, idx, cnt, col_ptr, pairs);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     if (nnz == 0) return hipSuccess;
-    int64_t g = ceil_div(nnz, 256);
-    if (g > 65536) g = 65536;
-    csc_finish_kernel<<<(unsigned)g, 256, 0, s>>>(n_rows, nnz, ptr, pairs, vals, row_idx, perm, vals_t);
+    csc_emit_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, mask, pos, vals, cnt, col_ptr, row_idx, perm,
+                                                 vals_t);
     return hipGetLastError();
 }
 

@@ -29,8 +29,8 @@ size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz);
 // the (row chunk, column tile) grid of the build fits the launch limits
 bool csc_grid_fits(int n_rows, int n_cols);
 hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
-                            const float *vals, int *col_ptr, int *row_idx, int *perm,
-                            float *vals_t, void *ws, hipStream_t s);
+                            const float *vals, const unsigned *mask, const int *pos, int *col_ptr, int *row_idx,
+                            int *perm, float *vals_t, void *ws, hipStream_t s);
 // vals_t[q] = vals[perm[q]] for q < col_ptr[n_cols] (read on the device)
 hipError_t launch_csc_gather_vals(int n_cols, int64_t nnz_bound, const int *col_ptr, const int *perm,
                                   const float *vals, float *vals_t, hipStream_t s);

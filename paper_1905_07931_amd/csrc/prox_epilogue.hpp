@@ -28,8 +28,8 @@ __device__ __forceinline__ float soft_threshold(float w, float g, double eta, do
 
 // kernel argument of a GEMM with the prox epilogue
 struct prox_epi {
-    const unsigned *mask;  // [M][kw]
-    const int *pos;        // [M][kw]
+    const unsigned *mask;  // [kw][M] (word-major)
+    const int *pos;        // [kw][M]
     const float *vals;     // W's values (CSR order)
     double eta, t;
     int kw;                // 32-column words per row, ceil(Nn / 32)
@@ -46,14 +46,14 @@ __device__ __forceinline__ void prox_stage(const prox_epi &P, int M, int m0, int
     constexpr int WPT = BN / 32;
     const int w0 = n0 >> 5;
     for (int i = threadIdx.x; i < BM * WPT; i += NT) {
-        const int r = i / WPT, w = i - r * WPT;
+        const int w = i / BM, r = i - w * BM;  // consecutive threads: consecutive rows of a word
         const int row = m0 + r, gw = w0 + w;
         int2 v = make_int2(0, 0);
         if (row < M && gw < P.kw) {
-            const int64_t o = (int64_t)row * P.kw + gw;
+            const int64_t o = (int64_t)gw * M + row;
             v = make_int2((int)P.mask[o], P.pos[o]);
         }
-        stage[i] = v;
+        stage[r * WPT + w] = v;
     }
     __syncthreads();
 }

@@ -29,8 +29,10 @@ constexpr int kCompactCols = 3072;  // columns per compaction workgroup (whole 3
 constexpr int kCompactThreads = 256;
 constexpr int kCompactVecs = kCompactCols / (4 * kCompactThreads);  // float4 per thread: 3
 
-// mask[row][w] bit c: column 32w + c is stored; pos[row][w]: CSR position of
+// mask[w][row] bit c: column 32w + c is stored; pos[w][row]: CSR position of
 // the row's first entry with column >= 32w (row_ptr[row + 1] past the last).
+// Word-major ([ceil(n_cols / 32)][n_rows]): a GEMM tile reads a run of rows of
+// each of its words, and the CSC build walks all rows of one word.
 // A wave takes kBitmapSpan consecutive entries of one row (grid: rows x
 // spans; waves past their row's end only handle an empty row), 64 at a time.
 // Entries of one word sit in consecutive positions (columns are sorted), so a
@@ -50,14 +52,16 @@ __global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spa
     if (row >= n_rows) return;
     const int lane = threadIdx.x & 63;
     const int s = ptr[row], e = ptr[row + 1];
-    unsigned *mr = mask + (int64_t)row * kw;
-    int *pr = pos + (int64_t)row * kw;
+    // word x of this row at mr[x * n_rows]
+    unsigned *mr = mask + row;
+    int *pr = pos + row;
+    const int64_t st = n_rows;
     const int b0 = s + span * kBitmapSpan;
     if (s == e) {  // an empty row: every word empty, pos = the row's start
         if (span == 0)
             for (int x = lane; x < kw; x += kWave) {
-                mr[x] = 0u;
-                pr[x] = s;
+                mr[x * st] = 0u;
+                pr[x * st] = s;
             }
         return;
     }
@@ -104,23 +108,23 @@ __global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spa
         const int n = min(kWave, b1 - base);
         int wn = __shfl_down(w, 1, kWave);
         if (lane == n - 1) wn = base + n < b1 ? lane_bcast(cu[u + 1 < U ? u + 1 : u], 0) >> 5 : after;
-        if (valid && wn != w) mr[w] = v;  // the word's last entry in the row
+        if (valid && wn != w) mr[w * st] = v;  // the word's last entry in the row
         int pw = __shfl_up(w, 1, kWave);
         if (lane == 0) pw = prevw;
         if (valid && w != pw) {
             for (int x = pw + 1; x < w; ++x) {  // empty words before this one
-                mr[x] = 0u;
-                pr[x] = p;
+                mr[x * st] = 0u;
+                pr[x * st] = p;
             }
-            pr[w] = p;
+            pr[w * st] = p;
         }
         prevw = lane_bcast(w, n - 1);
         carry = (unsigned)lane_bcast((int)v, n - 1);
     }
     if (b1 == e)
         for (int x = prevw + 1 + lane; x < kw; x += kWave) {  // words past the row's last entry
-            mr[x] = 0u;
-            pr[x] = e;
+            mr[x * st] = 0u;
+            pr[x * st] = e;
         }
 }
 
@@ -138,7 +142,7 @@ __global__ __launch_bounds__(256) void prox_words_kernel(int n_rows, int n_cols,
         const bool valid = col < n_cols;
         float o = 0.f;
         if (valid) {
-            const int64_t wo = (int64_t)row * P.kw + (col >> 5);
+            const int64_t wo = (int64_t)(col >> 5) * n_rows + row;
             const unsigned m = P.mask[wo];
             const bool stored = (m >> (lane & 31)) & 1u;
             const float w = stored ? P.vals[P.pos[wo] + __popc(m & below)] : 0.f;

@@ -21,12 +21,12 @@ gradient of Y.  The calls keep the dependencies of a training loop and run on
 two streams of equal (default) priority:
 
     main:  fwd ──────────┬── dW GEMM + prox ──── recompress ───┐
-    side:  CSC, bitmap ──┴─────── bwd (W^T dY) ────────────────┴─ join
+    side:  bitmap ─┴─ CSC ──────── bwd (W^T dY) ───────────────┴─ join
 
-The CSC copy and the bitmap index that the GEMM's prox epilogue reads W
-through depend on W only, so they fill the gaps of the forward product's
-planning launches; the backward product needs dY and the CSC and runs beside
-the weight update.  Every launch is deterministic, so the outputs equal those
+W's bitmap index (read by the GEMM's prox epilogue and by the CSC build)
+and the CSC copy depend on W only, so they fill the gaps of the forward
+product's planning launches; the backward product needs dY and the CSC and
+runs beside the weight update.  Every launch is deterministic, so the outputs equal those
 of the same calls made one after another on one stream, bit for bit.
 
 The overlap pays where a product takes the tiled path (a workspace for its
@@ -86,7 +86,7 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
     precision selects the dense weight gradient's arithmetic (F32 or BF16X3).
     side: the stream to fork onto (default: one per device).  events: optional
     {call name: (start, end)} torch events, recorded around that call on the
-    stream it runs on ("csc_build", "csr_bitmap_build", "csr_spmm_fwd",
+    stream it runs on ("csr_bitmap_build", "csc_build", "csr_spmm_fwd",
     "csr_spmm_bwd_t", "dense_wgrad_prox", "csr_recompress_counted"; adaptive:
     "dense_wgrad",
     "prox_adaptive_recompress").  schedule: "two_stream", "serial" (every call on the
@@ -94,7 +94,8 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
     adaptive: Prox-RMSProp / Prox-ADAM state with dense [N][K] m, v; the step
     then ends with prox_adaptive_recompress (state updated in place, t
     advanced) instead of dense_wgrad_prox + csr_recompress_counted.  bitmap: buffers for
-    W's bitmap index (Bitmap.empty(N, K)); allocated per call if None.  All
+    W's bitmap index (Bitmap.empty(N, K), shared by the CSC build and the weight
+    update); allocated per call if None.  All
     outputs are ready on the
     caller's stream when the call returns.  Returns out.
     """
@@ -120,16 +121,15 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
             ev[1].record(stream)
 
     fork = side is not main
-    if adaptive is None and bitmap is None:
+    if bitmap is None:
         bitmap = Bitmap.empty(W.n_rows, W.n_cols, X.device)  # on the caller's stream
     if fork:
         side.wait_stream(main)  # W, X, dY as the caller left them
-    call("csc_build", side, lambda: csc_build(W, csc, stream=side))
-    if adaptive is None:
-        call("csr_bitmap_build", side, lambda: csr_bitmap_build(W, bitmap, stream=side))
-        if fork:
-            indexed = torch.cuda.Event()
-            indexed.record(side)
+    call("csr_bitmap_build", side, lambda: csr_bitmap_build(W, bitmap, stream=side))
+    if fork:
+        indexed = torch.cuda.Event()
+        indexed.record(side)
+    call("csc_build", side, lambda: csc_build(W, csc, bitmap=bitmap, stream=side))
     call("csr_spmm_fwd", main, lambda: csr_spmm_fwd(W, X, Y, stream=main))
     if fork:
         side.wait_stream(main)  # dY follows Y; the CSC is on side already

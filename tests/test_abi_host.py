@@ -112,8 +112,8 @@ def _setup(lib):
                                        C.c_void_p, C.c_int64, C.c_void_p, C.c_int64, C.c_int32,
                                        C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
     lib.csc_build.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
-                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
-                              C.c_void_p]
+                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                              C.c_void_p, C.c_size_t, C.c_void_p]
     lib.csr_spmm_bwd_t.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_void_p,
                                    C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_int64, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p,
@@ -183,7 +183,9 @@ def test_invalid_arguments_are_rejected_before_launch(lib):
     # SDDMM: missing output
     assert lib.sddmm_masked_wgrad(4, 4, 3, P, P, P, 8, P, 8, 8, NUL, P, 1 << 20, S) == EINVAL
     # CSC build: missing workspace
-    assert lib.csc_build(4, 4, 3, P, P, P, P, P, P, P, NUL, 0, S) == EINVAL
+    assert lib.csc_build(4, 4, 3, P, P, P, NUL, NUL, P, P, P, P, NUL, 0, S) == EINVAL
+    # CSC build: half a bitmap index
+    assert lib.csc_build(4, 4, 3, P, P, P, P, NUL, P, P, P, P, P, 1 << 20, S) == EINVAL
     # backward: half a CSC (row_idx without col_ptr)
     assert lib.csr_spmm_bwd_t(4, 4, 3, P, P, P, NUL, P, NUL, P, 8, 8, P, 8, NUL, 0, S) == EINVAL
 

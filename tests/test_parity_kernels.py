@@ -165,13 +165,30 @@ def test_csc_build_bit_exact(shape):
 
 
 def test_csc_build_wide_matrix_column_tiles():
-    # more than one LDS tile of columns and a ragged row chunk
+    # many 32-column words, a ragged last word
     L = synth.fc_layer(45, 40000, 1, 30000, seed=12)
     csc = L1.csc_build(_W(L))
     cp, ri, pm = csc_reference(L.row_ptr, L.col_idx, L.K)
     assert bits_equal(h(csc.col_ptr), cp)
     assert bits_equal(h(csc.row_idx)[: L.nnz], ri)
     assert bits_equal(h(csc.perm)[: L.nnz], pm)
+
+
+@pytest.mark.parametrize("shape", [(10000, 70, 1, 300000, 14), (9216, 4096, 1, 3397386, 15), (12289, 1, 1, 9000, 16)],
+                         ids=_ids)
+def test_csc_build_tall_matrices_row_blocks(shape):
+    # several 4096-row blocks per word (ragged last block), a one-column
+    # matrix, and the transposed shape of the 9216 -> 4096 layer; built with
+    # a bitmap index from csr_bitmap_build (as the step does) and without
+    N, K, B, nnz, seed = shape
+    L = synth.fc_layer(N, K, B, nnz, seed=seed)
+    W = _W(L)
+    cp, ri, pm = csc_reference(L.row_ptr, L.col_idx, L.K)
+    for csc in (L1.csc_build(W), L1.csc_build(W, bitmap=L1.csr_bitmap_build(W))):
+        assert bits_equal(h(csc.col_ptr), cp)
+        assert bits_equal(h(csc.row_idx)[: L.nnz], ri)
+        assert bits_equal(h(csc.perm)[: L.nnz], pm)
+        assert bits_equal(h(csc.vals_t)[: L.nnz], L.vals[pm])
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=_ids)

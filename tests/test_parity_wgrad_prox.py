@@ -205,9 +205,9 @@ def test_bitmap_index_bit_exact(case):
     W = L1.CSR.from_host(rp, ci, vals, K, device=cuda())
     bm = L1.csr_bitmap_build(W)
     mask, pos = _bitmap_reference(rp, ci, N, K)
-    kw = (K + 31) // 32
-    assert bits_equal(h(bm.mask).reshape(-1)[: N * kw].reshape(N, kw), mask)
-    assert bits_equal(h(bm.pos).reshape(-1)[: N * kw].reshape(N, kw), pos)
+    kw = (K + 31) // 32  # word-major on the device: [kw][N]
+    assert bits_equal(np.ascontiguousarray(h(bm.mask).reshape(-1)[: N * kw].reshape(kw, N).T), mask)
+    assert bits_equal(np.ascontiguousarray(h(bm.pos).reshape(-1)[: N * kw].reshape(kw, N).T), pos)
 
 
 def test_fused_update_with_prebuilt_bitmap():
