@@ -18,6 +18,10 @@ informational JSON line; bench.py's default line is the metric.
     conv2_direct  LeNet-5 conv2 from real 20 x 12 x 12 maps, batch 256: direct
                   sparse conv forward and input gradient, im2col + filter
                   gradient (dense and pattern-sampled), prox + recompression
+    hbm_kernels   one line per call of the memory-bound shapes (conv2 as im2col,
+                  4096 x 4096 at 1% density): warm and cold-cache (1 GiB
+                  written before each call) time, algorithmic bytes, their
+                  rate against 8 TB/s and against a measured device copy
 """
 from __future__ import annotations
 
@@ -499,7 +503,185 @@ def conv2_direct(args, dev):
                 note="value over the l1-step calls; the sampled filter gradient is the debiasing phase's")
 
 
+PEAK_HBM_GBS = 8000.0
+HBM_COUNTERS = os.path.join(ROOT, "profiles", "hbm_kernels_conv2_fc4096d1_counters.txt")
+
+
+def csrc_hash():
+    """Hash of every kernel source: counter bytes are used only if they were
+    taken on the current sources."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_1905_07931_amd", "csrc")
+    h = hashlib.sha256()
+    for n in sorted(os.listdir(d)):
+        if n.endswith((".hip", ".hpp")):
+            with open(os.path.join(d, n), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _counter_bytes():
+    """{"workload/call": FETCH+WRITE bytes per call} from the committed counter
+    summary, or {} if it is missing or was taken on other sources."""
+    if not os.path.exists(HBM_COUNTERS):
+        return {}
+    with open(HBM_COUNTERS) as f:
+        for line in f:
+            if line.startswith("counters_json:"):
+                d = json.loads(line.split(":", 1)[1])
+                if d.get("source_hash") == csrc_hash():
+                    return d.get("bytes_per_call", {})
+    return {}
+
+
+def _copy_ceiling(torch, dev):
+    """Bytes moved (read + write) per second by a 1 GiB device-to-device copy."""
+    x = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        y.copy_(x)
+    b.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * (1 << 30) / (a.elapsed_time(b) / 5 * 1e-3) / 1e9
+    del x, y
+    return gbs
+
+
+def _call_times(torch, call, reps, flush, order, tag):
+    """Median event time of `call` warm (back-to-back calls) and cold (a 1 GiB
+    write before each call, so neither L2 nor the 256 MB MALL holds its
+    operands).  Cold calls are appended to `order` (the counter summary maps
+    the kernels between two flushes to that call)."""
+    call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        call()
+        b.record()
+    torch.cuda.synchronize()
+    warm = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    for a, b in ev:
+        flush.fill_(1.0)
+        order.append(tag)
+        a.record()
+        call()
+        b.record()
+    torch.cuda.synchronize()
+    cold = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    return warm, cold
+
+
+def hbm_kernels(args, dev):
+    import torch
+    import paper_1905_07931_amd as L1
+    from paper_1905_07931_amd import synth
+    copy_gbs = _copy_ceiling(torch, dev)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+    counted = _counter_bytes()
+    order = []
+    reps = max(args.steps, 10)
+    lines = []
+
+    def emit(workload, cfg, call, ms_warm, ms_cold, alg, note):
+        tag = f"{workload}/{call}"
+        cb = counted.get(tag)
+        g_cold = alg / (ms_cold * 1e-3) / 1e9
+        g_warm = alg / (ms_warm * 1e-3) / 1e9
+        lines.append({"metric": "achieved HBM GB/s (algorithmic bytes)", "value": round(g_cold, 1), "unit": "GB/s",
+                      "n_gpus": 1, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+                      "config": dict(workload=workload, call=call, **cfg), "informational": True,
+                      "ms_cold": round(ms_cold, 4), "ms_warm": round(ms_warm, 4), "algorithmic_bytes": alg,
+                      "hbm_gbs_cold": round(g_cold, 1), "hbm_gbs_warm": round(g_warm, 1),
+                      "frac_of_8tbs_cold": round(g_cold / PEAK_HBM_GBS, 4),
+                      "frac_of_copy_cold": round(g_cold / copy_gbs, 4), "copy_ceiling_gbs": round(copy_gbs, 1),
+                      "counter_bytes": cb, "counter_over_alg": round(cb / alg, 3) if cb else None,
+                      "note": note})
+
+    # LeNet-5 conv2 lowered by im2col: W 50 x 500 at 10%, X[500][16384]
+    L = synth.conv2_im2col(seed=0)
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, L.K, device=dev)
+    vals0 = W.vals.clone()
+    X, dY = torch.from_numpy(L.X).to(dev), torch.from_numpy(L.dY).to(dev)
+    Y = torch.empty((L.N, L.B), dtype=torch.float32, device=dev)
+    dX = torch.empty((L.K, L.B), dtype=torch.float32, device=dev)
+    gv = torch.empty(L.nnz, dtype=torch.float32, device=dev)
+    csc = L1.CSC.empty(L.K, L.nnz, dev)
+    L1.csc_build(W, csc)
+    Wc = L1.CSR(L.N, L.K, torch.empty(L.N + 1, dtype=torch.int32, device=dev),
+                torch.empty(L.nnz, dtype=torch.int32, device=dev),
+                torch.empty(L.nnz, dtype=torch.float32, device=dev), None)
+    N, K, B, nnz = L.N, L.K, L.B, L.nnz
+    wl, cfg = "conv2_im2col_50x500_b16384_d10", dict(N=N, K=K, B=B, nnz=nnz)
+    csr_b = 8.0 * nnz + 4.0 * (N + 1)
+    calls = [
+        ("csr_spmm_fwd", lambda: L1.csr_spmm_fwd(W, X, Y), csr_b + 4.0 * (K + N) * B, "CSR + X in, Y out"),
+        ("csc_build", lambda: L1.csc_build(W, csc), csr_b + 12.0 * nnz + 4.0 * (K + 1),
+         "CSR in; col_ptr, row_idx, perm, vals_t out"),
+        ("csr_spmm_bwd_t", lambda: L1.csr_spmm_bwd_t(W, dY, csc, dX), 8.0 * nnz + 4.0 * (K + 1) + 4.0 * (K + N) * B,
+         "CSC + dY in, dX out"),
+        ("sddmm_masked_wgrad", lambda: L1.sddmm_masked_wgrad(W, dY, X, gv), csr_b + 4.0 * (K + N) * B + 4.0 * nnz,
+         "pattern + dY + X in, gv out"),
+        ("prox_l1_step_csr", lambda: L1.prox_l1_step(L1.PROX_CSR, W, gv, L.eta, L.lam), 12.0 * nnz,
+         "vals and gv in, vals out (support-restricted prox)"),
+        ("csr_compact", lambda: L1.csr_compact(W, Wc), csr_b + 8.0 * nnz + 4.0 * (N + 1),
+         "CSR in, CSR without stored zeros out"),
+    ]
+    for name, fn, alg, note in calls:
+        def fnr(fn=fn):
+            fn()
+        w, c = _call_times(torch, fnr, reps, flush, order, f"{wl}/{name}")
+        W.vals.copy_(vals0)
+        emit(wl, cfg, name, w, c, alg, note)
+    del X, dY, Y, dX
+
+    # the 4096 x 4096 layer at 1% density, batch 512 (one l1 iteration's calls)
+    L = synth.fc4096_sweep(0.01)
+    lam = json.load(open(os.path.join(ROOT, "tests", "golden", "fc4096_lambda.json")))["lambda"]["1"]
+    x_, d_ = synth.fc4096_batch(0)
+    X, dY = torch.from_numpy(x_).to(dev), torch.from_numpy(d_).to(dev)
+    N, K, B, nnz = L.N, L.K, L.B, L.nnz
+    W = L1.CSR.from_host(L.row_ptr, L.col_idx, L.vals, K, device=dev)
+    Y = torch.empty((N, B), dtype=torch.float32, device=dev)
+    dX = torch.empty((K, B), dtype=torch.float32, device=dev)
+    gv = torch.empty(nnz, dtype=torch.float32, device=dev)
+    dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+    Z = torch.empty((N, K), dtype=torch.float32, device=dev)
+    csc = L1.CSC.empty(K, nnz, dev)
+    L1.csc_build(W, csc)
+    bm = L1.csr_bitmap_build(W)
+    L1.dense_wgrad(dY, X, dW)
+    out = _csr_out(L1, torch, N, K, dev)
+    _, wc = L1.dense_wgrad_prox(W, dY, X, L.eta, lam, bm, Z=Z)
+    L1.csr_recompress_counted(Z, wc, out=out)
+    nnz_out = out.host_nnz()
+    wl, cfg = "fc4096_b512_d1", dict(N=N, K=K, B=B, nnz=nnz, nnz_out=nnz_out)
+    csr_b = 8.0 * nnz + 4.0 * (N + 1)
+    kw = (K + 31) // 32
+    calls = [
+        ("csr_spmm_fwd", lambda: L1.csr_spmm_fwd(W, X, Y), csr_b + 4.0 * (K + N) * B, "CSR + X in, Y out"),
+        ("csr_spmm_bwd_t", lambda: L1.csr_spmm_bwd_t(W, dY, csc, dX), 8.0 * nnz + 4.0 * (K + 1) + 4.0 * (K + N) * B,
+         "CSC + dY in, dX out"),
+        ("sddmm_masked_wgrad", lambda: L1.sddmm_masked_wgrad(W, dY, X, gv), csr_b + 4.0 * (K + N) * B + 4.0 * nnz,
+         "pattern + dY + X in, gv out"),
+        ("prox_l1_recompress", lambda: L1.prox_l1_recompress(W, dW, L.eta, lam, out=out, capacity=N * K),
+         4.0 * N * K + csr_b + 8.0 * nnz_out + 4.0 * (N + 1), "dW + CSR in (dW once), CSR' out"),
+        ("csr_recompress_counted", lambda: L1.csr_recompress_counted(Z, wc, out=out, capacity=N * K),
+         4.0 * N * K + 4.0 * N * kw + 8.0 * nnz_out + 4.0 * (N + 1), "Z + word counts in, CSR' out"),
+        ("csr_bitmap_build", lambda: L1.csr_bitmap_build(W, bm), csr_b + 8.0 * N * kw, "CSR in, mask + pos out"),
+    ]
+    for name, fn, alg, note in calls:
+        w, c = _call_times(torch, fn, reps, flush, order, f"{wl}/{name}")
+        emit(wl, cfg, name, w, c, alg, note)
+    lines.append({"hbm_kernels_cold_order": order, "source_hash": csrc_hash(), "informational": True})
+    yield from lines
+
+
 def run(name, args, dev):
     return {"fc784x300": fc784x300, "mlp784": mlp784, "conv2": conv2, "fc4096_sweep": fc4096_sweep,
             "fc9216x4096_adaptive": fc9216x4096_adaptive, "lenet5_inference": lenet5_inference,
-            "conv2_direct": conv2_direct}[name](args, dev)
+            "conv2_direct": conv2_direct, "hbm_kernels": hbm_kernels}[name](args, dev)

@@ -107,8 +107,13 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
  * of stored entries (row_ptr[n_rows]) or an upper bound on it (it only picks
  * the kernel).  ws (nullable) enables the LDS-tiled kernel and must then hold
  * l1csr_workspace_bytes(L1CSR_OP_SPMM, n_rows, n_cols, nnz, B) bytes; without
- * it a row-per-wave kernel runs.  Each Y entry is summed by one wave in
- * ascending p order (fp32 fused multiply-adds), so results are reproducible.
+ * it a row-per-wave kernel runs.  Summation order (fp32 fused multiply-adds):
+ * the row-per-wave kernel sums each Y entry in ascending p order; the tiled
+ * kernel sums a row in ascending p order too unless it cuts the row into k
+ * strided pieces (long rows: piece j takes p = row_ptr[i] + j, + j + k, ...),
+ * each summed in ascending p order and the k partial sums then added in piece
+ * order.  Either order is fixed by the operands alone, so results are
+ * reproducible run to run and under any schedule.
  */
 int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
                  const int32_t *row_ptr, const int32_t *col_idx, const float *vals,

@@ -95,12 +95,19 @@ __global__ __launch_bounds__(256) void csc_colscan_kernel(int n_chunks, int n_co
 // ballot ranks them.  Columns are taken eight at a time: every entry goes to
 // an LDS run of its column (the first kRunCap of the block's entries of that
 // column; any further ones, only in very dense columns, are stored directly),
-// and the runs are then written with consecutive lanes on consecutive
-// positions, the values gathered there.
+// and the eight runs are then written as one sequence, consecutive threads on
+// consecutive positions, with all of a thread's value gathers issued before
+// its stores.
+//
+// Work items are (row block, word) in row-block-major order, and the blocks
+// are dealt to the 8 XCDs in contiguous ranges: one XCD takes neighbouring
+// words of a row block, whose entries share the cache lines of W's values
+// (a row's entries of consecutive words are consecutive in the CSR).
 constexpr int kRunCols = 8;
 constexpr int kRunCap = 256;
+constexpr int kRunPer = kRunCols * kRunCap / kCscThreads;  // staged entries per thread per chunk
 
-__global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n_cols,
+__global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n_cols, int kw,
                                                                const unsigned *__restrict__ mask,
                                                                const int *__restrict__ pos,
                                                                const float *__restrict__ vals,
@@ -111,12 +118,21 @@ __global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n
                                                                float *__restrict__ vals_t) {
     constexpr int NW = kCscThreads / kWave, G = kWaveRows / kWave;
     __shared__ int start[NW + 1][32];  // [j][c]: column c's entries of waves < j (row NW: block total)
+    __shared__ int64_t dst0[32];       // first output position of column c's entries of this block
     __shared__ int run_row[kRunCols][kRunCap];
     __shared__ int run_p[kRunCols][kRunCap];
-    const int w = blockIdx.x, rb = blockIdx.y;
+    int64_t item = blockIdx.x;
+    {
+        const int64_t total = (int64_t)gridDim.x, per = total / 8;
+        if (item < per * 8) item = (item % 8) * per + item / 8;
+    }
+    const int rb = (int)(item / kw), w = (int)(item - (int64_t)rb * kw);
     const int r0 = rb * kRowBlock, r1 = min(n_rows, r0 + kRowBlock);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nc = min(32, n_cols - 32 * w);
     const int64_t o = (int64_t)w * n_rows;
+    if (threadIdx.x < nc)
+        dst0[threadIdx.x] = (int64_t)col_ptr[32 * w + threadIdx.x] + cnt[(int64_t)rb * n_cols + 32 * w + threadIdx.x];
     unsigned m[G];
     int ps[G];
 #pragma unroll
@@ -146,7 +162,6 @@ __global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n
         start[NW][threadIdx.x] = run;
     }
     __syncthreads();
-    const int nc = min(32, n_cols - 32 * w);
     for (int c0 = 0; c0 < nc; c0 += kRunCols) {
 #pragma unroll
         for (int cc = 0; cc < kRunCols; ++cc) {
@@ -166,7 +181,7 @@ __global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n
                         run_row[cc][q] = row;
                         run_p[cc][q] = p;
                     } else {  // beyond the staged run: straight to the output
-                        const int64_t d = (int64_t)col_ptr[32 * w + c] + cnt[(int64_t)rb * n_cols + 32 * w + c] + q;
+                        const int64_t d = dst0[c] + q;
                         row_idx[d] = row;
                         perm[d] = p;
                         vals_t[d] = vals[p];
@@ -176,17 +191,35 @@ __global__ __launch_bounds__(kCscThreads) void csc_emit_kernel(int n_rows, int n
             }
         }
         __syncthreads();
-        // the staged runs, consecutive threads on consecutive positions
-        for (int cc = 0; cc < kRunCols && c0 + cc < nc; ++cc) {
-            const int c = 32 * w + c0 + cc;
-            const int n = min(kRunCap, start[NW][c0 + cc]);
-            const int64_t d0 = (int64_t)col_ptr[c] + cnt[(int64_t)rb * n_cols + c];
-            for (int q = threadIdx.x; q < n; q += kCscThreads) {
-                const int p = run_p[cc][q];
-                row_idx[d0 + q] = run_row[cc][q];
-                perm[d0 + q] = p;
-                vals_t[d0 + q] = vals[p];
+        // the staged runs of the chunk's columns back to back: entry i of the
+        // sequence is entry i - roff[cc] of column cc's run
+        int roff[kRunCols + 1];
+        roff[0] = 0;
+#pragma unroll
+        for (int cc = 0; cc < kRunCols; ++cc)
+            roff[cc + 1] = roff[cc] + (c0 + cc < nc ? min(kRunCap, start[NW][c0 + cc]) : 0);
+        int qc[kRunPer], pv[kRunPer];
+        float vv[kRunPer];
+#pragma unroll
+        for (int u = 0; u < kRunPer; ++u) {
+            const int i = threadIdx.x + u * kCscThreads;
+            int cc = 0;
+#pragma unroll
+            for (int j = 1; j < kRunCols; ++j) cc += i >= roff[j] ? 1 : 0;
+            qc[u] = i < roff[kRunCols] ? (cc << 16) | (i - roff[cc]) : -1;
+            if (qc[u] >= 0) {
+                pv[u] = run_p[cc][i - roff[cc]];
+                vv[u] = vals[pv[u]];
             }
+        }
+#pragma unroll
+        for (int u = 0; u < kRunPer; ++u) {
+            if (qc[u] < 0) continue;
+            const int cc = qc[u] >> 16, q = qc[u] & 0xffff;
+            const int64_t d = dst0[c0 + cc] + q;
+            row_idx[d] = run_row[cc][q];
+            perm[d] = pv[u];
+            vals_t[d] = vv[u];
         }
         __syncthreads();  // the runs are refilled by the next columns
     }
@@ -219,7 +252,7 @@ csc_layout layout(int n_rows, int n_cols) {
 }  // namespace
 
 bool csc_grid_fits(int n_rows, int n_cols) {
-    return ceil_div(n_cols, 32) <= INT32_MAX && ceil_div(n_rows, kRowBlock) <= 65535;
+    return ceil_div(n_cols, 32) * ceil_div(n_rows, kRowBlock) <= INT32_MAX && ceil_div(n_rows, kRowBlock) <= 65535;
 }
 
 size_t csc_workspace_bytes(int n_rows, int n_cols, int64_t nnz) {
@@ -252,8 +285,8 @@ hipError_t launch_csc_build(int n_rows, int n_cols, int64_t nnz, const int *ptr,
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(tot, col_ptr, n_cols, nullptr, s)) != hipSuccess) return e;
     if (nnz == 0) return hipSuccess;
-    csc_emit_kernel<<<grid, kCscThreads, 0, s>>>(n_rows, n_cols, mask, pos, vals, cnt, col_ptr, row_idx, perm,
-                                                 vals_t);
+    csc_emit_kernel<<<(unsigned)((int64_t)l.kw * l.n_blocks), kCscThreads, 0, s>>>(
+        n_rows, n_cols, l.kw, mask, pos, vals, cnt, col_ptr, row_idx, perm, vals_t);
     return hipGetLastError();
 }
 

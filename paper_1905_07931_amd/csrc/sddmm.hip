@@ -3,14 +3,15 @@
 //
 // Work items.  The batch is cut into ranges of NCH chunks (a chunk is 64 lanes
 // x VEC floats) and the columns into ranges of 2^shift, sized so that one
-// (batch range, column range) "unit" of X is about 1 MB.  Every row gets
+// (batch range, column range) "unit" of X is about 2 MB.  Every row gets
 // k = ceil(len / lsplit) pieces; piece j of a row takes the row's entries
 // j, j + k, j + 2k, ... that fall inside the unit's column range.  An item is
 // (unit, piece), and one wave handles one item: it keeps its batch range of
 // the dY row in registers, reads the X rows of the piece's entries (coalesced,
-// lanes over the batch), and multiplies.  Items are numbered unit-major and
-// the grid walks them in order, so at any time the chip works on about one
-// unit and every XCD's L2 holds the same 1 MB of X.
+// lanes over the batch), and multiplies.  Items are numbered unit-major; the
+// units are split into one contiguous range per XCD, and each XCD's waves walk
+// their range in order, so an XCD works on about one unit at a time, with that
+// unit's 2 MB of X in its own 4 MB L2, and no X row is fetched by two XCDs.
 //
 // Reduction over the lanes.  Four entries are reduced together: two
 // permlane32 swaps and one permlane16 swap turn four 64-lane partial vectors
@@ -27,7 +28,7 @@ namespace {
 
 constexpr int kGatherThreads = 256;                 // 4 waves
 constexpr int kGatherBlocks = 256 * 8;              // persistent grid: 8 blocks per CU
-constexpr int64_t kUnitBytes = 1 << 20;             // X bytes per (batch range, column range)
+constexpr int64_t kUnitBytes = 2 << 20;             // X bytes per (batch range, column range)
 constexpr int kTargetItems = 8192;                  // enough waves to fill the chip
 
 template <int CTRL>
@@ -153,6 +154,11 @@ __device__ __forceinline__ float item_block(const float *__restrict__ X, int64_t
 
 // One wave per item, persistent grid.  seg (R > 1) holds the column-range
 // bounds of every row: seg[row][cr] = first entry with column >= cr << shift.
+// With at least 8 units (and a grid of a multiple of 8 blocks) the units are
+// split into 8 contiguous ranges and block b walks range b mod 8 only: blocks
+// are dealt to the XCDs round-robin, so every unit is read by one XCD and its
+// X rows are fetched into one L2 (the entries of different rows that share a
+// column then hit there); otherwise all blocks walk all items.
 template <int VEC, int NCH, int G>
 __global__ __launch_bounds__(kGatherThreads) void sddmm_gather_kernel(
     int n_rows, const int *__restrict__ ptr, const int *__restrict__ idx,
@@ -161,17 +167,29 @@ __global__ __launch_bounds__(kGatherThreads) void sddmm_gather_kernel(
     const int *__restrict__ ext_n, float *__restrict__ out, int64_t nnz) {
     constexpr int CH = kWave * VEC;   // batch entries per chunk
     constexpr int BRW = NCH * CH;     // batch entries per range
+    constexpr int WPB = kGatherThreads / kWave;
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
     const int P = n_rows + (ext_n ? uniform(*ext_n) : 0);
-    const int64_t total = (int64_t)P * R * nbr;
-    const int64_t stride = (int64_t)gridDim.x * (kGatherThreads / kWave);
-    const int64_t t0 = (int64_t)blockIdx.x * (kGatherThreads / kWave) + wave;
-    // item t = u * P + q, stepped incrementally
+    const int64_t units = (int64_t)R * nbr;
+    const bool by_xcd = units >= 8 && gridDim.x % 8 == 0;
+    int64_t u_lo = 0, u_hi = units, stride, t0;
+    if (by_xcd) {
+        const int x = blockIdx.x % 8;
+        u_lo = units * x / 8;
+        u_hi = units * (x + 1) / 8;
+        stride = (int64_t)(gridDim.x / 8) * WPB;
+        t0 = (int64_t)(blockIdx.x / 8) * WPB + wave;
+    } else {
+        stride = (int64_t)gridDim.x * WPB;
+        t0 = (int64_t)blockIdx.x * WPB + wave;
+    }
+    const int64_t total = (u_hi - u_lo) * P;
+    // item t = (u - u_lo) * P + q, stepped incrementally
     const int64_t du = stride / P;
     const int dq = (int)(stride - du * P);
-    int64_t u = t0 / P;
-    int q = (int)(t0 - u * P);
+    int64_t u = u_lo + t0 / P;
+    int q = (int)(t0 % P);
 
     for (int64_t t = t0; t < total; t += stride) {
         const int br = (int)(u / R);
@@ -340,7 +358,7 @@ void launch_gather(const gplan &pl, const gwork &w, int n_rows, int64_t nnz, con
     const int64_t items = plan_items(n_rows, nnz, pl.R, pl.nbr, pl.lsplit);
     int64_t blocks = ceil_div(items, kGatherThreads / kWave);
     if (blocks > kGatherBlocks) blocks = kGatherBlocks;
-    if (blocks < 1) blocks = 1;
+    blocks = ceil_div(blocks, 8) * 8;  // whole rounds of the 8 XCDs
     sddmm_gather_kernel<VEC, NCH, G><<<(unsigned)blocks, kGatherThreads, 0, s>>>(
         n_rows, ptr, idx, dY, ldy, X, ldx, B, pl.R, pl.nbr, pl.lsplit, w.seg, w.ext, w.ext_n, out, nnz);
 }

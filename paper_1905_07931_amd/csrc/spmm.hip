@@ -76,14 +76,28 @@ __global__ __launch_bounds__(256) void seg_kernel(int n_rows, int ntiles, int sh
     const int lane = threadIdx.x & 63;
     const int s = ptr[row], e = ptr[row + 1];
     int *sr = seg + (int64_t)row * (ntiles + 1);
-    // one binary search per tile boundary (lanes over tiles); the result stays
-    // inside [s, e] even for a malformed row
+    // one search per tile boundary (lanes over tiles): 8-ary steps (seven
+    // probes loaded together) while the interval is long, then binary.  The
+    // answer stays in [lo, hi] ⊆ [s, e], also for a malformed row.
     for (int t = lane; t <= ntiles; t += kWave) {
         int lo = s, hi = e;
         if (t == 0) {
             hi = s;
         } else if (t < ntiles) {
             const int key = t << shift;
+            while (hi - lo >= 8) {
+                const int step = (hi - lo) >> 3;
+                int v[7];
+#pragma unroll
+                for (int u = 0; u < 7; ++u) v[u] = idx[lo + (u + 1) * step];
+                int c = 0;
+#pragma unroll
+                for (int u = 0; u < 7; ++u) c += v[u] < key ? 1 : 0;
+                // probes 1..c lie before the answer, probe c + 1 (if any) at or after it
+                const int nlo = c > 0 ? lo + c * step + 1 : lo;
+                hi = c < 7 ? lo + (c + 1) * step : hi;
+                lo = nlo;
+            }
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (idx[mid] < key) lo = mid + 1; else hi = mid;
@@ -114,10 +128,38 @@ __device__ __forceinline__ int length_key(int len) {
     return 1 + b * (1 << kBucketBits) + sub;
 }
 
-constexpr int kPlanThreads = 1024;
+// The planner cuts rows into pieces and deals them to the waves:
+//   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces
+//           (cap = max(64, ceil(nnz / (2 nw))), so there are at most
+//           n_rows + 2 nw pieces), piece j taking every k-th entry from the
+//           j-th; pbeg[row] = index of the row's first piece (pieces are
+//           numbered row by row, which is the order the fix-up sums them in);
+//   deal:   pieces by decreasing length bucket, the piece at sorted position
+//           p going to slot i = p / nw of wave g = p mod nw, snake order over
+//           rounds (odd rounds reversed).  The order inside a bucket only
+//           decides which wave computes a piece, never how it is summed.
+//   table:  slot i of wave g = (row, first strided position, k, entries), row
+//           = -1 for an empty slot.
+// Two launches over contiguous row blocks (a counting sort by bucket):
+// plan_hist_kernel writes every block's bucket histogram and piece count;
+// plan_deal_kernel derives its block's start in every bucket and its pieces'
+// numbers from all blocks' counts, then deals its pieces with LDS cursors.
+constexpr int kPlanThreads = 256;
+constexpr int kPlanMaxBlocks = 64;
 
-// block-wide inclusive scan of one value per thread (all threads must call it)
-__device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total) {
+__device__ __forceinline__ int plan_cap(const int *__restrict__ ptr, int n_rows, int nw) {
+    // pieces of at most half the mean load per wave (from the actual number of
+    // entries, read on the device): with the snake deal the heaviest and
+    // lightest waves then differ by a few percent even for power-law row
+    // lengths (a cap of the full mean leaves ~30%)
+    const int64_t nnz = ptr[n_rows] - ptr[0];
+    const int64_t cap64 = (nnz + 2 * (int64_t)nw - 1) / (2 * (int64_t)nw);
+    return (int)(cap64 < 64 ? 64 : (cap64 > INT32_MAX ? INT32_MAX : cap64));
+}
+
+// block-wide exclusive scan of one value per thread (all kPlanThreads threads
+// call it); total = the block's sum
+__device__ __forceinline__ int plan_excl_scan(int v, int *wave_tot, int &total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int incl = wave_incl_scan(v);
     if (lane == 63) wave_tot[wave] = incl;
@@ -131,118 +173,118 @@ __device__ __forceinline__ int block_incl_scan(int v, int *wave_tot, int &total)
         total += t;
     }
     __syncthreads();  // wave_tot is reused by the next call
-    return before + incl;
+    return before + incl - v;
 }
 
-// One workgroup plans the pieces and the deal:
-//   pieces: a row of len > cap entries is cut into k = ceil(len / cap) pieces
-//           (cap = max(64, ceil(nnz / (2 nw))), so there are at most
-//           n_rows + 2 nw pieces), piece j taking every k-th entry from the
-//           j-th; pbeg[row] = index of the row's first piece (pieces are
-//           numbered row by row, which is the order the fix-up sums them in);
-//   deal:   pieces by decreasing length bucket, the piece at sorted position
-//           p going to slot i = p / nw of wave g = p mod nw, snake order over
-//           rounds (odd rounds reversed).  The order inside a bucket only
-//           decides which wave computes a piece, never how it is summed.
-//   table:  slot i of wave g = (row, first strided position, k, entries), row
-//           = -1 for an empty slot.
-// Rows are taken kPlanRows at a time (kPlanPer per thread, all loads issued
-// together) and kept in registers between the histogram and the deal.
-constexpr int kPlanPer = 8;
-constexpr int kPlanRows = kPlanThreads * kPlanPer;
-
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(int n_rows, const int *__restrict__ ptr,
-                                                            int nw, int rw,
-                                                            int *__restrict__ pbeg,
-                                                            int4 *__restrict__ table) {
-    __shared__ int wave_tot[kPlanThreads / kWave];
+// a row of len entries in k pieces: len % k pieces of ceil(len / k) entries,
+// the rest of floor(len / k)
+__global__ __launch_bounds__(kPlanThreads) void plan_hist_kernel(int n_rows, const int *__restrict__ ptr, int nw,
+                                                                 int rpb, int *__restrict__ bh,
+                                                                 int *__restrict__ bsum) {
     __shared__ int hist[kBuckets];
-    __shared__ int start[kBuckets];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // pieces of at most half the mean load per wave (from the actual number of
-    // entries, read on the device): with the snake deal the heaviest and
-    // lightest waves then differ by a few percent even for power-law row
-    // lengths (a cap of the full mean leaves ~30%)
-    const int64_t nnz = ptr[n_rows] - ptr[0];
-    int64_t cap64 = (nnz + 2 * (int64_t)nw - 1) / (2 * (int64_t)nw);
-    const int cap = (int)(cap64 < 64 ? 64 : (cap64 > INT32_MAX ? INT32_MAX : cap64));
-    for (int b = tid; b < kBuckets; b += kPlanThreads) hist[b] = 0;
+    __shared__ int wave_tot[kPlanThreads / kWave];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int cap = plan_cap(ptr, n_rows, nw);
+    for (int i = tid; i < kBuckets; i += kPlanThreads) hist[i] = 0;
     __syncthreads();
-    // pass 1: pieces per row, pbeg, bucket histogram
-    int carry = 0;
-    for (int base = 0; base < n_rows; base += kPlanRows) {
-        int first[kPlanPer + 1];
-#pragma unroll
-        for (int u = 0; u <= kPlanPer; ++u) {
-            const int r = min(base + tid * kPlanPer + u, n_rows);
-            first[u] = ptr[r];
-        }
-        int kk[kPlanPer], mine = 0;
-#pragma unroll
-        for (int u = 0; u < kPlanPer; ++u) {
-            const int len = first[u + 1] - first[u];
-            kk[u] = base + tid * kPlanPer + u < n_rows ? (len > cap ? (len + cap - 1) / cap : 1) : 0;
-            mine += kk[u];
-        }
-        int total;
-        int v = carry + block_incl_scan(mine, wave_tot, total) - mine;
-#pragma unroll
-        for (int u = 0; u < kPlanPer; ++u) {
-            const int r = base + tid * kPlanPer + u;
-            if (r < n_rows) pbeg[r] = v;
-            const int len = first[u + 1] - first[u];
-            for (int j = 0; j < kk[u]; ++j) atomicAdd(&hist[length_key(piece_len(len, j, kk[u]))], 1);
-            v += kk[u];
-        }
-        carry += total;
+    const int r0 = b * rpb, r1 = min(n_rows, r0 + rpb);
+    int mine = 0;
+    for (int r = r0 + tid; r < r1; r += kPlanThreads) {
+        const int len = ptr[r + 1] - ptr[r];
+        const int k = len > cap ? (len + cap - 1) / cap : 1;
+        const int big = len % k, lo = len / k;
+        if (big) atomicAdd(&hist[length_key(lo + 1)], big);
+        atomicAdd(&hist[length_key(lo)], k - big);
+        mine += k;
     }
-    const int n_pieces = carry;
-    if (tid == 0) pbeg[n_rows] = n_pieces;
-    __syncthreads();
-    // bucket starts, largest bucket first (one wave, kBPL buckets per lane)
-    constexpr int kBPL = (kBuckets + kWave - 1) / kWave;
-    if (wave == 0) {
-        int h[kBPL], sum = 0;
+    int total;
+    plan_excl_scan(mine, wave_tot, total);  // (ends with a barrier: hist is complete)
+    for (int i = tid; i < kBuckets; i += kPlanThreads) bh[(int64_t)b * kBuckets + i] = hist[i];
+    if (tid == 0) bsum[b] = total;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_deal_kernel(int n_rows, const int *__restrict__ ptr, int nw,
+                                                                 int rw, int rpb, int nb,
+                                                                 const int *__restrict__ bh,
+                                                                 const int *__restrict__ bsum,
+                                                                 int *__restrict__ pbeg,
+                                                                 int4 *__restrict__ table) {
+    constexpr int KPT = (kBuckets + kPlanThreads - 1) / kPlanThreads;  // buckets per thread
+    __shared__ int cursor[kBuckets];
+    __shared__ int wave_tot[kPlanThreads / kWave];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int cap = plan_cap(ptr, n_rows, nw);
+    // this block's start in every bucket: all pieces of larger buckets, plus
+    // the pieces of the same bucket in earlier blocks.  Thread t holds the
+    // buckets at descending positions KPT*t .. KPT*t + KPT - 1.
+    // (the blocks' counts are read 8 blocks at a time, all loads in flight)
+    int all[KPT], before[KPT], sum = 0;
 #pragma unroll
-        for (int q = 0; q < kBPL; ++q) {
-            const int b = kBuckets - 1 - (lane * kBPL + q);
-            h[q] = b >= 0 ? hist[b] : 0;
-            sum += h[q];
-        }
-        int run = wave_incl_scan(sum) - sum;
+    for (int q = 0; q < KPT; ++q) {
+        const int key = kBuckets - 1 - (KPT * tid + q);
+        all[q] = 0;
+        before[q] = 0;
+        if (key >= 0)
+            for (int c0 = 0; c0 < nb; c0 += 8) {
+                int h[8];
 #pragma unroll
-        for (int q = 0; q < kBPL; ++q) {
-            const int b = kBuckets - 1 - (lane * kBPL + q);
-            if (b >= 0) start[b] = run;
-            run += h[q];
-        }
-    }
-    __syncthreads();
-    // pass 2: deal every piece straight into its slot
-    for (int base = 0; base < n_rows; base += kPlanRows) {
-        int first[kPlanPer + 1];
+                for (int u = 0; u < 8; ++u) h[u] = c0 + u < nb ? bh[(int64_t)(c0 + u) * kBuckets + key] : 0;
 #pragma unroll
-        for (int u = 0; u <= kPlanPer; ++u) {
-            const int r = min(base + tid * kPlanPer + u, n_rows);
-            first[u] = ptr[r];
-        }
-#pragma unroll
-        for (int u = 0; u < kPlanPer; ++u) {
-            const int r = base + tid * kPlanPer + u;
-            if (r >= n_rows) continue;
-            const int len = first[u + 1] - first[u];
-            const int k = len > cap ? (len + cap - 1) / cap : 1;
-            for (int j = 0; j < k; ++j) {
-                const int plen = piece_len(len, j, k);
-                const int pos = atomicAdd(&start[length_key(plen)], 1);
-                const int i = pos / nw, gq = pos - i * nw;
-                const int g = (i & 1) ? nw - 1 - gq : gq;
-                if (i < rw) table[(int64_t)g * rw + i] = make_int4(r, first[u] + j, k, plen);
+                for (int u = 0; u < 8; ++u) {
+                    all[q] += h[u];
+                    before[q] += c0 + u < b ? h[u] : 0;
+                }
             }
+        sum += all[q];
+    }
+    int total;
+    int run = plan_excl_scan(sum, wave_tot, total);
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+        const int key = kBuckets - 1 - (KPT * tid + q);
+        if (key >= 0) cursor[key] = run + before[q];
+        run += all[q];
+    }
+    // pieces before this block, and the total
+    int first_piece = 0, n_pieces = 0;
+    for (int c0 = 0; c0 < nb; c0 += 8) {
+        int h[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) h[u] = c0 + u < nb ? bsum[c0 + u] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            first_piece += c0 + u < b ? h[u] : 0;
+            n_pieces += h[u];
         }
     }
+    // pbeg of the block's rows: each thread takes a contiguous run of rows
+    const int r0 = b * rpb, r1 = min(n_rows, r0 + rpb);
+    const int per = (rpb + kPlanThreads - 1) / kPlanThreads;
+    const int t0 = min(r1, r0 + tid * per), t1 = min(r1, t0 + per);
+    int mine = 0;
+    for (int r = t0; r < t1; ++r) {
+        const int len = ptr[r + 1] - ptr[r];
+        mine += len > cap ? (len + cap - 1) / cap : 1;
+    }
+    int blk_total;
+    int v = first_piece + plan_excl_scan(mine, wave_tot, blk_total);  // (barrier: cursors visible)
+    for (int r = t0; r < t1; ++r) {
+        const int s = ptr[r], len = ptr[r + 1] - s;
+        const int k = len > cap ? (len + cap - 1) / cap : 1;
+        pbeg[r] = v;
+        v += k;
+        for (int j = 0; j < k; ++j) {
+            const int plen = piece_len(len, j, k);
+            const int pos = atomicAdd(&cursor[length_key(plen)], 1);
+            const int i = pos / nw, gq = pos - i * nw;
+            const int g = (i & 1) ? nw - 1 - gq : gq;
+            if (i < rw) table[(int64_t)g * rw + i] = make_int4(r, s + j, k, plen);
+        }
+    }
+    if (b == nb - 1 && tid == 0) pbeg[n_rows] = n_pieces;
     // empty slots
-    for (int64_t pos = n_pieces + tid; pos < (int64_t)nw * rw; pos += kPlanThreads) {
+    for (int64_t pos = n_pieces + (int64_t)b * kPlanThreads + tid; pos < (int64_t)nw * rw;
+         pos += (int64_t)nb * kPlanThreads) {
         const int i = (int)(pos / nw), gq = (int)(pos - (int64_t)i * nw);
         const int g = (i & 1) ? nw - 1 - gq : gq;
         table[(int64_t)g * rw + i] = make_int4(-1, 0, 1, 0);
@@ -875,6 +917,8 @@ spmm_plan make_plan(int n_rows, int n_cols, int64_t nnz, int B, bool x4) {
 }
 
 struct spmm_ws {
+    int *bh;      // [plan blocks][kBuckets]: the planner's bucket histograms
+    int *bsum;    // [plan blocks]: pieces per plan block
     int *pbeg;    // [n_rows + 1]
     int *seg;     // [n_rows][ntiles + 1]
     int4 *table;  // [nw][rw]: slot table
@@ -892,6 +936,10 @@ spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     const size_t nw = (size_t)pl.nrb * kNW;
     spmm_ws w{};
     size_t off = 0;
+    w.bh = reinterpret_cast<int *>(base + off);
+    off = al(off + sizeof(int) * (size_t)kPlanMaxBlocks * kBuckets);
+    w.bsum = reinterpret_cast<int *>(base + off);
+    off = al(off + sizeof(int) * (size_t)kPlanMaxBlocks);
     w.pbeg = reinterpret_cast<int *>(base + off);
     off = al(off + sizeof(int) * ((size_t)n_rows + 1));
     w.seg = reinterpret_cast<int *>(base + off);
@@ -919,7 +967,13 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
     const int nw = pl.nrb * kNW;
     hipError_t e;
-    plan_kernel<<<1, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, w.pbeg, w.table);
+    {
+        const int nb = (int)std::min<int64_t>(kPlanMaxBlocks, ceil_div(n_rows, kPlanThreads));
+        const int rpb = (int)ceil_div(n_rows, nb);
+        plan_hist_kernel<<<nb, kPlanThreads, 0, s>>>(n_rows, ptr, nw, rpb, w.bh, w.bsum);
+        plan_deal_kernel<<<nb, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, rpb, nb, w.bh, w.bsum, w.pbeg,
+                                                      w.table);
+    }
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,
                                                              ptr, idx, w.seg);
     stream_size_kernel<VEC, HALF><<<(unsigned)ceil_div(nw, 4), 256, 0, s>>>(nw, pl.rw, pl.ntiles, w.table, w.seg,
