@@ -20,10 +20,14 @@
 
 namespace l1csr {
 
+// S_t(z) = z - t for z > t, z + t for z < -t, else 0, written as
+// z - min(max(z, -t), t): the same single rounding of z - t or z + t, and
+// z - z = +-0 in between.  Adding +0.0f after the conversion makes every
+// zero +0.0 whatever the signs of the zeros min/max return.
 __device__ __forceinline__ float soft_threshold(float w, float g, double eta, double t) {
     const double z = (double)w - eta * (double)g;
-    const double s = z > t ? z - t : (z < -t ? z + t : 0.0);
-    return (float)s;
+    const double c = fmin(fmax(z, -t), t);
+    return (float)(z - c) + 0.0f;
 }
 
 // kernel argument of a GEMM with the prox epilogue
