@@ -324,6 +324,143 @@ __global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_large_kernel(
         }
 }
 
+// The 256x288 shape with its operand tiles brought in by direct global->LDS
+// loads (no round trip through VGPRs, no LDS stores before each barrier).
+// Rows are stored unpadded, 32 floats = eight 16-byte chunks, chunk c of tile
+// row r at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1): the fragment
+// reads (32 rows, one chunk each) then hit distinct banks in every group of 8
+// lanes on 32 banks and of 16 lanes on 64 banks.  Each lane fetches the chunk
+// that belongs at its position, so one load instruction fills 1 KB of LDS.
+// Used when the reduction length is a multiple of 32 (no partial K-step to
+// zero) and the operands are 16-byte aligned.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+typedef __attribute__((address_space(3))) void gemm_lds_void;
+
+template <int ROWS>
+__device__ __forceinline__ void dma_rows(const float *__restrict__ src, int64_t ld, int rows, int row0, int k0,
+                                         float *dst) {
+    constexpr int PIECES = ROWS * (BK / 4);  // 16-byte pieces of the tile
+    static_assert(PIECES % kWave == 0, "whole waves");
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int q0 = 0; q0 < PIECES; q0 += kLargeThreads) {
+        const int qw = q0 + wave * kWave;  // this wave's first piece
+        if (qw < PIECES) {
+            const int q = qw + lane;
+            const int r = q >> 3, c = (q & 7) ^ swz(r);
+            const int grow = row0 + r < rows ? row0 + r : rows - 1;  // rows past the matrix: never stored
+            __builtin_amdgcn_global_load_lds((const void *)(src + (int64_t)grow * ld + k0 + 4 * c),
+                                             (gemm_lds_void *)(dst + qw * 4), 16, 0, 0);
+        }
+    }
+}
+
+template <bool PROX>
+__global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_dma_kernel(
+    int M, int Nn, int Kr, const float *__restrict__ A, int64_t lda, const float *__restrict__ Bt,
+    int64_t ldb, float *__restrict__ C, int64_t ldc, prox_epi P) {
+    constexpr int TM = LBM / LWM / 32, TN = LBN / LWN / 32;
+    // the two buffers of each operand as separate arrays: the compiler can
+    // then tell the reads of one from the loads into the other
+    __shared__ __attribute__((aligned(16))) float A0[LBM * BK];
+    __shared__ __attribute__((aligned(16))) float A1[LBM * BK];
+    __shared__ __attribute__((aligned(16))) float B0[LBN * BK];
+    __shared__ __attribute__((aligned(16))) float B1[LBN * BK];
+    const int m0 = blockIdx.y * LBM, n0 = blockIdx.x * LBN;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wm = (wave / LWN) * (LBM / LWM), wn = (wave % LWN) * (LBN / LWN);
+    const int lr = lane & 31;
+    const int lh = lane >> 5;
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    // fragment offsets: lane (lr, lh) reads chunk 4 lh + q of rows wm + 32a + lr
+    // (A) and wn + 32b + lr (B); f of those rows is f(lr)
+    int oa[4], ob[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int pos = (lh * 4 + q) ^ swz(lr);
+        oa[q] = (wm + lr) * BK + 4 * pos;
+        ob[q] = (wn + lr) * BK + 4 * pos;
+    }
+    const int nchunks = Kr / BK;
+    auto step = [&](int c, const float *Ac, const float *Bc, float *An, float *Bn) {
+        if (c + 1 < nchunks) {
+            dma_rows<LBM>(A, lda, M, m0, (c + 1) * BK, An);
+            dma_rows<LBN>(Bt, ldb, Nn, n0, (c + 1) * BK, Bn);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            float av[TM][4], bv[TN][4];
+#pragma unroll
+            for (int a = 0; a < TM; ++a) {
+                const float4 x = *reinterpret_cast<const float4 *>(Ac + oa[q] + a * 32 * BK);
+                av[a][0] = x.x; av[a][1] = x.y; av[a][2] = x.z; av[a][3] = x.w;
+            }
+#pragma unroll
+            for (int b = 0; b < TN; ++b) {
+                const float4 x = *reinterpret_cast<const float4 *>(Bc + ob[q] + b * 32 * BK);
+                bv[b][0] = x.x; bv[b][1] = x.y; bv[b][2] = x.z; bv[b][3] = x.w;
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int a = 0; a < TM; ++a)
+#pragma unroll
+                    for (int b = 0; b < TN; ++b)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][s], bv[b][s], acc[a][b], 0, 0, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's loads of the next K-step landed
+        __syncthreads();                     // ... and every wave's; this K-step's tiles are free
+    };
+    dma_rows<LBM>(A, lda, M, m0, 0, A0);
+    dma_rows<LBN>(Bt, ldb, Nn, n0, 0, B0);
+    __builtin_amdgcn_s_waitcnt(0x0f70);
+    __syncthreads();
+    for (int c = 0; c < nchunks; c += 2) {
+        step(c, A0, B0, A1, B1);
+        if (c + 1 < nchunks) step(c + 1, A1, B1, A0, B0);
+    }
+    if constexpr (PROX) {
+        // the last K-step ended with a barrier: the operand buffers are free.
+        // The staged index words in A0, then a gather buffer of 2 MFMA tiles
+        // (8 KB) per wave: wave 0 after the words, waves 1-4 in A1, 5-8 in B0,
+        // 9-11 in B1.
+        constexpr int TPB = 2, GBF = 16 * TPB * kWave;  // floats per wave
+        constexpr int kStageFloats = 2 * LBM * (LBN / 32);
+        static_assert(TM == 2 && LWM * LWN == 12 && sizeof(A0) >= sizeof(float) * (kStageFloats + GBF) &&
+                          sizeof(A1) >= sizeof(float) * 4 * GBF && sizeof(B0) >= sizeof(float) * 4 * GBF &&
+                          sizeof(B1) >= sizeof(float) * 3 * GBF,
+                      "staging and gather space");
+        int2 *stage = reinterpret_cast<int2 *>(A0);
+        prox_stage<LBM, LBN, kLargeThreads>(P, M, m0, n0, stage);
+        float *gbuf = wave == 0 ? A0 + kStageFloats
+                                : (wave < 5 ? A1 + (wave - 1) * GBF : (wave < 9 ? B0 + (wave - 5) * GBF : B1 + (wave - 9) * GBF));
+        prox_store<TN, LBN, TPB>(acc, M, Nn, m0, n0, wm, wn, stage, gbuf, C, ldc, P);
+        return;
+    }
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+            const int col = n0 + wn + b * 32 + lr;
+            if (col >= Nn) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                if (row < M) C[(int64_t)row * ldc + col] = acc[a][b][r];
+            }
+        }
+}
+
 // measured rates of the two shapes (whole chip, TFLOP/s) and the per-CU round
 // model the host chooses by
 constexpr int kCUs = 256;
@@ -387,6 +524,10 @@ hipError_t launch_f32_tiles(int N, int K, int B, const float *dY, int64_t ldy, c
                             float *C, int64_t ldc, bool v4, const prox_epi &P, hipStream_t s) {
     if (f32_large(N, K, B)) {
         dim3 grid((unsigned)ceil_div(K, LBN), (unsigned)ceil_div(N, LBM));
+        if (v4 && B % BK == 0) {
+            wgrad_f32_dma_kernel<PROX><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
+            return hipGetLastError();
+        }
         if (v4)
             wgrad_f32_large_kernel<true, PROX><<<grid, kLargeThreads, 0, s>>>(N, K, B, dY, ldy, X, ldx, C, ldc, P);
         else
