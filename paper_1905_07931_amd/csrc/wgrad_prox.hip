@@ -44,18 +44,13 @@ constexpr int kCompactVecs = kCompactCols / (4 * kCompactThreads);  // float4 pe
 // word is written exactly once, by one lane; no atomics.
 constexpr int kBitmapSpan = 512;
 
-__global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spans, const int *__restrict__ ptr,
-                                                     const int *__restrict__ idx, unsigned *__restrict__ mask,
-                                                     int *__restrict__ pos) {
-    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int row = (int)(item / spans), span = (int)(item - (int64_t)row * spans);
-    if (row >= n_rows) return;
+// The words of one row's span: entries [s + span * kBitmapSpan, ...) of the
+// row's entries [s, e); word x of the row goes to mr[x * st], pr[x * st]
+// (global memory or an LDS block of rows).  One wave.
+template <typename MP, typename PP>
+__device__ __forceinline__ void bitmap_span(int s, int e, int span, int kw, const int *__restrict__ idx, MP mr,
+                                            PP pr, int st) {
     const int lane = threadIdx.x & 63;
-    const int s = ptr[row], e = ptr[row + 1];
-    // word x of this row at mr[x * n_rows]
-    unsigned *mr = mask + row;
-    int *pr = pos + row;
-    const int64_t st = n_rows;
     const int b0 = s + span * kBitmapSpan;
     if (s == e) {  // an empty row: every word empty, pos = the row's start
         if (span == 0)
@@ -126,6 +121,64 @@ __global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spa
             mr[x * st] = 0u;
             pr[x * st] = e;
         }
+}
+
+// A wave per (row, span) item, written straight to the word-major arrays
+// (rows with more words than the LDS block holds).
+__global__ __launch_bounds__(256) void bitmap_kernel(int n_rows, int kw, int spans, const int *__restrict__ ptr,
+                                                     const int *__restrict__ idx, unsigned *__restrict__ mask,
+                                                     int *__restrict__ pos) {
+    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int row = (int)(item / spans), span = (int)(item - (int64_t)row * spans);
+    if (row >= n_rows) return;
+    bitmap_span(ptr[row], ptr[row + 1], span, kw, idx, mask + row, pos + row, n_rows);
+}
+
+// A workgroup per 16 consecutive rows: the (row, span) items of its rows are
+// dealt to its 16 waves and written to an LDS block [word][16 rows], which then
+// goes out 16 rows of a word at a time (64-byte segments instead of 4-byte
+// writes down the columns).
+constexpr int kBitmapRows = 16;
+constexpr int kBitmapThreads = 1024;
+constexpr int kBitmapMaxWords = 320;  // LDS block: 320 words x 16 rows x 8 bytes = 40 KB
+
+__global__ __launch_bounds__(kBitmapThreads) void bitmap_block_kernel(int n_rows, int kw, const int *__restrict__ ptr,
+                                                           const int *__restrict__ idx,
+                                                           unsigned *__restrict__ mask, int *__restrict__ pos) {
+    __shared__ unsigned lm[kBitmapMaxWords * kBitmapRows];
+    __shared__ int lp[kBitmapMaxWords * kBitmapRows];
+    __shared__ int first_item[kBitmapRows + 1];
+    const int r0 = blockIdx.x * kBitmapRows;
+    const int nr = min(kBitmapRows, n_rows - r0);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    if (wave == 0) {  // items per row (an empty row still writes its words), exclusive scan
+        int n = 0;
+        if (lane < nr) {
+            const int len = ptr[r0 + lane + 1] - ptr[r0 + lane];
+            n = len == 0 ? 1 : (len + kBitmapSpan - 1) / kBitmapSpan;
+        }
+        const int incl = wave_incl_scan(n);
+        if (lane < kBitmapRows) first_item[lane] = incl - n;
+        if (lane == kBitmapRows - 1) first_item[kBitmapRows] = incl;
+    }
+    __syncthreads();
+    const int items = first_item[kBitmapRows];
+    for (int it = wave; it < items; it += kBitmapThreads / kWave) {
+        int j = 0;  // the row of item it: last j with first_item[j] <= it
+#pragma unroll
+        for (int d = kBitmapRows / 2; d > 0; d >>= 1)
+            if (first_item[j + d] <= it) j += d;
+        const int row = r0 + j;
+        bitmap_span(ptr[row], ptr[row + 1], it - first_item[j], kw, idx, lm + j, lp + j, kBitmapRows);
+    }
+    __syncthreads();
+    for (int i = tid; i < kw * kBitmapRows; i += kBitmapThreads) {
+        const int x = i / kBitmapRows, j = i - x * kBitmapRows;
+        if (j < nr) {
+            mask[(int64_t)x * n_rows + r0 + j] = lm[i];
+            pos[(int64_t)x * n_rows + r0 + j] = lp[i];
+        }
+    }
 }
 
 // Z <- S_t(W - eta * Z) in place (Z holds dW), counts per 32-column word:
@@ -259,6 +312,11 @@ hipError_t launch_bitmap(int n_rows, int n_cols, const int *ptr, const int *idx,
                          hipStream_t s) {
     if (n_rows == 0 || n_cols == 0) return hipSuccess;
     const int kw = (int)ceil_div(n_cols, 32);
+    if (kw <= kBitmapMaxWords) {
+        bitmap_block_kernel<<<(unsigned)ceil_div(n_rows, kBitmapRows), kBitmapThreads, 0, s>>>(n_rows, kw, ptr, idx,
+                                                                                               mask, pos);
+        return hipGetLastError();
+    }
     const int spans = (int)ceil_div(n_cols, kBitmapSpan);  // a row holds at most n_cols entries
     const int64_t blocks = ceil_div((int64_t)n_rows * spans, 4);
     if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;

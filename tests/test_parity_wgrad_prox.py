@@ -178,11 +178,12 @@ def _bitmap_reference(row_ptr, col_idx, N, K):
     return mask.astype(np.uint32).view(np.int32), pos.astype(np.int32)
 
 
-@pytest.mark.parametrize("case", ["zipf", "banded", "narrow", "empty_rows"])
+@pytest.mark.parametrize("case", ["zipf", "banded", "narrow", "empty_rows", "wide", "block_edge"])
 def test_bitmap_index_bit_exact(case):
     # long rows cross the 512-entry spans of the build (words straddling a
     # span boundary), dense rows fill every word, empty rows and columns that
-    # are not a multiple of 32
+    # are not a multiple of 32; up to 320 words a row block is built in LDS
+    # (a partial last block of 16 rows), wider rows go word by word to memory
     rng = np.random.default_rng(61)
     if case == "zipf":
         N, K = 700, 9216
@@ -196,6 +197,15 @@ def test_bitmap_index_bit_exact(case):
     elif case == "narrow":
         N, K = 1000, 45
         rp, ci = synth.uniform_pattern(rng, N, K, 20000)
+    elif case == "wide":
+        N, K = 90, 20000  # 625 words: past the LDS block
+        rp, ci = synth.zipf_pattern(rng, N, K, 150000, 1.1)
+    elif case == "block_edge":
+        N, K = 33, 10240  # 320 words: the LDS block's limit; 33 rows: two full blocks and one row
+        dense = rng.random((N, K)) < 0.05
+        dense[[0, 31, 32], :] = True
+        dense[5] = False
+        rp, ci = synth.pattern_from_positions(N, K, np.flatnonzero(dense.reshape(-1)))
     else:
         N, K = 200, 1001
         dense = rng.random((N, K)) < 0.3
