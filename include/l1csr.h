@@ -121,6 +121,33 @@ int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz,
                  float *Y, int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * csr_spmm_fwd in two parts, for callers that can plan a product before its
+ * dense operand exists (Section 3.2's products; the plan depends on W and B
+ * only).  csr_spmm_plan enqueues the planning launches of the tiled kernel
+ * (row pieces, their deal to the waves, the pair stream holding W's column
+ * offsets and values) into the caller's buffer plan; csr_spmm_planned then
+ * computes Y = W . X from it, the same bits as csr_spmm_fwd with the same
+ * arguments.  Arguments as for csr_spmm_fwd; plan must hold
+ * l1csr_workspace_bytes(L1CSR_OP_SPMM, n_rows, n_cols, nnz, B) bytes (0: the
+ * product does not take the tiled path, plan may be NULL and csr_spmm_plan
+ * enqueues nothing).  Preconditions: both calls get the same n_rows, n_cols,
+ * nnz, row_ptr, col_idx, vals and B; W and plan are not modified in between;
+ * csr_spmm_planned runs after csr_spmm_plan (same stream, or ordered by the
+ * caller).  If X or Y is not 16-byte aligned with ldx, ldy and B multiples of
+ * 4, csr_spmm_planned runs the row-per-wave kernel and does not read the plan.
+ * A Y overlapping the plan is L1CSR_EINVAL.  For the backward product over a
+ * CSC copy pass (n_cols, n_rows, nnz, col_ptr, row_idx, vals_t) as the CSR and
+ * dY, dX as X, Y.
+ */
+int csr_spmm_plan(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                  const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                  int32_t B, void *plan, size_t plan_bytes, hipStream_t stream);
+int csr_spmm_planned(int32_t n_rows, int32_t n_cols, int64_t nnz,
+                     const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+                     const float *X, int64_t ldx, int32_t B, float *Y, int64_t ldy,
+                     const void *plan, size_t plan_bytes, hipStream_t stream);
+
+/*
  * Column-major copy of W (CSC) for the backward product.  Section 3.2 notes
  * that the dense x compressed product reads W by columns and cannot be
  * coalesced unless such a column-wise copy is stored; this builds it:

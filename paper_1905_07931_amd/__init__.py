@@ -21,7 +21,8 @@ __all__ = [
     "prox_adaptive_step", "prox_adaptive_recompress", "SOLVER_RMSPROP", "SOLVER_ADAM", "AdaptiveState",
     "ConvGeom", "csr_conv_fwd", "csr_conv_bwd_data", "conv_im2col", "maxpool_fwd",
     "l1_step", "side_stream", "prox_l1_recompress_noalloc", "dense_wgrad_prox", "csr_recompress_counted",
-    "dense_wgrad_prox_recompress", "csr_bitmap_build", "Bitmap",
+    "dense_wgrad_prox_recompress", "csr_bitmap_build", "Bitmap", "SpmmPlan", "csr_spmm_plan", "csr_spmm_planned",
+    "csr_spmm_bwd_t_plan", "csr_spmm_bwd_t_planned",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libl1csr.so")
@@ -60,6 +61,8 @@ def lib():
         L.l1csr_workspace_bytes.argtypes = [C.c_int, i32, i32, i64, i32]
         L.l1csr_workspace_bytes.restype = sz
         L.csr_spmm_fwd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
+        L.csr_spmm_plan.argtypes = [i32, i32, i64, vp, vp, vp, i32, vp, sz, vp]
+        L.csr_spmm_planned.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
         L.csc_build.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.csc_update_vals.argtypes = [i32, i64, vp, vp, vp, vp, vp]
         L.csr_spmm_bwd_t.argtypes = [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i32, vp, i64,
@@ -93,7 +96,7 @@ def lib():
         L.l1csr_relu_fwd.argtypes = [i64, vp, vp, vp]
         L.l1csr_relu_bwd.argtypes = [i64, vp, vp, vp, vp]
         L.l1csr_softmax_xent.argtypes = [i32, i32, vp, i64, vp, vp, vp, vp, sz, vp]
-        for name in ("csr_spmm_fwd", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
+        for name in ("csr_spmm_fwd", "csr_spmm_plan", "csr_spmm_planned", "csc_build", "csc_update_vals", "csr_spmm_bwd_t", "dense_wgrad",
                      "sddmm_masked_wgrad", "prox_l1_step", "csr_recompress", "prox_l1_recompress",
                      "prox_l1_recompress_noalloc", "dense_wgrad_prox", "csr_recompress_counted", "csr_bitmap_build",
                      "csr_compact", "csr_validate", "l1csr_relu_fwd", "l1csr_relu_bwd", "l1csr_softmax_xent",
@@ -318,6 +321,68 @@ def csr_spmm_fwd(W: CSR, X, Y=None, stream=None):
                               _p(X), ldx, B, _p(Y), ldy, _p(ws), wsb, _stream(stream)),
            "csr_spmm_fwd")
     return Y
+
+
+class SpmmPlan:
+    """A caller-owned plan of a tiled product (csr_spmm_plan): its device
+    buffer and the (n_rows, n_cols, nnz, B) it was made for."""
+
+    def __init__(self, n_rows, n_cols, nnz, B, device):
+        torch = _torch()
+        self.key = (n_rows, n_cols, nnz, B)
+        self.nbytes = workspace_bytes(OP_SPMM, n_rows, n_cols, nnz, B)
+        self.buf = torch.empty(max(self.nbytes, 1), dtype=torch.uint8, device=device) if self.nbytes else None
+
+
+def _plan_args(plan, key):
+    if plan.key != key:
+        raise ValueError(f"plan made for (n_rows, n_cols, nnz, B) = {plan.key}, used for {key}")
+    return _p(plan.buf), plan.nbytes
+
+
+def csr_spmm_plan(W: CSR, B: int, plan: SpmmPlan | None = None, stream=None) -> SpmmPlan:
+    """The planning launches of Y = W . X for a batch of B columns (no X needed)."""
+    nnz = W.validate_shapes()
+    key = (W.n_rows, W.n_cols, nnz, int(B))
+    if plan is None:
+        plan = SpmmPlan(*key, W.row_ptr.device)
+    pp, pb = _plan_args(plan, key)
+    _check(lib().csr_spmm_plan(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), int(B), pp, pb,
+                               _stream(stream)), "csr_spmm_plan")
+    return plan
+
+
+def csr_spmm_planned(W: CSR, X, plan: SpmmPlan, Y=None, stream=None):
+    """Y = W . X from a plan made by csr_spmm_plan(W, B)."""
+    torch = _torch()
+    nnz = W.validate_shapes()
+    K, B, ldx = _mat(X, "X")
+    if K != W.n_cols:
+        raise ValueError(f"X has {K} rows, W has {W.n_cols} columns")
+    if Y is None:
+        Y = torch.empty((W.n_rows, B), dtype=torch.float32, device=X.device)
+    N, By, ldy = _mat(Y, "Y")
+    if N != W.n_rows or By != B:
+        raise ValueError("Y must be [n_rows][B]")
+    pp, pb = _plan_args(plan, (W.n_rows, W.n_cols, nnz, B))
+    _check(lib().csr_spmm_planned(W.n_rows, W.n_cols, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(X), ldx, B,
+                                  _p(Y), ldy, pp, pb, _stream(stream)), "csr_spmm_planned")
+    return Y
+
+
+def _csc_as_csr(W: CSR, csc: CSC) -> CSR:
+    """W^T in CSR form: the CSC copy's arrays (for the planned backward product)."""
+    return CSR(W.n_cols, W.n_rows, csc.col_ptr, csc.row_idx, csc.vals_t, W.host_nnz())
+
+
+def csr_spmm_bwd_t_plan(W: CSR, csc: CSC, B: int, plan: SpmmPlan | None = None, stream=None) -> SpmmPlan:
+    """The planning launches of dX = W^T . dY over the CSC copy (needs W's pattern and values only)."""
+    return csr_spmm_plan(_csc_as_csr(W, csc), B, plan, stream)
+
+
+def csr_spmm_bwd_t_planned(W: CSR, dY, csc: CSC, plan: SpmmPlan, dX=None, stream=None):
+    """dX = W^T . dY from a plan made by csr_spmm_bwd_t_plan (the same bits as csr_spmm_bwd_t)."""
+    return csr_spmm_planned(_csc_as_csr(W, csc), dY, plan, dX, stream)
 
 
 def csc_build(W: CSR, out: CSC | None = None, bitmap: "Bitmap | None" = None, stream=None) -> CSC:

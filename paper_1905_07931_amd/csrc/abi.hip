@@ -266,6 +266,29 @@ int csr_spmm_fwd(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row
                                   stream));
 }
 
+int csr_spmm_plan(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,
+                  const float *vals, int32_t B, void *plan, size_t plan_bytes, hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true) || B < 0) return L1CSR_EINVAL;
+    const size_t need = spmm_workspace_bytes(n_rows, n_cols, nnz, B);
+    if (need > 0 && (plan == nullptr || plan_bytes < need)) return L1CSR_EINVAL;
+    if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    return hip_status(launch_spmm_plan(n_rows, n_cols, nnz, row_ptr, col_idx, vals, B, need > 0 ? plan : nullptr,
+                                       stream));
+}
+
+int csr_spmm_planned(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr, const int32_t *col_idx,
+                     const float *vals, const float *X, int64_t ldx, int32_t B, float *Y, int64_t ldy,
+                     const void *plan, size_t plan_bytes, hipStream_t stream) {
+    if (bad_csr(n_rows, n_cols, nnz, row_ptr, col_idx, vals, true) || B < 0) return L1CSR_EINVAL;
+    if (bad_dense(X, n_cols, B, ldx) || bad_dense(Y, n_rows, B, ldy)) return L1CSR_EINVAL;
+    const size_t need = spmm_workspace_bytes(n_rows, n_cols, nnz, B);
+    if (need > 0 && (plan == nullptr || plan_bytes < need)) return L1CSR_EINVAL;
+    if (ceil_div(B, kWave) > kMaxGridY) return L1CSR_EUNSUPPORTED;
+    if (need > 0 && bytes_overlap(Y, dense_bytes(n_rows, B, ldy), plan, need)) return L1CSR_EINVAL;
+    return hip_status(launch_spmm_planned(n_rows, n_cols, nnz, row_ptr, col_idx, vals, X, ldx, B, Y, ldy,
+                                          need > 0 ? plan : nullptr, stream));
+}
+
 int csc_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,
               const int32_t *col_idx, const float *vals, const uint32_t *mask, const int32_t *pos,
               int32_t *col_ptr, int32_t *row_idx, int32_t *perm, float *vals_t, void *ws, size_t ws_bytes,

@@ -17,6 +17,13 @@ size_t spmm_workspace_bytes(int n_rows, int n_cols, int64_t nnz, int B);
 hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
                        const float *vals, const float *X, int64_t ldx, int B, float *Y,
                        int64_t ldy, void *ws, hipStream_t s);
+// the tiled product in two parts: its planning launches (depend on W and B
+// only) into plan, then the product from that plan
+hipError_t launch_spmm_plan(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx, const float *vals,
+                            int B, void *plan, hipStream_t s);
+hipError_t launch_spmm_planned(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                               const float *vals, const float *X, int64_t ldx, int B, float *Y, int64_t ldy,
+                               const void *plan, hipStream_t s);
 hipError_t launch_spmm_scatter_atomic(int n_rows, int n_cols, const int *ptr, const int *idx,
                                       const float *vals, const float *dY, int64_t ldy, int B,
                                       float *dX, int64_t ldx, hipStream_t s);

@@ -960,10 +960,11 @@ spmm_ws carve(const spmm_plan &pl, int n_rows, int B, uintptr_t base) {
     return w;
 }
 
+// the planning launches of a tiled product: pieces and the deal, per-(row,
+// tile) bounds, chunk sizes and offsets, the pair stream (with W's values)
 template <int VEC, bool HALF>
-hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr, const int *idx,
-                     const float *vals, const float *X, int64_t ldx, int B, float *Y, int64_t ldy,
-                     void *ws, hipStream_t s) {
+hipError_t plan_tiled(const spmm_plan &pl, int n_rows, const int *ptr, const int *idx, const float *vals, int B,
+                      void *ws, hipStream_t s) {
     const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
     const int nw = pl.nrb * kNW;
     hipError_t e;
@@ -980,12 +981,19 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
                                                                        w.coff, w.wsize);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
-    {
-        constexpr int TPW = kWave / (tiled_cfg<VEC, HALF>::MAXRW <= 16 ? 16 : 32);
-        const int64_t fill_waves = (int64_t)nw * ceil_div(pl.ntiles, TPW);
-        stream_fill_kernel<VEC, HALF><<<(unsigned)ceil_div(fill_waves, 4), 256, 0, s>>>(
-            nw, pl.rw, pl.ntiles, idx, vals, w.table, w.seg, w.coff, w.woff, w.stream);
-    }
+    constexpr int TPW = kWave / (tiled_cfg<VEC, HALF>::MAXRW <= 16 ? 16 : 32);
+    const int64_t fill_waves = (int64_t)nw * ceil_div(pl.ntiles, TPW);
+    stream_fill_kernel<VEC, HALF><<<(unsigned)ceil_div(fill_waves, 4), 256, 0, s>>>(
+        nw, pl.rw, pl.ntiles, idx, vals, w.table, w.seg, w.coff, w.woff, w.stream);
+    return hipGetLastError();
+}
+
+// the product from a plan: the streamed kernel, then the fix-up of split rows
+template <int VEC, bool HALF>
+hipError_t exec_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr, const float *X, int64_t ldx, int B,
+                      float *Y, int64_t ldy, const void *ws, hipStream_t s) {
+    const spmm_ws w = carve(pl, n_rows, B, reinterpret_cast<uintptr_t>(ws));
+    hipError_t e;
     const unsigned nblocks = (unsigned)((int64_t)pl.nrb * pl.nch);
     spmm_stream_kernel<VEC, HALF><<<nblocks, kNW * kWave, 0, s>>>(pl.rw, n_cols, pl.ntiles, w.table, w.pbeg,
                                                             ptr, w.stream, w.woff, X, ldx, B, Y,
@@ -994,6 +1002,46 @@ hipError_t run_tiled(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr
     fixup_kernel<<<dim3((unsigned)n_rows, (unsigned)ceil_div(B, kFixupCols)), 256, 0, s>>>(
         n_rows, w.pbeg, w.part, B, Y, ldy);
     return hipGetLastError();
+}
+
+hipError_t plan_any(const spmm_plan &pl, int n_rows, const int *ptr, const int *idx, const float *vals, int B,
+                    void *ws, hipStream_t s) {
+    if (pl.vec == 4 && pl.half) return plan_tiled<4, true>(pl, n_rows, ptr, idx, vals, B, ws, s);
+    if (pl.vec == 4) return plan_tiled<4, false>(pl, n_rows, ptr, idx, vals, B, ws, s);
+    return plan_tiled<2, false>(pl, n_rows, ptr, idx, vals, B, ws, s);
+}
+
+hipError_t exec_any(const spmm_plan &pl, int n_rows, int n_cols, const int *ptr, const float *X, int64_t ldx, int B,
+                    float *Y, int64_t ldy, const void *ws, hipStream_t s) {
+    if (pl.vec == 4 && pl.half) return exec_tiled<4, true>(pl, n_rows, n_cols, ptr, X, ldx, B, Y, ldy, ws, s);
+    if (pl.vec == 4) return exec_tiled<4, false>(pl, n_rows, n_cols, ptr, X, ldx, B, Y, ldy, ws, s);
+    return exec_tiled<2, false>(pl, n_rows, n_cols, ptr, X, ldx, B, Y, ldy, ws, s);
+}
+
+// the row-per-wave kernel (no workspace)
+hipError_t launch_rows(int n_rows, const int *ptr, const int *idx, const float *vals, const float *X, int64_t ldx,
+                       int B, float *Y, int64_t ldy, int vec, hipStream_t s) {
+    const int64_t nrb = ceil_div(n_rows, kRowsPerBlock), nch = ceil_div(B, kWave * vec);
+    if (nrb * nch > INT32_MAX) return hipErrorInvalidConfiguration;
+    const unsigned grid = (unsigned)(nrb * nch);
+    if (vec == 4)
+        spmm_rows_kernel<4><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
+    else if (vec == 2)
+        spmm_rows_kernel<2><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
+    else
+        spmm_rows_kernel<1><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
+    return hipGetLastError();
+}
+
+bool spmm_v4(const float *X, int64_t ldx, int B, const float *Y, int64_t ldy) {
+    return (B % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) && aligned16(Y);
+}
+
+int spmm_vec(const float *X, int64_t ldx, int B, const float *Y, int64_t ldy) {
+    if (spmm_v4(X, ldx, B, Y, ldy)) return 4;
+    const bool v2 = (B % 2 == 0) && (ldx % 2 == 0) && (ldy % 2 == 0) &&
+                    ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 7u) == 0;
+    return v2 ? 2 : 1;
 }
 
 }  // namespace
@@ -1015,27 +1063,31 @@ hipError_t launch_spmm(int n_rows, int n_cols, int64_t nnz, const int *ptr, cons
                        const float *vals, const float *X, int64_t ldx, int B, float *Y,
                        int64_t ldy, void *ws, hipStream_t s) {
     if (n_rows == 0 || B == 0) return hipSuccess;
-    const bool v4 = (B % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) && aligned16(Y);
-    const bool v2 = (B % 2 == 0) && (ldx % 2 == 0) && (ldy % 2 == 0) &&
-                    ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 7u) == 0;
-    const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, ws != nullptr && v4);
+    const int vec = spmm_vec(X, ldx, B, Y, ldy);
+    const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, ws != nullptr && vec == 4);
     if (pl.tiled) {
-        if (pl.vec == 4 && pl.half)
-            return run_tiled<4, true>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
-        if (pl.vec == 4) return run_tiled<4, false>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
-        return run_tiled<2, false>(pl, n_rows, n_cols, ptr, idx, vals, X, ldx, B, Y, ldy, ws, s);
+        hipError_t e = plan_any(pl, n_rows, ptr, idx, vals, B, ws, s);
+        if (e != hipSuccess) return e;
+        return exec_any(pl, n_rows, n_cols, ptr, X, ldx, B, Y, ldy, ws, s);
     }
-    const int vec = v4 ? 4 : (v2 ? 2 : 1);
-    const int64_t nrb = ceil_div(n_rows, kRowsPerBlock), nch = ceil_div(B, kWave * vec);
-    if (nrb * nch > INT32_MAX) return hipErrorInvalidConfiguration;
-    const unsigned grid = (unsigned)(nrb * nch);
-    if (vec == 4)
-        spmm_rows_kernel<4><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
-    else if (vec == 2)
-        spmm_rows_kernel<2><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
-    else
-        spmm_rows_kernel<1><<<grid, 256, 0, s>>>(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, (int)nrb);
-    return hipGetLastError();
+    return launch_rows(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, vec, s);
+}
+
+hipError_t launch_spmm_plan(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx, const float *vals,
+                            int B, void *plan, hipStream_t s) {
+    if (n_rows == 0 || B == 0) return hipSuccess;
+    const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, plan != nullptr);
+    return pl.tiled ? plan_any(pl, n_rows, ptr, idx, vals, B, plan, s) : hipSuccess;
+}
+
+hipError_t launch_spmm_planned(int n_rows, int n_cols, int64_t nnz, const int *ptr, const int *idx,
+                               const float *vals, const float *X, int64_t ldx, int B, float *Y, int64_t ldy,
+                               const void *plan, hipStream_t s) {
+    if (n_rows == 0 || B == 0) return hipSuccess;
+    const int vec = spmm_vec(X, ldx, B, Y, ldy);
+    const spmm_plan pl = make_plan(n_rows, n_cols, nnz, B, plan != nullptr && vec == 4);
+    if (pl.tiled) return exec_any(pl, n_rows, n_cols, ptr, X, ldx, B, Y, ldy, plan, s);
+    return launch_rows(n_rows, ptr, idx, vals, X, ldx, B, Y, ldy, vec, s);
 }
 
 hipError_t launch_spmm_scatter_atomic(int n_rows, int n_cols, const int *ptr, const int *idx,

@@ -20,13 +20,14 @@ Only the forward product has to finish before the rest: dY is the upstream
 gradient of Y.  The calls keep the dependencies of a training loop and run on
 two streams of equal (default) priority:
 
-    main:  fwd ──────────┬── dW GEMM + prox ──── recompress ───┐
-    side:  bitmap ─┴─ CSC ──────── bwd (W^T dY) ───────────────┴─ join
+    main:  fwd ─────────────────────┬── dW GEMM + prox ──── recompress ───┐
+    side:  bitmap ─┴─ CSC ─ bwd plan ─┴─ bwd (W^T dY) ─────────────────────┴─ join
 
-W's bitmap index (read by the GEMM's prox epilogue and by the CSC build)
-and the CSC copy depend on W only, so they fill the gaps of the forward
-product's planning launches; the backward product needs dY and the CSC and
-runs beside the weight update.  Every launch is deterministic, so the outputs equal those
+W's bitmap index (read by the GEMM's prox epilogue and by the CSC build),
+the CSC copy and the backward product's plan (csr_spmm_plan over the CSC)
+depend on W only, so they fill the gaps of the forward product's planning
+launches; the backward product itself needs dY and runs beside the weight
+update.  Every launch is deterministic, so the outputs equal those
 of the same calls made one after another on one stream, bit for bit.
 
 The overlap pays where a product takes the tiled path (a workspace for its
@@ -45,11 +46,23 @@ for every entry point under capture, W's nnz must be known on the host
 """
 from __future__ import annotations
 
-from . import (CSC, CSR, F32, OP_SPMM, AdaptiveState, Bitmap, csc_build, csr_bitmap_build, csr_recompress_counted,
-               csr_spmm_bwd_t, csr_spmm_fwd, dense_wgrad, dense_wgrad_prox, prox_adaptive_recompress,
-               workspace_bytes)
+from . import (CSC, CSR, F32, OP_SPMM, AdaptiveState, Bitmap, SpmmPlan, csc_build, csr_bitmap_build,
+               csr_recompress_counted, csr_spmm_bwd_t, csr_spmm_bwd_t_plan, csr_spmm_bwd_t_planned, csr_spmm_fwd,
+               dense_wgrad, dense_wgrad_prox, prox_adaptive_recompress, workspace_bytes)
 
 _side_streams: dict = {}
+_plans: dict = {}
+
+
+def _bwd_plan(W: CSR, csc: CSC, B: int, side) -> SpmmPlan:
+    """The backward product's plan buffer for this shape and side stream (kept,
+    so its memory is never handed to other work while the side stream uses it)."""
+    key = (side.cuda_stream, W.n_cols, W.n_rows, W.host_nnz(), B)
+    p = _plans.get(key)
+    if p is None:
+        p = SpmmPlan(W.n_cols, W.n_rows, W.host_nnz(), B, csc.col_ptr.device)
+        _plans[key] = p
+    return p
 
 
 def side_stream(device):
@@ -87,7 +100,8 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
     side: the stream to fork onto (default: one per device).  events: optional
     {call name: (start, end)} torch events, recorded around that call on the
     stream it runs on ("csr_bitmap_build", "csc_build", "csr_spmm_fwd",
-    "csr_spmm_bwd_t", "dense_wgrad_prox", "csr_recompress_counted"; adaptive:
+    "csr_spmm_bwd_t_plan" (two streams only), "csr_spmm_bwd_t",
+    "dense_wgrad_prox", "csr_recompress_counted"; adaptive:
     "dense_wgrad",
     "prox_adaptive_recompress").  schedule: "two_stream", "serial" (every call on the
     caller's stream) or "auto" (two_stream where a product is tiled).
@@ -125,15 +139,24 @@ def l1_step(W: CSR, X, dY, eta: float, lam: float, *, Y, dX, dW, csc: CSC, out: 
         bitmap = Bitmap.empty(W.n_rows, W.n_cols, X.device)  # on the caller's stream
     if fork:
         side.wait_stream(main)  # W, X, dY as the caller left them
+    # the forward product is enqueued first, so its launches reach the GPU first
+    call("csr_spmm_fwd", main, lambda: csr_spmm_fwd(W, X, Y, stream=main))
     call("csr_bitmap_build", side, lambda: csr_bitmap_build(W, bitmap, stream=side))
     if fork:
         indexed = torch.cuda.Event()
         indexed.record(side)
     call("csc_build", side, lambda: csc_build(W, csc, bitmap=bitmap, stream=side))
-    call("csr_spmm_fwd", main, lambda: csr_spmm_fwd(W, X, Y, stream=main))
+    plan = None
     if fork:
-        side.wait_stream(main)  # dY follows Y; the CSC is on side already
-    call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t(W, dY, csc, dX, stream=side))
+        # the backward product's planning needs W (its CSC) only: it runs here,
+        # beside the forward product's planning, not behind the weight-gradient
+        # GEMM (whose workgroups fill every CU once it starts)
+        plan = _bwd_plan(W, csc, dY.shape[1], side)
+        call("csr_spmm_bwd_t_plan", side, lambda: csr_spmm_bwd_t_plan(W, csc, dY.shape[1], plan, stream=side))
+        side.wait_stream(main)  # dY follows Y; the CSC and the plan are on side already
+        call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t_planned(W, dY, csc, plan, dX, stream=side))
+    else:
+        call("csr_spmm_bwd_t", side, lambda: csr_spmm_bwd_t(W, dY, csc, dX, stream=side))
     if adaptive is None:
         if fork:
             main.wait_event(indexed)

@@ -358,3 +358,43 @@ def test_fused_weight_update_arguments_are_rejected_before_launch(lib):
     assert bb(-1, 4, 0, P, P, P, Q, S) == EINVAL
     assert bb(4, 4, 3, P, P, None, Q, S) == EINVAL
     assert bb(4, 64, 3, P, P, P, C.c_void_p((1 << 26) + 8), S) == EINVAL  # mask and pos overlap
+
+
+def test_planned_product_arguments_are_rejected_before_launch(lib):
+    """csr_spmm_plan / csr_spmm_planned check the CSR, B, the dense operands
+    and the plan buffer on the host; a shape without a tiled plan needs no
+    buffer and enqueues nothing."""
+    vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    pl = lib.csr_spmm_plan
+    pl.argtypes = [i32, i32, i64, vp, vp, vp, i32, vp, sz, vp]
+    pd = lib.csr_spmm_planned
+    pd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
+    names = ["rp", "ci", "v", "X", "Y", "plan"]
+    base = {n: (i + 1) << 30 for i, n in enumerate(names)}
+    N, K, B, nnz = 4096, 512, 512, 400000
+    need = lib.l1csr_workspace_bytes(4, N, K, nnz, B)  # L1CSR_OP_SPMM
+    assert need > 0  # the tiled path at this shape
+
+    def args(o):
+        a = dict(base)
+        a.update({k: v for k, v in o.items() if k in a})
+        return {k: (None if x is None else C.c_void_p(x)) for k, x in a.items()}
+
+    def plan(**o):
+        p = args(o)
+        return pl(o.get("N", N), K, nnz, p["rp"], p["ci"], p["v"], o.get("B", B), p["plan"], o.get("pb", need), S)
+
+    def planned(**o):
+        p = args(o)
+        return pd(o.get("N", N), K, nnz, p["rp"], p["ci"], p["v"], p["X"], o.get("ldx", B), o.get("B", B), p["Y"],
+                  o.get("ldy", B), p["plan"], o.get("pb", need), S)
+
+    assert plan() == EHIP and planned() == EHIP  # valid: only the launch fails without a GPU
+    for bad in [dict(B=-1), dict(N=-1), dict(rp=None), dict(plan=None), dict(pb=need - 1)]:
+        assert plan(**bad) == EINVAL, bad
+    for bad in [dict(B=-1), dict(rp=None), dict(X=None), dict(ldx=B - 1), dict(ldy=B - 1), dict(plan=None),
+                dict(pb=need - 1), dict(Y=base["plan"] + 4096)]:
+        assert planned(**bad) == EINVAL, bad
+    # no tiled plan at a small shape: nothing to plan, no buffer needed
+    assert lib.l1csr_workspace_bytes(4, 64, 100, 300, 16) == 0
+    assert pl(64, 100, 300, C.c_void_p(1 << 30), C.c_void_p(2 << 30), C.c_void_p(3 << 30), 16, None, 0, S) == OK

@@ -100,6 +100,53 @@ def test_spmm_power_law_rows_dyadic_bit_exact():
     assert bits_equal(h(L1.csr_spmm_fwd(W, t(X))), oracle.spmm_fwd(rp, ci, vals, X))
 
 
+# The tiled product split into its planning launches and the product from
+# the plan: the same bits as the one-call form, forward and backward, on the
+# half-wave, full-wave and VEC-2 plans and a shape with no plan; the plan is
+# made before the dense operand is written.
+PLANNED = [  # (N, K, B, nnz, seed)
+    (4096, 300, 1024, 200000, 70),    # VEC 4 half-wave (forward), full-wave (backward over 300 CSC rows)
+    (8000, 1000, 128, 1400000, 71),   # VEC 2
+    (9000, 333, 1020, 200000, 72),    # ragged tile, row block and batch chunk
+    (300, 784, 64, 23520, 73),        # no tiled plan: the rows kernel
+]
+
+
+@pytest.mark.parametrize("shape", PLANNED, ids=_ids)
+def test_planned_product_equals_one_call(shape):
+    import torch
+    L = _layer(shape)
+    W = _W(L)
+    csc = L1.csc_build(W)
+    X = torch.empty((L.K, L.B), dtype=torch.float32, device=cuda())
+    dY = torch.empty((L.N, L.B), dtype=torch.float32, device=cuda())
+    pf = L1.csr_spmm_plan(W, L.B)           # before X and dY hold anything
+    pb = L1.csr_spmm_bwd_t_plan(W, csc, L.B)
+    X.copy_(t(L.X))
+    dY.copy_(t(L.dY))
+    Yp = h(L1.csr_spmm_planned(W, X, pf))
+    dXp = h(L1.csr_spmm_bwd_t_planned(W, dY, csc, pb))
+    assert bits_equal(Yp, h(L1.csr_spmm_fwd(W, X)))
+    assert bits_equal(dXp, h(L1.csr_spmm_bwd_t(W, dY, csc)))
+    ref = oracle.spmm_fwd(L.row_ptr, L.col_idx, L.vals, L.X)
+    assert_scaled_close(Yp, ref, oracle.spmm_fwd(L.row_ptr, L.col_idx, np.abs(L.vals), np.abs(L.X)), what="Y")
+    # operands the tiled kernel cannot take (ld not a multiple of 4): the plan
+    # is ignored and the rows kernel gives the one-call result
+    if L.B % 4 == 0:
+        Xs = torch.zeros((L.K, L.B + 1), dtype=torch.float32, device=cuda())
+        Xs[:, :L.B] = X
+        Xv = Xs[:, :L.B]
+        assert bits_equal(h(L1.csr_spmm_planned(W, Xv, pf)), h(L1.csr_spmm_fwd(W, Xv)))
+
+
+def test_plan_is_checked_against_its_shape():
+    L = _layer((4096, 300, 1024, 200000, 74))
+    W = _W(L)
+    p = L1.csr_spmm_plan(W, 1024)
+    with pytest.raises(ValueError):
+        L1.csr_spmm_planned(W, t(L.X[:, :512]), p)  # made for B = 1024
+
+
 def _banded_dyadic(seed):
     """4096 x 9216 at batch 1024 with every row dense over the first 128
     columns, two fully dense rows, and uniform entries elsewhere (~2.9 M in
