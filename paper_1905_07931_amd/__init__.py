@@ -328,10 +328,19 @@ class SpmmPlan:
     buffer and the (n_rows, n_cols, nnz, B) it was made for."""
 
     def __init__(self, n_rows, n_cols, nnz, B, device):
+        self.buf = None
+        self.device = device
+        self.reshape(n_rows, n_cols, nnz, B)
+
+    def reshape(self, n_rows, n_cols, nnz, B):
+        """Take this buffer for another shape, growing it if it is too small
+        (the caller orders the reuse after the last use of the old plan)."""
         torch = _torch()
         self.key = (n_rows, n_cols, nnz, B)
         self.nbytes = workspace_bytes(OP_SPMM, n_rows, n_cols, nnz, B)
-        self.buf = torch.empty(max(self.nbytes, 1), dtype=torch.uint8, device=device) if self.nbytes else None
+        if self.nbytes and (self.buf is None or self.buf.numel() < self.nbytes):
+            self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=self.device)
+        return self
 
 
 def _plan_args(plan, key):

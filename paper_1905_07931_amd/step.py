@@ -55,13 +55,21 @@ _plans: dict = {}
 
 
 def _bwd_plan(W: CSR, csc: CSC, B: int, side) -> SpmmPlan:
-    """The backward product's plan buffer for this shape and side stream (kept,
-    so its memory is never handed to other work while the side stream uses it)."""
-    key = (side.cuda_stream, W.n_cols, W.n_rows, W.host_nnz(), B)
+    """The backward product's plan buffer of this side stream, taken for this
+    shape (one buffer per side stream, grown when a larger plan needs it and
+    never freed, so its memory is not handed to other work while the side
+    stream may still use it; the steps on one side stream use it in order)."""
+    import torch
+    key = (side.cuda_stream, csc.col_ptr.device)
     p = _plans.get(key)
-    if p is None:
-        p = SpmmPlan(W.n_cols, W.n_rows, W.host_nnz(), B, csc.col_ptr.device)
-        _plans[key] = p
+    # allocated with the side stream current, like the call workspaces: a
+    # replaced buffer goes back to the caching allocator in that stream's order
+    with torch.cuda.stream(side):
+        if p is None:
+            p = SpmmPlan(W.n_cols, W.n_rows, W.host_nnz(), B, csc.col_ptr.device)
+            _plans[key] = p
+        else:
+            p.reshape(W.n_cols, W.n_rows, W.host_nnz(), B)
     return p
 
 

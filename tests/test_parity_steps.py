@@ -722,3 +722,7 @@ def test_l1_step_loop_carries_W_forward(which):
         outb.track_nnz()
         Wa, Wb = outa, outb
     torch.cuda.synchronize()
+    # the backward plans of steps with different nnz share one buffer per side stream
+    from paper_1905_07931_amd import step as step_mod
+    side = step_mod.side_stream(dev)
+    assert sum(1 for k in step_mod._plans if k[0] == side.cuda_stream) <= 1
