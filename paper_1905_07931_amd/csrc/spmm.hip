@@ -178,12 +178,18 @@ __device__ __forceinline__ int plan_excl_scan(int v, int *wave_tot, int &total) 
 
 // a row of len entries in k pieces: len % k pieces of ceil(len / k) entries,
 // the rest of floor(len / k)
+// wsize[g] is set to wbase = a bound on the bytes of wave g's stream that do
+// not depend on its pieces' lengths (chunk headers, 16 bytes per slot and
+// tile for padding); plan_deal_kernel adds 8 bytes per entry of every piece it
+// deals to g, rounded up to 16, so every stream starts 16-byte aligned.
 __global__ __launch_bounds__(kPlanThreads) void plan_hist_kernel(int n_rows, const int *__restrict__ ptr, int nw,
                                                                  int rpb, int *__restrict__ bh,
-                                                                 int *__restrict__ bsum) {
+                                                                 int *__restrict__ bsum, int *__restrict__ wsize,
+                                                                 int wbase) {
     __shared__ int hist[kBuckets];
     __shared__ int wave_tot[kPlanThreads / kWave];
     const int b = blockIdx.x, tid = threadIdx.x;
+    for (int g = b * kPlanThreads + tid; g < nw; g += gridDim.x * kPlanThreads) wsize[g] = wbase;
     const int cap = plan_cap(ptr, n_rows, nw);
     for (int i = tid; i < kBuckets; i += kPlanThreads) hist[i] = 0;
     __syncthreads();
@@ -208,7 +214,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_deal_kernel(int n_rows, con
                                                                  const int *__restrict__ bh,
                                                                  const int *__restrict__ bsum,
                                                                  int *__restrict__ pbeg,
-                                                                 int4 *__restrict__ table) {
+                                                                 int4 *__restrict__ table,
+                                                                 int *__restrict__ wsize) {
     constexpr int KPT = (kBuckets + kPlanThreads - 1) / kPlanThreads;  // buckets per thread
     __shared__ int cursor[kBuckets];
     __shared__ int wave_tot[kPlanThreads / kWave];
@@ -278,7 +285,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_deal_kernel(int n_rows, con
             const int pos = atomicAdd(&cursor[length_key(plen)], 1);
             const int i = pos / nw, gq = pos - i * nw;
             const int g = (i & 1) ? nw - 1 - gq : gq;
-            if (i < rw) table[(int64_t)g * rw + i] = make_int4(r, s + j, k, plen);
+            if (i < rw) {
+                table[(int64_t)g * rw + i] = make_int4(r, s + j, k, plen);
+                atomicAdd(&wsize[g], 8 * (plen + (plen & 1)));  // 16-byte multiples; integer sum
+            }
         }
     }
     if (b == nb - 1 && tid == 0) pbeg[n_rows] = n_pieces;
@@ -453,6 +463,166 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
             if (q < total[tt]) pp[tt][q] = v[tt];
     }
 }
+
+// The pair stream of wave g in one workgroup (used while the per-(slot, tile)
+// tables fit in 64 KB of LDS; the launches above otherwise).  A piece's
+// entries are sorted by column, so its entries in tile t form one contiguous
+// run: with n[i][t] the count of slot i's entries in tile t and start[i][t]
+// their prefix over the tiles, entry m of slot i in tile t is pair
+// m - start[i][t] of its run.  Counts go into LDS (integer atomics, order-
+// independent), then the run starts, the runs' offsets inside each chunk and
+// the chunks' offsets inside the stream are prefix sums, and every entry, the
+// chunk headers and the padding pairs of odd runs are written to their places:
+// the same bytes as the launches above, without the per-(row, tile) bounds.
+// The stream starts at woff[g] (the exclusive scan of the per-wave bounds of
+// plan_deal_kernel); the main kernel finds each chunk from the one before.
+constexpr int kBucketThreads = 1024;
+
+template <int VEC, bool HALF>
+__global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, int ntiles, const int *__restrict__ idx,
+                                                            const float *__restrict__ vals,
+                                                            const int4 *__restrict__ table,
+                                                            const int *__restrict__ woff, char *__restrict__ stream) {
+    constexpr int BB = tiled_cfg<VEC, HALF>::BB, KT = tiled_cfg<VEC, HALF>::KT, SHIFT = tiled_cfg<VEC, HALF>::SHIFT;
+    constexpr int MAXRW = tiled_cfg<VEC, HALF>::MAXRW, HDR = tiled_cfg<VEC, HALF>::HDR;
+    extern __shared__ int bsm[];
+    int *cnt = bsm;                     // [rw][ntiles]: counts, then run starts (prefix over the tiles)
+    int *roff = cnt + rw * ntiles;      // [rw][ntiles]: pair offset of the run inside its chunk
+    int *choff = roff + rw * ntiles;    // [ntiles + 1]: byte offset of each chunk inside the stream
+    __shared__ int4 slot[MAXRW];
+    __shared__ int pfx[MAXRW + 1];      // entries before each slot
+    __shared__ int wave_tot[kBucketThreads / kWave];
+    const int g = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nrw = rw < MAXRW ? rw : MAXRW;
+    if (tid < nrw) {
+        int4 e = table[(int64_t)g * rw + tid];
+        if (e.x < 0) e.w = 0;
+        slot[tid] = e;
+    }
+    for (int x = tid; x < nrw * ntiles; x += kBucketThreads) cnt[x] = 0;
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int i = 0; i < nrw; ++i) {
+            pfx[i] = run;
+            run += slot[i].w;
+        }
+        pfx[nrw] = run;
+    }
+    __syncthreads();
+    const int total = pfx[nrw];
+    auto find = [&](int e) {  // the slot of entry e: last i with pfx[i] <= e
+        int i = 0;
+        for (int d = 16; d > 0; d >>= 1)
+            if (i + d < nrw && pfx[i + d] <= e) i += d;
+        return i;
+    };
+    // (entries U at a time per thread: their loads in flight together)
+    constexpr int U = 4;
+    for (int e0 = tid; e0 < total; e0 += U * kBucketThreads) {
+        int ii[U], cc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = e0 + u * kBucketThreads;
+            ii[u] = -1;
+            if (e < total) {
+                ii[u] = find(e);
+                const int4 sl = slot[ii[u]];
+                cc[u] = idx[sl.y + (e - pfx[ii[u]]) * sl.z];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ii[u] >= 0) atomicAdd(&cnt[ii[u] * ntiles + (cc[u] >> SHIFT)], 1);
+    }
+    __syncthreads();
+    // run starts per slot (one wave per slot) and, per tile, the runs' offsets
+    // inside the chunk (padded to whole pairs of pairs)
+    for (int i = wave; i < nrw; i += kBucketThreads / kWave) {
+        int carry = 0;
+        for (int t0 = 0; t0 < ntiles; t0 += kWave) {
+            const int t = t0 + lane;
+            const int n = t < ntiles ? cnt[i * ntiles + t] : 0;
+            const int incl = wave_incl_scan(n);
+            if (t < ntiles) cnt[i * ntiles + t] = carry + incl - n;
+            carry += lane_bcast(incl, kWave - 1);
+        }
+    }
+    __syncthreads();
+    int mine = 0;  // this thread's tiles' chunk bytes (tiles tid * per .. + per)
+    const int per = (ntiles + kBucketThreads - 1) / kBucketThreads;
+    const int ta = min(ntiles, tid * per), tb = min(ntiles, ta + per);
+    for (int t = ta; t < tb; ++t) {
+        int r = 0;
+        for (int i = 0; i < nrw; ++i) {
+            const int st = cnt[i * ntiles + t];
+            const int n = (t + 1 < ntiles ? cnt[i * ntiles + t + 1] : slot[i].w) - st;
+            roff[i * ntiles + t] = r;
+            r += n + (n & 1);
+        }
+        mine += HDR + 8 * r;
+    }
+    {
+        const int incl = wave_incl_scan(mine);
+        if (lane == 63) wave_tot[wave] = incl;
+        __syncthreads();
+        int before = 0;
+        for (int w = 0; w < wave; ++w) before += wave_tot[w];
+        int c = before + incl - mine;
+        for (int t = ta; t < tb; ++t) {
+            choff[t] = c;
+            int r = 0;
+            for (int i = 0; i < nrw; ++i) {
+                const int st = cnt[i * ntiles + t];
+                const int n = (t + 1 < ntiles ? cnt[i * ntiles + t + 1] : slot[i].w) - st;
+                r += n + (n & 1);
+            }
+            c += HDR + 8 * r;
+        }
+    }
+    __syncthreads();
+    char *base = stream + woff[g];
+    // headers: uint16 padded count per slot (zero past rw); padding pairs of odd runs
+    for (int x = tid; x < ntiles * (HDR / 2); x += kBucketThreads) {
+        const int t = x / (HDR / 2), i = x - t * (HDR / 2);
+        int np = 0;
+        if (i < nrw) {
+            const int st = cnt[i * ntiles + t];
+            const int n = (t + 1 < ntiles ? cnt[i * ntiles + t + 1] : slot[i].w) - st;
+            np = n + (n & 1);
+            if (n & 1)
+                *reinterpret_cast<int2 *>(base + choff[t] + HDR + 8 * (roff[i * ntiles + t] + n)) = make_int2(0, 0);
+        }
+        reinterpret_cast<unsigned short *>(base + choff[t])[i] = (unsigned short)np;
+    }
+    for (int e0 = tid; e0 < total; e0 += U * kBucketThreads) {
+        int ii[U], mm[U], cc[U];
+        float vv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = e0 + u * kBucketThreads;
+            ii[u] = -1;
+            if (e < total) {
+                ii[u] = find(e);
+                const int4 sl = slot[ii[u]];
+                mm[u] = e - pfx[ii[u]];
+                const int p = sl.y + mm[u] * sl.z;
+                cc[u] = idx[p];
+                vv[u] = vals[p];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (ii[u] < 0) continue;
+            const int i = ii[u], t = cc[u] >> SHIFT;
+            const int q = roff[i * ntiles + t] + mm[u] - cnt[i * ntiles + t];
+            *reinterpret_cast<int2 *>(base + choff[t] + HDR + 8 * q) =
+                make_int2((cc[u] - t * KT) * (BB * 4), __float_as_int(vv[u]));
+        }
+    }
+}
+
+size_t bucket_lds_bytes(int rw, int ntiles) { return sizeof(int) * ((size_t)2 * rw * ntiles + ntiles + 1); }
 
 // ---------------------------------------------------------------------------
 // streamed tiled kernel
@@ -884,7 +1054,9 @@ bool shape_plan(spmm_plan &p, int n_rows, int n_cols, int64_t nnz, int B) {
     // (wave, tile); too much padding means the operand is too sparse per tile
     const int64_t slot_tiles = nw * rw * (int64_t)p.ntiles;
     if (slot_tiles > 2 * nnz + 4096) return false;
-    p.stream_bytes = 8 * (nnz + slot_tiles) + (int64_t)cfg::HDR * nw * p.ntiles + kChunk + 256;
+    // (the bound the per-wave streams are placed by: 16 bytes per slot and
+    // tile, entries rounded to pairs of pairs per piece)
+    p.stream_bytes = 8 * (nnz + p.max_pieces) + 16 * slot_tiles + (int64_t)cfg::HDR * nw * p.ntiles + kChunk + 256;
     if (p.stream_bytes > INT32_MAX / 2 || (int64_t)nrb * p.nch > INT32_MAX) return false;
     return true;
 }
@@ -971,9 +1143,19 @@ hipError_t plan_tiled(const spmm_plan &pl, int n_rows, const int *ptr, const int
     {
         const int nb = (int)std::min<int64_t>(kPlanMaxBlocks, ceil_div(n_rows, kPlanThreads));
         const int rpb = (int)ceil_div(n_rows, nb);
-        plan_hist_kernel<<<nb, kPlanThreads, 0, s>>>(n_rows, ptr, nw, rpb, w.bh, w.bsum);
+        const int wbase = pl.ntiles * (tiled_cfg<VEC, HALF>::HDR + 16 * pl.rw);
+        plan_hist_kernel<<<nb, kPlanThreads, 0, s>>>(n_rows, ptr, nw, rpb, w.bh, w.bsum, w.wsize, wbase);
         plan_deal_kernel<<<nb, kPlanThreads, 0, s>>>(n_rows, ptr, nw, pl.rw, rpb, nb, w.bh, w.bsum, w.pbeg,
-                                                      w.table);
+                                                      w.table, w.wsize);
+    }
+    const size_t blds = bucket_lds_bytes(pl.rw, pl.ntiles);
+    if (pl.rw <= tiled_cfg<VEC, HALF>::MAXRW && blds <= 65536) {
+        // streams at the exclusive scan of their bounds, each written by one workgroup
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
+        stream_bucket_kernel<VEC, HALF><<<(unsigned)nw, kBucketThreads, blds, s>>>(pl.rw, pl.ntiles, idx, vals,
+                                                                                  w.table, w.woff, w.stream);
+        return hipGetLastError();
     }
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,
                                                              ptr, idx, w.seg);
