@@ -9,6 +9,7 @@ informational JSON line; bench.py's default line is the metric.
                   fwd, CSC, bwd, masked dW (SDDMM), support-restricted prox, compaction
     fc4096_sweep  4096 x 4096, batch 512, densities 1/5/20/50%: 20 alternating
                   l1 / debiasing iterations with the CSR rebuilt after every l1 step
+                  (the l1 update fused: dense_wgrad_prox + csr_recompress_counted)
     fc9216x4096_adaptive
                   the 9216 -> 4096 l1 step with Prox-ADAM (Algorithm 2) and with
                   Prox-RMSProp (Algorithm 1) in place of the plain proximal step
@@ -264,6 +265,8 @@ def fc4096_sweep(args, dev):
         dW = torch.empty((N, K), dtype=torch.float32, device=dev)
         gv = torch.empty(N * K, dtype=torch.float32, device=dev)
         csc = L1.CSC.empty(K, N * K, dev)
+        bm = L1.Bitmap.empty(N, K, dev)
+        wcs = torch.empty((N, (K + 31) // 32), dtype=torch.int32, device=dev)
         # one untimed pass learns the nnz of every iteration (the host passes it
         # to the calls, as a training loop that sizes its buffers would)
         nnz_seq = []
@@ -279,10 +282,14 @@ def fc4096_sweep(args, dev):
                         L1.csc_build(W, csc)
                     L1.csr_spmm_fwd(W, Xs[t], Y)
                     L1.csr_spmm_bwd_t(W, dYs[t], csc, dX)
-                    L1.dense_wgrad(dYs[t], Xs[t], dW)
                     out = bufs[k % 2]
                     k += 1
-                    L1.prox_l1_recompress(W, dW, L.eta, lam, out=out)
+                    # the l1 update as the step makes it: Z = prox(W - eta dY X^T) from
+                    # the GEMM's epilogue, then Z -> CSR (the bits of dense_wgrad +
+                    # prox_l1_recompress)
+                    L1.csr_bitmap_build(W, bm)
+                    _, wc = L1.dense_wgrad_prox(W, dYs[t], Xs[t], L.eta, lam, bm, Z=dW, word_counts=wcs)
+                    L1.csr_recompress_counted(dW, wc, out=out, capacity=N * K)
                     W = out
                     if timed_nnz is None:
                         nnz_seq.append(W.host_nnz())
