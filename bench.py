@@ -287,7 +287,7 @@ def main():
     wg_tflops = wg_flops / (wg_live_ms * 1e-3) / 1e12  # live, inside the timed steps
     traffic = counter_traffic("dense_wgrad_prox_fc9216x4096_pmc.txt",
                               source_hash("gemm.hip", "prox_epilogue.hpp"))
-    roof = {"kernel": "dense_wgrad_prox (wgrad_f32_large_kernel with the prox epilogue)", "bound": "mfma",
+    roof = {"kernel": "dense_wgrad_prox (wgrad_f32_dma_kernel<true>: direct global->LDS tiles, prox epilogue)", "bound": "mfma",
             "achieved": round(wg_tflops, 2), "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
             "frac": round(wg_tflops / PEAK_MFMA_F32_TFLOPS, 4), "traffic": traffic,
             "algorithmic_flops": wg_flops, "launch_ms": round(wg_live_ms, 4)}

@@ -561,11 +561,15 @@ def _copy_ceiling(torch, dev):
 def _call_times(torch, call, reps, flush, order, tag):
     """Median event time of `call` warm (back-to-back calls) and cold (a 1 GiB
     write before each call, so neither L2 nor the 256 MB MALL holds its
-    operands).  Cold calls are appended to `order` (the counter summary maps
-    the kernels between two flushes to that call)."""
+    operands).  The warm calls are queued behind a spin kernel of a few ms, so
+    they run back to back however long the host takes to enqueue them (a call
+    of a few us is shorter than its Python launch).  Cold calls are appended
+    to `order` (the counter summary maps the kernels between two flushes to
+    that call)."""
     call()
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda._sleep(int(2.4e9 * 300e-6 * reps))  # ~300 us of GPU clock per queued call
     for a, b in ev:
         a.record()
         call()

@@ -328,7 +328,10 @@ int dense_wgrad_prox(int32_t N, int32_t K, int32_t B,
  * Dense -> CSR (Section 3.1) from the per-word nonzero counts that
  * dense_wgrad_prox wrote with Z: keeps the nonzero Z entries (|Z| > 0) in
  * row-major order, bit-identical to csr_recompress(Z, t = 0).  Row pointers
- * come from the counts (row sums and their exclusive scan), so Z is read once.
+ * come from the counts (row sums, then their prefix sums), so Z is read once:
+ * with capacity >= n_rows * n_cols and n_rows <= 16384 the compaction adds up
+ * each row's start itself from per-row and per-64-row totals (two launches,
+ * no host synchronisation); otherwise a scan writes row_ptr_out first.
  * row_ptr_out [n_rows+1], col_idx_out / vals_out [capacity]; capacity,
  * d_nnz_out and h_nnz_required behave as in csr_recompress.  The outputs
  * must not overlap each other, Z, the counts or ws.  ws holds

@@ -243,7 +243,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
     if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return 0;
     switch (op) {
         case L1CSR_OP_CSC_BUILD: return round_up(csc_workspace_bytes(n_rows, n_cols, nnz));
-        case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * ((size_t)n_rows + 1));
+        case L1CSR_OP_RECOMPRESS: return round_up(sizeof(int) * counted_ws_ints(n_rows));
         case L1CSR_OP_SDDMM: return round_up(sddmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_SPMM: return round_up(spmm_workspace_bytes(n_rows, n_cols, nnz, B));
         case L1CSR_OP_COMPACT: return round_up(sizeof(int) * ((size_t)n_rows + 1));
@@ -502,13 +502,14 @@ int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64
     if (bad_dense(Z, n_rows, n_cols, ldz) || row_ptr_out == nullptr) return L1CSR_EINVAL;
     if (total > 0 && word_counts == nullptr) return L1CSR_EINVAL;
     if (capacity > 0 && (col_idx_out == nullptr || vals_out == nullptr)) return L1CSR_EINVAL;
-    if (n_rows > 0 && (ws == nullptr || ws_bytes < sizeof(int) * ((size_t)n_rows + 1))) return L1CSR_EINVAL;
+    const size_t wsn = sizeof(int) * counted_ws_ints(n_rows);
+    if (n_rows > 0 && (ws == nullptr || ws_bytes < wsn)) return L1CSR_EINVAL;
     {  // outputs apart from each other and from Z and the counts
         const size_t cap = sizeof(int32_t) * (size_t)capacity, rp = sizeof(int32_t) * ((size_t)n_rows + 1);
         const void *outs[3] = {row_ptr_out, col_idx_out, vals_out};
         const size_t ob[3] = {rp, cap, cap};
         const void *ins[3] = {Z, word_counts, ws};
-        const size_t ib[3] = {dense_bytes(n_rows, n_cols, ldz), word_counts_bytes(n_rows, n_cols), rp};
+        const size_t ib[3] = {dense_bytes(n_rows, n_cols, ldz), word_counts_bytes(n_rows, n_cols), wsn};
         for (int o = 0; o < 3; ++o) {
             for (int q = o + 1; q < 3; ++q)
                 if (bytes_overlap(outs[o], ob[o], outs[q], ob[q])) return L1CSR_EINVAL;
@@ -523,8 +524,15 @@ int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64
         if (h_nnz_required) *h_nnz_required = capacity < total ? 0 : -1;
         return hip_status(e);
     }
-    e = launch_counted_row_ptr(n_rows, n_cols, word_counts, static_cast<int *>(ws), row_ptr_out, stream);
+    int *sums = static_cast<int *>(ws);
+    e = launch_counted_sums(n_rows, n_cols, word_counts, sums, stream);
     if (e != hipSuccess) return L1CSR_EHIP;
+    // row_ptr' added up inside the compaction unless the host needs nnz' first
+    const bool prefix_here = capacity >= total && counted_prefix_in_compact(n_rows);
+    if (!prefix_here) {
+        e = launch_counted_row_ptr(n_rows, sums, row_ptr_out, stream);
+        if (e != hipSuccess) return L1CSR_EHIP;
+    }
     if (capacity < total) {
         int32_t h = 0;
         e = hipMemcpyAsync(&h, row_ptr_out + n_rows, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
@@ -538,8 +546,8 @@ int csr_recompress_counted(int32_t n_rows, int32_t n_cols, const float *Z, int64
     } else if (h_nnz_required) {
         *h_nnz_required = -1;
     }
-    return hip_status(launch_counted_compact(n_rows, n_cols, Z, ldz, word_counts, row_ptr_out, col_idx_out, vals_out,
-                                             capacity, d_nnz_out, stream));
+    return hip_status(launch_counted_compact(n_rows, n_cols, Z, ldz, word_counts, sums, prefix_here, row_ptr_out,
+                                             col_idx_out, vals_out, capacity, d_nnz_out, stream));
 }
 
 int csr_bitmap_build(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *row_ptr,

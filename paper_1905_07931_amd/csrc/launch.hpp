@@ -89,20 +89,27 @@ hipError_t launch_wgrad_bf16x3_prox(int N, int K, int B, const float *dY, int64_
 //   launch_wgrad_prox: Z and the per-(row, 32-column word) nonzero counts
 //     (counts [N][ceil(K / 32)]) from W's bitmap index (mask / pos); split_ws
 //     holds wgrad_prox_split_bytes() (fp32 products that split their batch);
-//   launch_counted_row_ptr: row_ptr_out (row_ptr_out[N] = nnz') from the
-//     counts, row_counts holding N + 1 ints;
-//   launch_counted_compact: col_out / val_out (< capacity), nnz' to d_nnz_out.
+//   launch_counted_sums: the row totals of the counts and their totals per
+//     block of 64 rows into ws (counted_ws_ints(N) ints);
+//   launch_counted_row_ptr: row_ptr_out (row_ptr_out[N] = nnz') by a scan of
+//     the row totals;
+//   launch_counted_compact: col_out / val_out (< capacity), nnz' to d_nnz_out;
+//     prefix_here (only where counted_prefix_in_compact(N)): the workgroups
+//     add up each row's start from the totals and write row_ptr_out
+//     themselves, else they read it (launch_counted_row_ptr first).
 size_t word_counts_bytes(int N, int K);
 size_t wgrad_prox_split_bytes(int N, int K, int B, int precision);
 hipError_t launch_wgrad_prox(int N, int K, int B, const float *dY, int64_t ldy, const float *X,
                              int64_t ldx, int precision, const float *vals, const unsigned *mask, const int *pos,
                              float eta, double t, float *Z, int64_t ldz, int *counts, void *split_ws,
                              hipStream_t s);
-hipError_t launch_counted_row_ptr(int N, int K, const int *counts, int *row_counts, int *row_ptr_out,
-                                  hipStream_t s);
-hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts,
-                                  const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
-                                  int *d_nnz_out, hipStream_t s);
+size_t counted_ws_ints(int N);
+bool counted_prefix_in_compact(int N);
+hipError_t launch_counted_sums(int N, int K, const int *counts, int *ws, hipStream_t s);
+hipError_t launch_counted_row_ptr(int N, const int *ws, int *row_ptr_out, hipStream_t s);
+hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts, const int *ws,
+                                  bool prefix_here, int *row_ptr_out, int *col_out, float *val_out,
+                                  int64_t capacity, int *d_nnz_out, hipStream_t s);
 // bitmap index of a CSR pattern: mask / pos [n_rows][ceil(n_cols / 32)]
 hipError_t launch_bitmap(int n_rows, int n_cols, const int *ptr, const int *idx, unsigned *mask, int *pos,
                          hipStream_t s);

@@ -6,10 +6,18 @@
 //   2. the weight-gradient GEMM with the prox epilogue (prox_epilogue.hpp):
 //      Z = S_t(W - eta * dY.X^T) and the nonzero count of every 32-column
 //      word of every row;
-//   3. row totals of the word counts, their exclusive scan = row_ptr';
+//   3. row totals of the word counts and their totals per block of 64 rows
+//      (row_block_sums_kernel);
 //   4. compaction of Z into col_idx', vals' (compact_kernel): a workgroup per
 //      (row, 3072-column chunk) starts at row_ptr'[row] plus the counts of
 //      the row's words before the chunk, so no second pass over the gradient.
+//      row_ptr'[row] is the sum of the block totals before the row's block
+//      and of the row totals before it in its block, added up by each
+//      workgroup itself (at most 256 + 63 integers, cached); the first chunk
+//      of a row writes it.  Where the caller's capacity is below n_rows *
+//      n_cols the host needs nnz' first, and past 256 blocks the sums grow
+//      long: an exclusive scan of the row totals writes row_ptr' instead and
+//      the compaction reads it.
 //
 // Shapes whose GEMM has no prox epilogue (bf16 operands, or an fp32 product
 // that splits its reduction) write dW into Z first and run the same prox in
@@ -28,6 +36,9 @@ namespace {
 constexpr int kCompactCols = 3072;  // columns per compaction workgroup (whole 32-column words)
 constexpr int kCompactThreads = 256;
 constexpr int kCompactVecs = kCompactCols / (4 * kCompactThreads);  // float4 per thread: 3
+constexpr int kPrefixRows = 64;        // rows per block of the two-level row prefix (16 waves x 4 rows)
+constexpr int kPrefixMaxBlocks = 256;  // block totals a compaction workgroup adds up at most
+static_assert(kPrefixMaxBlocks <= kCompactThreads && kPrefixRows <= kCompactThreads, "one load per thread");
 
 // mask[w][row] bit c: column 32w + c is stored; pos[w][row]: CSR position of
 // the row's first entry with column >= 32w (row_ptr[row + 1] past the last).
@@ -209,31 +220,61 @@ __global__ __launch_bounds__(256) void prox_words_kernel(int n_rows, int n_cols,
     }
 }
 
-// row_counts[row] = sum of the row's word counts (one wave per row)
-__global__ __launch_bounds__(256) void slab_rowsum_kernel(int n_rows, int slabs, const int *__restrict__ counts,
-                                                          int *__restrict__ row_counts) {
-    // (slabs: the counts per row)
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= n_rows) return;
-    const int lane = threadIdx.x & 63;
-    const int *c = counts + (int64_t)row * slabs;
-    int v = 0;
-    for (int j = lane; j < slabs; j += kWave) v += c[j];
-    v = wave_sum_int(v);
-    if (lane == 0) row_counts[row] = v;
+// row_counts[row] = sum of the row's word counts; blk[b] = sum over rows
+// [64b, 64b + 64).  A workgroup of 16 waves per 64 rows, a wave per 4 rows;
+// each round issues 4 words of each of the 4 rows (16 loads) before adding.
+__global__ __launch_bounds__(1024) void row_block_sums_kernel(int n_rows, int kw, const int *__restrict__ counts,
+                                                              int *__restrict__ row_counts, int *__restrict__ blk) {
+    __shared__ int part[1024 / kWave];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r0 = blockIdx.x * kPrefixRows + wave * 4;
+    int v[4] = {0, 0, 0, 0};
+    for (int j0 = lane; j0 < kw; j0 += 4 * kWave) {
+        int a[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * kWave;
+                a[q][u] = r0 + q < n_rows && j < kw ? counts[(int64_t)(r0 + q) * kw + j] : 0;
+            }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] += a[q][0] + a[q][1] + a[q][2] + a[q][3];
+    }
+    int mine = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int tot = wave_sum_int(v[q]);
+        if (r0 + q < n_rows) {
+            if (lane == 0) row_counts[r0 + q] = tot;
+            mine += tot;
+        }
+    }
+    if (lane == 0) part[wave] = mine;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int b = 0;
+#pragma unroll
+        for (int w = 0; w < 1024 / kWave; ++w) b += part[w];
+        blk[blockIdx.x] = b;
+    }
 }
 
 // Z -> col_idx', vals' for columns [c0, c0 + 3072) of one row, nonzeros in
-// column order.  Thread t holds the float4s t, t + 256, t + 512 of the chunk;
+// column order.  With blk, the row's start is row_ptr'[row] = blk[0 .. b) +
+// row_counts[64b .. row) (b = row / 64), and the row's first chunk writes it
+// (the last row's also row_ptr'[n_rows] and *d_nnz); without, row_ptr holds
+// it.  Thread t holds the float4s t, t + 256, t + 512 of the chunk;
 // ranks come from four ballots per float4 slot and the wave totals of all
 // three slots are exchanged through LDS in one barrier.  The chunk's output
 // is assembled in LDS and then written with every store instruction covering
 // 64 consecutive positions (scattered per-lane stores measured 1.5x slower).
 template <bool V4>
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
-    int n_cols, int chunks, const float *__restrict__ Z, int64_t ldz, int kw,
-    const int *__restrict__ counts, const int *__restrict__ row_ptr, int *__restrict__ col_out,
-    float *__restrict__ val_out, int64_t capacity) {
+    int n_rows, int n_cols, int chunks, const float *__restrict__ Z, int64_t ldz, int kw,
+    const int *__restrict__ counts, const int *__restrict__ row_counts, const int *__restrict__ blk,
+    int *__restrict__ row_ptr, int *__restrict__ d_nnz, int *__restrict__ col_out, float *__restrict__ val_out,
+    int64_t capacity) {
     __shared__ int red[kCompactThreads / kWave];
     __shared__ int tot[kCompactVecs][kCompactThreads / kWave];
     const int row = blockIdx.x / chunks, ch = blockIdx.x - row * chunks;
@@ -256,7 +297,13 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     const int s0 = c0 / 32;
     int before = 0;
     for (int j = tid; j < s0; j += kCompactThreads) before += counts[(int64_t)row * kw + j];
-    before = wave_sum_int(before);
+    int prefix = 0;  // row_ptr'[row], when added up here
+    if (blk) {
+        const int b = row / kPrefixRows, r0 = b * kPrefixRows;
+        if (tid < b) prefix += blk[tid];
+        if (tid < row - r0) prefix += row_counts[r0 + tid];
+    }
+    before = wave_sum_int(before + prefix);
     if (lane == 0) red[wave] = before;
     int below_lane[kCompactVecs];
 #pragma unroll
@@ -272,9 +319,17 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
         if (lane == 0) tot[u][wave] = sum;
     }
     __syncthreads();
-    int64_t base = row_ptr[row];
+    int64_t base = blk ? 0 : row_ptr[row];
 #pragma unroll
     for (int w = 0; w < kCompactThreads / kWave; ++w) base += red[w];
+    if (blk && ch == 0 && tid == 0) {  // base = row_ptr'[row] (no words before the first chunk)
+        row_ptr[row] = (int)base;
+        if (row == n_rows - 1) {
+            const int nnz = (int)base + row_counts[row];
+            row_ptr[n_rows] = nnz;
+            if (d_nnz) *d_nnz = nnz;
+        }
+    }
     __shared__ int lcol[kCompactCols];
     __shared__ float lval[kCompactCols];
     int lo = 0;  // position inside the chunk's output
@@ -358,34 +413,43 @@ hipError_t launch_wgrad_prox(int N, int K, int B, const float *dY, int64_t ldy, 
     return hipGetLastError();
 }
 
-hipError_t launch_counted_row_ptr(int N, int K, const int *counts, int *row_counts, int *row_ptr_out,
-                                  hipStream_t s) {
+size_t counted_ws_ints(int N) { return (size_t)N + 1 + (size_t)ceil_div(N, kPrefixRows); }
+
+bool counted_prefix_in_compact(int N) { return ceil_div(N, kPrefixRows) <= kPrefixMaxBlocks; }
+
+hipError_t launch_counted_sums(int N, int K, const int *counts, int *ws, hipStream_t s) {
+    if (N == 0) return hipSuccess;
     const int kw = (int)ceil_div(K, 32);
-    slab_rowsum_kernel<<<(unsigned)ceil_div(N, 4), 256, 0, s>>>(N, kw, counts, row_counts);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_exclusive_scan(row_counts, row_ptr_out, N, nullptr, s);  // row_ptr_out[N] = nnz'
+    row_block_sums_kernel<<<(unsigned)ceil_div(N, kPrefixRows), 1024, 0, s>>>(N, kw, counts, ws, ws + N + 1);
+    return hipGetLastError();
 }
 
-hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts,
-                                  const int *row_ptr_out, int *col_out, float *val_out, int64_t capacity,
-                                  int *d_nnz_out, hipStream_t s) {
+hipError_t launch_counted_row_ptr(int N, const int *ws, int *row_ptr_out, hipStream_t s) {
+    return launch_exclusive_scan(ws, row_ptr_out, N, nullptr, s);  // row_ptr_out[N] = nnz'
+}
+
+hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, const int *counts, const int *ws,
+                                  bool prefix_here, int *row_ptr_out, int *col_out, float *val_out,
+                                  int64_t capacity, int *d_nnz_out, hipStream_t s) {
     const int kw = (int)ceil_div(K, 32);
     const int chunks = (int)ceil_div(K, kCompactCols);
     const int64_t blocks = (int64_t)N * chunks;
     if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+    if (prefix_here && !counted_prefix_in_compact(N)) return hipErrorInvalidValue;
+    const int *blk = prefix_here ? ws + N + 1 : nullptr;
+    int *dn = prefix_here ? d_nnz_out : nullptr;
     hipError_t e = hipSuccess;
     if (blocks > 0) {
         const bool v4 = (ldz % 4 == 0) && aligned16(Z);
         if (v4)
-            compact_kernel<true><<<(unsigned)blocks, kCompactThreads, 0, s>>>(K, chunks, Z, ldz, kw, counts,
-                                                                              row_ptr_out, col_out, val_out, capacity);
+            compact_kernel<true><<<(unsigned)blocks, kCompactThreads, 0, s>>>(
+                N, K, chunks, Z, ldz, kw, counts, ws, blk, row_ptr_out, dn, col_out, val_out, capacity);
         else
-            compact_kernel<false><<<(unsigned)blocks, kCompactThreads, 0, s>>>(K, chunks, Z, ldz, kw, counts,
-                                                                               row_ptr_out, col_out, val_out, capacity);
+            compact_kernel<false><<<(unsigned)blocks, kCompactThreads, 0, s>>>(
+                N, K, chunks, Z, ldz, kw, counts, ws, blk, row_ptr_out, dn, col_out, val_out, capacity);
         e = hipGetLastError();
     }
-    if (e == hipSuccess && d_nnz_out) e = launch_copy_i32(row_ptr_out + N, d_nnz_out, s);
+    if (e == hipSuccess && d_nnz_out && !prefix_here) e = launch_copy_i32(row_ptr_out + N, d_nnz_out, s);
     return e;
 }
 

@@ -340,7 +340,7 @@ def test_fused_weight_update_arguments_are_rejected_before_launch(lib):
         a.update({k: v for k, v in o.items() if k in a})
         p = {k: (None if x is None else C.c_void_p(x)) for k, x in a.items()}
         return g(o.get("N", N), o.get("K", K), p["Z"], o.get("ldz", K), p["wc"], p["rpo"], p["cio"], p["vo"],
-                 N * K, None, None, p["ws"], o.get("wsb", 4 * (N + 1)), S)
+                 N * K, None, None, p["ws"], o.get("wsb", lib.l1csr_workspace_bytes(2, N, K, 0, 0)), S)
 
     assert lib.l1csr_workspace_bytes(9, N, K, nnz, B) == 0  # no split at this shape
     assert prox() == EHIP and rec() == EHIP  # valid: only the launch fails without a GPU
@@ -349,7 +349,9 @@ def test_fused_weight_update_arguments_are_rejected_before_launch(lib):
                 dict(Z=base["mk"] + 4), dict(wc=base["ci"])]:
         assert prox(**bad) == EINVAL, bad
     assert prox(N=65536, K=65536, ldz=65536) == EUNSUPPORTED
-    for bad in [dict(N=-1), dict(ldz=K - 1), dict(wc=None), dict(rpo=None), dict(wsb=4 * N), dict(ws=None),
+    # the workspace: row totals (N + 1) and one total per 64 rows
+    assert lib.l1csr_workspace_bytes(2, N, K, 0, 0) >= 4 * (N + 1 + (N + 63) // 64)
+    for bad in [dict(N=-1), dict(ldz=K - 1), dict(wc=None), dict(rpo=None), dict(wsb=4 * (N + 1)), dict(ws=None),
                 dict(cio=base["Z"] + 4), dict(vo=base["wc"]), dict(rpo=base["cio"] + 4 * (N * K - 1)),
                 dict(vo=base["ws"])]:
         assert rec(**bad) == EINVAL, bad

@@ -19,6 +19,7 @@ SHAPES = [  # (N, K, B, nnz, seed)
     (1, 1, 1, 1, 0), (7, 5, 3, 12, 1), (64, 65, 63, 700, 2), (65, 64, 64, 2000, 3),
     (33, 90, 17, 0, 4), (300, 784, 64, 23520, 0), (130, 257, 65, 9000, 5), (40, 300, 256, 5000, 6),
     (16, 20, 1, 120, 7), (3, 4100, 129, 6000, 8),
+    (51, 500, 130, 2550, 9),          # conv2-like rows (mean 50), VEC 2, the last row block one row
 ]
 
 

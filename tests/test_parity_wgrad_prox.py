@@ -144,6 +144,45 @@ def test_fused_update_capacity_paths():
     assert bool((out.col_idx == -7).all()) and bool((out.vals == -7.0).all())
 
 
+@pytest.mark.parametrize("N", [64, 16384, 16385])
+def test_counted_recompress_row_prefix_paths(N):
+    # each row's start is added up inside the compaction (up to 256 blocks of
+    # 64 rows, capacity >= N * K) or written by a scan first (more blocks, or
+    # a smaller capacity whose check needs nnz' on the host): the same CSR as
+    # the oracle's recompression on every path, nnz' in d_nnz_out
+    import ctypes as C
+    import torch
+    rng = np.random.default_rng(N)
+    K = 40
+    Zh = np.where(rng.random((N, K)) < 0.3, rng.standard_normal((N, K)), 0.0).astype(np.float32)
+    Zh[::7] = 0.0  # empty rows, also the first
+    Zh[-1] = np.where(np.arange(K) % 3 == 0, 1.5, 0.0)  # the last row's entries close the count
+    kw = (K + 31) // 32
+    pad = np.zeros((N, kw * 32), bool)
+    pad[:, :K] = Zh != 0
+    wc = t(pad.reshape(N, kw, 32).sum(2).astype(np.int32))
+    Z = t(Zh)
+    rp, ci, v = oracle.recompress(Zh)
+    n = int(rp[-1])
+    ws = torch.empty(L1.workspace_bytes(L1.OP_RECOMPRESS, N, K, 0, 0), dtype=torch.uint8, device=cuda())
+    for cap in (N * K, n):
+        rpo = torch.full((N + 1,), -3, dtype=torch.int32, device=cuda())
+        cio = torch.full((cap,), -3, dtype=torch.int32, device=cuda())
+        vo = torch.full((cap,), -3.0, dtype=torch.float32, device=cuda())
+        dn = torch.full((1,), -3, dtype=torch.int32, device=cuda())
+        need = C.c_int64(-5)
+        st = L1.lib().csr_recompress_counted(N, K, L1._p(Z), K, L1._p(wc), L1._p(rpo), L1._p(cio), L1._p(vo), cap,
+                                             L1._p(dn), C.byref(need), L1._p(ws), ws.numel(), L1._stream())
+        torch.cuda.synchronize()
+        assert st == 0, (cap, st)
+        assert need.value == (-1 if cap >= N * K else n)
+        assert int(h(dn)[0]) == n
+        assert bits_equal(h(rpo), rp), cap
+        assert bits_equal(h(cio)[:n], ci) and bits_equal(h(vo)[:n], v), cap
+        if cap > n:
+            assert bool((cio[n:] == -3).all()) and bool((vo[n:] == -3.0).all())
+
+
 def test_fused_update_padded_leading_dimensions():
     import torch
     L = synth.fc_layer(130, 300, 40, 4000, seed=11)
