@@ -479,10 +479,11 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
 constexpr int kBucketThreads = 1024;
 
 template <int VEC, bool HALF>
-__global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, int ntiles, const int *__restrict__ idx,
+__global__ __launch_bounds__(kBucketThreads, 8) void stream_bucket_kernel(int rw, int ntiles, const int *__restrict__ idx,
                                                             const float *__restrict__ vals,
                                                             const int4 *__restrict__ table,
-                                                            const int *__restrict__ woff, char *__restrict__ stream) {
+                                                            const int *__restrict__ wsize, int *__restrict__ woff,
+                                                            char *__restrict__ stream) {
     constexpr int BB = tiled_cfg<VEC, HALF>::BB, KT = tiled_cfg<VEC, HALF>::KT, SHIFT = tiled_cfg<VEC, HALF>::SHIFT;
     constexpr int MAXRW = tiled_cfg<VEC, HALF>::MAXRW, HDR = tiled_cfg<VEC, HALF>::HDR;
     extern __shared__ int bsm[];
@@ -500,7 +501,25 @@ __global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, i
         slot[tid] = e;
     }
     for (int x = tid; x < nrw * ntiles; x += kBucketThreads) cnt[x] = 0;
+    if (wsize) {  // this stream's offset = the bounds of the streams before it, added up here
+        int sz = 0;
+        for (int x = tid; x < g; x += kBucketThreads) sz += wsize[x];
+        sz = wave_sum_int(sz);
+        if (lane == 0) wave_tot[wave] = sz;
+    }
     __syncthreads();
+    int wo;
+    if (wsize) {
+        wo = 0;
+#pragma unroll
+        for (int w = 0; w < kBucketThreads / kWave; ++w) wo += wave_tot[w];
+        if (tid == 0) {
+            woff[g] = wo;  // for the product kernel
+            if (g == (int)gridDim.x - 1) woff[g + 1] = wo + wsize[g];
+        }
+    } else {
+        wo = woff[g];
+    }
     if (tid == 0) {
         int run = 0;
         for (int i = 0; i < nrw; ++i) {
@@ -517,23 +536,62 @@ __global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, i
             if (i + d < nrw && pfx[i + d] <= e) i += d;
         return i;
     };
-    // (entries U at a time per thread: their loads in flight together)
-    constexpr int U = 4;
-    for (int e0 = tid; e0 < total; e0 += U * kBucketThreads) {
-        int ii[U], cc[U];
+    // Entries U at a time per thread, their loads in flight together; the
+    // first round's entries (slot, column, position in the piece, value) stay
+    // in registers for the write pass.  The 64 lanes of a wave hold 64
+    // consecutive entries, so equal (slot, tile) keys come in runs (a piece's
+    // columns are sorted): the first lane of each run adds the run's length,
+    // one LDS atomic per run.  Every thread makes the same number of rounds,
+    // so the whole wave takes part in the lane exchanges (lanes past the end
+    // hold the key -1).
+    constexpr int U = 8;
+    auto count_runs = [&](const int (&kk)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int e = e0 + u * kBucketThreads;
-            ii[u] = -1;
+            const int prev = __shfl_up(kk[u], 1, kWave);
+            const bool head = lane == 0 || kk[u] != prev;
+            const uint64_t heads = __ballot(head);
+            const uint64_t above = heads & ~((2ull << lane) - 1ull);  // heads past this lane (none for lane 63)
+            const int next = above ? __builtin_ctzll(above) : kWave;
+            if (head && kk[u] >= 0) atomicAdd(&cnt[kk[u]], next - lane);
+        }
+    };
+    int ki[U], kc[U], km[U];
+    float kv[U];
+    {
+        int kk[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = tid + u * kBucketThreads;
+            ki[u] = kk[u] = -1;
+            kc[u] = km[u] = 0;
+            kv[u] = 0.f;
             if (e < total) {
-                ii[u] = find(e);
-                const int4 sl = slot[ii[u]];
-                cc[u] = idx[sl.y + (e - pfx[ii[u]]) * sl.z];
+                const int i = find(e);
+                const int4 sl = slot[i];
+                const int p = sl.y + (e - pfx[i]) * sl.z;
+                ki[u] = i;
+                km[u] = e - pfx[i];
+                kc[u] = idx[p];
+                kv[u] = vals[p];
+                kk[u] = i * ntiles + (kc[u] >> SHIFT);
             }
         }
+        count_runs(kk);
+    }
+    for (int e0 = U * kBucketThreads; e0 < total; e0 += U * kBucketThreads) {
+        int kk[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (ii[u] >= 0) atomicAdd(&cnt[ii[u] * ntiles + (cc[u] >> SHIFT)], 1);
+        for (int u = 0; u < U; ++u) {
+            const int e = e0 + tid + u * kBucketThreads;
+            kk[u] = -1;
+            if (e < total) {
+                const int i = find(e);
+                const int4 sl = slot[i];
+                kk[u] = i * ntiles + (idx[sl.y + (e - pfx[i]) * sl.z] >> SHIFT);
+            }
+        }
+        count_runs(kk);
     }
     __syncthreads();
     // run starts per slot (one wave per slot) and, per tile, the runs' offsets
@@ -581,7 +639,7 @@ __global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, i
         }
     }
     __syncthreads();
-    char *base = stream + woff[g];
+    char *base = stream + wo;
     // headers: uint16 padded count per slot (zero past rw); padding pairs of odd runs
     for (int x = tid; x < ntiles * (HDR / 2); x += kBucketThreads) {
         const int t = x / (HDR / 2), i = x - t * (HDR / 2);
@@ -595,7 +653,15 @@ __global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, i
         }
         reinterpret_cast<unsigned short *>(base + choff[t])[i] = (unsigned short)np;
     }
-    for (int e0 = tid; e0 < total; e0 += U * kBucketThreads) {
+    auto put = [&](int i, int c, int m, float v) {  // entry m of slot i, column c, into its place
+        const int t = c >> SHIFT;
+        const int q = roff[i * ntiles + t] + m - cnt[i * ntiles + t];
+        *reinterpret_cast<int2 *>(base + choff[t] + HDR + 8 * q) = make_int2((c - t * KT) * (BB * 4), __float_as_int(v));
+    };
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        if (ki[u] >= 0) put(ki[u], kc[u], km[u], kv[u]);
+    for (int e0 = U * kBucketThreads + tid; e0 < total; e0 += U * kBucketThreads) {
         int ii[U], mm[U], cc[U];
         float vv[U];
 #pragma unroll
@@ -612,13 +678,8 @@ __global__ __launch_bounds__(kBucketThreads) void stream_bucket_kernel(int rw, i
             }
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (ii[u] < 0) continue;
-            const int i = ii[u], t = cc[u] >> SHIFT;
-            const int q = roff[i * ntiles + t] + mm[u] - cnt[i * ntiles + t];
-            *reinterpret_cast<int2 *>(base + choff[t] + HDR + 8 * q) =
-                make_int2((cc[u] - t * KT) * (BB * 4), __float_as_int(vv[u]));
-        }
+        for (int u = 0; u < U; ++u)
+            if (ii[u] >= 0) put(ii[u], cc[u], mm[u], vv[u]);
     }
 }
 
@@ -1150,11 +1211,14 @@ hipError_t plan_tiled(const spmm_plan &pl, int n_rows, const int *ptr, const int
     }
     const size_t blds = bucket_lds_bytes(pl.rw, pl.ntiles);
     if (pl.rw <= tiled_cfg<VEC, HALF>::MAXRW && blds <= 65536) {
-        // streams at the exclusive scan of their bounds, each written by one workgroup
+        // each stream written by one workgroup at the exclusive scan of the
+        // streams' bounds; up to 4 bounds per thread the workgroups add up
+        // their own offsets, else a scan launch writes them first
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
-        stream_bucket_kernel<VEC, HALF><<<(unsigned)nw, kBucketThreads, blds, s>>>(pl.rw, pl.ntiles, idx, vals,
-                                                                                  w.table, w.woff, w.stream);
+        const bool own = nw <= 4 * kBucketThreads;
+        if (!own && (e = launch_exclusive_scan(w.wsize, w.woff, nw, nullptr, s)) != hipSuccess) return e;
+        stream_bucket_kernel<VEC, HALF><<<(unsigned)nw, kBucketThreads, blds, s>>>(
+            pl.rw, pl.ntiles, idx, vals, w.table, own ? w.wsize : nullptr, w.woff, w.stream);
         return hipGetLastError();
     }
     seg_kernel<<<(unsigned)ceil_div(n_rows, 4), 256, 0, s>>>(n_rows, pl.ntiles, tiled_cfg<VEC, HALF>::SHIFT,

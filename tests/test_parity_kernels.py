@@ -65,6 +65,7 @@ TILED = [  # (N, K, B, nnz, seed)
     (4096, 300, 1024, 200000, 22),    # VEC 4
     (4096, 300, 1020, 200000, 23),    # VEC 4, ragged last batch chunk
     (9000, 333, 1024, 200000, 24),    # VEC 4, ragged tile and row block
+    (60000, 300, 256, 900000, 28),    # 6000 waves: the stream offsets come from a scan launch
 ]
 
 
