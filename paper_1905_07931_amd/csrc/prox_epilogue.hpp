@@ -64,15 +64,21 @@ __device__ __forceinline__ void prox_stage(const prox_epi &P, int M, int m0, int
 
 typedef __attribute__((address_space(3))) void prox_lds_void;
 
+// A zero in device memory: the gather's source for the positions W does not
+// store, so every lane loads (no branch per register) and the loaded value is
+// w itself.
+static __device__ float kProxZero = 0.f;
+
 // The epilogue of one wave holding a (2*32) x (TN*32) block of the tile at
 // (m0 + wm, n0 + wn) in the D layout of the 32x32 MFMAs: lane l, register r
 // of MFMA tile (a, b) holds row 32a + 8(r/4) + 4(l/32) + r%4, column
 // 32b + l%32.  W's values are gathered TPB MFMA tiles (16*TPB registers) at a
 // time with direct global->LDS loads into this wave's buffer gbuf (lane l's
-// value of register j of the batch at gbuf[j*64 + l]), so a batch costs one
-// memory round trip and no registers; then the batch is thresholded, stored
-// and counted (ballots over the lanes of each row half; lane l accumulates
-// the counts of the wave's row l, one per 32-column word).
+// value of register j of the batch at gbuf[j*64 + l]; lanes at positions W
+// does not store load a zero), so a batch costs one memory round trip and no
+// registers; then the batch is thresholded, stored and counted (ballots over
+// the lanes of each row half; lane l accumulates the counts of the wave's
+// row l, one per 32-column word).
 template <int TN, int BN, int TPB>
 __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, int Nn, int m0, int n0,
                                            int wm, int wn, const int2 *stage, float *gbuf,
@@ -83,36 +89,51 @@ __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, 
     const int lr = lane & 31, lh = lane >> 5;
     const unsigned below = (1u << lr) - 1u;
     int mine[TN] = {};  // this lane's counts (wave row `lane`) per word of the block
+    // the wave's gather buffer as one wave-uniform LDS address; the zero's
+    // address taken once (kept in registers rather than rebuilt per load)
+    const unsigned gb = (unsigned)uniform((int)(uintptr_t)(prox_lds_void *)gbuf);
+    const uint64_t zero = (uint64_t)(uintptr_t)&kProxZero;
+    // this lane's output column per word of the block, whether it is inside
+    // the matrix (as a wave mask), and its first row: register r of MFMA tile
+    // (a, b) is row rbase + ro(a, r), ro(a, r) = 32a + 8(r/4) + r%4 (the same
+    // for the whole wave), so its address is cb[b] + ro * ldc
+    const int rbase = m0 + wm + 4 * lh;
+    float *cb[TN];
+    bool colok[TN];
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+        const int col = n0 + wn + b * 32 + lr;
+        colok[b] = col < Nn;
+        cb[b] = C + (int64_t)rbase * ldc + col;
+    }
 #pragma unroll
     for (int q0 = 0; q0 < NTILE; q0 += TPB) {
-        uint64_t smask = 0;  // bit j: register j of the batch holds a stored weight
 #pragma unroll
         for (int j = 0; j < 16 * TPB; ++j) {
             const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
             const int rt = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
             const int2 mp = stage[(wm + rt) * WPT + ((wn >> 5) + b)];
             const unsigned m = (unsigned)mp.x;
-            if ((m >> lr) & 1u) {
-                smask |= 1ull << j;
-                __builtin_amdgcn_global_load_lds((const void *)(P.vals + mp.y + __popc(m & below)),
-                                                 (prox_lds_void *)(gbuf + j * kWave), 4, 0, 0);
-            }
+            const uint64_t stored = (uint64_t)(uintptr_t)(P.vals + mp.y + __popc(m & below));
+            const uint64_t src = (m >> lr) & 1u ? stored : zero;
+            __builtin_amdgcn_global_load_lds((const void *)(uintptr_t)src,
+                                             (prox_lds_void *)(uintptr_t)(gb + 4u * j * kWave), 4, 0, 0);
         }
         __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the gathered values are in LDS
 #pragma unroll
         for (int j = 0; j < 16 * TPB; ++j) {
             const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
-            const int col = n0 + wn + b * 32 + lr;
-            const int rt = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);  // row inside the wave block
-            const int row = m0 + wm + rt;
-            const float w = (smask >> j) & 1u ? gbuf[j * kWave + lane] : 0.f;
+            const int ro = a * 32 + 8 * (r >> 2) + (r & 3);
+            const float w = gbuf[j * kWave + lane];
             const float o = soft_threshold(w, acc[a][b][r], P.eta, P.t);
-            const bool valid = row < M && col < Nn;
-            if (valid) C[(int64_t)row * ldc + col] = o;
+            const bool valid = rbase + ro < M && colok[b];
+            if (valid) cb[b][(int64_t)ro * ldc] = o;
             const uint64_t k = __ballot(valid && o != 0.f);
-            // wave rows rt(lh = 0) = rt0 and rt(lh = 1) = rt0 + 4
-            const int rt0 = a * 32 + 8 * (r >> 2) + (r & 3);
-            mine[b] += lane == rt0 ? __popcll(k & 0xffffffffull) : (lane == rt0 + 4 ? __popcll(k >> 32) : 0);
+            // row ro (lanes 0-31) and row ro + 4 (lanes 32-63) of the wave block:
+            // their nonzero counts in word b go to the lanes of those rows
+            const int c_lo = __popcll(k & 0xffffffffull), c_hi = __popcll(k >> 32);
+            asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(mine[b]) : "s"(c_lo), "I"(ro));
+            asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(mine[b]) : "s"(c_hi), "I"(ro + 4));
         }
     }
     const int row = m0 + wm + lane;
