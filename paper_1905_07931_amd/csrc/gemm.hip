@@ -431,10 +431,10 @@ __global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_dma_kernel(
     }
     if constexpr (PROX) {
         // the last K-step ended with a barrier: the operand buffers are free.
-        // The staged index words in A0, then a gather buffer of 2 MFMA tiles
-        // (8 KB) per wave: wave 0 after the words, waves 1-4 in A1, 5-8 in B0,
-        // 9-11 in B1.
-        constexpr int TPB = 2, GBF = 16 * TPB * kWave;  // floats per wave
+        // The staged index words in A0, then two gather buffers of one MFMA
+        // tile each (8 KB) per wave: wave 0 after the words, waves 1-4 in A1,
+        // 5-8 in B0, 9-11 in B1.
+        constexpr int TPB = 1, GBF = 2 * 16 * TPB * kWave;  // floats per wave
         constexpr int kStageFloats = 2 * LBM * (LBN / 32);
         static_assert(TM == 2 && LWM * LWN == 12 && sizeof(A0) >= sizeof(float) * (kStageFloats + GBF) &&
                           sizeof(A1) >= sizeof(float) * 4 * GBF && sizeof(B0) >= sizeof(float) * 4 * GBF &&
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(kLargeThreads, 1) void wgrad_f32_dma_kernel(
         prox_stage<LBM, LBN, kLargeThreads>(P, M, m0, n0, stage);
         float *gbuf = wave == 0 ? A0 + kStageFloats
                                 : (wave < 5 ? A1 + (wave - 1) * GBF : (wave < 9 ? B0 + (wave - 5) * GBF : B1 + (wave - 9) * GBF));
-        prox_store<TN, LBN, TPB>(acc, M, Nn, m0, n0, wm, wn, stage, gbuf, C, ldc, P);
+        prox_store<TN, LBN, TPB, 2>(acc, M, Nn, m0, n0, wm, wn, stage, gbuf, C, ldc, P);
         return;
     }
 #pragma unroll

@@ -77,14 +77,16 @@ static __device__ float kProxZero = 0.f;
 // value of register j of the batch at gbuf[j*64 + l]; lanes at positions W
 // does not store load a zero), so a batch costs one memory round trip and no
 // registers; then the batch is thresholded, stored and counted (ballots over
-// the lanes of each row half; lane l accumulates the counts of the wave's
-// row l, one per 32-column word).
-template <int TN, int BN, int TPB>
+// the lanes of each row half; lane l holds the counts of the wave's row l,
+// one per 32-column word).  NBUF = 2: gbuf holds two batches, and the next
+// batch's gather is in flight while the current one is thresholded.
+template <int TN, int BN, int TPB, int NBUF = 1>
 __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, int Nn, int m0, int n0,
                                            int wm, int wn, const int2 *stage, float *gbuf,
                                            float *__restrict__ C, int64_t ldc, const prox_epi &P) {
     constexpr int WPT = BN / 32, NTILE = 2 * TN;
     static_assert(NTILE % TPB == 0, "batches of whole MFMA tiles");
+    static_assert(NBUF == 1 || NBUF == 2, "one or two gather buffers");
     const int lane = threadIdx.x & 63;
     const int lr = lane & 31, lh = lane >> 5;
     const unsigned below = (1u << lr) - 1u;
@@ -106,8 +108,7 @@ __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, 
         colok[b] = col < Nn;
         cb[b] = C + (int64_t)rbase * ldc + col;
     }
-#pragma unroll
-    for (int q0 = 0; q0 < NTILE; q0 += TPB) {
+    auto gather = [&](int q0, unsigned base) {  // issue the loads of batch q0 into the buffer at base
 #pragma unroll
         for (int j = 0; j < 16 * TPB; ++j) {
             const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
@@ -117,14 +118,15 @@ __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, 
             const uint64_t stored = (uint64_t)(uintptr_t)(P.vals + mp.y + __popc(m & below));
             const uint64_t src = (m >> lr) & 1u ? stored : zero;
             __builtin_amdgcn_global_load_lds((const void *)(uintptr_t)src,
-                                             (prox_lds_void *)(uintptr_t)(gb + 4u * j * kWave), 4, 0, 0);
+                                             (prox_lds_void *)(uintptr_t)(base + 4u * j * kWave), 4, 0, 0);
         }
-        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the gathered values are in LDS
+    };
+    auto threshold = [&](int q0, const float *gv) {  // prox, store and count batch q0 (values in gv)
 #pragma unroll
         for (int j = 0; j < 16 * TPB; ++j) {
             const int q = q0 + j / 16, a = q / TN, b = q % TN, r = j % 16;
             const int ro = a * 32 + 8 * (r >> 2) + (r & 3);
-            const float w = gbuf[j * kWave + lane];
+            const float w = gv[j * kWave + lane];
             const float o = soft_threshold(w, acc[a][b][r], P.eta, P.t);
             const bool valid = rbase + ro < M && colok[b];
             if (valid) cb[b][(int64_t)ro * ldc] = o;
@@ -134,6 +136,26 @@ __device__ __forceinline__ void prox_store(const floatx16 (&acc)[2][TN], int M, 
             const int c_lo = __popcll(k & 0xffffffffull), c_hi = __popcll(k >> 32);
             asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(mine[b]) : "s"(c_lo), "I"(ro));
             asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(mine[b]) : "s"(c_hi), "I"(ro + 4));
+        }
+    };
+    constexpr unsigned kBatchBytes = 4u * 16 * TPB * kWave;
+    if constexpr (NBUF == 1) {
+#pragma unroll
+        for (int q0 = 0; q0 < NTILE; q0 += TPB) {
+            gather(q0, gb);
+            __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the gathered values are in LDS
+            threshold(q0, gbuf);
+        }
+    } else {
+        gather(0, gb);
+#pragma unroll
+        for (int q0 = 0; q0 < NTILE; q0 += TPB) {
+            const int cur = (q0 / TPB) & 1;
+            // vmcnt(0): batch q0's values are in LDS (and the previous batch's
+            // stores are done); the other buffer was read by that batch
+            __builtin_amdgcn_s_waitcnt(0x0f70);
+            if (q0 + TPB < NTILE) gather(q0 + TPB, gb + (cur ^ 1) * kBatchBytes);
+            threshold(q0, gbuf + cur * 16 * TPB * kWave);
         }
     }
     const int row = m0 + wm + lane;
