@@ -321,7 +321,7 @@ def main():
                        "hbm_gbs": round(rc_gbs, 1), "hbm_frac": round(rc_gbs / PEAK_HBM_GBS, 4),
                        "hbm_frac_cold": round(bytes_recompress / (cold["csr_recompress_counted"] * 1e-3) / 1e9
                                               / PEAK_HBM_GBS, 4),
-                       "note": "csr_recompress_counted (row and 64-row block totals of the word counts, then the compaction of Z, which adds up its row starts): Z and its word counts "
+                       "note": "csr_recompress_counted (row and row-block totals of the word counts, then the compaction of Z, which adds up its row starts): Z and its word counts "
                                "read once, W' written; ms is the call alone, ms_live_in_step shares the GPU with "
                                "the backward SpMM on the other stream"},
         "weight_update_ms": round(per["dense_wgrad_prox"] + rc_ms, 4),

@@ -99,6 +99,18 @@ const char *l1csr_status_str(int status);
 size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz, int32_t B);
 
 /*
+ * Pinned host memory that kernels can write directly, for small results the
+ * host reads after the call (a d_nnz_out below, say), so that no copy has to
+ * be queued behind the call: `bytes` bytes from hipHostMalloc (mapped,
+ * coherent); *host receives the host address, *dev the address kernels use.
+ * The caller owns the memory and frees it with l1csr_host_free_mapped once
+ * no queued work can still write it.  L1CSR_EINVAL for bytes == 0 or a NULL
+ * out-pointer; L1CSR_EHIP if the runtime refuses (nothing allocated then).
+ */
+int l1csr_host_alloc_mapped(size_t bytes, void **host, void **dev);
+int l1csr_host_free_mapped(void *host);
+
+/*
  * Forward product, Section 3.2 "Forward: X_T <- X_B W'" (dense x compressed'),
  * in batch-contiguous layout:
  *     Y[i][b] = sum_{p = row_ptr[i]}^{row_ptr[i+1]-1} vals[p] * X[col_idx[p]][b]
@@ -269,7 +281,8 @@ int prox_l1_step(int mode, int32_t n_rows, int32_t n_cols, int64_t nnz,
  * writes the canonical CSR: row_ptr_out[n_rows+1], col_idx_out[nnz'],
  * vals_out[nnz'].  row_counts (nullable) are the per-row counts prox_l1_step
  * produced for the same Z and t = 0; when NULL they are recomputed.
- * d_nnz_out (nullable, device) receives nnz'.
+ * d_nnz_out (nullable; device memory or l1csr_host_alloc_mapped's *dev)
+ * receives nnz'.
  *   capacity >= n_rows*n_cols: never overflows and never waits (hot path).
  *   capacity <  n_rows*n_cols: the call counts first, waits for the stream,
  *     and returns L1CSR_ECAPACITY with *h_nnz_required (host, nullable) = nnz'
@@ -330,7 +343,7 @@ int dense_wgrad_prox(int32_t N, int32_t K, int32_t B,
  * row-major order, bit-identical to csr_recompress(Z, t = 0).  Row pointers
  * come from the counts (row sums, then their prefix sums), so Z is read once:
  * with capacity >= n_rows * n_cols and n_rows <= 16384 the compaction adds up
- * each row's start itself from per-row and per-64-row totals (two launches,
+ * each row's start itself from per-row and per-block (16-64 rows) totals (two launches,
  * no host synchronisation); otherwise a scan writes row_ptr_out first.
  * row_ptr_out [n_rows+1], col_idx_out / vals_out [capacity]; capacity,
  * d_nnz_out and h_nnz_required behave as in csr_recompress.  The outputs

@@ -60,6 +60,8 @@ def lib():
         L.l1csr_status_str.restype = C.c_char_p
         L.l1csr_workspace_bytes.argtypes = [C.c_int, i32, i32, i64, i32]
         L.l1csr_workspace_bytes.restype = sz
+        L.l1csr_host_alloc_mapped.argtypes = [sz, C.POINTER(vp), C.POINTER(vp)]
+        L.l1csr_host_free_mapped.argtypes = [vp]
         L.csr_spmm_fwd.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
         L.csr_spmm_plan.argtypes = [i32, i32, i64, vp, vp, vp, i32, vp, sz, vp]
         L.csr_spmm_planned.argtypes = [i32, i32, i64, vp, vp, vp, vp, i64, i32, vp, i64, vp, sz, vp]
@@ -133,13 +135,89 @@ def _p(t):
     return None if t is None else C.c_void_p(t.data_ptr())
 
 
+class _HostWord:
+    """One int32 of pinned host memory that kernels write directly
+    (l1csr_host_alloc_mapped), as a call's d_nnz_out: the count reaches the
+    host with the call's own kernels, and no copy is queued behind it."""
+
+    def __init__(self, host: int, dev: int):
+        self.host, self.dev, self.event = host, dev, None
+
+    def value(self) -> int:
+        return C.c_int32.from_address(self.host).value
+
+
+class _HostWords:
+    """A CSR holds one word for its lifetime; when it goes, the word returns
+    here and is handed out again only after the event recorded behind its
+    last write has completed.  Pages are never freed (queued work may still
+    write them)."""
+    PAGE = 1024  # words per page
+
+    def __init__(self):
+        self.free: list = []
+        self.disabled = False
+
+    def acquire(self):
+        for i, w in enumerate(self.free):
+            if w.event is None or w.event.query():
+                return self.free.pop(i)
+        if self.disabled:
+            return None
+        h, d = C.c_void_p(), C.c_void_p()
+        if lib().l1csr_host_alloc_mapped(4 * self.PAGE, C.byref(h), C.byref(d)) != 0:
+            self.disabled = True  # the runtime refused: the calls fall back to a queued copy
+            return None
+        words = [_HostWord(h.value + 4 * i, d.value + 4 * i) for i in range(self.PAGE)]
+        self.free.extend(words[1:])
+        return words[0]
+
+    def release(self, w):
+        self.free.append(w)
+
+
+_words = _HostWords()
+
+
+def _nnz_word(out):
+    """The word `out` has kernels write its nnz into (acquired on first use),
+    or None under graph capture or where no mapped memory is available."""
+    import weakref
+    torch = _torch()
+    if torch.cuda.is_current_stream_capturing():
+        return None
+    w = getattr(out, "_word", None)
+    if w is None:
+        w = _words.acquire()
+        if w is not None:
+            out._word = w
+            weakref.finalize(out, _words.release, w)
+    return w
+
+
+def _nnz_dev(out):
+    w = _nnz_word(out)
+    return None if w is None else C.c_void_p(w.dev)
+
+
 def _set_nnz(out, need, stream):
-    """The host count a call returned (>= 0), else the queued pinned copy."""
+    """The host count a call returned (>= 0), else the count its kernels
+    wrote into out's host word (an event behind them), else a queued copy."""
     if need >= 0:
         out.nnz = int(need)
         out._pending = None
-    else:
+        return
+    torch = _torch()
+    w = getattr(out, "_word", None)
+    if w is None or torch.cuda.is_current_stream_capturing():
         out.track_nnz(stream)
+        return
+    s = torch.cuda.current_stream(out.row_ptr.device) if stream is None else stream
+    ev = torch.cuda.Event()
+    ev.record(s)
+    w.event = ev
+    out.nnz = None
+    out._pending = (w, ev)
 
 
 def _stream(stream=None):
@@ -219,14 +297,14 @@ class CSR:
     col_idx: "object"
     vals: "object"
     nnz: int | None = None
-    _pending: "object" = None  # (pinned int32 copy of row_ptr[-1], its event)
+    _pending: "object" = None  # (pinned int32 holding nnz (a copy or a word kernels write), its event)
 
     def host_nnz(self) -> int:
         if self.nnz is None:
             if self._pending is not None:
                 host, ev = self._pending
                 ev.synchronize()
-                self.nnz = int(host[0])
+                self.nnz = host.value() if isinstance(host, _HostWord) else int(host[0])
             else:
                 self.nnz = int(self.row_ptr[-1].item())
         self._pending = None
@@ -526,7 +604,7 @@ def csr_recompress(Z, t=0.0, row_counts=None, capacity=None, out: CSR | None = N
     ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev, stream)
     need = C.c_int64(-1)
     _check(lib().csr_recompress(N, K, _p(Z), ldz, float(t), _p(row_counts), _p(out.row_ptr),
-                                _p(out.col_idx), _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
+                                _p(out.col_idx), _p(out.vals), cap, _nnz_dev(out), C.byref(need), _p(ws), wsb,
                                 _stream(stream)), "csr_recompress")
     _set_nnz(out, need.value, stream)
     return out
@@ -606,7 +684,7 @@ def csr_recompress_counted(Z, word_counts, out: CSR | None = None, capacity=None
     ws, wsb = _workspace(workspace_bytes(OP_RECOMPRESS, N, K, 0, 0), dev, stream)
     need = C.c_int64(-1)
     _check(lib().csr_recompress_counted(N, K, _p(Z), ldz, _p(word_counts), _p(out.row_ptr), _p(out.col_idx),
-                                        _p(out.vals), cap, None, C.byref(need), _p(ws), wsb, _stream(stream)),
+                                        _p(out.vals), cap, _nnz_dev(out), C.byref(need), _p(ws), wsb, _stream(stream)),
            "csr_recompress_counted")
     _set_nnz(out, need.value, stream)
     return out
@@ -637,7 +715,7 @@ def prox_l1_recompress_noalloc(W: CSR, G, eta, lam, out: CSR, capacity=None, str
     need = C.c_int64(-1)
     _check(lib().prox_l1_recompress_noalloc(N, K, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(G),
                                             ldg, float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
-                                            _p(out.vals), cap, None, C.byref(need), _stream(stream)),
+                                            _p(out.vals), cap, _nnz_dev(out), C.byref(need), _stream(stream)),
            "prox_l1_recompress_noalloc")
     _set_nnz(out, need.value, stream)
     return out
@@ -661,7 +739,7 @@ def prox_l1_recompress(W: CSR, G, eta, lam, capacity=None, out: CSR | None = Non
     need = C.c_int64(-1)
     _check(lib().prox_l1_recompress(N, K, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(G), ldg,
                                     float(eta), float(lam), _p(out.row_ptr), _p(out.col_idx),
-                                    _p(out.vals), cap, None, C.byref(need), _p(ws), wsb,
+                                    _p(out.vals), cap, _nnz_dev(out), C.byref(need), _p(ws), wsb,
                                     _stream(stream)), "prox_l1_recompress")
     _set_nnz(out, need.value, stream)
     return out
@@ -771,7 +849,7 @@ def prox_adaptive_recompress(W: CSR, G, st: AdaptiveState, eta, lam, capacity=No
                                           _p(W.vals), _p(G), ldg, _p(m), _p(st.v), lds, float(eta),
                                           float(lam), float(st.eps), float(st.beta1),
                                           float(st.beta2), int(st.t), _p(out.row_ptr),
-                                          _p(out.col_idx), _p(out.vals), cap, None, C.byref(need),
+                                          _p(out.col_idx), _p(out.vals), cap, _nnz_dev(out), C.byref(need),
                                           _p(ws), wsb, _stream(stream)), "prox_adaptive_recompress")
     st.t += 1
     _set_nnz(out, need.value, stream)
@@ -892,9 +970,9 @@ def csr_compact(W: CSR, out: CSR | None = None, stream=None) -> CSR:
                   torch.empty(cap, dtype=torch.float32, device=dev), None)
     ws, wsb = _workspace(workspace_bytes(OP_COMPACT, W.n_rows, 0, nnz, 0), dev, stream)
     _check(lib().csr_compact(W.n_rows, nnz, _p(W.row_ptr), _p(W.col_idx), _p(W.vals), _p(out.row_ptr),
-                             _p(out.col_idx), _p(out.vals), None, _p(ws), wsb, _stream(stream)),
+                             _p(out.col_idx), _p(out.vals), _nnz_dev(out), _p(ws), wsb, _stream(stream)),
            "csr_compact")
-    out.track_nnz(stream)
+    _set_nnz(out, -1, stream)
     return out
 
 

@@ -239,6 +239,25 @@ const char *l1csr_status_str(int status) {
     }
 }
 
+int l1csr_host_alloc_mapped(size_t bytes, void **host, void **dev) {
+    if (bytes == 0 || host == nullptr || dev == nullptr) return L1CSR_EINVAL;
+    void *h = nullptr;
+    if (hipHostMalloc(&h, bytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) return L1CSR_EHIP;
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess || d == nullptr) {
+        (void)hipHostFree(h);
+        return L1CSR_EHIP;
+    }
+    *host = h;
+    *dev = d;
+    return L1CSR_OK;
+}
+
+int l1csr_host_free_mapped(void *host) {
+    if (host == nullptr) return L1CSR_EINVAL;
+    return hipHostFree(host) == hipSuccess ? L1CSR_OK : L1CSR_EHIP;
+}
+
 size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz, int32_t B) {
     if (n_rows < 0 || n_cols < 0 || nnz < 0 || B < 0) return 0;
     switch (op) {

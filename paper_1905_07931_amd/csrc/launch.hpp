@@ -90,7 +90,7 @@ hipError_t launch_wgrad_bf16x3_prox(int N, int K, int B, const float *dY, int64_
 //     (counts [N][ceil(K / 32)]) from W's bitmap index (mask / pos); split_ws
 //     holds wgrad_prox_split_bytes() (fp32 products that split their batch);
 //   launch_counted_sums: the row totals of the counts and their totals per
-//     block of 64 rows into ws (counted_ws_ints(N) ints);
+//     block of 16-64 rows into ws (counted_ws_ints(N) ints);
 //   launch_counted_row_ptr: row_ptr_out (row_ptr_out[N] = nnz') by a scan of
 //     the row totals;
 //   launch_counted_compact: col_out / val_out (< capacity), nnz' to d_nnz_out;

@@ -6,8 +6,8 @@
 //   2. the weight-gradient GEMM with the prox epilogue (prox_epilogue.hpp):
 //      Z = S_t(W - eta * dY.X^T) and the nonzero count of every 32-column
 //      word of every row;
-//   3. row totals of the word counts and their totals per block of 64 rows
-//      (row_block_sums_kernel);
+//   3. row totals of the word counts and their totals per block of 16-64
+//      rows (row_block_sums_kernel);
 //   4. compaction of Z into col_idx', vals' (compact_kernel): a workgroup per
 //      (row, 3072-column chunk) starts at row_ptr'[row] plus the counts of
 //      the row's words before the chunk, so no second pass over the gradient.
@@ -36,9 +36,17 @@ namespace {
 constexpr int kCompactCols = 3072;  // columns per compaction workgroup (whole 32-column words)
 constexpr int kCompactThreads = 256;
 constexpr int kCompactVecs = kCompactCols / (4 * kCompactThreads);  // float4 per thread: 3
-constexpr int kPrefixRows = 64;        // rows per block of the two-level row prefix (16 waves x 4 rows)
-constexpr int kPrefixMaxBlocks = 256;  // block totals a compaction workgroup adds up at most
-static_assert(kPrefixMaxBlocks <= kCompactThreads && kPrefixRows <= kCompactThreads, "one load per thread");
+// rows per block of the two-level row prefix: 16, 32 or 64 (a workgroup of
+// that many rows / 4 waves), the smallest that keeps the blocks of N rows to
+// kPrefixMaxBlocks, the block totals a compaction workgroup adds up at most
+constexpr int kPrefixMinRows = 16, kPrefixMaxRows = 64;
+constexpr int kPrefixMaxBlocks = 256;
+static_assert(kPrefixMaxBlocks <= kCompactThreads && kPrefixMaxRows <= kCompactThreads, "one load per thread");
+int prefix_rows(int N) {
+    int r = kPrefixMinRows;
+    while (r < kPrefixMaxRows && ceil_div(N, r) > kPrefixMaxBlocks) r *= 2;
+    return r;
+}
 
 // mask[w][row] bit c: column 32w + c is stored; pos[w][row]: CSR position of
 // the row's first entry with column >= 32w (row_ptr[row + 1] past the last).
@@ -221,13 +229,13 @@ __global__ __launch_bounds__(256) void prox_words_kernel(int n_rows, int n_cols,
 }
 
 // row_counts[row] = sum of the row's word counts; blk[b] = sum over rows
-// [64b, 64b + 64).  A workgroup of 16 waves per 64 rows, a wave per 4 rows;
+// [R b, R b + R), R = 4 x the waves of the workgroup.  A wave per 4 rows;
 // each round issues 4 words of each of the 4 rows (16 loads) before adding.
 __global__ __launch_bounds__(1024) void row_block_sums_kernel(int n_rows, int kw, const int *__restrict__ counts,
                                                               int *__restrict__ row_counts, int *__restrict__ blk) {
     __shared__ int part[1024 / kWave];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int r0 = blockIdx.x * kPrefixRows + wave * 4;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x / kWave;
+    const int r0 = (blockIdx.x * nwaves + wave) * 4;
     int v[4] = {0, 0, 0, 0};
     for (int j0 = lane; j0 < kw; j0 += 4 * kWave) {
         int a[4][4];
@@ -254,15 +262,14 @@ __global__ __launch_bounds__(1024) void row_block_sums_kernel(int n_rows, int kw
     __syncthreads();
     if (threadIdx.x == 0) {
         int b = 0;
-#pragma unroll
-        for (int w = 0; w < 1024 / kWave; ++w) b += part[w];
+        for (int w = 0; w < nwaves; ++w) b += part[w];
         blk[blockIdx.x] = b;
     }
 }
 
 // Z -> col_idx', vals' for columns [c0, c0 + 3072) of one row, nonzeros in
 // column order.  With blk, the row's start is row_ptr'[row] = blk[0 .. b) +
-// row_counts[64b .. row) (b = row / 64), and the row's first chunk writes it
+// row_counts[R b .. row) (b = row / R, R = prows), and the row's first chunk writes it
 // (the last row's also row_ptr'[n_rows] and *d_nnz); without, row_ptr holds
 // it.  Thread t holds the float4s t, t + 256, t + 512 of the chunk;
 // ranks come from four ballots per float4 slot and the wave totals of all
@@ -272,7 +279,7 @@ __global__ __launch_bounds__(1024) void row_block_sums_kernel(int n_rows, int kw
 template <bool V4>
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     int n_rows, int n_cols, int chunks, const float *__restrict__ Z, int64_t ldz, int kw,
-    const int *__restrict__ counts, const int *__restrict__ row_counts, const int *__restrict__ blk,
+    const int *__restrict__ counts, const int *__restrict__ row_counts, const int *__restrict__ blk, int prows,
     int *__restrict__ row_ptr, int *__restrict__ d_nnz, int *__restrict__ col_out, float *__restrict__ val_out,
     int64_t capacity) {
     __shared__ int red[kCompactThreads / kWave];
@@ -299,7 +306,7 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     for (int j = tid; j < s0; j += kCompactThreads) before += counts[(int64_t)row * kw + j];
     int prefix = 0;  // row_ptr'[row], when added up here
     if (blk) {
-        const int b = row / kPrefixRows, r0 = b * kPrefixRows;
+        const int b = row / prows, r0 = b * prows;
         if (tid < b) prefix += blk[tid];
         if (tid < row - r0) prefix += row_counts[r0 + tid];
     }
@@ -413,14 +420,14 @@ hipError_t launch_wgrad_prox(int N, int K, int B, const float *dY, int64_t ldy, 
     return hipGetLastError();
 }
 
-size_t counted_ws_ints(int N) { return (size_t)N + 1 + (size_t)ceil_div(N, kPrefixRows); }
+size_t counted_ws_ints(int N) { return (size_t)N + 1 + (size_t)ceil_div(N, kPrefixMinRows); }
 
-bool counted_prefix_in_compact(int N) { return ceil_div(N, kPrefixRows) <= kPrefixMaxBlocks; }
+bool counted_prefix_in_compact(int N) { return ceil_div(N, kPrefixMaxRows) <= kPrefixMaxBlocks; }
 
 hipError_t launch_counted_sums(int N, int K, const int *counts, int *ws, hipStream_t s) {
     if (N == 0) return hipSuccess;
-    const int kw = (int)ceil_div(K, 32);
-    row_block_sums_kernel<<<(unsigned)ceil_div(N, kPrefixRows), 1024, 0, s>>>(N, kw, counts, ws, ws + N + 1);
+    const int kw = (int)ceil_div(K, 32), r = prefix_rows(N);
+    row_block_sums_kernel<<<(unsigned)ceil_div(N, r), 16 * r, 0, s>>>(N, kw, counts, ws, ws + N + 1);
     return hipGetLastError();
 }
 
@@ -443,10 +450,12 @@ hipError_t launch_counted_compact(int N, int K, const float *Z, int64_t ldz, con
         const bool v4 = (ldz % 4 == 0) && aligned16(Z);
         if (v4)
             compact_kernel<true><<<(unsigned)blocks, kCompactThreads, 0, s>>>(
-                N, K, chunks, Z, ldz, kw, counts, ws, blk, row_ptr_out, dn, col_out, val_out, capacity);
+                N, K, chunks, Z, ldz, kw, counts, ws, blk, prefix_rows(N), row_ptr_out, dn, col_out, val_out,
+                capacity);
         else
             compact_kernel<false><<<(unsigned)blocks, kCompactThreads, 0, s>>>(
-                N, K, chunks, Z, ldz, kw, counts, ws, blk, row_ptr_out, dn, col_out, val_out, capacity);
+                N, K, chunks, Z, ldz, kw, counts, ws, blk, prefix_rows(N), row_ptr_out, dn, col_out, val_out,
+                capacity);
         e = hipGetLastError();
     }
     if (e == hipSuccess && d_nnz_out && !prefix_here) e = launch_copy_i32(row_ptr_out + N, d_nnz_out, s);

@@ -349,8 +349,8 @@ def test_fused_weight_update_arguments_are_rejected_before_launch(lib):
                 dict(Z=base["mk"] + 4), dict(wc=base["ci"])]:
         assert prox(**bad) == EINVAL, bad
     assert prox(N=65536, K=65536, ldz=65536) == EUNSUPPORTED
-    # the workspace: row totals (N + 1) and one total per 64 rows
-    assert lib.l1csr_workspace_bytes(2, N, K, 0, 0) >= 4 * (N + 1 + (N + 63) // 64)
+    # the workspace: row totals (N + 1) and one total per block of 16 or more rows
+    assert lib.l1csr_workspace_bytes(2, N, K, 0, 0) >= 4 * (N + 1 + (N + 15) // 16)
     for bad in [dict(N=-1), dict(ldz=K - 1), dict(wc=None), dict(rpo=None), dict(wsb=4 * (N + 1)), dict(ws=None),
                 dict(cio=base["Z"] + 4), dict(vo=base["wc"]), dict(rpo=base["cio"] + 4 * (N * K - 1)),
                 dict(vo=base["ws"])]:
@@ -400,3 +400,17 @@ def test_planned_product_arguments_are_rejected_before_launch(lib):
     # no tiled plan at a small shape: nothing to plan, no buffer needed
     assert lib.l1csr_workspace_bytes(4, 64, 100, 300, 16) == 0
     assert pl(64, 100, 300, C.c_void_p(1 << 30), C.c_void_p(2 << 30), C.c_void_p(3 << 30), 16, None, 0, S) == OK
+
+
+def test_mapped_host_memory_arguments_are_checked(lib):
+    """l1csr_host_alloc_mapped rejects a zero size and missing out-pointers
+    before it asks the runtime for anything; freeing NULL is an error too."""
+    a = lib.l1csr_host_alloc_mapped
+    a.argtypes = [C.c_size_t, C.POINTER(C.c_void_p), C.POINTER(C.c_void_p)]
+    f = lib.l1csr_host_free_mapped
+    f.argtypes = [C.c_void_p]
+    h, d = C.c_void_p(), C.c_void_p()
+    assert a(0, C.byref(h), C.byref(d)) == EINVAL
+    assert a(64, None, C.byref(d)) == EINVAL
+    assert a(64, C.byref(h), None) == EINVAL
+    assert f(None) == EINVAL

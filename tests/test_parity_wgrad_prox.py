@@ -144,12 +144,13 @@ def test_fused_update_capacity_paths():
     assert bool((out.col_idx == -7).all()) and bool((out.vals == -7.0).all())
 
 
-@pytest.mark.parametrize("N", [64, 16384, 16385])
+@pytest.mark.parametrize("N", [64, 4097, 16384, 16385])
 def test_counted_recompress_row_prefix_paths(N):
     # each row's start is added up inside the compaction (up to 256 blocks of
-    # 64 rows, capacity >= N * K) or written by a scan first (more blocks, or
-    # a smaller capacity whose check needs nnz' on the host): the same CSR as
-    # the oracle's recompression on every path, nnz' in d_nnz_out
+    # 16, 32 or 64 rows, capacity >= N * K) or written by a scan first (more
+    # rows than 256 blocks of 64 hold, or a smaller capacity whose check needs
+    # nnz' on the host): the same CSR as the oracle's recompression on every
+    # path, nnz' in d_nnz_out
     import ctypes as C
     import torch
     rng = np.random.default_rng(N)
@@ -170,17 +171,52 @@ def test_counted_recompress_row_prefix_paths(N):
         cio = torch.full((cap,), -3, dtype=torch.int32, device=cuda())
         vo = torch.full((cap,), -3.0, dtype=torch.float32, device=cuda())
         dn = torch.full((1,), -3, dtype=torch.int32, device=cuda())
-        need = C.c_int64(-5)
-        st = L1.lib().csr_recompress_counted(N, K, L1._p(Z), K, L1._p(wc), L1._p(rpo), L1._p(cio), L1._p(vo), cap,
-                                             L1._p(dn), C.byref(need), L1._p(ws), ws.numel(), L1._stream())
-        torch.cuda.synchronize()
-        assert st == 0, (cap, st)
-        assert need.value == (-1 if cap >= N * K else n)
-        assert int(h(dn)[0]) == n
+        hw = L1._words.acquire()  # and a word of mapped host memory the kernels write
+        assert hw is not None
+        C.c_int32.from_address(hw.host).value = -3
+        for sink in (L1._p(dn), C.c_void_p(hw.dev)):
+            need = C.c_int64(-5)
+            st = L1.lib().csr_recompress_counted(N, K, L1._p(Z), K, L1._p(wc), L1._p(rpo), L1._p(cio), L1._p(vo),
+                                                 cap, sink, C.byref(need), L1._p(ws), ws.numel(), L1._stream())
+            torch.cuda.synchronize()
+            assert st == 0, (cap, st)
+            assert need.value == (-1 if cap >= N * K else n)
+        assert int(h(dn)[0]) == n and hw.value() == n
+        L1._words.release(hw)
         assert bits_equal(h(rpo), rp), cap
         assert bits_equal(h(cio)[:n], ci) and bits_equal(h(vo)[:n], v), cap
         if cap > n:
             assert bool((cio[n:] == -3).all()) and bool((vo[n:] == -3.0).all())
+
+
+def test_counts_reach_the_host_through_mapped_words():
+    # a call at full capacity leaves nnz' in pinned host memory written by its
+    # own kernels (no copy queued behind it); the word stays with its CSR and
+    # later calls into the same CSR overwrite it in stream order; when the CSR
+    # goes, the word is handed out again only after its last write is done
+    import gc
+    import torch
+    L = synth.fc_layer(257, 1000, 70, 30000, seed=13)
+    W = _W(L)
+    bm = L1.csr_bitmap_build(W)
+    out = None
+    for lam in (0.02, 0.5, 0.0, 1e6):
+        Z, wc = L1.dense_wgrad_prox(W, t(L.dY), t(L.X), L.eta, lam, bm)
+        out = L1.csr_recompress_counted(Z, wc, out=out)
+        assert out.nnz is None and isinstance(out._pending[0], L1._HostWord)
+        n = out.host_nnz()
+        assert n == int(out.row_ptr[-1].item()) == int((h(Z) != 0).sum())
+        assert out._pending is None and out.nnz == n
+    assert n == 0  # the last threshold deletes every weight
+    w = out._word
+    del out
+    gc.collect()
+    assert w in L1._words.free
+    torch.cuda.synchronize()
+    again = [L1._words.acquire() for _ in range(len(L1._words.free))]
+    assert w in again  # its event has completed
+    for x in again:
+        L1._words.release(x)
 
 
 def test_fused_update_padded_leading_dimensions():
