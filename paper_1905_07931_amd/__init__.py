@@ -285,10 +285,12 @@ class CSR:
     ``nnz`` is the host-side count when known.  A call that writes a CSR
     without waiting (:func:`csr_recompress`, :func:`prox_l1_recompress`, ...
     at full capacity) leaves it ``None``: ``row_ptr[-1]`` holds it on the
-    device, and the call has queued a copy of it into pinned host memory
-    behind its last kernel.  The first use of the matrix then waits for that
-    copy only (an event), not for the whole device; set ``nnz`` beforehand
-    (e.g. under graph capture) to avoid the wait.
+    device, and the call's own kernels have also written it into a word of
+    mapped pinned host memory that the CSR keeps (or, where the runtime gives
+    no such memory, the call has queued a copy behind its last kernel).  The
+    first use of the matrix then waits for that call only (an event), not for
+    the whole device; set ``nnz`` beforehand (e.g. under graph capture) to
+    avoid the wait.
     ``col_idx``/``vals`` may be longer than nnz (capacity).
     """
     n_rows: int
