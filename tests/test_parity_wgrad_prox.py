@@ -219,6 +219,23 @@ def test_counts_reach_the_host_through_mapped_words():
         L1._words.release(x)
 
 
+def test_counts_fall_back_to_a_queued_copy_without_mapped_memory(monkeypatch):
+    # where the runtime gives no mapped host memory, the binding queues a
+    # copy of row_ptr[-1] behind the call instead: the same counts
+    import torch
+    words = L1._HostWords()
+    words.disabled = True
+    monkeypatch.setattr(L1, "_words", words)
+    L = synth.fc_layer(257, 1000, 70, 30000, seed=13)
+    W = _W(L)
+    Z, wc = L1.dense_wgrad_prox(W, t(L.dY), t(L.X), L.eta, 0.02, L1.csr_bitmap_build(W))
+    out = L1.csr_recompress_counted(Z, wc)
+    assert getattr(out, "_word", None) is None and out.nnz is None
+    assert not isinstance(out._pending[0], L1._HostWord)
+    torch.cuda.synchronize()
+    assert out.host_nnz() == int(out.row_ptr[-1].item()) == int((h(Z) != 0).sum())
+
+
 def test_fused_update_padded_leading_dimensions():
     import torch
     L = synth.fc_layer(130, 300, 40, 4000, seed=11)
