@@ -474,8 +474,12 @@ __global__ __launch_bounds__(256) void stream_fill_kernel(
 // the chunks' offsets inside the stream are prefix sums, and every entry, the
 // chunk headers and the padding pairs of odd runs are written to their places:
 // the same bytes as the launches above, without the per-(row, tile) bounds.
-// The stream starts at woff[g] (the exclusive scan of the per-wave bounds of
-// plan_deal_kernel); the main kernel finds each chunk from the one before.
+// The stream starts at woff[g], the exclusive scan of the per-wave bounds of
+// plan_deal_kernel: with wsize given, each workgroup adds up the bounds before
+// its stream itself and writes woff[g] (and woff[nw] at the last); without, a
+// scan launch has written woff.  The main kernel finds each chunk from the
+// one before.  At most 64 VGPRs (8 waves per SIMD), so that two workgroups
+// share a CU.
 constexpr int kBucketThreads = 1024;
 
 template <int VEC, bool HALF>

@@ -15,9 +15,9 @@
 //      and of the row totals before it in its block, added up by each
 //      workgroup itself (at most 256 + 63 integers, cached); the first chunk
 //      of a row writes it.  Where the caller's capacity is below n_rows *
-//      n_cols the host needs nnz' first, and past 256 blocks the sums grow
-//      long: an exclusive scan of the row totals writes row_ptr' instead and
-//      the compaction reads it.
+//      n_cols the host needs nnz' first, and past 16384 rows (256 blocks of
+//      64) the sums grow long: an exclusive scan of the row totals writes
+//      row_ptr' instead and the compaction reads it.
 //
 // Shapes whose GEMM has no prox epilogue (bf16 operands, or an fp32 product
 // that splits its reduction) write dW into Z first and run the same prox in
