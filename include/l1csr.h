@@ -101,7 +101,7 @@ size_t l1csr_workspace_bytes(int op, int32_t n_rows, int32_t n_cols, int64_t nnz
 /*
  * Pinned host memory that kernels can write directly, for small results the
  * host reads after the call (a d_nnz_out below, say), so that no copy has to
- * be queued behind the call: `bytes` bytes from hipHostMalloc (mapped,
+ * be queued behind the call: `bytes` bytes from hipHostMalloc (mapped, portable,
  * coherent); *host receives the host address, *dev the address kernels use.
  * The caller owns the memory and frees it with l1csr_host_free_mapped once
  * no queued work can still write it.  L1CSR_EINVAL for bytes == 0 or a NULL

@@ -242,7 +242,8 @@ const char *l1csr_status_str(int status) {
 int l1csr_host_alloc_mapped(size_t bytes, void **host, void **dev) {
     if (bytes == 0 || host == nullptr || dev == nullptr) return L1CSR_EINVAL;
     void *h = nullptr;
-    if (hipHostMalloc(&h, bytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) return L1CSR_EHIP;
+    if (hipHostMalloc(&h, bytes, hipHostMallocMapped | hipHostMallocPortable | hipHostMallocCoherent) != hipSuccess)
+        return L1CSR_EHIP;
     void *d = nullptr;
     if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess || d == nullptr) {
         (void)hipHostFree(h);
