@@ -87,6 +87,16 @@ def test_fused_update_full_size_9216x4096(precision):
     assert 0 < n < L.N * L.K
 
 
+def test_fused_update_direct_load_tiles_with_ragged_edges():
+    # 4036 x 9116 at batch 64: the 256 x 288 direct-load tiles (512 of them,
+    # two rounds), the last row block 196 rows high and the last column block
+    # 188 wide, so the epilogue's row and column bounds and its double-buffered
+    # gathers meet partial tiles
+    L = synth.fc_layer(4036, 9116, 64, synth.nnz_for(4036, 9116, 0.09), seed=14)
+    n = _fused_vs_unfused(L, L1.F32, lam=0.5)
+    assert 0 < n < L.N * L.K
+
+
 def test_fused_update_split_reduction_fallback():
     # 50 x 500 with a reduction of 16384: the fp32 product splits its batch
     # (no fused epilogue there), so dW goes through Z and the prox runs after
