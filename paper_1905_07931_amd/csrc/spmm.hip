@@ -2,8 +2,8 @@
 // over the CSC copy, backward dX = W^T.dY).
 //
 // Streamed tiled kernel (the hot path).  One 1024-thread workgroup per CU owns
-// a chunk of BB = 64*VEC batch columns and a set of rows; every lane keeps VEC
-// accumulators for each of the wave's row pieces.  The dense operand passes
+// a chunk of BB = 64*VEC batch columns (32*VEC with half-wave units) and a set
+// of rows; every lane keeps VEC accumulators for each of the wave's row pieces.  The dense operand passes
 // through LDS in 64 KB tiles of KT rows, double buffered: while the waves work
 // on tile t, the direct global->LDS loads of tile t+1 are in flight.
 //
