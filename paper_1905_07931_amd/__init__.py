@@ -54,6 +54,12 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_1905_07931_amd.build`")
+        # torch ships its own libamdhip64.so.7; loaded first, it is the copy the
+        # dynamic linker hands the library, so the process holds one HIP
+        # runtime and torch's streams and memory are valid in the library's
+        # launches (loaded the other way round, the library would bind the
+        # system runtime and torch a second one)
+        import torch  # noqa: F401
         L = C.CDLL(LIB_PATH)
         i32, i64, f32, vp, sz = C.c_int32, C.c_int64, C.c_float, C.c_void_p, C.c_size_t
         L.l1csr_status_str.argtypes = [C.c_int]

@@ -414,3 +414,24 @@ def test_mapped_host_memory_arguments_are_checked(lib):
     assert a(64, None, C.byref(d)) == EINVAL
     assert a(64, C.byref(h), None) == EINVAL
     assert f(None) == EINVAL
+
+
+def test_binding_and_torch_share_one_hip_runtime():
+    """The binding loads the library after torch, so that the library binds
+    torch's own HIP runtime: a second runtime in the process would not know
+    torch's streams or memory.  Checked in a fresh interpreter that asks for
+    the library before anything else imports torch."""
+    import ast
+    import subprocess
+    import sys
+    if not os.path.exists(LIB):
+        from paper_1905_07931_amd import build
+        build.build(verbose=False)
+    code = ("import paper_1905_07931_amd as L1\n"
+            "L1.lib()\n"
+            "import torch\n"
+            "print(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    runtimes = ast.literal_eval(r.stdout.strip().splitlines()[-1])
+    assert len(runtimes) == 1, runtimes
