@@ -102,6 +102,33 @@ def test_spmm_power_law_rows_dyadic_bit_exact():
     assert bits_equal(h(L1.csr_spmm_fwd(W, t(X))), oracle.spmm_fwd(rp, ci, vals, X))
 
 
+@pytest.mark.parametrize("case", ["zipf_steep", "mostly_empty_rows"])
+def test_spmm_tiled_skewed_patterns_both_directions(case):
+    # the planner's pieces, deal and bucketing on skewed patterns: a steep
+    # power law (a few rows split into many strided pieces, most rows short)
+    # and a layer whose rows are three quarters empty, through the tiled
+    # kernel forward and backward, against the oracle
+    rng = np.random.default_rng(29 if case == "zipf_steep" else 30)
+    if case == "zipf_steep":
+        N, K, B = 4096, 2048, 512
+        rp, ci = synth.zipf_pattern(rng, N, K, 400000, 1.5)
+    else:
+        N, K, B = 8192, 1000, 1024
+        dense = rng.random((N, K)) < 0.15
+        dense[rng.random(N) < 0.75] = False
+        rp, ci = synth.pattern_from_positions(N, K, np.flatnonzero(dense.reshape(-1)))
+    vals = rng.standard_normal(ci.shape[0]).astype(np.float32)
+    X = rng.random((K, B), dtype=np.float32)
+    dY = rng.standard_normal((N, B)).astype(np.float32)
+    assert L1.workspace_bytes(L1.OP_SPMM, N, K, len(ci), B) > 0  # the tiled path
+    W = L1.CSR.from_host(rp, ci, vals, K, device=cuda())
+    Y = h(L1.csr_spmm_fwd(W, t(X)))
+    assert_scaled_close(Y, oracle.spmm_fwd(rp, ci, vals, X), oracle.spmm_fwd(rp, ci, np.abs(vals), X), what="Y")
+    dX = h(L1.csr_spmm_bwd_t(W, t(dY), L1.csc_build(W)))
+    assert_scaled_close(dX, oracle.spmm_bwd_t(rp, ci, vals, dY, K),
+                        oracle.spmm_bwd_t(rp, ci, np.abs(vals), np.abs(dY), K), what="dX")
+
+
 # The tiled product split into its planning launches and the product from
 # the plan: the same bits as the one-call form, forward and backward, on the
 # half-wave, full-wave and VEC-2 plans and a shape with no plan; the plan is
