@@ -208,20 +208,26 @@ def _nnz_dev(out):
 
 def _set_nnz(out, need, stream):
     """The host count a call returned (>= 0), else the count its kernels
-    wrote into out's host word (an event behind them), else a queued copy."""
+    wrote into out's host word (an event behind them), else a queued copy.
+    Whenever the call was given the word, the event goes behind it even if
+    the host count is known: its kernels write the word all the same, and the
+    pool hands the word to another CSR only once that write is done."""
+    torch = _torch()
+    w = getattr(out, "_word", None)
+    capturing = torch.cuda.is_current_stream_capturing()
+    ev = None
+    if w is not None and not capturing:
+        s = torch.cuda.current_stream(out.row_ptr.device) if stream is None else stream
+        ev = torch.cuda.Event()
+        ev.record(s)
+        w.event = ev
     if need >= 0:
         out.nnz = int(need)
         out._pending = None
         return
-    torch = _torch()
-    w = getattr(out, "_word", None)
-    if w is None or torch.cuda.is_current_stream_capturing():
+    if ev is None:
         out.track_nnz(stream)
         return
-    s = torch.cuda.current_stream(out.row_ptr.device) if stream is None else stream
-    ev = torch.cuda.Event()
-    ev.record(s)
-    w.event = ev
     out.nnz = None
     out._pending = (w, ev)
 

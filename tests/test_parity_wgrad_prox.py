@@ -229,6 +229,23 @@ def test_counts_reach_the_host_through_mapped_words():
         L1._words.release(x)
 
 
+def test_word_of_a_call_with_a_host_count_waits_for_its_kernels():
+    # a call that returns nnz' on the host (a capacity below N*K) still hands
+    # its kernels the CSR's host word: the word gets an event behind the call,
+    # so the pool cannot give it to another CSR while that write is queued
+    import torch
+    rng = np.random.default_rng(14)
+    Zh = (rng.standard_normal((64, 300)) * (rng.random((64, 300)) < 0.3)).astype(np.float32)
+    out = L1.csr_recompress(t(Zh), capacity=64 * 300 - 1)
+    assert out.nnz == int((Zh != 0).sum())
+    w = getattr(out, "_word", None)
+    if w is None:
+        pytest.skip("no mapped host memory on this runtime")
+    assert w.event is not None
+    torch.cuda.synchronize()
+    assert w.event.query()
+
+
 def test_counts_fall_back_to_a_queued_copy_without_mapped_memory(monkeypatch):
     # where the runtime gives no mapped host memory, the binding queues a
     # copy of row_ptr[-1] behind the call instead: the same counts
