@@ -282,7 +282,9 @@ int prox_l1_step(int mode, int32_t n_rows, int32_t n_cols, int64_t nnz,
  * vals_out[nnz'].  row_counts (nullable) are the per-row counts prox_l1_step
  * produced for the same Z and t = 0; when NULL they are recomputed.
  * d_nnz_out (nullable; device memory or l1csr_host_alloc_mapped's *dev)
- * receives nnz'.
+ * receives nnz' from the call's kernels, in both capacity modes below (so a
+ * mapped word is written in stream order even when *h_nnz_required already
+ * gives the count on the host).
  *   capacity >= n_rows*n_cols: never overflows and never waits (hot path).
  *   capacity <  n_rows*n_cols: the call counts first, waits for the stream,
  *     and returns L1CSR_ECAPACITY with *h_nnz_required (host, nullable) = nnz'
