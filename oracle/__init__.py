@@ -89,6 +89,7 @@ def lib():
                                      C.POINTER(C.c_int64)]
         L.orc_compact.argtypes = [i32, _i32p, _i32p, _f32p, _i32p, _i32p, _f32p,
                                   C.POINTER(C.c_int64)]
+        L.orc_csc.argtypes = [i32, i32, _i32p, _i32p, _f32p, _i32p, _i32p, _i32p, _f32p]
         L.orc_relu_fwd.argtypes = [i64, _f32p, _f32p]
         L.orc_relu_bwd.argtypes = [i64, _f32p, _f32p, _f32p]
         L.orc_softmax_xent.argtypes = [i32, i32, _f32p, i64, _i32p, _f32p,
@@ -339,6 +340,21 @@ def recompress(Z, t=0.0):
     v = np.empty(max(cap, 1), np.float32)
     _check(lib().orc_recompress(N, K, Z, K, t, rp, ci, v, cap, C.byref(nnz)), "recompress")
     return rp, ci[: nnz.value].copy(), v[: nnz.value].copy()
+
+
+def csc(row_ptr, col_idx, vals, n_cols):
+    """The canonical CSC of an N x n_cols CSR matrix (Section 3.2's column-wise
+    copy): (col_ptr, row_idx, perm, vals_t), the entries of each column in
+    ascending row order, perm[q] the CSR position of CSC entry q."""
+    rp, ci, v = _csr(row_ptr, col_idx, vals)
+    N = rp.shape[0] - 1
+    n = ci.shape[0]
+    cp = np.empty(n_cols + 1, np.int32)
+    ri = np.empty(max(n, 1), np.int32)
+    pm = np.empty(max(n, 1), np.int32)
+    vt = np.empty(max(n, 1), np.float32)
+    _check(lib().orc_csc(N, n_cols, rp, ci, v, cp, ri, pm, vt), "csc")
+    return cp, ri[:n].copy(), pm[:n].copy(), vt[:n].copy()
 
 
 def compact(row_ptr, col_idx, vals):

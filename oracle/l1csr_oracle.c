@@ -624,6 +624,38 @@ int orc_recompress(int32_t N, int32_t K, const float *Z, int64_t ldz, float t,
 }
 
 /* ------------------------------------------------------------------------
+ * CSR -> CSC, the column-wise copy of W that the backward product reads
+ * (Section 3.2, "Backward": it needs W by columns).  The canonical CSC: the
+ * entries of a column in ascending row order.  col_ptr[K+1], row_idx[nnz],
+ * perm[nnz] (the CSR position of each CSC entry) and, if vals and vals_t are
+ * both given, vals_t[q] = vals[perm[q]].  Counts per column, their prefix
+ * sums, then the entries placed row by row.
+ * ---------------------------------------------------------------------- */
+int orc_csc(int32_t N, int32_t K, const int32_t *row_ptr, const int32_t *col_idx, const float *vals,
+            int32_t *col_ptr, int32_t *row_idx, int32_t *perm, float *vals_t) {
+    if (N < 0 || K < 0) return ORC_EINVAL;
+    for (int32_t k = 0; k <= K; ++k) col_ptr[k] = 0;
+    for (int32_t i = 0; i < N; ++i)
+        for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+            if (col_idx[p] < 0 || col_idx[p] >= K) return ORC_EINVAL;
+            ++col_ptr[col_idx[p] + 1];
+        }
+    for (int32_t k = 0; k < K; ++k) col_ptr[k + 1] += col_ptr[k];
+    int32_t *next = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
+    if (!next) return ORC_EINVAL;
+    for (int32_t k = 0; k < K; ++k) next[k] = col_ptr[k];
+    for (int32_t i = 0; i < N; ++i)
+        for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+            const int32_t q = next[col_idx[p]]++;
+            row_idx[q] = i;
+            perm[q] = p;
+            if (vals && vals_t) vals_t[q] = vals[p];
+        }
+    free(next);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
  * CSR -> CSR without its explicit zeros (after a support-restricted prox).
  * Out-of-place: the output arrays must not alias the input ones.
  * ---------------------------------------------------------------------- */

@@ -50,11 +50,9 @@ def bits_equal(a, b):
 
 
 def csc_reference(row_ptr, col_idx, n_cols):
-    """CSC of a CSR structure by a stable sort on (column, row): col_ptr, row_idx, perm."""
-    rp = np.asarray(row_ptr, np.int64)
-    rows = np.repeat(np.arange(rp.shape[0] - 1), np.diff(rp))
-    cols = np.asarray(col_idx, np.int64)
-    order = np.lexsort((rows, cols))
-    col_ptr = np.zeros(n_cols + 1, np.int64)
-    np.cumsum(np.bincount(cols, minlength=n_cols), out=col_ptr[1:])
-    return col_ptr.astype(np.int32), rows[order].astype(np.int32), order.astype(np.int32)
+    """The oracle's canonical CSC of a CSR structure: col_ptr, row_idx, perm
+    (pinned against scipy's CSR -> CSC conversion in the oracle pins)."""
+    import oracle
+    ci = np.asarray(col_idx, np.int32)
+    cp, ri, pm, _ = oracle.csc(row_ptr, ci, np.zeros(ci.shape[0], np.float32), n_cols)
+    return cp, ri, pm

@@ -358,6 +358,52 @@ def test_compact_drops_stored_zeros():
 
 
 # --------------------------------------------------------------------------
+# CSC: the column-wise copy the backward product reads (Section 3.2)
+# --------------------------------------------------------------------------
+
+def _csc_layers():
+    out = _layers()
+    rng = np.random.default_rng(6)
+    rp, ci = synth.zipf_pattern(rng, 300, 257, 9000, 1.1)  # power-law rows, some full
+    out.append(synth.Layer(300, 257, 1, rp, ci, rng.standard_normal(ci.shape[0]).astype(np.float32),
+                           np.zeros((257, 1), np.float32), np.zeros((300, 1), np.float32), 0.0, 0.0, "zipf"))
+    return out
+
+
+@pytest.mark.parametrize("L", _csc_layers(), ids=lambda L: f"N{L.N}K{L.K}nnz{L.col_idx.shape[0]}")
+def test_csc_matches_scipy_and_transposes_back(L):
+    cp, ri, pm, vt = oracle.csc(L.row_ptr, L.col_idx, L.vals, L.K)
+    n = L.col_idx.shape[0]
+    # scipy's CSR -> CSC conversion (sorted indices) is the canonical CSC
+    A = sp.csr_matrix((np.arange(1, n + 1, dtype=np.int64), L.col_idx, L.row_ptr), shape=(L.N, L.K)).tocsc()
+    A.sort_indices()
+    assert cp.tolist() == A.indptr.tolist()
+    assert ri.tolist() == A.indices.tolist()
+    assert (pm + 1).tolist() == A.data.tolist()  # the data carried the CSR positions
+    # perm is a bijection onto the CSR positions, and every field follows it
+    assert sorted(pm.tolist()) == list(range(n))
+    rows = np.repeat(np.arange(L.N), np.diff(L.row_ptr))
+    assert np.array_equal(ri, rows[pm]) and np.array_equal(L.col_idx[pm], np.repeat(np.arange(L.K), np.diff(cp)))
+    assert np.array_equal(vt.view(np.int32), L.vals[pm].view(np.int32))
+    # the CSC read as the CSR of W^T, transposed once more, gives W back
+    cp2, ri2, pm2, vt2 = oracle.csc(cp, ri, vt, L.N)
+    assert np.array_equal(cp2, L.row_ptr) and np.array_equal(ri2, L.col_idx)
+    assert np.array_equal(vt2.view(np.int32), L.vals.view(np.int32))
+    assert np.array_equal(oracle.densify(cp, ri, vt, L.N), _dense(L).T.astype(np.float32))
+
+
+def test_csc_of_fig1(fig1):
+    # the worked example's matrix, column by column: rows in ascending order
+    A, g = fig1
+    rp, ci, v = oracle.recompress(A)
+    cp, ri, pm, vt = oracle.csc(rp, ci, v, A.shape[1])
+    for k in range(A.shape[1]):
+        rows = ri[cp[k]:cp[k + 1]]
+        assert rows.tolist() == np.flatnonzero(A[:, k]).tolist()
+        assert vt[cp[k]:cp[k + 1]].tolist() == A[rows, k].tolist()
+
+
+# --------------------------------------------------------------------------
 # The proximal gradient step converges to the textbook LASSO solution
 # --------------------------------------------------------------------------
 
