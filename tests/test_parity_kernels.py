@@ -562,6 +562,24 @@ def test_sddmm_dense_patterns(shape):
     assert_scaled_close(gv, ref, m, what="gv")
 
 
+# X larger than one XCD's L2 (4096 or 4000 columns by a batch of 512 or 500:
+# 8 MB) with many entries per row: the planner cuts the columns into 8 ranges,
+# one per XCD, instead of 4; ragged columns and batch in the second shape
+@pytest.mark.parametrize("shape", [(1024, 4096, 512, 838861, 13), (700, 4000, 500, 600000, 14)], ids=_ids)
+def test_sddmm_xcd_column_split(shape):
+    L = _layer(shape)
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    ref = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
+    m = oracle.sddmm(L.row_ptr, L.col_idx, np.abs(L.dY), L.X)
+    assert_scaled_close(gv, ref, m, what="gv")
+
+
+def test_sddmm_xcd_column_split_dyadic_bit_exact():
+    L = synth.dyadic_layer(512, 4096, 512, 419430, seed=15, empty_rows=(5,), full_rows=(9,))
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    assert bits_equal(gv, oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X))
+
+
 def test_sddmm_dyadic_bit_exact():
     L = synth.dyadic_layer(40, 60, 1100, 900, seed=6, empty_rows=(2,), full_rows=(7,))
     gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
