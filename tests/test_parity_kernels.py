@@ -564,8 +564,11 @@ def test_sddmm_dense_patterns(shape):
 
 # X larger than one XCD's L2 (4096 or 4000 columns by a batch of 512 or 500:
 # 8 MB) with many entries per row: the planner cuts the columns into 8 ranges,
-# one per XCD, instead of 4; ragged columns and batch in the second shape
-@pytest.mark.parametrize("shape", [(1024, 4096, 512, 838861, 13), (700, 4000, 500, 600000, 14)], ids=_ids)
+# one per XCD, instead of 4; ragged columns and batch in the second shape, a
+# batch of 513 (scalar loads, three batch ranges, the last one column wide) in
+# the third
+@pytest.mark.parametrize("shape", [(1024, 4096, 512, 838861, 13), (700, 4000, 500, 600000, 14),
+                                   (600, 4096, 513, 400000, 16)], ids=_ids)
 def test_sddmm_xcd_column_split(shape):
     L = _layer(shape)
     gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
