@@ -583,6 +583,24 @@ def test_sddmm_xcd_column_split_dyadic_bit_exact():
     assert bits_equal(gv, oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X))
 
 
+# a third of the entries stored or more, with vector loads: the row-block
+# kernel (8-row blocks, 64-column windows); rows not a multiple of 8, columns
+# not a multiple of 64, a batch whose last range is partial
+@pytest.mark.parametrize("shape", [(300, 1000, 260, 150000, 17), (1027, 4096, 512, 2400000, 18)], ids=_ids)
+def test_sddmm_row_blocks(shape):
+    L = _layer(shape)
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    ref = oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X)
+    m = oracle.sddmm(L.row_ptr, L.col_idx, np.abs(L.dY), L.X)
+    assert_scaled_close(gv, ref, m, what="gv")
+
+
+def test_sddmm_row_blocks_dyadic_bit_exact():
+    L = synth.dyadic_layer(301, 1000, 516, 120000, seed=19, empty_rows=(4,), full_rows=(0, 300))
+    gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
+    assert bits_equal(gv, oracle.sddmm(L.row_ptr, L.col_idx, L.dY, L.X))
+
+
 def test_sddmm_dyadic_bit_exact():
     L = synth.dyadic_layer(40, 60, 1100, 900, seed=6, empty_rows=(2,), full_rows=(7,))
     gv = h(L1.sddmm_masked_wgrad(_W(L), t(L.dY), t(L.X)))[: L.nnz]
