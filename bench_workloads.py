@@ -320,9 +320,21 @@ def fc4096_sweep(args, dev):
             else:
                 flops += 6.0 * prev * B
         flops /= iters
+        # the debiasing gradient alone, on the layer's starting pattern
+        # (median of 10 event-timed calls)
+        evs = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            L1.sddmm_masked_wgrad(W0, dYs[1], Xs[1], gv)
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        sd_us = float(np.median([e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]))
         yield _line(f"fc4096_b512_d{pct}_alternating_l1_debias", flops, ms,
                     dict(N=N, K=K, B=B, nnz=L.nnz, density=pct / 100, lam=lam, iterations=iters),
-                    None, nnz_after_l1_steps=nnz_seq)
+                    None, nnz_after_l1_steps=nnz_seq, debias_sddmm_us=round(sd_us, 1),
+                    debias_sddmm_tflops=round(2.0 * L.nnz * B / (sd_us * 1e-6) / 1e12, 2))
 
 
 def fc9216x4096_adaptive(args, dev):
